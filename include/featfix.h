@@ -1,0 +1,261 @@
+/*
+ * featfix.h -- C ABI of libfeatfix.so, the MI355X (gfx950) implementation of the
+ * FeatFix cached diffusion-transformer denoising step.
+ *
+ * The operations follow the paper's statement of the problem (FeatFix, Sec. 3):
+ *   ff_block_exact     exact block output h_f = B_l(u; t, c)                    (Eq. 1)
+ *   ff_cache_update    feature history refreshed at exact refreshes            (Eq. 2)
+ *   ff_draft_forecast  order-K Taylor draft h_d = D(u) from that history       (Eq. 2)
+ *   ff_verify_replace  same-input pair, rel-L1 audit, forwarding rule          (Eq. 3-5)
+ *   ff_denoise_step    one denoising step over a fixed site set, with the
+ *                      Verify / Exact-only / Vanilla controls and accounting   (Sec. 3.3)
+ *
+ * Conventions (all calls):
+ *  - Every device buffer belongs to the caller (weights, latents, stream tensors, cache,
+ *    workspace, audit).  The library never allocates or frees device memory and owns
+ *    only the host objects ff_plan and ff_ctx.  Pointers must stay valid until the work
+ *    queued on the stream has completed.
+ *  - Layouts are row-major.  Weight matrices are [out, in].  Activations are [B, N, C]
+ *    with N = n_txt + n_img rows per sample, text rows first.  The cache is
+ *    [L][S][B*N*C], contiguous, in the model dtype.
+ *  - "dtype" tensors are fp32 (FF_F32) or bf16 (FF_BF16) as the model descriptor says.
+ *    Conditioning vectors, the latent, modulation and audit values are always fp32.
+ *  - Every pointer passed as a device pointer must be 16-byte aligned.
+ *  - All validation happens on the host before anything is launched; on error nothing
+ *    is launched, outputs are untouched and ff_last_error() describes the problem.
+ *    Asynchronous device faults surface at the caller's stream synchronisation (or as
+ *    FF_E_HIP from a later call).  No C++ exception crosses the ABI.
+ *  - Calls are re-entrant; use one ff_ctx per stream.  Calls that share a workspace or
+ *    cache must be ordered on one stream.
+ *  - All kernels are deterministic: the same inputs give bitwise identical outputs.
+ */
+#ifndef FEATFIX_H
+#define FEATFIX_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define FF_ABI_VERSION 1
+#define FF_MAX_K 3          /* largest supported forecast order K */
+#define FF_MAX_SLOTS 8      /* largest supported ring size S      */
+#define FF_TEMB_DIM 256     /* sinusoidal time-embedding width    */
+
+typedef int32_t ff_status;
+enum {
+  FF_OK = 0,
+  FF_E_NULL = -1,        /* a required pointer is NULL                                */
+  FF_E_SHAPE = -2,       /* inconsistent or unsupported sizes                         */
+  FF_E_DTYPE = -3,       /* unknown dtype                                             */
+  FF_E_RANGE = -4,       /* layer / step / slot / order / mode out of range           */
+  FF_E_STATE = -5,       /* slot never written, draft before first refresh, step order */
+  FF_E_WORKSPACE = -6,   /* workspace or cache buffer too small                      */
+  FF_E_HIP = -7,         /* a HIP runtime call failed                                 */
+  FF_E_UNSUPPORTED = -8  /* valid request this build does not implement              */
+};
+
+enum { FF_DIT = 0, FF_MMDIT_DOUBLE = 1, FF_MMDIT_SINGLE = 2 };          /* block kinds  */
+enum { FF_F32 = 0, FF_BF16 = 1 };                                        /* dtypes       */
+enum { FF_VANILLA = 0, FF_DRAFT = 1, FF_VERIFY = 2, FF_FEATFIX = 3, FF_EXACT_ONLY = 4 };
+enum { FF_RESIDUAL = 0, FF_OUTPUT = 1 };                                 /* feature mode */
+enum { FF_STEP_REFRESH = 0, FF_STEP_CACHED = 1 };                        /* step kinds   */
+enum { FF_ACT_EXACT = 0, FF_ACT_DRAFT = 1, FF_ACT_SITE = 2 };            /* actions      */
+
+/* HIP stream handle (the same type as hipStream_t); NULL is the default stream. */
+typedef struct ihipStream_t* ff_stream_t;
+
+/* Model shape.  Block kinds: FF_DIT (adaLN DiT block), FF_MMDIT_DOUBLE (separate text /
+ * image weight sets, joint attention, per-head QK RMSNorm), FF_MMDIT_SINGLE (one weight
+ * set, fused attention+MLP input projection).  FF_DIT requires n_txt == 0.
+ * Requirements: C == H*d, d in [8, 128] and d % 8 == 0, C % 8 == 0, mlp_hidden % 8 == 0,
+ * 1 <= B, lat_f % pt == lat_h % ph == lat_w % pw == 0,
+ * n_img == (lat_f/pt)*(lat_h/ph)*(lat_w/pw), (pt*ph*pw*lat_c) % 8 == 0. */
+typedef struct {
+  int32_t n_layers;
+  const int32_t* kinds;   /* host array [n_layers]; copied where it is kept */
+  int32_t C, H, d, mlp_hidden;
+  int32_t n_img, n_txt, B;
+  int32_t lat_c, lat_f, lat_h, lat_w;
+  int32_t pt, ph, pw;
+  int32_t dtype;
+  float ln_eps;           /* LayerNorm / RMSNorm epsilon */
+} ff_model_desc;
+
+/* One stream's weights of one block (device pointers, model dtype, [out, in]).
+ * FF_DIT and the two streams of FF_MMDIT_DOUBLE use:
+ *   mod_w [6C, C], mod_b [6C]   -> shift1, scale1, gate1, shift2, scale2, gate2
+ *   qkv_w [3C, C], qkv_b [3C]   -> columns s*C + h*d + e, s in {q, k, v}
+ *   o_w [C, C], o_b [C];  fc1_w [M, C], fc1_b [M];  fc2_w [C, M], fc2_b [C]
+ *   q_g [d], k_g [d]            -> QK RMSNorm gains (MMDiT only)
+ * FF_MMDIT_SINGLE uses:
+ *   mod_w [3C, C], mod_b [3C]   -> shift, scale, gate
+ *   lin1_w [3C+M, C], lin1_b    -> q | k | v | mlp input
+ *   lin2_w [C, C+M], lin2_b [C] -> applied to [attention | GELU(mlp input)]
+ *   q_g [d], k_g [d] */
+typedef struct {
+  const void *mod_w, *mod_b;
+  const void *qkv_w, *qkv_b;
+  const void *o_w, *o_b;
+  const void *fc1_w, *fc1_b;
+  const void *fc2_w, *fc2_b;
+  const void *lin1_w, *lin1_b;
+  const void *lin2_w, *lin2_b;
+  const void *q_g, *k_g;
+} ff_stream_weights;
+
+/* s[0]: the DiT / single-stream weights, or the text stream of a double block;
+ * s[1]: the image stream of a double block (unused otherwise). */
+typedef struct {
+  ff_stream_weights s[2];
+} ff_layer_weights;
+
+/* Embedders and final layer (device pointers, model dtype), P = pt*ph*pw*lat_c:
+ *   t1_w [C, 256], t1_b [C], t2_w [C, C], t2_b [C]   time-embedding MLP
+ *   pe_w [C, P], pe_b [C]                             patch embedding
+ *   fmod_w [2C, C], fmod_b [2C]                       final adaLN (shift, scale)
+ *   f_w [P, C], f_b [P]                               final linear */
+typedef struct {
+  const void *t1_w, *t1_b, *t2_w, *t2_b;
+  const void *pe_w, *pe_b;
+  const void *fmod_w, *fmod_b, *f_w, *f_b;
+} ff_global_weights;
+
+/* Schedule: T steps, full refresh every R steps (steps i with i % R == 0), forecast
+ * order K (0 <= K <= FF_MAX_K), ring of S slots (K+1 <= S <= FF_MAX_SLOTS), rel-L1
+ * epsilon eps > 0, mode (FF_VANILLA .. FF_EXACT_ONLY), feature_mode (FF_RESIDUAL caches
+ * h - u and drafts u + F; FF_OUTPUT caches h and drafts F). */
+typedef struct {
+  int32_t T, R, K, S;
+  float eps;
+  int32_t mode;
+  int32_t feature_mode;
+} ff_sched_desc;
+
+/* Separate accounting of full-refresh steps, paid exact-block checks and forwarded
+ * corrections (Sec. 3.3, matched-compute controls and accounting). */
+typedef struct {
+  int64_t n_full_refresh, n_paid_checks, n_forwarded;
+} ff_counts;
+
+typedef struct ff_plan ff_plan;
+typedef struct ff_ctx ff_ctx;
+
+/* ABI version (FF_ABI_VERSION). */
+int32_t ff_abi_version(void);
+
+/* Message for the last failing ff_* call on this thread ("" if none).  Thread-local;
+ * valid until the next ff_* call on the same thread. */
+const char* ff_last_error(void);
+
+/* ---------------------------------------------------------------- schedule (host only)
+ * Builds the fixed schedule (Sec. 3.3: sites frozen before evaluation; Eq. 2: finite
+ * differences estimated at exact refreshes).  site_mask is a host uint8 array [T*L],
+ * step-major; bits on refresh steps are ignored and Draft mode ignores all bits.
+ * Per step i: refresh iff mode == FF_VANILLA or i % R == 0; refresh ordinal
+ * j = (#refreshes up to i) - 1; k_eff = min(K, j); refresh steps write slot j % S (none
+ * in Vanilla); cached steps read slots (j - m) % S for m = 0..k_eff with coefficients
+ * c_m such that F(i) = sum_m c_m * Delta_{j-m} equals the Taylor forecast of Eq. 2.
+ * Per (i, l): EXACT on refresh steps, SITE where the mask is set in Verify / FeatFix /
+ * Exact-only, DRAFT otherwise.  *out is owned by the caller (ff_plan_destroy).
+ * Errors: FF_E_NULL, FF_E_RANGE (T, R, K, S, mode, feature_mode, n_layers, eps). */
+ff_status ff_plan_build(const ff_sched_desc* s, int32_t n_layers, const uint8_t* site_mask,
+                        ff_plan** out);
+void ff_plan_destroy(ff_plan* p);
+
+/* Copies the plan's decisions into host arrays (any may be NULL to skip it):
+ * step_kind[T], refresh_ord[T], k_eff[T], read_slots[T*(K+1)] (-1 padded),
+ * write_slot[T] (-1 if none), action[T*L], coeffs[T*(K+1)] (fp32, 0 padded), counts
+ * (totals over the whole schedule).  Errors: FF_E_NULL if p is NULL. */
+ff_status ff_plan_export(const ff_plan* p, int32_t* step_kind, int32_t* refresh_ord,
+                         int32_t* k_eff, int32_t* read_slots, int32_t* write_slot,
+                         int32_t* action, float* coeffs, ff_counts* counts);
+
+/* ---------------------------------------------------------------- sizing
+ * Bytes of a cache with n_slots ring slots per layer: L * n_slots * B*N*C * dtype size.
+ * Bytes of workspace ff_denoise_step needs (ff_block_exact and ff_verify_replace need
+ * no more than this).  Both return 0 for an invalid descriptor. */
+size_t ff_cache_bytes(const ff_model_desc* m, int32_t n_slots);
+size_t ff_workspace_bytes(const ff_model_desc* m);
+
+/* ---------------------------------------------------------------- block operations
+ * Exact block output (Eq. 1): h = B_layer(u; c_t) for the block kind m->kinds[layer].
+ * c_t: device fp32 [B, C] conditioning (class/text vector plus time embedding);
+ * u, h: device [B, N, C] dtype; h must not overlap u or ws.  ws: device workspace of
+ * at least ff_workspace_bytes(m) bytes.  Deterministic (bitwise reproducible).
+ * Errors: FF_E_NULL, FF_E_RANGE (layer), FF_E_SHAPE, FF_E_DTYPE, FF_E_WORKSPACE. */
+ff_status ff_block_exact(const ff_model_desc* m, int32_t layer, const ff_layer_weights* w,
+                         const float* c_t, const void* u, void* h, void* ws, size_t ws_bytes,
+                         ff_stream_t stream);
+
+/* Refresh of the feature history (Eq. 2, estimated at exact refreshes):
+ * cache[layer][slot] <- h - u (FF_RESIDUAL, rounded to dtype) or h (FF_OUTPUT; u unused,
+ * may be NULL).  cache holds n_slots slots per layer.
+ * Errors: FF_E_NULL, FF_E_RANGE (layer, slot, n_slots, feature_mode), FF_E_SHAPE. */
+ff_status ff_cache_update(const ff_model_desc* m, void* cache, int32_t n_slots, int32_t layer,
+                          int32_t slot, const void* u, const void* h, int32_t feature_mode,
+                          ff_stream_t stream);
+
+/* Draft forecast (Eq. 2): h_d = u + sum_{m=0..k_eff} coeffs[m] * cache[layer][slots[m]]
+ * (u == NULL selects FF_OUTPUT: h_d = sum_m coeffs[m] * cache[layer][slots[m]]).
+ * slots and coeffs are host arrays [k_eff+1].  Sums in fp32, one rounding to dtype.
+ * h_d may alias u exactly (in-place); no other overlap is allowed.
+ * Errors: FF_E_NULL, FF_E_RANGE (layer, k_eff, slot, n_slots), FF_E_SHAPE. */
+ff_status ff_draft_forecast(const ff_model_desc* m, const void* cache, int32_t n_slots,
+                            int32_t layer, int32_t k_eff, const int32_t* slots,
+                            const float* coeffs, const void* u, void* h_d, ff_stream_t stream);
+
+/* Paid verification and forwarding (Eq. 3-5) in one pass over the site tensor:
+ * rebuilds h_d = D(u) as ff_draft_forecast does (u == NULL for FF_OUTPUT), computes per
+ * sample b the normalised relative-L1 discrepancy
+ *     rel_l1[b] = sum|h_d - h_f| / (sum|h_f| + eps)       (Eq. 4; fp32, fixed-order sums)
+ * and writes h_out = h_f if forward_exact (FeatFix: bit-identical copy of h_f) or h_d
+ * (Verify).  h_out may alias u exactly; it must not overlap h_f.  rel_l1 is a device
+ * fp32 [B] array or NULL.  ws holds the partial sums (at least ff_workspace_bytes(m)).
+ * Errors: FF_E_NULL, FF_E_RANGE, FF_E_SHAPE, FF_E_WORKSPACE. */
+ff_status ff_verify_replace(const ff_model_desc* m, const void* cache, int32_t n_slots,
+                            int32_t layer, int32_t k_eff, const int32_t* slots,
+                            const float* coeffs, const void* u, const void* h_f, void* h_out,
+                            int32_t forward_exact, float eps, float* rel_l1, void* ws,
+                            size_t ws_bytes, ff_stream_t stream);
+
+/* ---------------------------------------------------------------- step executor
+ * A context binds a model, its weights (layer_w is a host array [n_layers]; the device
+ * pointers inside are kept, the host arrays are copied), a plan (copied), a cache of at
+ * least ff_cache_bytes(m, plan S) bytes and a workspace of at least
+ * ff_workspace_bytes(m) bytes.  *out is owned by the caller (ff_ctx_destroy).
+ * Errors: FF_E_NULL, FF_E_SHAPE, FF_E_DTYPE, FF_E_WORKSPACE, FF_E_RANGE. */
+ff_status ff_ctx_create(const ff_model_desc* m, const ff_layer_weights* layer_w,
+                        const ff_global_weights* g, const ff_plan* p, void* cache,
+                        size_t cache_bytes, void* ws, size_t ws_bytes, ff_ctx** out);
+void ff_ctx_destroy(ff_ctx* c);
+
+/* Rewinds the context to step 0, forgets the cache history and zeroes the counts. */
+ff_status ff_ctx_reset(ff_ctx* c);
+
+/* Counts of the steps executed since creation / the last reset. */
+ff_status ff_get_counts(const ff_ctx* c, ff_counts* out);
+
+/* One denoising step i = step (must be the context's next step, 0..T-1 in order):
+ *   c_t = cond + TimeMLP(sinusoid(1000 t_i)), t_i = 1 - i/T
+ *   X = [txt ; PatchEmbed(patchify(x))]
+ *   for each layer l, by the plan's action:
+ *     EXACT: X <- B_l(X); refresh the history of l (not in Vanilla)
+ *     DRAFT: X <- D_l(X)
+ *     SITE : h_f = B_l(X); audit and forward per mode (FeatFix / Exact-only: h_f,
+ *            Verify: the draft); Exact-only skips the draft and the audit
+ *   v = unpatchify(FinalLayer(X_img)); x <- x + (t_{i+1} - t_i) v
+ * x: device fp32 latent [B, lat_c, lat_f, lat_h, lat_w], updated in place.
+ * cond: device fp32 [B, C].  txt: device dtype [B, n_txt, C] (NULL iff n_txt == 0).
+ * audit: device fp32 [T*L*B] or NULL; entry (i*L + l)*B + b receives rel_l1 at paid
+ * checks (other entries are not written).
+ * Errors: FF_E_NULL, FF_E_STATE (step out of order), FF_E_HIP. */
+ff_status ff_denoise_step(ff_ctx* c, int32_t step, float* x, const float* cond,
+                          const void* txt, float* audit, ff_stream_t stream);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* FEATFIX_H */

@@ -1,0 +1,91 @@
+// Device-side helpers shared by the gfx950 kernels: bf16 storage conversions and
+// 16-byte vector access.  bf16 values are stored as raw uint16 bit patterns.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+#include "kernels.h"
+
+namespace ff {
+
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));  // 16-byte moves (native vector, not a struct)
+typedef uint32_t u32x2_t __attribute__((ext_vector_type(2)));
+
+__device__ __forceinline__ float bf2f(uint16_t b) { return __uint_as_float((uint32_t)b << 16); }
+
+// fp32 -> bf16, round to nearest even (NaN stays NaN).
+__device__ __forceinline__ uint16_t f2bf(float f) {
+  uint32_t u = __float_as_uint(f);
+  if ((u & 0x7fffffffu) > 0x7f800000u) return (uint16_t)((u >> 16) | 0x40u);
+  u += 0x7fffu + ((u >> 16) & 1u);
+  return (uint16_t)(u >> 16);
+}
+
+// Storage traits: 8 elements per 16-byte chunk for bf16, 4 for fp32.
+template <int DT> struct St;
+template <> struct St<DT_BF16> {
+  static constexpr int V = 8;
+  __device__ __forceinline__ static void load(const void* p, size_t i, float* v) {
+    uint4 w = *reinterpret_cast<const uint4*>(reinterpret_cast<const uint16_t*>(p) + i);
+    uint32_t a[4] = {w.x, w.y, w.z, w.w};
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      v[2 * j] = __uint_as_float(a[j] << 16);
+      v[2 * j + 1] = __uint_as_float(a[j] & 0xffff0000u);
+    }
+  }
+  __device__ __forceinline__ static void store(void* p, size_t i, const float* v) {
+    uint32_t a[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) a[j] = (uint32_t)f2bf(v[2 * j]) | ((uint32_t)f2bf(v[2 * j + 1]) << 16);
+    *reinterpret_cast<uint4*>(reinterpret_cast<uint16_t*>(p) + i) = make_uint4(a[0], a[1], a[2], a[3]);
+  }
+  __device__ __forceinline__ static float rnd(float x) { return bf2f(f2bf(x)); }
+  __device__ __forceinline__ static float ld1(const void* p, size_t i) {
+    return bf2f(reinterpret_cast<const uint16_t*>(p)[i]);
+  }
+  __device__ __forceinline__ static void st1(void* p, size_t i, float x) {
+    reinterpret_cast<uint16_t*>(p)[i] = f2bf(x);
+  }
+};
+template <> struct St<DT_F32> {
+  static constexpr int V = 4;
+  __device__ __forceinline__ static void load(const void* p, size_t i, float* v) {
+    float4 w = *reinterpret_cast<const float4*>(reinterpret_cast<const float*>(p) + i);
+    v[0] = w.x; v[1] = w.y; v[2] = w.z; v[3] = w.w;
+  }
+  __device__ __forceinline__ static void store(void* p, size_t i, const float* v) {
+    *reinterpret_cast<float4*>(reinterpret_cast<float*>(p) + i) = make_float4(v[0], v[1], v[2], v[3]);
+  }
+  __device__ __forceinline__ static float rnd(float x) { return x; }
+  __device__ __forceinline__ static float ld1(const void* p, size_t i) {
+    return reinterpret_cast<const float*>(p)[i];
+  }
+  __device__ __forceinline__ static void st1(void* p, size_t i, float x) {
+    reinterpret_cast<float*>(p)[i] = x;
+  }
+};
+
+__device__ __forceinline__ float silu_f(float x) { return x / (1.0f + expf(-x)); }
+
+__device__ __forceinline__ float gelu_tanh_f(float z) {
+  const float k0 = 0.7978845608028654f;  // sqrt(2/pi)
+  return 0.5f * z * (1.0f + tanhf(k0 * (z + 0.044715f * z * z * z)));
+}
+
+// Sum over the 64 lanes of a wavefront (fixed butterfly order: deterministic).
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
+  return v;
+}
+__device__ __forceinline__ float wave_max(float v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, 64));
+  return v;
+}
+
+inline int cdiv(long a, long b) { return (int)((a + b - 1) / b); }
+
+}  // namespace ff

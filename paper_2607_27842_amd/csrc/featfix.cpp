@@ -1,0 +1,733 @@
+// Host side of libfeatfix.so: argument validation, the fixed schedule (plan), the
+// exact-block composer, the per-step executor and the C ABI of include/featfix.h.
+// The library owns host objects only; every device buffer is the caller's.
+#include <hip/hip_runtime.h>
+
+#include <math.h>
+#include <stdarg.h>
+#include <stdio.h>
+#include <string.h>
+
+#include <new>
+#include <vector>
+
+#include "featfix.h"
+#include "kernels.h"
+
+using namespace ff;
+
+namespace {
+
+thread_local char g_err[512] = "";
+
+ff_status fail(ff_status code, const char* fmt, ...) {
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(g_err, sizeof(g_err), fmt, ap);
+  va_end(ap);
+  return code;
+}
+ff_status ok() {
+  g_err[0] = 0;
+  return FF_OK;
+}
+ff_status hip_fail(hipError_t e, const char* where) {
+  return fail(FF_E_HIP, "%s: %s", where, hipGetErrorString(e));
+}
+#define HIP_TRY(expr, where)              \
+  do {                                    \
+    hipError_t _e = (expr);               \
+    if (_e != hipSuccess) return hip_fail(_e, where); \
+  } while (0)
+
+constexpr int kGemvMaxB = 8;
+constexpr size_t kAlign = 256;
+inline size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
+
+// ---------------------------------------------------------------- model validation
+struct Model {
+  int L = 0;
+  std::vector<int> kinds;
+  int C = 0, H = 0, d = 0, M = 0, n_img = 0, n_txt = 0, B = 0, N = 0, P = 0;
+  int lat_c = 0, lat_f = 0, lat_h = 0, lat_w = 0, pt = 0, ph = 0, pw = 0;
+  int dtype = 0;
+  float ln_eps = 0.f;
+  bool any_single = false;
+  size_t es() const { return dsize(dtype); }
+  size_t E() const { return (size_t)B * N * C; }
+};
+
+bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
+
+ff_status check_model(const ff_model_desc* m, Model* out) {
+  if (!m) return fail(FF_E_NULL, "model descriptor is NULL");
+  if (m->dtype != FF_F32 && m->dtype != FF_BF16) return fail(FF_E_DTYPE, "unknown dtype %d", m->dtype);
+  if (m->n_layers < 1 || m->n_layers > 4096) return fail(FF_E_SHAPE, "n_layers %d out of range", m->n_layers);
+  if (!m->kinds) return fail(FF_E_NULL, "kinds is NULL");
+  Model r;
+  r.L = m->n_layers;
+  r.C = m->C; r.H = m->H; r.d = m->d; r.M = m->mlp_hidden;
+  r.n_img = m->n_img; r.n_txt = m->n_txt; r.B = m->B;
+  r.lat_c = m->lat_c; r.lat_f = m->lat_f; r.lat_h = m->lat_h; r.lat_w = m->lat_w;
+  r.pt = m->pt; r.ph = m->ph; r.pw = m->pw;
+  r.dtype = m->dtype;
+  r.ln_eps = m->ln_eps;
+  for (int l = 0; l < r.L; ++l) {
+    const int k = m->kinds[l];
+    if (k != FF_DIT && k != FF_MMDIT_DOUBLE && k != FF_MMDIT_SINGLE)
+      return fail(FF_E_SHAPE, "layer %d: unknown block kind %d", l, k);
+    if (k == FF_DIT && r.n_txt != 0) return fail(FF_E_SHAPE, "layer %d: DiT blocks need n_txt == 0", l);
+    if (k == FF_MMDIT_SINGLE) r.any_single = true;
+    r.kinds.push_back(k);
+  }
+  if (r.B < 1 || r.B > kGemvMaxB) return fail(FF_E_SHAPE, "batch %d outside [1, %d]", r.B, kGemvMaxB);
+  if (r.H < 1 || r.d < 8 || r.d > 128 || r.d % 8 || (long)r.H * r.d != r.C)
+    return fail(FF_E_SHAPE, "need C == H*d, 8 <= d <= 128, d %% 8 == 0 (C=%d H=%d d=%d)", r.C, r.H, r.d);
+  const int cmax = r.dtype == FF_BF16 ? 4096 : 2048;
+  if (r.C % 8 || r.C > cmax) return fail(FF_E_SHAPE, "C=%d must be a multiple of 8 and <= %d", r.C, cmax);
+  if (r.M < 8 || r.M % 8) return fail(FF_E_SHAPE, "mlp_hidden=%d must be a positive multiple of 8", r.M);
+  if (r.n_img < 1 || r.n_txt < 0) return fail(FF_E_SHAPE, "bad token counts n_img=%d n_txt=%d", r.n_img, r.n_txt);
+  if (r.pt < 1 || r.ph < 1 || r.pw < 1 || r.lat_c < 1 || r.lat_f < 1 || r.lat_h < 1 || r.lat_w < 1)
+    return fail(FF_E_SHAPE, "bad latent / patch geometry");
+  if (r.lat_f % r.pt || r.lat_h % r.ph || r.lat_w % r.pw) return fail(FF_E_SHAPE, "latent not divisible by patch");
+  const long nimg = (long)(r.lat_f / r.pt) * (r.lat_h / r.ph) * (r.lat_w / r.pw);
+  if (nimg != r.n_img) return fail(FF_E_SHAPE, "n_img=%d but the latent has %ld patches", r.n_img, nimg);
+  r.P = r.pt * r.ph * r.pw * r.lat_c;
+  if (r.P % 8) return fail(FF_E_SHAPE, "patch features %d must be a multiple of 8", r.P);
+  r.N = r.n_img + r.n_txt;
+  if ((long)r.B * r.N > (1L << 30) / 8) return fail(FF_E_SHAPE, "too many rows");
+  if (!(r.ln_eps > 0.f)) return fail(FF_E_RANGE, "ln_eps must be > 0");
+  *out = r;
+  return FF_OK;
+}
+
+// ---------------------------------------------------------------- workspace layout
+struct Ws {
+  size_t X0, X1, HF, LNA, QKV, ATT, X1F, HID, MOD, CT, CS, TMP, PHI, PATCH, YF, PART, total;
+};
+
+Ws ws_layout(const Model& m) {
+  Ws w{};
+  size_t off = 0;
+  auto take = [&](size_t bytes) { size_t o = off; off += align_up(bytes); return o; };
+  const size_t es = m.es(), rows = (size_t)m.B * m.N;
+  w.X0 = take(rows * m.C * es);
+  w.X1 = take(rows * m.C * es);
+  w.HF = take(rows * m.C * es);
+  w.LNA = take(rows * m.C * es);
+  w.QKV = take(rows * 3 * (size_t)m.C * es);
+  w.ATT = take(rows * (size_t)(m.any_single ? m.C + m.M : m.C) * es);
+  w.X1F = take(rows * m.C * 4);
+  w.HID = take(rows * (size_t)m.M * es);
+  w.MOD = take((size_t)m.B * 12 * m.C * 4);
+  w.CT = take((size_t)m.B * m.C * 4);
+  w.CS = take((size_t)m.B * m.C * 4);
+  w.TMP = take((size_t)m.B * m.C * 4);
+  w.PHI = take(FF_TEMB_DIM * 4);
+  w.PATCH = take((size_t)m.B * m.n_img * m.P * es);
+  w.YF = take((size_t)m.B * m.n_img * m.P * 4);
+  w.PART = take(verify_partials_floats(m.B) * 4);
+  w.total = off;
+  return w;
+}
+
+template <class T = void>
+T* at(void* base, size_t off) { return reinterpret_cast<T*>(reinterpret_cast<char*>(base) + off); }
+
+// ---------------------------------------------------------------- weights
+bool stream_ok(const ff_stream_weights& s, int kind) {
+  if (!s.mod_w || !s.mod_b || !aligned16(s.mod_w)) return false;
+  if (kind == FF_MMDIT_SINGLE) {
+    if (!s.lin1_w || !s.lin1_b || !s.lin2_w || !s.lin2_b) return false;
+    if (!aligned16(s.lin1_w) || !aligned16(s.lin2_w)) return false;
+  } else {
+    if (!s.qkv_w || !s.qkv_b || !s.o_w || !s.o_b || !s.fc1_w || !s.fc1_b || !s.fc2_w || !s.fc2_b) return false;
+    if (!aligned16(s.qkv_w) || !aligned16(s.o_w) || !aligned16(s.fc1_w) || !aligned16(s.fc2_w)) return false;
+  }
+  if (kind != FF_DIT && (!s.q_g || !s.k_g)) return false;
+  return true;
+}
+
+ff_status check_layer_weights(const ff_layer_weights* w, int kind, int layer) {
+  if (!w) return fail(FF_E_NULL, "layer %d: weights are NULL", layer);
+  if (!stream_ok(w->s[0], kind) || (kind == FF_MMDIT_DOUBLE && !stream_ok(w->s[1], kind)))
+    return fail(FF_E_NULL, "layer %d: a required weight pointer is NULL or not 16-byte aligned", layer);
+  return FF_OK;
+}
+
+// ---------------------------------------------------------------- exact block (Eq. 1)
+RowMap whole(const Model& m) { return RowMap{m.N, m.N, 0}; }
+
+GemmArgs gemm_args(const void* A, int lda, RowMap amap, const void* W, const void* bias, int M, int N, int K,
+                   int epi, void* out, int ldo, RowMap omap) {
+  GemmArgs g{};
+  g.A = A; g.lda = lda; g.amap = amap;
+  g.W = W; g.ldw = K;
+  g.bias = bias;
+  g.M = M; g.N = N; g.K = K;
+  g.epi = epi;
+  g.out = out; g.ldo = ldo; g.omap = omap; g.out_f32 = 0;
+  return g;
+}
+
+const void* offset_rows(const void* p, size_t rows, size_t cols, size_t es) {
+  return reinterpret_cast<const char*>(p) + rows * cols * es;
+}
+
+// h = B_l(u; c_t) with cs = SiLU(c_t) [B, C] fp32 already in the workspace.
+ff_status exec_block(const Model& m, int kind, const ff_layer_weights& w, const float* cs, const void* u,
+                     void* h, void* ws, hipStream_t st) {
+  const Ws L = ws_layout(m);
+  const int C = m.C, Mh = m.M, dt = m.dtype;
+  const size_t es = m.es();
+  void* lna = at(ws, L.LNA);
+  void* qkv = at(ws, L.QKV);
+  void* att = at(ws, L.ATT);
+  float* x1f = at<float>(ws, L.X1F);
+  void* hid = at(ws, L.HID);
+  float* mod = at<float>(ws, L.MOD);
+  const float scale = 1.0f / sqrtf((float)m.d);
+
+  AttnArgs aa{};
+  aa.qkv = qkv; aa.ldq = 3 * C; aa.B = m.B; aa.N = m.N; aa.H = m.H; aa.d = m.d; aa.C = C; aa.scale = scale;
+
+  if (kind == FF_MMDIT_SINGLE) {
+    const ff_stream_weights& s = w.s[0];
+    const RowMap all = whole(m);
+    const int rows = m.B * m.N;
+    GemvArgs gv{cs, C, 0, s.mod_w, s.mod_b, 3 * C, C, m.B, mod, 3 * C, 0, nullptr, 0};
+    HIP_TRY(gemv(dt, gv, st), "single: modulation");
+    LnModArgs ln{u, 0, C, all, rows, C, m.ln_eps, mod, mod + C, 3 * C, lna, C};
+    HIP_TRY(ln_modulate(dt, ln, st), "single: ln");
+    GemmArgs g1 = gemm_args(lna, C, all, s.lin1_w, s.lin1_b, rows, 3 * C, C, EPI_BIAS, qkv, 3 * C, all);
+    HIP_TRY(gemm(dt, g1, st), "single: lin1 qkv");
+    const int ldy = C + Mh;
+    GemmArgs g2 = gemm_args(lna, C, all, offset_rows(s.lin1_w, 3 * (size_t)C, C, es),
+                            offset_rows(s.lin1_b, 3 * (size_t)C, 1, es), rows, Mh, C, EPI_BIAS_GELU,
+                            at(att, (size_t)C * es), ldy, all);
+    HIP_TRY(gemm(dt, g2, st), "single: lin1 mlp");
+    RmsArgs rq{qkv, 3 * C, all, rows, m.H, m.d, 0, s.q_g, m.ln_eps};
+    HIP_TRY(rms_heads(dt, rq, st), "single: q norm");
+    RmsArgs rk{qkv, 3 * C, all, rows, m.H, m.d, C, s.k_g, m.ln_eps};
+    HIP_TRY(rms_heads(dt, rk, st), "single: k norm");
+    aa.out = att; aa.ldo = ldy;
+    HIP_TRY(attention(dt, aa, st), "single: attention");
+    GemmArgs g3 = gemm_args(att, ldy, all, s.lin2_w, s.lin2_b, rows, C, C + Mh, EPI_GATED, h, C, all);
+    g3.resid = u; g3.ldr = C; g3.resid_f32 = 0; g3.gate = mod + 2 * C; g3.ldg = 3 * C;
+    HIP_TRY(gemm(dt, g3, st), "single: lin2");
+    return FF_OK;
+  }
+
+  // DiT block (one stream) or MMDiT double block (text rows, then image rows).
+  const int nstreams = kind == FF_MMDIT_DOUBLE ? 2 : 1;
+  RowMap maps[2];
+  int nseg[2];
+  if (kind == FF_MMDIT_DOUBLE) {
+    maps[0] = RowMap{m.n_txt > 0 ? m.n_txt : 1, m.N, 0}; nseg[0] = m.n_txt;
+    maps[1] = RowMap{m.n_img, m.N, m.n_txt}; nseg[1] = m.n_img;
+  } else {
+    maps[0] = whole(m); nseg[0] = m.N;
+  }
+  const int ldm = 6 * C * nstreams;
+  for (int si = 0; si < nstreams; ++si) {
+    const ff_stream_weights& s = w.s[si];
+    const int rows = m.B * nseg[si];
+    float* ms = mod + 6 * C * si;
+    GemvArgs gv{cs, C, 0, s.mod_w, s.mod_b, 6 * C, C, m.B, ms, ldm, 0, nullptr, 0};
+    HIP_TRY(gemv(dt, gv, st), "block: modulation");
+    if (rows == 0) continue;
+    LnModArgs ln{u, 0, C, maps[si], rows, C, m.ln_eps, ms, ms + C, ldm, lna, C};
+    HIP_TRY(ln_modulate(dt, ln, st), "block: ln1");
+    GemmArgs g = gemm_args(lna, C, maps[si], s.qkv_w, s.qkv_b, rows, 3 * C, C, EPI_BIAS, qkv, 3 * C, maps[si]);
+    HIP_TRY(gemm(dt, g, st), "block: qkv");
+    if (kind == FF_MMDIT_DOUBLE) {
+      RmsArgs rq{qkv, 3 * C, maps[si], rows, m.H, m.d, 0, s.q_g, m.ln_eps};
+      HIP_TRY(rms_heads(dt, rq, st), "double: q norm");
+      RmsArgs rk{qkv, 3 * C, maps[si], rows, m.H, m.d, C, s.k_g, m.ln_eps};
+      HIP_TRY(rms_heads(dt, rk, st), "double: k norm");
+    }
+  }
+  aa.out = att; aa.ldo = C;
+  HIP_TRY(attention(dt, aa, st), "block: attention");
+  for (int si = 0; si < nstreams; ++si) {
+    const ff_stream_weights& s = w.s[si];
+    const int rows = m.B * nseg[si];
+    if (rows == 0) continue;
+    float* ms = mod + 6 * C * si;
+    GemmArgs go = gemm_args(att, C, maps[si], s.o_w, s.o_b, rows, C, C, EPI_GATED, x1f, C, maps[si]);
+    go.out_f32 = 1; go.resid = u; go.ldr = C; go.resid_f32 = 0; go.gate = ms + 2 * C; go.ldg = ldm;
+    HIP_TRY(gemm(dt, go, st), "block: proj");
+    LnModArgs ln{x1f, 1, C, maps[si], rows, C, m.ln_eps, ms + 3 * C, ms + 4 * C, ldm, lna, C};
+    HIP_TRY(ln_modulate(dt, ln, st), "block: ln2");
+    GemmArgs g1 = gemm_args(lna, C, maps[si], s.fc1_w, s.fc1_b, rows, Mh, C, EPI_BIAS_GELU, hid, Mh, maps[si]);
+    HIP_TRY(gemm(dt, g1, st), "block: fc1");
+    GemmArgs g2 = gemm_args(hid, Mh, maps[si], s.fc2_w, s.fc2_b, rows, C, Mh, EPI_GATED, h, C, maps[si]);
+    g2.resid = x1f; g2.ldr = C; g2.resid_f32 = 1; g2.gate = ms + 5 * C; g2.ldg = ldm;
+    HIP_TRY(gemm(dt, g2, st), "block: fc2");
+  }
+  return FF_OK;
+}
+
+// ---------------------------------------------------------------- schedule
+}  // namespace
+
+struct ff_plan {
+  ff_sched_desc s;
+  int L;
+  std::vector<int32_t> step_kind, refresh_ord, k_eff, read_slots, write_slot, action;
+  std::vector<float> coeffs;
+  ff_counts counts;
+};
+
+struct ff_ctx {
+  Model m;
+  std::vector<ff_layer_weights> lw;
+  ff_global_weights g;
+  ff_plan plan;
+  void* cache;
+  void* ws;
+  int next_step;
+  std::vector<uint8_t> written;  // [L * S]: slot holds a refresh of this run
+  ff_counts counts;
+};
+
+namespace {
+
+// Coefficients of the Taylor draft in terms of the ring of raw refresh features.
+// D^k at refresh j is kept as a combination sum_m W[k][m] * Delta_{j-m}; the recursion
+// D^{k+1}_new = (D^k_new - D^k_old) / (tau_j - tau_{j-1}) becomes a recursion on W
+// (D^k_old's combination refers to refresh j-1, i.e. is shifted by one ring position).
+struct CoefState {
+  int K;
+  int j = -1;
+  double tau = 0;
+  double Wk[FF_MAX_K + 1][FF_MAX_K + 2] = {};
+  explicit CoefState(int k) : K(k) {}
+  void refresh(double tau_new) {
+    const int jn = j + 1;
+    double nw[FF_MAX_K + 1][FF_MAX_K + 2] = {};
+    nw[0][0] = 1.0;
+    const int upto = jn < K ? jn : K;
+    for (int k = 0; k < upto; ++k) {
+      const double gap = tau_new - tau;
+      for (int q = 0; q <= K; ++q) {
+        const double old_shift = q >= 1 ? Wk[k][q - 1] : 0.0;
+        nw[k + 1][q] = (nw[k][q] - old_shift) / gap;
+      }
+    }
+    memcpy(Wk, nw, sizeof(Wk));
+    j = jn;
+    tau = tau_new;
+  }
+  // c_q for the forecast at step i: sum_k (i - tau)^k / k! * W[k][q], k <= min(K, j)
+  void coeffs(double i, float* c) const {
+    const int ke = j < K ? j : K;
+    double fact = 1.0, pw = 1.0;
+    double acc[FF_MAX_K + 2] = {};
+    for (int k = 0; k <= ke; ++k) {
+      if (k > 0) { fact *= k; pw *= (i - tau); }
+      for (int q = 0; q <= K; ++q) acc[q] += pw / fact * Wk[k][q];
+    }
+    for (int q = 0; q <= K; ++q) c[q] = (float)acc[q];
+  }
+};
+
+ff_status check_sched(const ff_sched_desc* s, int L) {
+  if (!s) return fail(FF_E_NULL, "schedule descriptor is NULL");
+  if (s->T < 1 || s->T > 100000) return fail(FF_E_RANGE, "T=%d out of range", s->T);
+  if (s->R < 1) return fail(FF_E_RANGE, "R=%d must be >= 1", s->R);
+  if (s->K < 0 || s->K > FF_MAX_K) return fail(FF_E_RANGE, "K=%d outside [0, %d]", s->K, FF_MAX_K);
+  if (s->S < s->K + 1 || s->S > FF_MAX_SLOTS) return fail(FF_E_RANGE, "S=%d must be in [K+1, %d]", s->S, FF_MAX_SLOTS);
+  if (s->mode < FF_VANILLA || s->mode > FF_EXACT_ONLY) return fail(FF_E_RANGE, "mode=%d unknown", s->mode);
+  if (s->feature_mode != FF_RESIDUAL && s->feature_mode != FF_OUTPUT)
+    return fail(FF_E_RANGE, "feature_mode=%d unknown", s->feature_mode);
+  if (!(s->eps > 0.f)) return fail(FF_E_RANGE, "eps must be > 0");
+  if (L < 1 || L > 4096) return fail(FF_E_RANGE, "n_layers=%d out of range", L);
+  return FF_OK;
+}
+
+void build_plan(const ff_sched_desc& s, int L, const uint8_t* mask, ff_plan* p) {
+  const int T = s.T, K = s.K, S = s.S;
+  p->s = s;
+  p->L = L;
+  p->step_kind.assign(T, 0);
+  p->refresh_ord.assign(T, 0);
+  p->k_eff.assign(T, 0);
+  p->read_slots.assign((size_t)T * (K + 1), -1);
+  p->write_slot.assign(T, -1);
+  p->action.assign((size_t)T * L, FF_ACT_EXACT);
+  p->coeffs.assign((size_t)T * (K + 1), 0.f);
+  p->counts = ff_counts{0, 0, 0};
+  CoefState cs(K);
+  int j = -1;
+  const bool paid_mode = s.mode == FF_VERIFY || s.mode == FF_FEATFIX || s.mode == FF_EXACT_ONLY;
+  for (int i = 0; i < T; ++i) {
+    const bool refresh = s.mode == FF_VANILLA || i % s.R == 0;
+    if (refresh) {
+      ++j;
+      cs.refresh((double)i);
+    }
+    p->refresh_ord[i] = j;
+    const int ke = j < K ? j : K;
+    p->k_eff[i] = ke;
+    if (refresh) {
+      p->step_kind[i] = FF_STEP_REFRESH;
+      if (s.mode != FF_VANILLA) p->write_slot[i] = j % S;
+      p->counts.n_full_refresh++;
+      continue;
+    }
+    p->step_kind[i] = FF_STEP_CACHED;
+    for (int q = 0; q <= ke; ++q) p->read_slots[(size_t)i * (K + 1) + q] = ((j - q) % S + S) % S;
+    float c[FF_MAX_K + 2] = {};
+    cs.coeffs((double)i, c);
+    for (int q = 0; q <= ke; ++q) p->coeffs[(size_t)i * (K + 1) + q] = c[q];
+    for (int l = 0; l < L; ++l) {
+      const bool site = paid_mode && mask[(size_t)i * L + l];
+      p->action[(size_t)i * L + l] = site ? FF_ACT_SITE : FF_ACT_DRAFT;
+      if (site) {
+        p->counts.n_paid_checks++;
+        if (s.mode == FF_FEATFIX || s.mode == FF_EXACT_ONLY) p->counts.n_forwarded++;
+      }
+    }
+  }
+}
+
+ff_status check_terms(const Model& m, int n_slots, int layer, int k_eff, const int32_t* slots, const float* coeffs,
+                      const void* cache, Terms* t) {
+  if (!cache || !slots || !coeffs) return fail(FF_E_NULL, "cache, slots or coeffs is NULL");
+  if (layer < 0 || layer >= m.L) return fail(FF_E_RANGE, "layer %d out of range", layer);
+  if (n_slots < 1 || n_slots > FF_MAX_SLOTS) return fail(FF_E_RANGE, "n_slots %d out of range", n_slots);
+  if (k_eff < 0 || k_eff > FF_MAX_K) return fail(FF_E_RANGE, "k_eff %d out of range", k_eff);
+  t->n = k_eff + 1;
+  const size_t slot_bytes = m.E() * m.es();
+  for (int q = 0; q <= k_eff; ++q) {
+    if (slots[q] < 0 || slots[q] >= n_slots) return fail(FF_E_RANGE, "slot %d out of range", slots[q]);
+    t->slot[q] = reinterpret_cast<const char*>(cache) + ((size_t)layer * n_slots + slots[q]) * slot_bytes;
+    t->c[q] = coeffs[q];
+  }
+  for (int q = k_eff + 1; q < kMaxTerms; ++q) { t->slot[q] = nullptr; t->c[q] = 0.f; }
+  if (!aligned16(cache)) return fail(FF_E_SHAPE, "cache must be 16-byte aligned");
+  return FF_OK;
+}
+
+}  // namespace
+
+// ====================================================================== C ABI
+extern "C" {
+
+int32_t ff_abi_version(void) { return FF_ABI_VERSION; }
+
+const char* ff_last_error(void) { return g_err; }
+
+ff_status ff_plan_build(const ff_sched_desc* s, int32_t n_layers, const uint8_t* site_mask, ff_plan** out) {
+  try {
+    if (!out || !site_mask) return fail(FF_E_NULL, "out or site_mask is NULL");
+    ff_status e = check_sched(s, n_layers);
+    if (e) return e;
+    ff_plan* p = new ff_plan();
+    build_plan(*s, n_layers, site_mask, p);
+    *out = p;
+    return ok();
+  } catch (const std::bad_alloc&) {
+    return fail(FF_E_UNSUPPORTED, "out of host memory");
+  } catch (...) {
+    return fail(FF_E_UNSUPPORTED, "unexpected host exception");
+  }
+}
+
+void ff_plan_destroy(ff_plan* p) { delete p; }
+
+ff_status ff_plan_export(const ff_plan* p, int32_t* step_kind, int32_t* refresh_ord, int32_t* k_eff,
+                         int32_t* read_slots, int32_t* write_slot, int32_t* action, float* coeffs,
+                         ff_counts* counts) {
+  if (!p) return fail(FF_E_NULL, "plan is NULL");
+  const size_t T = p->s.T;
+  if (step_kind) memcpy(step_kind, p->step_kind.data(), T * 4);
+  if (refresh_ord) memcpy(refresh_ord, p->refresh_ord.data(), T * 4);
+  if (k_eff) memcpy(k_eff, p->k_eff.data(), T * 4);
+  if (read_slots) memcpy(read_slots, p->read_slots.data(), p->read_slots.size() * 4);
+  if (write_slot) memcpy(write_slot, p->write_slot.data(), T * 4);
+  if (action) memcpy(action, p->action.data(), p->action.size() * 4);
+  if (coeffs) memcpy(coeffs, p->coeffs.data(), p->coeffs.size() * 4);
+  if (counts) *counts = p->counts;
+  return ok();
+}
+
+size_t ff_cache_bytes(const ff_model_desc* m, int32_t n_slots) {
+  Model md;
+  if (check_model(m, &md) != FF_OK || n_slots < 1) return 0;
+  return (size_t)md.L * n_slots * md.E() * md.es();
+}
+
+size_t ff_workspace_bytes(const ff_model_desc* m) {
+  Model md;
+  if (check_model(m, &md) != FF_OK) return 0;
+  return ws_layout(md).total;
+}
+
+ff_status ff_block_exact(const ff_model_desc* m, int32_t layer, const ff_layer_weights* w, const float* c_t,
+                         const void* u, void* h, void* ws, size_t ws_bytes, ff_stream_t stream) {
+  try {
+    Model md;
+    ff_status e = check_model(m, &md);
+    if (e) return e;
+    if (layer < 0 || layer >= md.L) return fail(FF_E_RANGE, "layer %d out of range [0, %d)", layer, md.L);
+    if (!c_t || !u || !h || !ws) return fail(FF_E_NULL, "c_t, u, h or ws is NULL");
+    e = check_layer_weights(w, md.kinds[layer], layer);
+    if (e) return e;
+    const Ws L = ws_layout(md);
+    if (ws_bytes < L.total) return fail(FF_E_WORKSPACE, "workspace %zu < %zu bytes", ws_bytes, L.total);
+    if (!aligned16(u) || !aligned16(h) || !aligned16(ws) || !aligned16(c_t))
+      return fail(FF_E_SHAPE, "device pointers must be 16-byte aligned");
+    const size_t tb = md.E() * md.es();
+    const char *pu = (const char*)u, *ph = (const char*)h, *pw = (const char*)ws;
+    if ((ph < pu + tb && pu < ph + tb) || (ph < pw + L.total && pw < ph + tb))
+      return fail(FF_E_SHAPE, "h overlaps u or the workspace");
+    hipStream_t st = reinterpret_cast<hipStream_t>(stream);
+    float* cs = at<float>(ws, L.CS);
+    HIP_TRY(silu_rows(c_t, cs, md.B, md.C, st), "block: silu(c_t)");
+    e = exec_block(md, md.kinds[layer], *w, cs, u, h, ws, st);
+    if (e) return e;
+    return ok();
+  } catch (...) {
+    return fail(FF_E_UNSUPPORTED, "unexpected host exception");
+  }
+}
+
+ff_status ff_cache_update(const ff_model_desc* m, void* cache, int32_t n_slots, int32_t layer, int32_t slot,
+                          const void* u, const void* h, int32_t feature_mode, ff_stream_t stream) {
+  Model md;
+  ff_status e = check_model(m, &md);
+  if (e) return e;
+  if (!cache || !h) return fail(FF_E_NULL, "cache or h is NULL");
+  if (feature_mode != FF_RESIDUAL && feature_mode != FF_OUTPUT) return fail(FF_E_RANGE, "feature_mode unknown");
+  if (feature_mode == FF_RESIDUAL && !u) return fail(FF_E_NULL, "u is NULL in residual mode");
+  if (layer < 0 || layer >= md.L) return fail(FF_E_RANGE, "layer %d out of range", layer);
+  if (n_slots < 1 || n_slots > FF_MAX_SLOTS || slot < 0 || slot >= n_slots)
+    return fail(FF_E_RANGE, "slot %d / n_slots %d out of range", slot, n_slots);
+  if (!aligned16(cache) || !aligned16(h) || (u && !aligned16(u))) return fail(FF_E_SHAPE, "pointers must be 16-byte aligned");
+  void* dst = (char*)cache + ((size_t)layer * n_slots + slot) * md.E() * md.es();
+  HIP_TRY(ff::cache_update(md.dtype, dst, feature_mode == FF_RESIDUAL ? u : nullptr, h, md.E(),
+                           reinterpret_cast<hipStream_t>(stream)), "cache update");
+  return ok();
+}
+
+ff_status ff_draft_forecast(const ff_model_desc* m, const void* cache, int32_t n_slots, int32_t layer, int32_t k_eff,
+                            const int32_t* slots, const float* coeffs, const void* u, void* h_d, ff_stream_t stream) {
+  Model md;
+  ff_status e = check_model(m, &md);
+  if (e) return e;
+  if (!h_d) return fail(FF_E_NULL, "h_d is NULL");
+  Terms t{};
+  e = check_terms(md, n_slots, layer, k_eff, slots, coeffs, cache, &t);
+  if (e) return e;
+  if (!aligned16(h_d) || (u && !aligned16(u))) return fail(FF_E_SHAPE, "pointers must be 16-byte aligned");
+  HIP_TRY(ff::draft(md.dtype, t, u, h_d, md.E(), reinterpret_cast<hipStream_t>(stream)), "draft");
+  return ok();
+}
+
+ff_status ff_verify_replace(const ff_model_desc* m, const void* cache, int32_t n_slots, int32_t layer, int32_t k_eff,
+                            const int32_t* slots, const float* coeffs, const void* u, const void* h_f, void* h_out,
+                            int32_t forward_exact, float eps, float* rel_l1, void* ws, size_t ws_bytes,
+                            ff_stream_t stream) {
+  Model md;
+  ff_status e = check_model(m, &md);
+  if (e) return e;
+  if (!h_f || !h_out || !ws) return fail(FF_E_NULL, "h_f, h_out or ws is NULL");
+  Terms t{};
+  e = check_terms(md, n_slots, layer, k_eff, slots, coeffs, cache, &t);
+  if (e) return e;
+  if (!(eps > 0.f)) return fail(FF_E_RANGE, "eps must be > 0");
+  const Ws L = ws_layout(md);
+  if (ws_bytes < L.total) return fail(FF_E_WORKSPACE, "workspace %zu < %zu bytes", ws_bytes, L.total);
+  const size_t tb = md.E() * md.es();
+  if ((const char*)h_out < (const char*)h_f + tb && (const char*)h_f < (const char*)h_out + tb)
+    return fail(FF_E_SHAPE, "h_out overlaps h_f");
+  if (!aligned16(h_f) || !aligned16(h_out) || (u && !aligned16(u))) return fail(FF_E_SHAPE, "pointers must be 16-byte aligned");
+  HIP_TRY(ff::verify(md.dtype, t, u, h_f, h_out, forward_exact ? 1 : 0, md.B, (size_t)md.N * md.C, eps, rel_l1,
+                     at<float>(ws, L.PART), reinterpret_cast<hipStream_t>(stream)), "verify");
+  return ok();
+}
+
+ff_status ff_ctx_create(const ff_model_desc* m, const ff_layer_weights* layer_w, const ff_global_weights* g,
+                        const ff_plan* p, void* cache, size_t cache_bytes, void* ws, size_t ws_bytes, ff_ctx** out) {
+  try {
+    if (!out) return fail(FF_E_NULL, "out is NULL");
+    Model md;
+    ff_status e = check_model(m, &md);
+    if (e) return e;
+    if (!layer_w || !g || !p || !cache || !ws) return fail(FF_E_NULL, "weights, plan, cache or ws is NULL");
+    if (p->L != md.L) return fail(FF_E_SHAPE, "plan has %d layers, model %d", p->L, md.L);
+    for (int l = 0; l < md.L; ++l) {
+      e = check_layer_weights(&layer_w[l], md.kinds[l], l);
+      if (e) return e;
+    }
+    if (!g->t1_w || !g->t1_b || !g->t2_w || !g->t2_b || !g->pe_w || !g->pe_b || !g->fmod_w || !g->fmod_b ||
+        !g->f_w || !g->f_b)
+      return fail(FF_E_NULL, "a global weight pointer is NULL");
+    const size_t need_cache = (size_t)md.L * p->s.S * md.E() * md.es();
+    if (cache_bytes < need_cache) return fail(FF_E_WORKSPACE, "cache %zu < %zu bytes", cache_bytes, need_cache);
+    const Ws L = ws_layout(md);
+    if (ws_bytes < L.total) return fail(FF_E_WORKSPACE, "workspace %zu < %zu bytes", ws_bytes, L.total);
+    if (!aligned16(cache) || !aligned16(ws)) return fail(FF_E_SHAPE, "cache and ws must be 16-byte aligned");
+    ff_ctx* c = new ff_ctx();
+    c->m = md;
+    c->lw.assign(layer_w, layer_w + md.L);
+    c->g = *g;
+    c->plan = *p;
+    c->cache = cache;
+    c->ws = ws;
+    c->next_step = 0;
+    c->written.assign((size_t)md.L * p->s.S, 0);
+    c->counts = ff_counts{0, 0, 0};
+    *out = c;
+    return ok();
+  } catch (const std::bad_alloc&) {
+    return fail(FF_E_UNSUPPORTED, "out of host memory");
+  } catch (...) {
+    return fail(FF_E_UNSUPPORTED, "unexpected host exception");
+  }
+}
+
+void ff_ctx_destroy(ff_ctx* c) { delete c; }
+
+ff_status ff_ctx_reset(ff_ctx* c) {
+  if (!c) return fail(FF_E_NULL, "ctx is NULL");
+  c->next_step = 0;
+  std::fill(c->written.begin(), c->written.end(), 0);
+  c->counts = ff_counts{0, 0, 0};
+  return ok();
+}
+
+ff_status ff_get_counts(const ff_ctx* c, ff_counts* out) {
+  if (!c || !out) return fail(FF_E_NULL, "ctx or out is NULL");
+  *out = c->counts;
+  return ok();
+}
+
+ff_status ff_denoise_step(ff_ctx* c, int32_t step, float* x, const float* cond, const void* txt, float* audit,
+                          ff_stream_t stream) {
+  try {
+    if (!c || !x || !cond) return fail(FF_E_NULL, "ctx, x or cond is NULL");
+    const Model& m = c->m;
+    const ff_plan& p = c->plan;
+    const ff_sched_desc& s = p.s;
+    if (m.n_txt > 0 && !txt) return fail(FF_E_NULL, "txt is NULL but n_txt = %d", m.n_txt);
+    if (step != c->next_step || step >= s.T)
+      return fail(FF_E_STATE, "step %d out of order (expected %d of %d)", step, c->next_step, s.T);
+    if (!aligned16(x) || !aligned16(cond) || (txt && !aligned16(txt))) return fail(FF_E_SHAPE, "pointers must be 16-byte aligned");
+    const int L = m.L, K = s.K, S = s.S, i = step;
+    // host-side state checks first: nothing is launched if the plan would read an unwritten slot
+    if (p.step_kind[i] == FF_STEP_CACHED) {
+      for (int l = 0; l < L; ++l) {
+        if (p.action[(size_t)i * L + l] == FF_ACT_EXACT) continue;
+        if (s.mode == FF_EXACT_ONLY && p.action[(size_t)i * L + l] == FF_ACT_SITE) continue;
+        for (int q = 0; q <= p.k_eff[i]; ++q) {
+          const int sl = p.read_slots[(size_t)i * (K + 1) + q];
+          if (sl < 0 || !c->written[(size_t)l * S + sl])
+            return fail(FF_E_STATE, "step %d layer %d reads slot %d that holds no refresh", i, l, sl);
+        }
+      }
+    }
+    hipStream_t st = reinterpret_cast<hipStream_t>(stream);
+    const Ws W = ws_layout(m);
+    void* ws = c->ws;
+    const int C = m.C, dt = m.dtype;
+    const size_t es = m.es(), E = m.E(), tb = E * es;
+    const double T = s.T;
+    const double t_i = 1.0 - i / T, t_n = 1.0 - (i + 1) / T;
+    float* phi = at<float>(ws, W.PHI);
+    float* tmp = at<float>(ws, W.TMP);
+    float* ct = at<float>(ws, W.CT);
+    float* cs = at<float>(ws, W.CS);
+    // conditioning: c_t = cond + W_t2 SiLU(W_t1 phi(1000 t) + b_t1) + b_t2
+    HIP_TRY(time_embed(1000.0 * t_i, phi, st), "time embedding");
+    GemvArgs g1{phi, 0, 0, c->g.t1_w, c->g.t1_b, C, FF_TEMB_DIM, m.B, tmp, C, 1, nullptr, 0};
+    HIP_TRY(gemv(dt, g1, st), "time mlp 1");
+    GemvArgs g2{tmp, C, 0, c->g.t2_w, c->g.t2_b, C, C, m.B, ct, C, 0, cond, C};
+    HIP_TRY(gemv(dt, g2, st), "time mlp 2");
+    HIP_TRY(silu_rows(ct, cs, m.B, C, st), "silu(c_t)");
+    // tokens: X = [txt ; patch_embed(patchify(x))]
+    PatchGeom pg{m.B, m.lat_c, m.lat_f, m.lat_h, m.lat_w, m.pt, m.ph, m.pw};
+    void* patches = at(ws, W.PATCH);
+    HIP_TRY(patchify(dt, x, patches, pg, st), "patchify");
+    void* cur = at(ws, W.X0);
+    void* alt = at(ws, W.X1);
+    const RowMap img{m.n_img, m.N, m.n_txt};
+    const RowMap ident{m.B * m.n_img, m.B * m.n_img, 0};
+    GemmArgs pe = gemm_args(patches, m.P, ident, c->g.pe_w, c->g.pe_b, m.B * m.n_img, C, m.P, EPI_BIAS, cur, C, img);
+    HIP_TRY(gemm(dt, pe, st), "patch embed");
+    if (m.n_txt > 0) HIP_TRY(copy_rows(dt, txt, cur, m.B, m.n_txt, m.N, 0, C, st), "text rows");
+    // layers by the plan
+    const int mode = s.mode;
+    const bool resid = s.feature_mode == FF_RESIDUAL;
+    for (int l = 0; l < L; ++l) {
+      const int act = p.action[(size_t)i * L + l];
+      if (act == FF_ACT_EXACT) {
+        ff_status e = exec_block(m, m.kinds[l], c->lw[l], cs, cur, alt, ws, st);
+        if (e) return e;
+        if (mode != FF_VANILLA) {
+          const int sl = p.write_slot[i];
+          void* dst = (char*)c->cache + ((size_t)l * S + sl) * tb;
+          HIP_TRY(ff::cache_update(dt, dst, resid ? cur : nullptr, alt, E, st), "cache update");
+        }
+        void* t = cur; cur = alt; alt = t;
+        continue;
+      }
+      if (act == FF_ACT_SITE && mode == FF_EXACT_ONLY) {
+        ff_status e = exec_block(m, m.kinds[l], c->lw[l], cs, cur, alt, ws, st);
+        if (e) return e;
+        void* t = cur; cur = alt; alt = t;
+        continue;
+      }
+      Terms tm{};
+      tm.n = p.k_eff[i] + 1;
+      for (int q = 0; q < tm.n; ++q) {
+        const int sl = p.read_slots[(size_t)i * (K + 1) + q];
+        tm.slot[q] = (const char*)c->cache + ((size_t)l * S + sl) * tb;
+        tm.c[q] = p.coeffs[(size_t)i * (K + 1) + q];
+      }
+      if (act == FF_ACT_DRAFT) {
+        HIP_TRY(ff::draft(dt, tm, resid ? cur : nullptr, cur, E, st), "draft");
+        continue;
+      }
+      // paid site: exact output from the same incoming state, then verify + forward
+      void* hf = at(ws, W.HF);
+      ff_status e = exec_block(m, m.kinds[l], c->lw[l], cs, cur, hf, ws, st);
+      if (e) return e;
+      float* rel = audit ? audit + ((size_t)i * L + l) * m.B : nullptr;
+      HIP_TRY(ff::verify(dt, tm, resid ? cur : nullptr, hf, cur, mode == FF_FEATFIX ? 1 : 0, m.B, (size_t)m.N * C,
+                         s.eps, rel, at<float>(ws, W.PART), st), "verify");
+    }
+    // final layer on the image rows, unpatchify and Euler
+    float* mod = at<float>(ws, W.MOD);
+    GemvArgs gf{cs, C, 0, c->g.fmod_w, c->g.fmod_b, 2 * C, C, m.B, mod, 2 * C, 0, nullptr, 0};
+    HIP_TRY(gemv(dt, gf, st), "final modulation");
+    void* lna = at(ws, W.LNA);
+    LnModArgs ln{cur, 0, C, img, m.B * m.n_img, C, m.ln_eps, mod, mod + C, 2 * C, lna, C};
+    HIP_TRY(ln_modulate(dt, ln, st), "final ln");
+    float* yf = at<float>(ws, W.YF);
+    GemmArgs gfl = gemm_args(lna, C, img, c->g.f_w, c->g.f_b, m.B * m.n_img, m.P, C, EPI_BIAS, yf, m.P, ident);
+    gfl.out_f32 = 1;
+    HIP_TRY(gemm(dt, gfl, st), "final linear");
+    HIP_TRY(unpatchify_euler(yf, x, (float)(t_n - t_i), pg, st), "unpatchify + euler");
+    // bookkeeping after a successful enqueue
+    if (p.step_kind[i] == FF_STEP_REFRESH) {
+      c->counts.n_full_refresh++;
+      if (mode != FF_VANILLA)
+        for (int l = 0; l < L; ++l) c->written[(size_t)l * S + p.write_slot[i]] = 1;
+    } else {
+      for (int l = 0; l < L; ++l) {
+        if (p.action[(size_t)i * L + l] != FF_ACT_SITE) continue;
+        c->counts.n_paid_checks++;
+        if (mode == FF_FEATFIX || mode == FF_EXACT_ONLY) c->counts.n_forwarded++;
+      }
+    }
+    c->next_step++;
+    return ok();
+  } catch (...) {
+    return fail(FF_E_UNSUPPORTED, "unexpected host exception");
+  }
+}
+
+}  // extern "C"

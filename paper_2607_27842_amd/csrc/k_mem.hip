@@ -1,0 +1,212 @@
+// HBM-bound kernels of the cached step: feature-history refresh, Taylor draft, and the
+// fused verify + replace pass.  Every thread moves 16-byte chunks (8 bf16 or 4 fp32) with
+// a grid-stride loop so that consecutive lanes touch consecutive chunks (fully coalesced).
+#include "dev_common.h"
+
+namespace ff {
+
+namespace {
+
+constexpr int kThreads = 256;
+
+inline int grid_for(size_t chunks) {
+  size_t g = (chunks + kThreads - 1) / kThreads;
+  if (g > 8192) g = 8192;
+  if (g < 1) g = 1;
+  return (int)g;
+}
+
+// History refresh (Eq. 2 is estimated from exact refreshes): Delta = h - u, or h itself.
+template <int DT, bool RES>
+__global__ __launch_bounds__(kThreads) void k_cache_update(void* __restrict__ slot, const void* __restrict__ u,
+                                                           const void* __restrict__ h, size_t nchunk) {
+  using S = St<DT>;
+  for (size_t c = (size_t)blockIdx.x * kThreads + threadIdx.x; c < nchunk; c += (size_t)gridDim.x * kThreads) {
+    const size_t i = c * S::V;
+    float hv[S::V];
+    S::load(h, i, hv);
+    if (RES) {
+      float uv[S::V];
+      S::load(u, i, uv);
+#pragma unroll
+      for (int j = 0; j < S::V; ++j) hv[j] = hv[j] - uv[j];
+    }
+    S::store(slot, i, hv);
+  }
+}
+
+// One chunk of the draft h_d = u + sum_m c_m * slot_m (Eq. 2 in coefficient form), fp32
+// sums with explicit fma so that the draft and verify kernels produce identical bits.
+template <int DT, bool RES>
+__device__ __forceinline__ void draft_chunk(const Terms& t, const void* u, size_t i, float* out) {
+  using S = St<DT>;
+  float f[S::V];
+#pragma unroll
+  for (int j = 0; j < S::V; ++j) f[j] = 0.0f;
+#pragma unroll
+  for (int m = 0; m < kMaxTerms; ++m) {
+    if (m < t.n) {
+      float s[S::V];
+      S::load(t.slot[m], i, s);
+#pragma unroll
+      for (int j = 0; j < S::V; ++j) f[j] = fmaf(t.c[m], s[j], f[j]);
+    }
+  }
+  if (RES) {
+    float uv[S::V];
+    S::load(u, i, uv);
+#pragma unroll
+    for (int j = 0; j < S::V; ++j) f[j] = uv[j] + f[j];
+  }
+#pragma unroll
+  for (int j = 0; j < S::V; ++j) out[j] = S::rnd(f[j]);
+}
+
+template <int DT, bool RES>
+__global__ __launch_bounds__(kThreads) void k_draft(Terms t, const void* u, void* hd, size_t nchunk) {
+  using S = St<DT>;
+  for (size_t c = (size_t)blockIdx.x * kThreads + threadIdx.x; c < nchunk; c += (size_t)gridDim.x * kThreads) {
+    float o[S::V];
+    draft_chunk<DT, RES>(t, u, c * S::V, o);
+    S::store(hd, c * S::V, o);
+  }
+}
+
+// Block-wide fixed-order sum of two values (wave butterflies, then waves in order).
+__device__ __forceinline__ void block_sum2(float& a, float& b) {
+  __shared__ float red[2][kThreads / 64];
+  a = wave_sum(a);
+  b = wave_sum(b);
+  const int w = threadIdx.x / 64, l = threadIdx.x % 64;
+  if (l == 0) { red[0][w] = a; red[1][w] = b; }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    float x = 0.f, y = 0.f;
+#pragma unroll
+    for (int i = 0; i < kThreads / 64; ++i) { x += red[0][i]; y += red[1][i]; }
+    a = x; b = y;
+  }
+}
+
+constexpr int kMaxVerifyBlocks = 256;  // partial-sum blocks per sample
+
+// Verify + replace (Eq. 3-5): rebuild the draft from the same incoming u, accumulate
+// sum|h_d - h_f| and sum|h_f| for this sample, and forward h_f (FeatFix) or h_d (Verify).
+template <int DT, bool RES>
+__global__ __launch_bounds__(kThreads) void k_verify(Terms t, const void* u, const void* __restrict__ hf,
+                                                     void* hout, int forward_exact, size_t chunks_per_sample,
+                                                     float* __restrict__ partials) {
+  using S = St<DT>;
+  const int b = blockIdx.y;
+  const size_t base = (size_t)b * chunks_per_sample * S::V;
+  float num = 0.f, den = 0.f;
+  for (size_t c = (size_t)blockIdx.x * kThreads + threadIdx.x; c < chunks_per_sample;
+       c += (size_t)gridDim.x * kThreads) {
+    const size_t i = base + c * S::V;
+    float d[S::V], f[S::V];
+    draft_chunk<DT, RES>(t, u, i, d);
+    S::load(hf, i, f);
+#pragma unroll
+    for (int j = 0; j < S::V; ++j) {
+      num += fabsf(d[j] - f[j]);
+      den += fabsf(f[j]);
+    }
+    S::store(hout, i, forward_exact ? f : d);
+  }
+  block_sum2(num, den);
+  if (threadIdx.x == 0) {
+    float* p = partials + ((size_t)b * gridDim.x + blockIdx.x) * 2;
+    p[0] = num;
+    p[1] = den;
+  }
+}
+
+// Second stage: per sample, sum the partials in index order and form Eq. 4.
+__global__ __launch_bounds__(kThreads) void k_verify_finish(const float* __restrict__ partials, int nblk,
+                                                            float eps, float* __restrict__ rel) {
+  const int b = blockIdx.x;
+  float num = 0.f, den = 0.f;
+  for (int i = threadIdx.x; i < nblk; i += kThreads) {
+    num += partials[((size_t)b * nblk + i) * 2];
+    den += partials[((size_t)b * nblk + i) * 2 + 1];
+  }
+  block_sum2(num, den);
+  if (threadIdx.x == 0) rel[b] = num / (den + eps);
+}
+
+template <int DT>
+__global__ __launch_bounds__(kThreads) void k_copy_rows(const void* __restrict__ src, void* __restrict__ dst,
+                                                        int n, int N, int off, int C, size_t nchunk) {
+  using S = St<DT>;
+  const int cpr = C / S::V;  // chunks per row
+  for (size_t c = (size_t)blockIdx.x * kThreads + threadIdx.x; c < nchunk; c += (size_t)gridDim.x * kThreads) {
+    const size_t row = c / cpr;
+    const int col = (int)(c % cpr) * S::V;
+    const size_t b = row / n, i = row % n;
+    float v[S::V];
+    S::load(src, row * C + col, v);
+    S::store(dst, (b * N + off + i) * C + col, v);
+  }
+}
+
+}  // namespace
+
+hipError_t cache_update(int dtype, void* slot, const void* u, const void* h, size_t E, hipStream_t s) {
+  if (dtype == DT_BF16) {
+    size_t n = E / 8;
+    if (u) hipLaunchKernelGGL((k_cache_update<DT_BF16, true>), grid_for(n), kThreads, 0, s, slot, u, h, n);
+    else hipLaunchKernelGGL((k_cache_update<DT_BF16, false>), grid_for(n), kThreads, 0, s, slot, u, h, n);
+  } else {
+    size_t n = E / 4;
+    if (u) hipLaunchKernelGGL((k_cache_update<DT_F32, true>), grid_for(n), kThreads, 0, s, slot, u, h, n);
+    else hipLaunchKernelGGL((k_cache_update<DT_F32, false>), grid_for(n), kThreads, 0, s, slot, u, h, n);
+  }
+  return hipGetLastError();
+}
+
+hipError_t draft(int dtype, const Terms& t, const void* u, void* hd, size_t E, hipStream_t s) {
+  if (dtype == DT_BF16) {
+    size_t n = E / 8;
+    if (u) hipLaunchKernelGGL((k_draft<DT_BF16, true>), grid_for(n), kThreads, 0, s, t, u, hd, n);
+    else hipLaunchKernelGGL((k_draft<DT_BF16, false>), grid_for(n), kThreads, 0, s, t, u, hd, n);
+  } else {
+    size_t n = E / 4;
+    if (u) hipLaunchKernelGGL((k_draft<DT_F32, true>), grid_for(n), kThreads, 0, s, t, u, hd, n);
+    else hipLaunchKernelGGL((k_draft<DT_F32, false>), grid_for(n), kThreads, 0, s, t, u, hd, n);
+  }
+  return hipGetLastError();
+}
+
+size_t verify_partials_floats(int B) { return (size_t)B * kMaxVerifyBlocks * 2; }
+
+hipError_t verify(int dtype, const Terms& t, const void* u, const void* hf, void* hout, int forward_exact,
+                  int B, size_t Eb, float eps, float* rel_l1, float* partials, hipStream_t s) {
+  const int V = dtype == DT_BF16 ? 8 : 4;
+  const size_t cps = Eb / V;
+  int nblk = cdiv((long)cps, kThreads * 4);
+  if (nblk > kMaxVerifyBlocks) nblk = kMaxVerifyBlocks;
+  if (nblk < 1) nblk = 1;
+  dim3 grid(nblk, B);
+  if (dtype == DT_BF16) {
+    if (u) hipLaunchKernelGGL((k_verify<DT_BF16, true>), grid, kThreads, 0, s, t, u, hf, hout, forward_exact, cps, partials);
+    else hipLaunchKernelGGL((k_verify<DT_BF16, false>), grid, kThreads, 0, s, t, u, hf, hout, forward_exact, cps, partials);
+  } else {
+    if (u) hipLaunchKernelGGL((k_verify<DT_F32, true>), grid, kThreads, 0, s, t, u, hf, hout, forward_exact, cps, partials);
+    else hipLaunchKernelGGL((k_verify<DT_F32, false>), grid, kThreads, 0, s, t, u, hf, hout, forward_exact, cps, partials);
+  }
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  if (rel_l1) hipLaunchKernelGGL(k_verify_finish, dim3(B), kThreads, 0, s, partials, nblk, eps, rel_l1);
+  return hipGetLastError();
+}
+
+hipError_t copy_rows(int dtype, const void* src, void* dst, int B, int n, int N, int off, int C, hipStream_t st) {
+  const int V = dtype == DT_BF16 ? 8 : 4;
+  size_t nchunk = (size_t)B * n * (C / V);
+  if (nchunk == 0) return hipSuccess;
+  if (dtype == DT_BF16) hipLaunchKernelGGL(k_copy_rows<DT_BF16>, grid_for(nchunk), kThreads, 0, st, src, dst, n, N, off, C, nchunk);
+  else hipLaunchKernelGGL(k_copy_rows<DT_F32>, grid_for(nchunk), kThreads, 0, st, src, dst, n, N, off, C, nchunk);
+  return hipGetLastError();
+}
+
+}  // namespace ff

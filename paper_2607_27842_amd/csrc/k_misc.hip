@@ -1,0 +1,254 @@
+// Normalisation (adaLN-modulated LayerNorm, per-head QK RMSNorm), the modulation /
+// time-embedding GEMV, and the once-per-step latent kernels (patchify, sinusoidal
+// time embedding, unpatchify fused with the Euler update).
+#include "dev_common.h"
+
+namespace ff {
+
+namespace {
+
+// ---- 4-element access helpers (LayerNorm works in 4-element units for both dtypes)
+template <int DT> __device__ __forceinline__ void ld4(const void* p, size_t i, float* v);
+template <> __device__ __forceinline__ void ld4<DT_F32>(const void* p, size_t i, float* v) {
+  float4 w = *reinterpret_cast<const float4*>(reinterpret_cast<const float*>(p) + i);
+  v[0] = w.x; v[1] = w.y; v[2] = w.z; v[3] = w.w;
+}
+template <> __device__ __forceinline__ void ld4<DT_BF16>(const void* p, size_t i, float* v) {
+  uint2 w = *reinterpret_cast<const uint2*>(reinterpret_cast<const uint16_t*>(p) + i);
+  v[0] = __uint_as_float(w.x << 16); v[1] = __uint_as_float(w.x & 0xffff0000u);
+  v[2] = __uint_as_float(w.y << 16); v[3] = __uint_as_float(w.y & 0xffff0000u);
+}
+template <int DT> __device__ __forceinline__ void st4(void* p, size_t i, const float* v);
+template <> __device__ __forceinline__ void st4<DT_F32>(void* p, size_t i, const float* v) {
+  *reinterpret_cast<float4*>(reinterpret_cast<float*>(p) + i) = make_float4(v[0], v[1], v[2], v[3]);
+}
+template <> __device__ __forceinline__ void st4<DT_BF16>(void* p, size_t i, const float* v) {
+  uint2 w;
+  w.x = (uint32_t)f2bf(v[0]) | ((uint32_t)f2bf(v[1]) << 16);
+  w.y = (uint32_t)f2bf(v[2]) | ((uint32_t)f2bf(v[3]) << 16);
+  *reinterpret_cast<uint2*>(reinterpret_cast<uint16_t*>(p) + i) = w;
+}
+
+constexpr int kLnMaxUnits = 16;  // 4-element units per lane: C <= 64 * 16 * 4 = 4096
+
+// One wavefront per row: LN over C (biased variance, no affine), then adaLN modulation.
+template <int DT_IN, int DT_OUT>
+__global__ __launch_bounds__(256) void k_ln_modulate(LnModArgs a) {
+  const int lane = threadIdx.x % 64;
+  const int r = blockIdx.x * 4 + threadIdx.x / 64;
+  if (r >= a.rows) return;
+  const size_t pr = (size_t)a.map.phys(r);
+  const int b = a.map.sample(r);
+  const int units = a.C / 4;
+  float v[kLnMaxUnits][4];
+  float s = 0.f;
+#pragma unroll
+  for (int k = 0; k < kLnMaxUnits; ++k) {
+    const int u = k * 64 + lane;
+    if (u < units) {
+      ld4<DT_IN>(a.in, pr * a.ldi + u * 4, v[k]);
+      s += (v[k][0] + v[k][1]) + (v[k][2] + v[k][3]);
+    }
+  }
+  const float mean = wave_sum(s) / (float)a.C;
+  float q = 0.f;
+#pragma unroll
+  for (int k = 0; k < kLnMaxUnits; ++k) {
+    const int u = k * 64 + lane;
+    if (u < units) {
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const float dlt = v[k][j] - mean;
+        q += dlt * dlt;
+      }
+    }
+  }
+  const float rstd = 1.0f / sqrtf(wave_sum(q) / (float)a.C + a.eps);
+  const float* sh = a.shift + (size_t)b * a.ldm;
+  const float* sc = a.scale + (size_t)b * a.ldm;
+#pragma unroll
+  for (int k = 0; k < kLnMaxUnits; ++k) {
+    const int u = k * 64 + lane;
+    if (u < units) {
+      const float4 s4 = *reinterpret_cast<const float4*>(sh + u * 4);
+      const float4 c4 = *reinterpret_cast<const float4*>(sc + u * 4);
+      float o[4];
+      o[0] = (v[k][0] - mean) * rstd * (1.0f + c4.x) + s4.x;
+      o[1] = (v[k][1] - mean) * rstd * (1.0f + c4.y) + s4.y;
+      o[2] = (v[k][2] - mean) * rstd * (1.0f + c4.z) + s4.z;
+      o[3] = (v[k][3] - mean) * rstd * (1.0f + c4.w) + s4.w;
+      st4<DT_OUT>(a.out, pr * a.ldo + u * 4, o);
+    }
+  }
+}
+
+// One thread per (row, head): in-place RMSNorm over the head's d elements.
+template <int DT>
+__global__ __launch_bounds__(256) void k_rms_heads(RmsArgs a) {
+  using S = St<DT>;
+  const long t = (long)blockIdx.x * 256 + threadIdx.x;
+  if (t >= (long)a.rows * a.H) return;
+  const int r = (int)(t / a.H), h = (int)(t % a.H);
+  const size_t base = (size_t)a.map.phys(r) * a.ld + a.col0 + (size_t)h * a.d;
+  float ss = 0.f;
+  for (int e = 0; e < a.d; e += 4) {
+    float v[4];
+    ld4<DT>(a.x, base + e, v);
+    ss += (v[0] * v[0] + v[1] * v[1]) + (v[2] * v[2] + v[3] * v[3]);
+  }
+  const float inv = 1.0f / sqrtf(ss / (float)a.d + a.eps);
+  for (int e = 0; e < a.d; e += 4) {
+    float v[4];
+    ld4<DT>(a.x, base + e, v);
+#pragma unroll
+    for (int j = 0; j < 4; ++j) v[j] = v[j] * inv * S::ld1(a.g, e + j);
+    st4<DT>(a.x, base + e, v);
+  }
+}
+
+constexpr int kGemvMaxB = 8;
+
+// One wavefront per output feature n; lanes stride over K in 16-byte chunks of W.
+template <int DT>
+__global__ __launch_bounds__(256) void k_gemv(GemvArgs a) {
+  using S = St<DT>;
+  const int lane = threadIdx.x % 64;
+  const int n = blockIdx.x * 4 + threadIdx.x / 64;
+  if (n >= a.Nout) return;
+  float acc[kGemvMaxB];
+#pragma unroll
+  for (int b = 0; b < kGemvMaxB; ++b) acc[b] = 0.f;
+  const int chunks = a.K / S::V;
+  for (int c = lane; c < chunks; c += 64) {
+    float w[S::V];
+    S::load(a.W, (size_t)n * a.K + c * S::V, w);
+#pragma unroll
+    for (int b = 0; b < kGemvMaxB; ++b) {
+      if (b < a.B) {
+        const float* xr = a.x + (size_t)b * a.ldx + c * S::V;
+#pragma unroll
+        for (int j = 0; j < S::V; ++j) {
+          float xv = xr[j];
+          if (a.silu_in) xv = silu_f(xv);
+          acc[b] = fmaf(xv, w[j], acc[b]);
+        }
+      }
+    }
+  }
+  const float bias = S::ld1(a.bias, n);
+#pragma unroll
+  for (int b = 0; b < kGemvMaxB; ++b) {
+    if (b < a.B) {
+      float y = wave_sum(acc[b]) + bias;
+      if (a.silu_out) y = silu_f(y);
+      if (a.add) y += a.add[(size_t)b * a.ldadd + n];
+      if (lane == 0) a.y[(size_t)b * a.ldy + n] = y;
+    }
+  }
+}
+
+__global__ void k_time_embed(double s, float* phi) {
+  const int k = threadIdx.x;  // 0..127
+  const double f = exp(-log(10000.0) * (double)k / 128.0);
+  phi[k] = (float)cos(s * f);
+  phi[128 + k] = (float)sin(s * f);
+}
+
+__global__ void k_silu_rows(const float* x, float* y, long n) {
+  const long i = (long)blockIdx.x * 256 + threadIdx.x;
+  if (i < n) y[i] = silu_f(x[i]);
+}
+
+template <int DT>
+__global__ __launch_bounds__(256) void k_patchify(const float* __restrict__ x, void* __restrict__ out, PatchGeom g) {
+  const int Fp = g.F / g.pt, Hp = g.H / g.ph, Wp = g.W / g.pw;
+  const int P = g.pt * g.ph * g.pw * g.lat_c;
+  const long n_img = (long)Fp * Hp * Wp;
+  const long i = (long)blockIdx.x * 256 + threadIdx.x;
+  if (i >= (long)g.B * n_img * P) return;
+  const int feat = (int)(i % P);
+  const long row = i / P;
+  const int b = (int)(row / n_img);
+  const int tok = (int)(row % n_img);
+  const int wx = tok % Wp, hy = (tok / Wp) % Hp, f = tok / (Wp * Hp);
+  // feature order (channel, dt, dy, dx)
+  const int c = feat % g.pw, bb = (feat / g.pw) % g.ph, a = (feat / (g.pw * g.ph)) % g.pt;
+  const int ch = feat / (g.pw * g.ph * g.pt);
+  const size_t src = ((((size_t)b * g.lat_c + ch) * g.F + (f * g.pt + a)) * g.H + (hy * g.ph + bb)) * g.W +
+                     (wx * g.pw + c);
+  St<DT>::st1(out, (size_t)i, x[src]);
+}
+
+__global__ __launch_bounds__(256) void k_unpatchify_euler(const float* __restrict__ yv, float* __restrict__ x,
+                                                          float dt, PatchGeom g) {
+  const long n = (long)g.B * g.lat_c * g.F * g.H * g.W;
+  const long i = (long)blockIdx.x * 256 + threadIdx.x;
+  if (i >= n) return;
+  const int xx = (int)(i % g.W);
+  const int yy = (int)((i / g.W) % g.H);
+  const int ff = (int)((i / ((long)g.W * g.H)) % g.F);
+  const int ch = (int)((i / ((long)g.W * g.H * g.F)) % g.lat_c);
+  const int b = (int)(i / ((long)g.W * g.H * g.F * g.lat_c));
+  const int Fp = g.F / g.pt, Hp = g.H / g.ph, Wp = g.W / g.pw;
+  const int P = g.pt * g.ph * g.pw * g.lat_c;
+  const long tok = ((long)(ff / g.pt) * Hp + yy / g.ph) * Wp + xx / g.pw;
+  // feature order (dt, dy, dx, channel)
+  const int feat = (((ff % g.pt) * g.ph + yy % g.ph) * g.pw + xx % g.pw) * g.lat_c + ch;
+  const long n_img = (long)Fp * Hp * Wp;
+  x[i] = x[i] + dt * yv[((long)b * n_img + tok) * P + feat];
+}
+
+}  // namespace
+
+hipError_t ln_modulate(int dtype, const LnModArgs& a, hipStream_t s) {
+  if (a.rows == 0) return hipSuccess;
+  const int grid = cdiv(a.rows, 4);
+  if (dtype == DT_BF16) {
+    if (a.in_f32) hipLaunchKernelGGL((k_ln_modulate<DT_F32, DT_BF16>), grid, 256, 0, s, a);
+    else hipLaunchKernelGGL((k_ln_modulate<DT_BF16, DT_BF16>), grid, 256, 0, s, a);
+  } else {
+    hipLaunchKernelGGL((k_ln_modulate<DT_F32, DT_F32>), grid, 256, 0, s, a);
+  }
+  return hipGetLastError();
+}
+
+hipError_t rms_heads(int dtype, const RmsArgs& a, hipStream_t s) {
+  if (a.rows == 0) return hipSuccess;
+  const int grid = cdiv((long)a.rows * a.H, 256);
+  if (dtype == DT_BF16) hipLaunchKernelGGL(k_rms_heads<DT_BF16>, grid, 256, 0, s, a);
+  else hipLaunchKernelGGL(k_rms_heads<DT_F32>, grid, 256, 0, s, a);
+  return hipGetLastError();
+}
+
+hipError_t gemv(int dtype, const GemvArgs& a, hipStream_t s) {
+  const int grid = cdiv(a.Nout, 4);
+  if (dtype == DT_BF16) hipLaunchKernelGGL(k_gemv<DT_BF16>, grid, 256, 0, s, a);
+  else hipLaunchKernelGGL(k_gemv<DT_F32>, grid, 256, 0, s, a);
+  return hipGetLastError();
+}
+
+hipError_t time_embed(double sv, float* phi, hipStream_t st) {
+  hipLaunchKernelGGL(k_time_embed, 1, 128, 0, st, sv, phi);
+  return hipGetLastError();
+}
+
+hipError_t silu_rows(const float* x, float* y, int B, int n, hipStream_t st) {
+  const long tot = (long)B * n;
+  hipLaunchKernelGGL(k_silu_rows, cdiv(tot, 256), 256, 0, st, x, y, tot);
+  return hipGetLastError();
+}
+
+hipError_t patchify(int dtype, const float* x, void* patches, const PatchGeom& g, hipStream_t st) {
+  const long n = (long)g.B * g.lat_c * g.F * g.H * g.W;
+  if (dtype == DT_BF16) hipLaunchKernelGGL(k_patchify<DT_BF16>, cdiv(n, 256), 256, 0, st, x, patches, g);
+  else hipLaunchKernelGGL(k_patchify<DT_F32>, cdiv(n, 256), 256, 0, st, x, patches, g);
+  return hipGetLastError();
+}
+
+hipError_t unpatchify_euler(const float* yv, float* x, float dt, const PatchGeom& g, hipStream_t st) {
+  const long n = (long)g.B * g.lat_c * g.F * g.H * g.W;
+  hipLaunchKernelGGL(k_unpatchify_euler, cdiv(n, 256), 256, 0, st, yv, x, dt, g);
+  return hipGetLastError();
+}
+
+}  // namespace ff

@@ -1,0 +1,109 @@
+// Internal interface between the host library (featfix.cpp) and the gfx950 kernels.
+// Not part of the public ABI.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace ff {
+
+enum DType { DT_F32 = 0, DT_BF16 = 1 };
+constexpr int kMaxTerms = 4;  // forecast order K <= 3 -> at most 4 history terms
+
+inline size_t dsize(int dt) { return dt == DT_BF16 ? 2 : 4; }
+
+// Logical row r of a stream segment -> physical row of a [B, N, *] tensor:
+// sample b = r / n_seg, physical row b * N + off + r % n_seg.  For a whole tensor
+// n_seg == N and off == 0 (identity).  MMDiT text rows: (n_txt, N, 0); image rows:
+// (n_img, N, n_txt).
+struct RowMap {
+  int n_seg, N, off;
+  __host__ __device__ inline int phys(int r) const { return (r / n_seg) * N + off + r % n_seg; }
+  __host__ __device__ inline int sample(int r) const { return r / n_seg; }
+};
+
+// ---------------------------------------------------------------- GEMM  (dense contraction)
+// out[phys(r), n] = epi( sum_k A[phys(r), k] * W[n, k] + bias[n] ), r < M, n < N.
+enum Epi { EPI_BIAS = 0, EPI_BIAS_GELU = 1, EPI_GATED = 2 };
+struct GemmArgs {
+  const void* A; int lda; RowMap amap;   // model dtype
+  const void* W; int ldw;                // [N, K] model dtype
+  const void* bias;                      // [N] model dtype (never NULL)
+  int M, N, K;
+  int epi;
+  void* out; int ldo; RowMap omap; int out_f32;  // output fp32 or model dtype
+  // EPI_GATED: out = resid[omap.phys(r), n] + gate[sample(r) * ldg + n] * (acc + bias[n])
+  const void* resid; int ldr; int resid_f32;
+  const float* gate; int ldg;
+};
+hipError_t gemm(int dtype, const GemmArgs& a, hipStream_t s);
+
+// y[b, n] = (add ? add[b*ldadd + n] : 0) + act( sum_k f(x[b*ldx + k]) * W[n, k] + bias[n] )
+// x, y, add fp32; W, bias model dtype; f = SiLU if silu_in; act = SiLU if silu_out.
+struct GemvArgs {
+  const float* x; int ldx; int silu_in;
+  const void* W; const void* bias;
+  int Nout, K, B;
+  float* y; int ldy; int silu_out;
+  const float* add; int ldadd;
+};
+hipError_t gemv(int dtype, const GemvArgs& a, hipStream_t s);
+
+// ---------------------------------------------------------------- normalisation
+// out[phys(r), :C] = LN(in[phys(r), :C]) * (1 + scale[b*ldm + :]) + shift[b*ldm + :]
+struct LnModArgs {
+  const void* in; int in_f32; int ldi;
+  RowMap map; int rows, C; float eps;
+  const float* shift; const float* scale; int ldm;
+  void* out; int ldo;   // model dtype
+};
+hipError_t ln_modulate(int dtype, const LnModArgs& a, hipStream_t s);
+
+// In-place per-head RMSNorm of columns [col0, col0 + H*d) of x (model dtype):
+// x_h <- x_h * g / sqrt(mean(x_h^2) + eps) for each row r < rows (physical via map).
+struct RmsArgs {
+  void* x; int ld; RowMap map; int rows, H, d, col0;
+  const void* g; float eps;
+};
+hipError_t rms_heads(int dtype, const RmsArgs& a, hipStream_t s);
+
+// ---------------------------------------------------------------- attention
+// out[b*N + i, h*d + e] = softmax_j(q_i . k_j * scale) v_j,  q/k/v read from
+// qkv[(b*N + j) * ldq + {0, C, 2C} + h*d + e].
+struct AttnArgs {
+  const void* qkv; int ldq;
+  void* out; int ldo;
+  int B, N, H, d, C;
+  float scale;
+};
+hipError_t attention(int dtype, const AttnArgs& a, hipStream_t s);
+
+// ---------------------------------------------------------------- history / draft / verify
+struct Terms {
+  int n;                         // k_eff + 1
+  const void* slot[kMaxTerms];   // cache slots (model dtype, E elements each)
+  float c[kMaxTerms];            // forecast coefficients
+};
+// slot = round(h - u) (residual) or h (u == nullptr)
+hipError_t cache_update(int dtype, void* slot, const void* u, const void* h, size_t E, hipStream_t s);
+// hd = round((u ? u : 0) + sum_m c_m slot_m)
+hipError_t draft(int dtype, const Terms& t, const void* u, void* hd, size_t E, hipStream_t s);
+// Fused draft rebuild + rel-L1 partial sums + forwarding, then a fixed-order reduction.
+size_t verify_partials_floats(int B);
+hipError_t verify(int dtype, const Terms& t, const void* u, const void* hf, void* hout, int forward_exact,
+                  int B, size_t Eb, float eps, float* rel_l1, float* partials, hipStream_t s);
+
+// ---------------------------------------------------------------- small per-step kernels
+// phi[k] = cos(s f_k), phi[128 + k] = sin(s f_k), f_k = exp(-ln(1e4) k / 128), in fp64.
+hipError_t time_embed(double s, float* phi, hipStream_t st);
+// y[b*ld + k] = silu(x[b*ld + k]) for k < n
+hipError_t silu_rows(const float* x, float* y, int B, int n, hipStream_t st);
+// patches[(b*n_img + tok), feat] (model dtype) from latent x[B, lat_c, F, H, W] fp32
+struct PatchGeom { int B, lat_c, F, H, W, pt, ph, pw; };
+hipError_t patchify(int dtype, const float* x, void* patches, const PatchGeom& g, hipStream_t st);
+// x[b, ch, f, y, x] += dt * yv[(b*n_img + tok), feat], feat order (dt, dy, dx, ch)
+hipError_t unpatchify_euler(const float* yv, float* x, float dt, const PatchGeom& g, hipStream_t st);
+// dst[(b*N + off + i) * C + :] = src[(b*n + i) * C + :]  (model dtype rows)
+hipError_t copy_rows(int dtype, const void* src, void* dst, int B, int n, int N, int off, int C, hipStream_t st);
+
+}  // namespace ff

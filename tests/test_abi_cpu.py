@@ -1,0 +1,222 @@
+"""Host-only checks of the C ABI (no GPU): every declared symbol is exported, the plan
+is bit-exact with the oracle's schedule, coefficients match the closed forms, and
+invalid requests fail on the host with the documented codes before anything launches."""
+import ctypes as C
+import os
+import re
+
+import numpy as np
+import pytest
+
+import oracle as O
+import synth
+from paper_2607_27842_amd import abi, pipeline
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def test_every_declared_symbol_is_exported():
+    hdr = open(os.path.join(ROOT, "include", "featfix.h")).read()
+    declared = set(re.findall(r"\b(ff_[a-z_0-9]+)\s*\(", hdr))
+    assert declared == set(abi.EXPORTED)
+    L = abi.lib()
+    for name in declared:
+        assert hasattr(L, name), name
+    assert abi.ff_abi_version() == 1
+
+
+def sched(T, R, K, S, mode, fm=abi.FF_RESIDUAL, eps=1e-8):
+    return abi.ff_sched_desc(T, R, K, S, eps, mode, fm)
+
+
+def compare_plan(T, L, R, K, S, mask, mode):
+    p = abi.ff_plan_build(sched(T, R, K, S, mode), L, mask)
+    got = abi.ff_plan_export(p, T, L, K)
+    abi.ff_plan_destroy(p)
+    ref = O.make_plan(T, L, R, K, S, mask, mode)
+    for key in ("step_kind", "refresh_ord", "k_eff", "read_slots", "write_slot", "action"):
+        np.testing.assert_array_equal(got[key], ref[key], err_msg=key)
+    assert got["counts"] == ref["counts"]
+    return got
+
+
+@pytest.mark.parametrize("name", ["tiny", "dit_xl2", "flux", "qwen", "hunyuan"])
+@pytest.mark.parametrize("mode", [abi.FF_VANILLA, abi.FF_DRAFT, abi.FF_VERIFY, abi.FF_FEATFIX, abi.FF_EXACT_ONLY])
+def test_plan_bit_exact_with_oracle_on_workloads(name, mode):
+    cfg = synth.get_config(name)
+    mask = synth.site_mask(cfg)
+    compare_plan(cfg["T"], len(cfg["kinds"]), cfg["R"], cfg["K"], cfg["S"], mask, mode)
+
+
+def test_plan_bit_exact_random_schedules():
+    rng = np.random.default_rng(0)
+    for _ in range(200):
+        T = int(rng.integers(1, 60))
+        L = int(rng.integers(1, 20))
+        R = int(rng.integers(1, 9))
+        K = int(rng.integers(0, 4))
+        S = int(rng.integers(K + 1, 9))
+        mask = (rng.random((T, L)) < rng.random()).astype(np.uint8)
+        mode = int(rng.integers(0, 5))
+        compare_plan(T, L, R, K, S, mask, mode)
+
+
+@pytest.mark.parametrize("K,R", [(0, 3), (1, 6), (2, 5), (3, 4)])
+def test_plan_coefficients_equal_the_oracle_forecast_on_unit_histories(K, R):
+    """c_m is the forecast of the oracle's finite-difference recursion fed with the m-th
+    unit vector as the refresh history (the recursion is linear in the history)."""
+    T, L, S = 40, 1, K + 1
+    got = compare_plan(T, L, R, K, S, np.zeros((T, L), np.uint8), abi.FF_DRAFT)
+    for i in range(T):
+        if i % R == 0:
+            assert (got["coeffs"][i] == 0).all()
+            continue
+        j = i // R
+        ke = min(K, j)
+        cache = O.TaylorCache(K)
+        for jj in range(j + 1):
+            # history basis: Delta_{j-m} = e_m
+            e = np.zeros(K + 1)
+            if j - jj <= K:
+                e[j - jj] = 1.0
+            cache.refresh(e, jj * R)
+        ref = cache.forecast(i)
+        np.testing.assert_allclose(got["coeffs"][i][:ke + 1], ref[:ke + 1], rtol=2e-7, atol=1e-7)
+        assert (got["coeffs"][i][ke + 1:] == 0).all()
+
+
+def test_plan_coefficients_closed_forms():
+    # uniform gap R, m = i - tau_j: K=1 -> (1+a, -a); K=2 -> (1+a+b, -a-2b, b), a=m/R, b=m^2/(2R^2)
+    for K, R in ((1, 6), (2, 5)):
+        got = compare_plan(50, 1, R, K, K + 1, np.zeros((50, 1), np.uint8), abi.FF_DRAFT)
+        for i in range(2 * R + 1, 50):
+            if i % R == 0:
+                continue
+            m = i % R
+            a, b = m / R, m * m / (2.0 * R * R)
+            ref = [1 + a, -a] if K == 1 else [1 + a + b, -a - 2 * b, b]
+            np.testing.assert_allclose(got["coeffs"][i], ref, rtol=1e-6)
+
+
+def test_plan_errors():
+    mask = np.zeros(10, np.uint8)
+    bad = [sched(0, 1, 1, 2, 3), sched(10, 0, 1, 2, 3), sched(10, 1, 4, 5, 3), sched(10, 1, 1, 1, 3),
+           sched(10, 1, 1, 9, 3), sched(10, 1, 1, 2, 7), sched(10, 1, 1, 2, 3, fm=5), sched(10, 1, 1, 2, 3, eps=0.0)]
+    for s in bad:
+        with pytest.raises(abi.FFError) as e:
+            abi.ff_plan_build(s, 1, mask)
+        assert e.value.status == abi.FF_E_RANGE
+    out = C.c_void_p()
+    assert abi.lib().ff_plan_build(None, 1, None, C.byref(out)) == abi.FF_E_NULL
+    assert abi.lib().ff_plan_export(None, None, None, None, None, None, None, None, None) == abi.FF_E_NULL
+
+
+def tiny_desc(**over):
+    cfg = synth.get_config("tiny", **over)
+    return cfg, pipeline.model_desc(cfg)
+
+
+def test_sizing():
+    cfg, m = tiny_desc()
+    E = cfg["B"] * (cfg["n_img"] + cfg["n_txt"]) * cfg["C"]
+    assert abi.ff_cache_bytes(m, 2) == 4 * 2 * E * 4
+    assert abi.ff_workspace_bytes(m) >= 9 * E * 4
+    cfg, mb = tiny_desc(dtype=synth.BF16)
+    assert abi.ff_cache_bytes(mb, 3) == 4 * 3 * E * 2
+    bad = pipeline.model_desc(dict(cfg, C=250))
+    assert abi.ff_cache_bytes(bad, 2) == 0 and abi.ff_workspace_bytes(bad) == 0
+
+
+@pytest.mark.parametrize("over,code", [
+    (dict(C=260, H=4, d=65), abi.FF_E_SHAPE), (dict(d=60), abi.FF_E_SHAPE), (dict(B=9), abi.FF_E_SHAPE),
+    (dict(n_img=63), abi.FF_E_SHAPE), (dict(dtype=7), abi.FF_E_DTYPE), (dict(n_txt=4), abi.FF_E_SHAPE),
+    (dict(mlp=1001), abi.FF_E_SHAPE), (dict(ln_eps=0.0), abi.FF_E_RANGE)])
+def test_invalid_model_descriptors(over, code):
+    cfg = synth.get_config("tiny")
+    cfg.update(over)
+    m = pipeline.model_desc(cfg)
+    lw = abi.ff_layer_weights()
+    assert abi.lib().ff_block_exact(C.byref(m), 0, C.byref(lw), 16, 32, 48, 64, 1 << 30, None) == code
+    assert abi.ff_last_error() != ""
+
+
+def fake_weights(L, base=1 << 20):
+    """Distinct fake (never dereferenced) 16-byte aligned addresses for host-only validation."""
+    lw = (abi.ff_layer_weights * L)()
+    addr = base
+    for l in range(L):
+        for s in range(2):
+            for f, _ in abi.ff_stream_weights._fields_:
+                setattr(lw[l].s[s], f, addr)
+                addr += 4096
+    g = abi.ff_global_weights(**{f: base + 10_000_000 + 4096 * i for i, (f, _) in enumerate(abi.ff_global_weights._fields_)})
+    return lw, g
+
+
+def test_block_and_memory_op_errors_are_host_side():
+    cfg, m = tiny_desc()
+    L = abi.lib()
+    lw, _ = fake_weights(4)
+    ws = abi.ff_workspace_bytes(m)
+    # layer out of range, NULL tensors, short workspace, overlap, misalignment
+    assert L.ff_block_exact(C.byref(m), 4, C.byref(lw[0]), 16, 1 << 24, 2 << 24, 3 << 24, ws, None) == abi.FF_E_RANGE
+    assert L.ff_block_exact(C.byref(m), 0, C.byref(lw[0]), 16, None, 2 << 24, 3 << 24, ws, None) == abi.FF_E_NULL
+    assert L.ff_block_exact(C.byref(m), 0, C.byref(lw[0]), 16, 1 << 24, 2 << 24, 3 << 24, ws - 1, None) == abi.FF_E_WORKSPACE
+    assert L.ff_block_exact(C.byref(m), 0, C.byref(lw[0]), 16, 1 << 24, 1 << 24, 3 << 24, ws, None) == abi.FF_E_SHAPE
+    assert L.ff_block_exact(C.byref(m), 0, C.byref(lw[0]), 16, (1 << 24) + 4, 2 << 24, 3 << 24, ws, None) == abi.FF_E_SHAPE
+    lw0 = abi.ff_layer_weights()
+    assert L.ff_block_exact(C.byref(m), 0, C.byref(lw0), 16, 1 << 24, 2 << 24, 3 << 24, ws, None) == abi.FF_E_NULL
+    # cache update: bad slot / layer / mode
+    assert L.ff_cache_update(C.byref(m), 1 << 24, 2, 0, 2, 16, 32, 0, None) == abi.FF_E_RANGE
+    assert L.ff_cache_update(C.byref(m), 1 << 24, 2, 5, 0, 16, 32, 0, None) == abi.FF_E_RANGE
+    assert L.ff_cache_update(C.byref(m), 1 << 24, 2, 0, 0, 16, 32, 9, None) == abi.FF_E_RANGE
+    assert L.ff_cache_update(C.byref(m), 1 << 24, 2, 0, 0, None, 32, 0, None) == abi.FF_E_NULL
+    # draft / verify: bad order, bad slot, overlap
+    slots = (C.c_int32 * 4)(0, 1, 0, 0)
+    coef = (C.c_float * 4)(1, 0, 0, 0)
+    assert L.ff_draft_forecast(C.byref(m), 1 << 24, 2, 0, 4, slots, coef, 16, 32, None) == abi.FF_E_RANGE
+    bad_slots = (C.c_int32 * 4)(0, 2, 0, 0)
+    assert L.ff_draft_forecast(C.byref(m), 1 << 24, 2, 0, 1, bad_slots, coef, 16, 32, None) == abi.FF_E_RANGE
+    assert L.ff_draft_forecast(C.byref(m), None, 2, 0, 1, slots, coef, 16, 32, None) == abi.FF_E_NULL
+    assert L.ff_verify_replace(C.byref(m), 1 << 24, 2, 0, 1, slots, coef, 16, 1 << 26, 1 << 26, 1, C.c_float(1e-8),
+                               None, 1 << 28, ws, None) == abi.FF_E_SHAPE
+    assert L.ff_verify_replace(C.byref(m), 1 << 24, 2, 0, 1, slots, coef, 16, 1 << 26, 1 << 27, 1, C.c_float(0.0),
+                               None, 1 << 28, ws, None) == abi.FF_E_RANGE
+    assert L.ff_verify_replace(C.byref(m), 1 << 24, 2, 0, 1, slots, coef, 16, 1 << 26, 1 << 27, 1, C.c_float(1e-8),
+                               None, 1 << 28, ws - 1, None) == abi.FF_E_WORKSPACE
+
+
+def test_context_state_errors_are_host_side():
+    cfg, m = tiny_desc()
+    T, L = cfg["T"], 4
+    lw, g = fake_weights(L)
+    plan = abi.ff_plan_build(sched(T, 3, 1, 2, abi.FF_FEATFIX), L, synth.site_mask(cfg))
+    cb, wb = abi.ff_cache_bytes(m, 2), abi.ff_workspace_bytes(m)
+    Lb = abi.lib()
+    out = C.c_void_p()
+    assert Lb.ff_ctx_create(C.byref(m), lw, C.byref(g), plan, 1 << 30, cb - 1, 2 << 30, wb, C.byref(out)) == abi.FF_E_WORKSPACE
+    assert Lb.ff_ctx_create(C.byref(m), lw, C.byref(g), plan, 1 << 30, cb, 2 << 30, wb - 1, C.byref(out)) == abi.FF_E_WORKSPACE
+    g0 = abi.ff_global_weights()
+    assert Lb.ff_ctx_create(C.byref(m), lw, C.byref(g0), plan, 1 << 30, cb, 2 << 30, wb, C.byref(out)) == abi.FF_E_NULL
+    other = abi.ff_plan_build(sched(T, 3, 1, 2, abi.FF_FEATFIX), L + 1, np.zeros(T * (L + 1), np.uint8))
+    assert Lb.ff_ctx_create(C.byref(m), lw, C.byref(g), other, 1 << 30, cb, 2 << 30, wb, C.byref(out)) == abi.FF_E_SHAPE
+    ctx = abi.ff_ctx_create(m, lw, g, plan, 1 << 30, cb, 2 << 30, wb)
+    # steps must come in order: step 1 before step 0 is refused before any launch
+    assert Lb.ff_denoise_step(ctx, 1, 1 << 31, 3 << 30, None, None, None) == abi.FF_E_STATE
+    assert Lb.ff_denoise_step(ctx, 0, None, 3 << 30, None, None, None) == abi.FF_E_NULL
+    assert abi.ff_get_counts(ctx) == {"n_full_refresh": 0, "n_paid_checks": 0, "n_forwarded": 0}
+    abi.ff_ctx_reset(ctx)
+    abi.ff_ctx_destroy(ctx)
+    abi.ff_plan_destroy(plan)
+    abi.ff_plan_destroy(other)
+
+
+def test_text_rows_required_for_mmdit():
+    cfg = synth.get_config("tiny", kinds=[synth.MMDIT_DOUBLE] * 2, n_txt=8)
+    m = pipeline.model_desc(cfg)
+    lw, g = fake_weights(2)
+    plan = abi.ff_plan_build(sched(cfg["T"], 3, 1, 2, abi.FF_FEATFIX), 2, np.zeros(cfg["T"] * 2, np.uint8))
+    ctx = abi.ff_ctx_create(m, lw, g, plan, 1 << 30, abi.ff_cache_bytes(m, 2), 2 << 30, abi.ff_workspace_bytes(m))
+    assert abi.lib().ff_denoise_step(ctx, 0, 1 << 31, 3 << 30, None, None, None) == abi.FF_E_NULL
+    abi.ff_ctx_destroy(ctx)
+    abi.ff_plan_destroy(plan)

@@ -1,0 +1,128 @@
+"""GPU parity of the exact block (Eq. 1) through ff_block_exact: element-wise against the
+oracle at small ragged shapes (several tiles plus tails in every GEMM dimension, head dims
+64 and 72, token tails), and on sampled rows at the workloads' full shapes."""
+import numpy as np
+import pytest
+import torch
+
+import oracle as O
+import synth
+from paper_2607_27842_amd import abi, pipeline
+from gpu_util import TOL, dev, host, need_gpu, say
+
+pytestmark = pytest.mark.gpu
+
+
+def ragged_cfg(kind, dtype, d=64, H=5, n_txt=0, B=2, lat=(4, 1, 20, 20), mlp_ratio=2):
+    C = H * d
+    kinds = [kind]
+    n_img = (lat[1]) * (lat[2] // 2) * (lat[3] // 2)
+    return dict(name="ragged", kinds=kinds, C=C, H=H, d=d, mlp=mlp_ratio * C, n_img=n_img, n_txt=n_txt, B=B,
+                lat=lat, patch=(1, 2, 2), dtype=dtype, T=4, R=2, K=1, S=2, sites=[], site_rule="fixed",
+                ln_eps=1e-6, rel_eps=1e-8)
+
+
+def run_block(cfg, W, u_np, c_np, rows=None):
+    dt = pipeline.torch_dtype(cfg)
+    sets = [W["txt"], W["img"]] if cfg["kinds"][0] == synth.MMDIT_DOUBLE else [W]
+    tens = [{k: dev(v, dt) for k, v in s.items()} for s in sets]
+    lw = abi.ff_layer_weights()
+    for si, s in enumerate(tens):
+        for k, t in s.items():
+            setattr(lw.s[si], k, t.data_ptr())
+    m = pipeline.model_desc(cfg)
+    ws_bytes = abi.ff_workspace_bytes(m)
+    ws = torch.empty(ws_bytes, dtype=torch.uint8, device="cuda")
+    u = dev(u_np, dt)
+    c = dev(c_np, torch.float32)
+    h = torch.empty_like(u)
+    abi.ff_block_exact(m, 0, lw, c.data_ptr(), u.data_ptr(), h.data_ptr(), ws.data_ptr(), ws_bytes)
+    torch.cuda.synchronize()
+    h2 = torch.empty_like(u)
+    abi.ff_block_exact(m, 0, lw, c.data_ptr(), u.data_ptr(), h2.data_ptr(), ws.data_ptr(), ws_bytes)
+    torch.cuda.synchronize()
+    assert torch.equal(h, h2), "exact block is not deterministic"
+    return host(h)
+
+
+def boosted(W, kind):
+    # larger modulation weights make every gate O(1) so that each branch is visible in h - u
+    def b(s):
+        s = dict(s)
+        s["mod_w"] = (s["mod_w"] * 8).astype(np.float32)
+        return s
+    return {k: b(v) for k, v in W.items()} if kind == synth.MMDIT_DOUBLE else b(W)
+
+
+def check_block(cfg, W, seed=0, rows=None, tol=None):
+    kind = cfg["kinds"][0]
+    bf = cfg["dtype"] == synth.BF16
+    B, N, C = cfg["B"], cfg["n_img"] + cfg["n_txt"], cfg["C"]
+    u = synth.normal((B, N, C), 300 + seed, bf16=bf)
+    c = synth.normal((B, C), 400 + seed)
+    got = run_block(cfg, W, u, c)
+    u64 = u.astype(np.float64)
+    cs = O.silu(c.astype(np.float64))
+    ref = O.block(kind, u64, cs, W, cfg, rows=rows)
+    if bf:
+        ref = O.round_bf16(ref)
+    g = got if rows is None else got[:, rows]
+    uu = u64 if rows is None else u64[:, rows]
+    err = O.max_rel_err(g - uu, ref - uu)       # error relative to the block's own update h - u
+    tol = TOL[cfg["dtype"]] if tol is None else tol
+    say(f"  block kind={kind} dtype={cfg['dtype']} B={B} N={N} C={C} d={cfg['d']}: err(h-u)={err:.3e} tol={tol}")
+    assert err <= tol, err
+    return err
+
+
+@pytest.mark.parametrize("dtype", [synth.F32, synth.BF16])
+@pytest.mark.parametrize("d", [64, 72])
+def test_dit_block_ragged(dtype, d):
+    need_gpu()
+    cfg = ragged_cfg(synth.DIT, dtype, d=d)
+    W = boosted(synth.make_layer_weights(cfg, 0, bias_std=0.02, gain_std=0.1), synth.DIT)
+    say(f"dit ragged dtype={dtype} d={d}")
+    check_block(cfg, W)
+
+
+@pytest.mark.parametrize("dtype", [synth.F32, synth.BF16])
+@pytest.mark.parametrize("kind", [synth.MMDIT_DOUBLE, synth.MMDIT_SINGLE])
+def test_mmdit_blocks_ragged(dtype, kind):
+    need_gpu()
+    cfg = ragged_cfg(kind, dtype, d=64, H=3, n_txt=13, lat=(4, 1, 18, 22))
+    W = boosted(synth.make_layer_weights(cfg, 0, bias_std=0.02, gain_std=0.2), kind)
+    say(f"mmdit ragged kind={kind} dtype={dtype}")
+    check_block(cfg, W, seed=kind)
+
+
+def test_tiny_shape_block_fp32():
+    need_gpu()
+    cfg = synth.get_config("tiny", kinds=[synth.DIT])
+    W = synth.make_layer_weights(cfg, 0, bias_std=0.02, gain_std=0.1)
+    say("tiny block")
+    check_block(cfg, W)
+
+
+def test_dit_xl2_block_full_shape():
+    need_gpu()
+    cfg = synth.get_config("dit_xl2", kinds=[synth.DIT])
+    W = synth.make_layer_weights(cfg, 0, bias_std=0.02)
+    say("dit_xl2 full block B=8 N=256 C=1152 d=72")
+    check_block(cfg, W)
+
+
+SAMPLE_ROWS = {
+    "flux": [0, 1, 511, 512, 513, 2000, 4095, 4607],
+    "qwen": [0, 255, 256, 257, 3000, 4351],
+    "hunyuan": [0, 255, 256, 300, 7000, 14309, 14565],
+}
+
+
+@pytest.mark.parametrize("name,kind", [("flux", synth.MMDIT_SINGLE), ("flux", synth.MMDIT_DOUBLE),
+                                       ("qwen", synth.MMDIT_DOUBLE), ("hunyuan", synth.MMDIT_DOUBLE)])
+def test_mmdit_block_full_shape_sampled_rows(name, kind):
+    need_gpu()
+    cfg = synth.get_config(name, kinds=[kind])
+    W = synth.make_layer_weights(cfg, 0, bias_std=0.02, gain_std=0.1)
+    say(f"{name} full block kind={kind} N={cfg['n_img'] + cfg['n_txt']} (sampled rows)")
+    check_block(cfg, W, rows=np.array(SAMPLE_ROWS[name]))

@@ -1,0 +1,158 @@
+"""GPU parity of whole denoising loops through ff_denoise_step against the oracle, and
+the paper's invariants checked bit for bit on the GPU."""
+import numpy as np
+import pytest
+import torch
+
+import oracle as O
+import synth
+from paper_2607_27842_amd import abi, pipeline
+from gpu_util import TOL, host, need_gpu, say
+
+pytestmark = pytest.mark.gpu
+
+MODES = {"vanilla": abi.FF_VANILLA, "draft": abi.FF_DRAFT, "verify": abi.FF_VERIFY, "featfix": abi.FF_FEATFIX,
+         "exact_only": abi.FF_EXACT_ONLY}
+
+
+def gpu_run(cfg, W, inp, mode, mask, feature_mode=abi.FF_RESIDUAL, dm=None):
+    dm = dm or pipeline.DeviceModel.from_host(cfg, *W)
+    run = pipeline.Runner(dm, mode, mask, feature_mode=feature_mode)
+    x, c, txt = pipeline.host_inputs_to_device(cfg, inp)
+    xt, audit, counts = run.run(x, c, txt)
+    torch.cuda.synchronize()
+    plan = run.export_plan()
+    run.close()
+    return xt, audit, counts, plan
+
+
+def check_against_oracle(cfg, W, inp, mode, mask, feature_mode=abi.FF_RESIDUAL, dm=None):
+    xt, audit, counts, plan = gpu_run(cfg, W, inp, mode, mask, feature_mode, dm)
+    ref = O.run(cfg, mode, inp, W, mask, feature_mode=feature_mode)
+    err = O.max_rel_err(host(xt), ref["x"])
+    tol = TOL[cfg["dtype"]]
+    say(f"  {cfg['name']} mode={mode} fm={feature_mode}: max rel err {err:.3e} (tol {tol}) counts {counts}")
+    assert err <= tol, err
+    assert counts == ref["counts"]
+    for key in ("step_kind", "refresh_ord", "k_eff", "read_slots", "write_slot", "action"):
+        np.testing.assert_array_equal(plan[key], ref["plan"][key])
+    a = audit.cpu().numpy()
+    L = len(cfg["kinds"])
+    for (i, l), d in ref["audit"].items():
+        np.testing.assert_allclose(a[i, l], d, rtol=0, atol=tol)
+    paid = np.zeros((cfg["T"], L), bool)
+    for (i, l) in ref["audit"]:
+        paid[i, l] = True
+    assert np.isnan(a[~paid]).all()
+    return xt
+
+
+@pytest.mark.parametrize("mode", list(MODES))
+def test_tiny_fp32_loop_all_modes(mode):
+    need_gpu()
+    cfg = synth.get_config("tiny")
+    W = synth.make_weights(cfg, bias_std=0.02, gain_std=0.1)
+    inp = synth.make_inputs(cfg)
+    say(f"tiny fp32 loop mode={mode}")
+    check_against_oracle(cfg, W, inp, MODES[mode], synth.site_mask(cfg))
+
+
+def test_tiny_fp32_output_feature_mode():
+    need_gpu()
+    cfg = synth.get_config("tiny")
+    W = synth.make_weights(cfg, bias_std=0.02, gain_std=0.1)
+    inp = synth.make_inputs(cfg)
+    say("tiny fp32 loop, output feature mode")
+    check_against_oracle(cfg, W, inp, abi.FF_FEATFIX, synth.site_mask(cfg), feature_mode=abi.FF_OUTPUT)
+
+
+@pytest.mark.parametrize("dtype", [synth.F32, synth.BF16])
+def test_gpu_bitwise_invariants(dtype):
+    """FeatFix == Exact-only, Verify == Draft, all sites == Vanilla == R=1, runs repeat bitwise."""
+    need_gpu()
+    cfg = synth.get_config("tiny", dtype=dtype)
+    W = synth.make_weights(cfg, bias_std=0.02, gain_std=0.1)
+    inp = synth.make_inputs(cfg)
+    dm = pipeline.DeviceModel.from_host(cfg, *W)
+    mask = synth.site_mask(cfg)
+    say(f"bitwise invariants dtype={dtype}")
+    ff = gpu_run(cfg, W, inp, abi.FF_FEATFIX, mask, dm=dm)
+    ff2 = gpu_run(cfg, W, inp, abi.FF_FEATFIX, mask, dm=dm)
+    eo = gpu_run(cfg, W, inp, abi.FF_EXACT_ONLY, mask, dm=dm)
+    ve = gpu_run(cfg, W, inp, abi.FF_VERIFY, mask, dm=dm)
+    dr = gpu_run(cfg, W, inp, abi.FF_DRAFT, mask, dm=dm)
+    va = gpu_run(cfg, W, inp, abi.FF_VANILLA, mask, dm=dm)
+    ones = np.ones_like(mask)
+    al = gpu_run(cfg, W, inp, abi.FF_FEATFIX, ones, dm=dm)
+    assert torch.equal(ff[0], ff2[0]) and torch.equal(ff[1].nan_to_num(), ff2[1].nan_to_num())
+    assert torch.equal(ff[0], eo[0]), "FeatFix and Exact-only differ"
+    assert torch.equal(ve[0], dr[0]), "Verify and Draft differ"
+    assert torch.equal(al[0], va[0]), "all-sites FeatFix differs from Vanilla"
+    assert not torch.equal(ff[0], ve[0])
+    assert ff[2]["n_paid_checks"] == ve[2]["n_paid_checks"] == 12 and ve[2]["n_forwarded"] == 0
+    cfg1 = dict(cfg, R=1)
+    dm1 = pipeline.DeviceModel.from_host(cfg1, *W)
+    r1 = gpu_run(cfg1, W, inp, abi.FF_FEATFIX, mask, dm=dm1)
+    assert torch.equal(r1[0], va[0]), "R=1 differs from Vanilla"
+    # audit of the first paid check is the same in Verify and FeatFix (same incoming state)
+    a_f, a_v = ff[1].cpu().numpy(), ve[1].cpu().numpy()
+    np.testing.assert_array_equal(a_f[1, 1], a_v[1, 1])
+
+
+def test_dit_xl2_reduced_depth_loop():
+    """Full width / tokens / batch of DiT-XL/2, 4 blocks, 10 steps, R=5, K=2, sites {1,3}."""
+    need_gpu()
+    cfg = synth.get_config("dit_xl2", kinds=[synth.DIT] * 4, T=10, sites=[1, 3])
+    W = synth.make_weights(cfg, bias_std=0.02, gain_std=0.1)
+    inp = synth.make_inputs(cfg)
+    mask = synth.site_mask(cfg)
+    dm = pipeline.DeviceModel.from_host(cfg, *W)
+    for mode in (abi.FF_FEATFIX, abi.FF_VANILLA):
+        say(f"dit_xl2 reduced loop mode={mode}")
+        check_against_oracle(cfg, W, inp, mode, mask, dm=dm)
+
+
+def mmdit_small(name, kinds, n_txt, lat, C=256, H=2, sites=(1,)):
+    cfg = synth.get_config(name, kinds=kinds, C=C, H=H, d=C // H, mlp=4 * C, n_txt=n_txt, lat=lat,
+                           n_img=lat[1] * (lat[2] // 2) * (lat[3] // 2), T=8, R=3, sites=list(sites))
+    return cfg
+
+
+def test_flux_like_reduced_loop():
+    """FLUX-like structure (2 double + 3 single blocks, sites: last double, middle single,
+    last single) at reduced width, with text tokens and head dim 128."""
+    need_gpu()
+    cfg = mmdit_small("flux", [synth.MMDIT_DOUBLE] * 2 + [synth.MMDIT_SINGLE] * 3, 24, (16, 1, 20, 18),
+                      sites=(1, 2, 4))
+    W = synth.make_weights(cfg, bias_std=0.02, gain_std=0.1)
+    inp = synth.make_inputs(cfg)
+    mask = synth.site_mask(cfg)
+    dm = pipeline.DeviceModel.from_host(cfg, *W)
+    for mode in (abi.FF_FEATFIX, abi.FF_VERIFY):
+        say(f"flux-like reduced loop mode={mode}")
+        check_against_oracle(cfg, W, inp, mode, mask, dm=dm)
+
+
+def test_video_like_reduced_loop():
+    """HunyuanVideo-like 3-D latent (frames x rows x cols patches) with double blocks, K=1, S=3."""
+    need_gpu()
+    cfg = mmdit_small("hunyuan", [synth.MMDIT_DOUBLE] * 3, 16, (16, 3, 8, 10), sites=(1, 2))
+    W = synth.make_weights(cfg, bias_std=0.02, gain_std=0.1)
+    inp = synth.make_inputs(cfg)
+    say("video-like reduced loop")
+    check_against_oracle(cfg, W, inp, abi.FF_FEATFIX, synth.site_mask(cfg))
+
+
+def test_out_of_order_step_refused_on_gpu():
+    need_gpu()
+    cfg = synth.get_config("tiny")
+    W = synth.make_weights(cfg)
+    dm = pipeline.DeviceModel.from_host(cfg, *W)
+    run = pipeline.Runner(dm, abi.FF_FEATFIX, synth.site_mask(cfg))
+    x, c, _ = pipeline.host_inputs_to_device(cfg, synth.make_inputs(cfg))
+    xs, a = run.start(x)
+    run.step(0, xs, c)
+    with pytest.raises(abi.FFError) as e:
+        run.step(2, xs, c)
+    assert e.value.status == abi.FF_E_STATE
+    run.close()

@@ -1,0 +1,127 @@
+"""GPU parity of the HBM-bound kernels (history refresh, Taylor draft, verify+replace)
+against the oracle's finite-difference recursion, at the small shape and at every
+workload's real per-layer tensor size."""
+import numpy as np
+import pytest
+import torch
+
+import oracle as O
+import synth
+from paper_2607_27842_amd import abi, pipeline
+from gpu_util import dev, host, need_gpu, say, ulp_close
+
+pytestmark = pytest.mark.gpu
+
+def layer_cfg(name, **over):
+    cfg = synth.get_config(name, **over)
+    return cfg
+
+
+def rnd_for(cfg):
+    return O.round_bf16 if cfg["dtype"] == synth.BF16 else (lambda a: a)
+
+
+@pytest.mark.parametrize("name", ["tiny", "dit_xl2", "flux", "hunyuan"])
+@pytest.mark.parametrize("feature_mode", [abi.FF_RESIDUAL, abi.FF_OUTPUT])
+def test_refresh_draft_verify_match_oracle(name, feature_mode):
+    need_gpu()
+    cfg = layer_cfg(name)
+    B, N, C = cfg["B"], cfg["n_img"] + cfg["n_txt"], cfg["C"]
+    E = B * N * C
+    say(f"memkernels {name} E={E} feature_mode={feature_mode}")
+    T, R, K, S = cfg["T"], cfg["R"], cfg["K"], cfg["S"]
+    dt = pipeline.torch_dtype(cfg)
+    bf = cfg["dtype"] == synth.BF16
+    rnd = rnd_for(cfg)
+    m = pipeline.model_desc(cfg)
+    ws_bytes = abi.ff_workspace_bytes(m)
+    ws = torch.empty(ws_bytes, dtype=torch.uint8, device="cuda")
+    # one layer's cache only (layer index 0 of a view with n_slots S)
+    cache = torch.empty(S * E, dtype=dt, device="cuda")
+    # plan for the schedule, draft of layer 0 at the cached step two refreshes in (or the last one)
+    mask = np.zeros((T, len(cfg["kinds"])), np.uint8)
+    p = abi.ff_plan_build(abi.ff_sched_desc(T, R, K, S, 1e-8, abi.FF_FEATFIX, feature_mode), len(cfg["kinds"]), mask)
+    plan = abi.ff_plan_export(p, T, len(cfg["kinds"]), K)
+    abi.ff_plan_destroy(p)
+    i_star = (K + 1) * R + max(1, R // 2)   # a cached step with k_eff = K
+    assert i_star < T
+    assert plan["step_kind"][i_star] == abi.FF_STEP_CACHED
+    j = plan["refresh_ord"][i_star]
+    ke = int(plan["k_eff"][i_star])
+    slots = [int(s) for s in plan["read_slots"][i_star][:ke + 1]]
+    coeffs = [float(c) for c in plan["coeffs"][i_star][:ke + 1]]
+    # a smooth synthetic history: Delta_j = a + b tau + c tau^2 + noise, rounded where the GPU stores it
+    rng = np.random.default_rng(7)
+    base = [synth.normal((E,), 11 + q, std=1.0) for q in range(3)]
+    tc = O.TaylorCache(K)
+    for jj in range(j + 1):
+        tau = jj * R
+        u = synth.normal((E,), 100 + jj, bf16=bf)
+        delta = base[0] + 0.05 * tau * base[1] + 0.002 * tau * tau * base[2]
+        h = rnd(u.astype(np.float64) + delta).astype(np.float32)
+        ud, hd_ = dev(u, dt), dev(h, dt)
+        abi.ff_cache_update(m, cache.data_ptr(), S, 0, jj % S, ud.data_ptr() if feature_mode == abi.FF_RESIDUAL else None,
+                            hd_.data_ptr(), feature_mode)
+        tc.refresh(rnd(h.astype(np.float64) - u.astype(np.float64)) if feature_mode == abi.FF_RESIDUAL
+                   else h.astype(np.float64), tau)
+    torch.cuda.synchronize()
+    # the cached slot of the last refresh holds rnd(h - u) exactly
+    u_in = synth.normal((E,), 999, bf16=bf)
+    F = tc.forecast(i_star)
+    ref = rnd(u_in.astype(np.float64) + F) if feature_mode == abi.FF_RESIDUAL else rnd(F)
+    ud = dev(u_in, dt)
+    out = torch.empty(E, dtype=dt, device="cuda")
+    uptr = ud.data_ptr() if feature_mode == abi.FF_RESIDUAL else None
+    abi.ff_draft_forecast(m, cache.data_ptr(), S, 0, ke, slots, coeffs, uptr, out.data_ptr())
+    torch.cuda.synchronize()
+    got = host(out)
+    nbad = ulp_close(got, ref, cfg["dtype"])
+    say(f"  draft: k_eff={ke} slots={slots} max|d|={np.abs(got - ref).max():.3e} ulp-misses={nbad}")
+    assert nbad <= max(2, E // 100000), nbad
+    # in-place draft gives the same bits
+    inplace = ud.clone()
+    abi.ff_draft_forecast(m, cache.data_ptr(), S, 0, ke, slots, coeffs, inplace.data_ptr() if uptr else None,
+                          inplace.data_ptr())
+    if uptr is None:
+        pass
+    torch.cuda.synchronize()
+    if uptr is not None:
+        assert torch.equal(inplace, out)
+    # verify + replace
+    hf_np = synth.normal((E,), 555, bf16=bf)
+    hf = dev(hf_np, dt)
+    rel = torch.zeros(B, dtype=torch.float32, device="cuda")
+    for fwd in (1, 0):
+        hout = ud.clone()   # in place over u, as the step executor does
+        abi.ff_verify_replace(m, cache.data_ptr(), S, 0, ke, slots, coeffs, hout.data_ptr() if uptr else None,
+                              hf.data_ptr(), hout.data_ptr(), fwd, 1e-8, rel.data_ptr(), ws.data_ptr(), ws_bytes)
+        torch.cuda.synchronize()
+        if fwd:
+            assert torch.equal(hout, hf), "FeatFix must forward h_f bit for bit"
+        else:
+            assert torch.equal(hout, out), "Verify must forward exactly the draft"
+        ref_d = O.rel_l1(ref.reshape(B, -1), hf_np.astype(np.float64).reshape(B, -1), 1e-8)
+        got_d = rel.cpu().numpy().astype(np.float64)
+        say(f"  verify fwd={fwd}: rel_l1 gpu={got_d} oracle={ref_d}")
+        np.testing.assert_allclose(got_d, ref_d, rtol=1e-3)
+
+
+def test_memkernels_deterministic():
+    need_gpu()
+    cfg = synth.get_config("dit_xl2")
+    E = cfg["B"] * cfg["n_img"] * cfg["C"]
+    m = pipeline.model_desc(cfg)
+    ws = torch.empty(abi.ff_workspace_bytes(m), dtype=torch.uint8, device="cuda")
+    cache = torch.randn(3 * E, device="cuda").to(torch.bfloat16)
+    u = torch.randn(E, device="cuda").to(torch.bfloat16)
+    hf = torch.randn(E, device="cuda").to(torch.bfloat16)
+    outs, rels = [], []
+    for _ in range(2):
+        o = u.clone()
+        r = torch.zeros(8, device="cuda")
+        abi.ff_verify_replace(m, cache.data_ptr(), 3, 0, 2, [0, 2, 1], [1.7, -0.9, 0.2], o.data_ptr(), hf.data_ptr(),
+                              o.data_ptr(), 0, 1e-8, r.data_ptr(), ws.data_ptr(), ws.numel())
+        torch.cuda.synchronize()
+        outs.append(o)
+        rels.append(r)
+    assert torch.equal(outs[0], outs[1]) and torch.equal(rels[0], rels[1])
