@@ -1,0 +1,273 @@
+#!/usr/bin/env python3
+"""Throughput of the FeatFix cached denoising loop on one MI355X.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W]
+
+A bench step is one denoising step of the FeatFix schedule (time embedding, patch
+embedding, every layer's exact block / history refresh / Taylor draft / verify+replace as
+the plan says, final layer and Euler update); steps run in schedule order and wrap
+around to step 0 of a fresh loop after step T-1, so the default K = 2T times two whole
+loops (10 refresh + 40 cached steps each).  Inputs and weights are resident in HBM before
+the timed region.  Workload (value): DiT-XL/2 shape -- 28 DiT blocks, hidden 1152, 16
+heads of 72, 256 tokens, batch 8, bf16, T=50, refresh every 5 steps, second-order
+forecast, sites at layers 13 and 27 on every cached step.  The FLUX-like shape (19 double
++ 38 single blocks, 4096 + 512 tokens) and the Vanilla loops are reported alongside.
+
+Prints ONE JSON line.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "denoise steps/sec at DiT-XL/2 & FLUX-like shape; MFMA util %, HBM GB/s %"
+PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
+PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def device_inputs(cfg, seed=1):
+    import torch
+    g = torch.Generator(device="cuda")
+    g.manual_seed(seed)
+    c_lat, F, H, W = cfg["lat"]
+    x0 = torch.randn((cfg["B"], c_lat, F, H, W), generator=g, device="cuda", dtype=torch.float32)
+    cond = torch.randn((cfg["B"], cfg["C"]), generator=g, device="cuda", dtype=torch.float32)
+    txt = None
+    dt = torch.bfloat16 if cfg["dtype"] == 1 else torch.float32
+    cond = cond.to(dt).float()            # conditioning values are bf16-representable
+    if cfg["n_txt"] > 0:
+        txt = torch.randn((cfg["B"], cfg["n_txt"], cfg["C"]), generator=g, device="cuda").to(dt)
+    return x0, cond, txt
+
+
+class Loop:
+    """Steps through the plan, wrapping to a fresh loop (reset + initial latent) after T-1."""
+
+    def __init__(self, runner, x0, cond, txt):
+        import torch
+        self.r, self.x0, self.cond, self.txt = runner, x0, cond, txt
+        self.x = x0.clone()
+        self.audit = torch.full((runner.T * runner.L * x0.shape[0],), float("nan"), device="cuda")
+        self.pos = 0
+
+    def step(self):
+        i = self.pos % self.r.T
+        if i == 0:
+            from paper_2607_27842_amd import abi
+            abi.ff_ctx_reset(self.r.ctx)
+            self.x.copy_(self.x0)
+        self.r.step(i, self.x, self.cond, self.txt, self.audit)
+        self.pos += 1
+
+
+def timed_steps(loop, n):
+    import torch
+    torch.cuda.synchronize()
+    a = torch.cuda.Event(enable_timing=True)
+    b = torch.cuda.Event(enable_timing=True)
+    a.record()
+    for _ in range(n):
+        loop.step()
+    b.record()
+    torch.cuda.synchronize()
+    return a.elapsed_time(b)
+
+
+def per_step_kind_ms(loop):
+    """One loop with an event before every step: mean ms of refresh and of cached steps."""
+    import torch
+    T = loop.r.T
+    loop.pos = 0
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(T + 1)]
+    torch.cuda.synchronize()
+    for i in range(T):
+        ev[i].record()
+        loop.step()
+    ev[T].record()
+    torch.cuda.synchronize()
+    kinds = loop.r.export_plan()["step_kind"]
+    ms = [ev[i].elapsed_time(ev[i + 1]) for i in range(T)]
+    ref = [m for m, k in zip(ms, kinds) if k == 0]
+    cac = [m for m, k in zip(ms, kinds) if k == 1]
+    return sum(ref) / max(1, len(ref)), (sum(cac) / len(cac) if cac else 0.0)
+
+
+def profile_loop(loop):
+    """One whole loop with per-launch HIP events on the same stream (ff_ctx_profile)."""
+    import torch
+    from paper_2607_27842_amd import abi
+    loop.pos = 0
+    abi.ff_ctx_profile(loop.r.ctx, 1)
+    for _ in range(loop.r.T):
+        loop.step()
+    torch.cuda.synchronize()
+    stats = abi.ff_ctx_profile_read(loop.r.ctx)
+    abi.ff_ctx_profile(loop.r.ctx, 0)
+    return stats
+
+
+def kernel_table(stats):
+    out = {}
+    for k, s in stats.items():
+        if s["launches"] == 0:
+            continue
+        sec = s["ms"] / 1e3
+        out[k] = {"launches": s["launches"], "avg_us": round(s["ms"] * 1e3 / s["launches"], 3),
+                  "total_ms": round(s["ms"], 3),
+                  "tflops": round(s["flops"] / sec / 1e12, 1) if s["flops"] else None,
+                  "gbs": round(s["bytes"] / sec / 1e9, 1)}
+    return out
+
+
+def run_workload(name, mode_names, warmup_loops, timed_steps_n, with_profile):
+    import torch
+    import synth
+    from paper_2607_27842_amd import abi, pipeline
+    cfg = synth.get_config(name)
+    t0 = time.time()
+    dm = pipeline.DeviceModel.random(cfg, seed=0)
+    x0, cond, txt = device_inputs(cfg)
+    torch.cuda.synchronize()
+    log(f"[bench] {name}: weights on device in {time.time() - t0:.1f}s")
+    mask = synth.site_mask(cfg)
+    res = {"sites": synth.sites_of(cfg)}
+    for mode_name in mode_names:
+        mode = synth.MODE_NAMES[mode_name]
+        r = pipeline.Runner(dm, mode, mask)
+        loop = Loop(r, x0, cond, txt)
+        for _ in range(warmup_loops * r.T):
+            loop.step()
+        n = timed_steps_n if timed_steps_n else r.T
+        loop.pos = 0
+        ms = timed_steps(loop, n)
+        entry = {"steps": n, "ms": round(ms, 3), "steps_per_s": round(n / (ms / 1e3), 2),
+                 "counts_per_loop": None}
+        ref_ms, cac_ms = per_step_kind_ms(loop)
+        entry["ms_refresh_step"] = round(ref_ms, 4)
+        entry["ms_cached_step"] = round(cac_ms, 4)
+        entry["counts_per_loop"] = abi.ff_get_counts(r.ctx)
+        if with_profile and mode_name == "featfix":
+            entry["kernels"] = profile_loop(loop)
+        log(f"[bench] {name} {mode_name}: {entry['steps_per_s']} steps/s "
+            f"(refresh {ref_ms:.3f} ms, cached {cac_ms:.3f} ms)")
+        res[mode_name] = entry
+        r.close()
+    del dm
+    torch.cuda.empty_cache()
+    return res
+
+
+def cpu_baseline(steps=5, layers=8):
+    """The oracle on the host, on a bounded sample of the DiT-XL/2 FeatFix loop: the first
+    R=5 steps (1 refresh + 4 cached steps) at full width, tokens and batch but `layers`
+    blocks with sites at the middle (L/2 - 1) and last block, the rule that gives {13, 27}
+    at 28 blocks.  Exact blocks dominate the oracle's time (drafts are elementwise), so the
+    full-depth rate is extrapolated by exact-block count: 28 + 4*2 = 36 blocks per 5 steps
+    at full depth against layers + 4*2 in the sample."""
+    import oracle as O
+    import synth
+    cfg = synth.get_config("dit_xl2", T=steps, kinds=[synth.DIT] * layers, sites=[layers // 2 - 1, layers - 1])
+    W = synth.make_weights(cfg)
+    inp = synth.make_inputs(cfg)
+    mask = synth.site_mask(cfg)
+    try:
+        from threadpoolctl import threadpool_info
+        blas_threads = max((i.get("num_threads", 0) for i in threadpool_info()), default=0)
+    except Exception:
+        blas_threads = 0
+    t0 = time.perf_counter()
+    O.run(cfg, O.FEATFIX, inp, W, mask)
+    dt = time.perf_counter() - t0
+    sample_blocks = layers + (steps - 1) * 2
+    full_blocks = 28 + (steps - 1) * 2
+    est = dt * full_blocks / sample_blocks
+    cores = len(os.sched_getaffinity(0))
+    return {"value": round(steps / est, 5), "unit": "steps/s", "cores": min(cores, blas_threads or cores),
+            "kind": "oracle",
+            "sample": f"fp64 NumPy oracle: first {steps} steps (1 refresh + {steps - 1} cached, 2 paid sites each) "
+                      f"of the DiT-XL/2-shaped FeatFix loop with {layers} of 28 blocks (B=8, N=256, C=1152) took "
+                      f"{dt:.1f} s; scaled to 28 blocks by exact-block count ({sample_blocks} -> {full_blocks}); "
+                      f"host affinity {cores} cores, BLAS threads {blas_threads}"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=100)
+    ap.add_argument("--warmup", type=int, default=50)
+    ap.add_argument("--no-flux", action="store_true")
+    ap.add_argument("--no-vanilla", action="store_true")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py runs on one GPU only: the FeatFix path here is single-GPU "
+              "(no sharding or collectives); use --gpus 1", file=sys.stderr)
+        sys.exit(2)
+    import torch
+    import synth
+    from paper_2607_27842_amd import abi
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    abi.lib()
+
+    cfg = synth.get_config("dit_xl2")
+    T = cfg["T"]
+    warm_loops = max(1, -(-args.warmup // T))
+    modes = ["featfix"] + ([] if args.no_vanilla else ["vanilla"])
+    dit = run_workload("dit_xl2", modes, warm_loops, args.steps, with_profile=True)
+    ff = dit["featfix"]
+    ms_step = ff["ms"] / ff["steps"]
+    value = ff["steps"] / (ff["ms"] / 1e3)
+    kern = ff.pop("kernels")
+    g = kern["gemm"]
+    achieved = g["flops"] / (g["ms"] / 1e3) / 1e12
+    roof = {"bound": "mfma", "achieved": round(achieved, 1), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+            "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": None,
+            "kernel": "k_gemm_bf16 (all exact-block GEMM launches of one FeatFix loop)",
+            "avg_launch_us": round(g["ms"] * 1e3 / g["launches"], 3),
+            "flop_per_launch": g["flops"] / g["launches"]}
+    hbm = {}
+    for k in ("draft", "verify", "cache"):
+        s = kern[k]
+        if s["launches"]:
+            gbs = s["bytes"] / (s["ms"] / 1e3) / 1e9
+            hbm[k] = {"achieved_gbs": round(gbs, 1), "frac": round(gbs / PEAK_HBM_GBS, 4),
+                      "avg_launch_us": round(s["ms"] * 1e3 / s["launches"], 3),
+                      "bytes_per_launch": s["bytes"] / s["launches"]}
+    extra = {"dit_xl2": dit, "dit_kernels": kernel_table(kern), "hbm_roofline": hbm}
+    if "vanilla" in dit:
+        extra["dit_featfix_over_vanilla"] = round(value / dit["vanilla"]["steps_per_s"], 3)
+    if not args.no_flux:
+        flux = run_workload("flux", ["featfix"] + ([] if args.no_vanilla else ["vanilla"]), 1, 0,
+                            with_profile=True)
+        fk = flux["featfix"].pop("kernels")
+        flux["kernels"] = kernel_table(fk)
+        if "vanilla" in flux:
+            flux["featfix_over_vanilla"] = round(flux["featfix"]["steps_per_s"] / flux["vanilla"]["steps_per_s"], 3)
+        extra["flux"] = flux
+    out = {"metric": METRIC, "value": round(value, 3), "unit": "steps/s", "n_gpus": 1, "steps": ff["steps"],
+           "warmup": warm_loops * T, "ms_per_step": round(ms_step, 4), "higher_is_better": True, "scaling": "weak",
+           "vs_baseline": None, "dtype": "bf16",
+           "data": "synthetic: seeded N(0,1) latent and class vector, random-init N(0,0.02) weights",
+           "config": {"workload": "DiT-XL/2-shaped FeatFix loop: 28 DiT blocks, hidden 1152, 16x72 heads, "
+                                  "MLP 4608, 256 tokens, batch 8, bf16, T=50, R=5, K=2, S=3, sites {13,27}",
+                      "global_batch": cfg["B"], "seq_len": cfg["n_img"], "parallelism": "none (1 GPU)"},
+           "roofline": roof}
+    if not args.no_cpu_baseline:
+        log("[bench] timing the CPU oracle sample ...")
+        out["cpu_baseline"] = cpu_baseline()
+    out["extra"] = extra
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -140,6 +140,27 @@ typedef struct {
   int64_t n_full_refresh, n_paid_checks, n_forwarded;
 } ff_counts;
 
+/* Kernel classes of the optional per-launch profiler (ff_ctx_profile). */
+enum {
+  FF_PROF_GEMM = 0,    /* dense contractions of the exact block, patch embed, final linear */
+  FF_PROF_ATTN = 1,    /* softmax attention                                                 */
+  FF_PROF_NORM = 2,    /* adaLN LayerNorm, QK RMSNorm                                       */
+  FF_PROF_GEMV = 3,    /* modulation and time-embedding GEMVs                               */
+  FF_PROF_DRAFT = 4,   /* Taylor draft                                                      */
+  FF_PROF_VERIFY = 5,  /* fused verify + replace (+ its second reduction stage)             */
+  FF_PROF_CACHE = 6,   /* history refresh                                                   */
+  FF_PROF_OTHER = 7,   /* time embedding, patchify, text rows, unpatchify + Euler           */
+  FF_PROF_NCLASS = 8
+};
+
+/* Per-class totals: launches, summed event-measured duration (ms), algorithmic FLOPs
+ * (2*M*N*K per GEMM, 4*B*N^2*H*d per attention) and algorithmic HBM bytes (each
+ * operand read once, each output written once). */
+typedef struct {
+  int64_t launches;
+  double ms, flops, bytes;
+} ff_prof_stat;
+
 typedef struct ff_plan ff_plan;
 typedef struct ff_ctx ff_ctx;
 
@@ -254,6 +275,16 @@ ff_status ff_get_counts(const ff_ctx* c, ff_counts* out);
  * Errors: FF_E_NULL, FF_E_STATE (step out of order), FF_E_HIP. */
 ff_status ff_denoise_step(ff_ctx* c, int32_t step, float* x, const float* cond,
                           const void* txt, float* audit, ff_stream_t stream);
+
+/* ---------------------------------------------------------------- profiling
+ * Optional tracing of a context's launches (Sec. 4 reports latency per arm; this
+ * attributes it to kernels).  While enabled, ff_denoise_step brackets every kernel
+ * launch with a pair of HIP events recorded on the caller's stream; the events are
+ * created on first use and kept by the context.  ff_ctx_profile(c, 1) enables and clears,
+ * (c, 0) disables.  ff_ctx_profile_read waits for the recorded events, fills
+ * out[FF_PROF_NCLASS] and clears the record.  Errors: FF_E_NULL, FF_E_HIP. */
+ff_status ff_ctx_profile(ff_ctx* c, int32_t enable);
+ff_status ff_ctx_profile_read(ff_ctx* c, ff_prof_stat* out);
 
 #ifdef __cplusplus
 }

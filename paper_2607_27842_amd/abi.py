@@ -26,7 +26,8 @@ FF_MAX_K, FF_MAX_SLOTS, FF_TEMB_DIM = 3, 8, 256
 EXPORTED = ("ff_abi_version", "ff_last_error", "ff_plan_build", "ff_plan_destroy", "ff_plan_export",
             "ff_cache_bytes", "ff_workspace_bytes", "ff_block_exact", "ff_cache_update",
             "ff_draft_forecast", "ff_verify_replace", "ff_ctx_create", "ff_ctx_destroy",
-            "ff_ctx_reset", "ff_get_counts", "ff_denoise_step")
+            "ff_ctx_reset", "ff_get_counts", "ff_denoise_step", "ff_ctx_profile", "ff_ctx_profile_read")
+PROF_CLASSES = ("gemm", "attn", "norm", "gemv", "draft", "verify", "cache", "other")
 
 
 class ff_model_desc(C.Structure):
@@ -70,6 +71,10 @@ class ff_counts(C.Structure):
                 "n_forwarded": self.n_forwarded}
 
 
+class ff_prof_stat(C.Structure):
+    _fields_ = [("launches", C.c_int64), ("ms", C.c_double), ("flops", C.c_double), ("bytes", C.c_double)]
+
+
 class FFError(RuntimeError):
     def __init__(self, status, msg):
         super().__init__(f"featfix error {status}: {msg}")
@@ -108,6 +113,8 @@ def lib():
             "ff_ctx_reset": (i32, [vp]),
             "ff_get_counts": (i32, [vp, P(ff_counts)]),
             "ff_denoise_step": (i32, [vp, i32, vp, vp, vp, vp, vp]),
+            "ff_ctx_profile": (i32, [vp, i32]),
+            "ff_ctx_profile_read": (i32, [vp, P(ff_prof_stat)]),
         }
         for name, (res, args) in sig.items():
             fn = getattr(L, name)
@@ -222,3 +229,15 @@ def ff_get_counts(ctx):
 
 def ff_denoise_step(ctx, step, x, cond, txt, audit, stream=0):
     return check(lib().ff_denoise_step(ctx, step, x, cond, txt, audit, stream))
+
+
+def ff_ctx_profile(ctx, enable):
+    return check(lib().ff_ctx_profile(ctx, int(enable)))
+
+
+def ff_ctx_profile_read(ctx):
+    """Per kernel class: {class: dict(launches, ms, flops, bytes)} (synchronises the events)."""
+    out = (ff_prof_stat * len(PROF_CLASSES))()
+    check(lib().ff_ctx_profile_read(ctx, out))
+    return {n: {"launches": o.launches, "ms": o.ms, "flops": o.flops, "bytes": o.bytes}
+            for n, o in zip(PROF_CLASSES, out)}

@@ -134,6 +134,87 @@ Ws ws_layout(const Model& m) {
 template <class T = void>
 T* at(void* base, size_t off) { return reinterpret_cast<T*>(reinterpret_cast<char*>(base) + off); }
 
+
+// ---------------------------------------------------------------- launches (+ optional profiling)
+// Every kernel launch of the path goes through Exec so that a context with profiling
+// enabled can bracket it with HIP events on the same stream and attribute algorithmic
+// FLOPs / bytes to its kernel class.
+struct Prof {
+  bool on = false;
+  std::vector<hipEvent_t> pool;
+  size_t next = 0;
+  struct Rec { int cls; hipEvent_t a, b; double flops, bytes; };
+  std::vector<Rec> recs;
+  ~Prof() {
+    for (hipEvent_t e : pool) (void)hipEventDestroy(e);
+  }
+  hipError_t get(hipEvent_t* e) {
+    if (next == pool.size()) {
+      hipEvent_t n;
+      hipError_t r = hipEventCreate(&n);
+      if (r != hipSuccess) return r;
+      pool.push_back(n);
+    }
+    *e = pool[next++];
+    return hipSuccess;
+  }
+};
+
+struct Exec {
+  hipStream_t st;
+  Prof* prof;
+  int dt;
+  size_t es;
+
+  template <class F>
+  hipError_t timed(int cls, double flops, double bytes, F&& launch) {
+    if (!prof || !prof->on) return launch();
+    hipEvent_t a, b;
+    hipError_t e = prof->get(&a);
+    if (e == hipSuccess) e = prof->get(&b);
+    if (e != hipSuccess) return e;
+    e = hipEventRecord(a, st);
+    if (e != hipSuccess) return e;
+    e = launch();
+    if (e != hipSuccess) return e;
+    e = hipEventRecord(b, st);
+    prof->recs.push_back({cls, a, b, flops, bytes});
+    return e;
+  }
+  hipError_t gemm(const GemmArgs& a) {
+    const double bytes = ((double)a.M * a.K + (double)a.N * a.K) * es + (double)a.M * a.N * (a.out_f32 ? 4 : es);
+    return timed(FF_PROF_GEMM, 2.0 * a.M * a.N * a.K, bytes, [&] { return ff::gemm(dt, a, st); });
+  }
+  hipError_t attention(const AttnArgs& a) {
+    const double rows = (double)a.B * a.N;
+    return timed(FF_PROF_ATTN, 4.0 * a.B * (double)a.N * a.N * a.H * a.d, rows * 4.0 * a.C * es,
+                 [&] { return ff::attention(dt, a, st); });
+  }
+  hipError_t gemv(const GemvArgs& a) {
+    return timed(FF_PROF_GEMV, 2.0 * a.B * a.Nout * a.K, (double)a.Nout * a.K * es, [&] { return ff::gemv(dt, a, st); });
+  }
+  hipError_t ln(const LnModArgs& a) {
+    return timed(FF_PROF_NORM, 0, (double)a.rows * a.C * ((a.in_f32 ? 4 : es) + es),
+                 [&] { return ff::ln_modulate(dt, a, st); });
+  }
+  hipError_t rms(const RmsArgs& a) {
+    return timed(FF_PROF_NORM, 0, 2.0 * a.rows * a.H * a.d * es, [&] { return ff::rms_heads(dt, a, st); });
+  }
+  hipError_t cache(void* slot, const void* u, const void* h, size_t E) {
+    return timed(FF_PROF_CACHE, 0, (u ? 3.0 : 2.0) * E * es, [&] { return ff::cache_update(dt, slot, u, h, E, st); });
+  }
+  hipError_t draft(const Terms& t, const void* u, void* hd, size_t E) {
+    return timed(FF_PROF_DRAFT, 0, (t.n + (u ? 2.0 : 1.0)) * E * es, [&] { return ff::draft(dt, t, u, hd, E, st); });
+  }
+  hipError_t verify(const Terms& t, const void* u, const void* hf, void* hout, int fwd, int B, size_t Eb, float eps,
+                    float* rel, float* part) {
+    return timed(FF_PROF_VERIFY, 0, (t.n + (u ? 3.0 : 2.0)) * Eb * B * es,
+                 [&] { return ff::verify(dt, t, u, hf, hout, fwd, B, Eb, eps, rel, part, st); });
+  }
+  template <class F>
+  hipError_t other(double bytes, F&& launch) { return timed(FF_PROF_OTHER, 0, bytes, launch); }
+};
+
 // ---------------------------------------------------------------- weights
 bool stream_ok(const ff_stream_weights& s, int kind) {
   if (!s.mod_w || !s.mod_b || !aligned16(s.mod_w)) return false;
@@ -176,7 +257,7 @@ const void* offset_rows(const void* p, size_t rows, size_t cols, size_t es) {
 
 // h = B_l(u; c_t) with cs = SiLU(c_t) [B, C] fp32 already in the workspace.
 ff_status exec_block(const Model& m, int kind, const ff_layer_weights& w, const float* cs, const void* u,
-                     void* h, void* ws, hipStream_t st) {
+                     void* h, void* ws, Exec& ex) {
   const Ws L = ws_layout(m);
   const int C = m.C, Mh = m.M, dt = m.dtype;
   const size_t es = m.es();
@@ -196,25 +277,25 @@ ff_status exec_block(const Model& m, int kind, const ff_layer_weights& w, const 
     const RowMap all = whole(m);
     const int rows = m.B * m.N;
     GemvArgs gv{cs, C, 0, s.mod_w, s.mod_b, 3 * C, C, m.B, mod, 3 * C, 0, nullptr, 0};
-    HIP_TRY(gemv(dt, gv, st), "single: modulation");
+    HIP_TRY(ex.gemv(gv), "single: modulation");
     LnModArgs ln{u, 0, C, all, rows, C, m.ln_eps, mod, mod + C, 3 * C, lna, C};
-    HIP_TRY(ln_modulate(dt, ln, st), "single: ln");
+    HIP_TRY(ex.ln(ln), "single: ln");
     GemmArgs g1 = gemm_args(lna, C, all, s.lin1_w, s.lin1_b, rows, 3 * C, C, EPI_BIAS, qkv, 3 * C, all);
-    HIP_TRY(gemm(dt, g1, st), "single: lin1 qkv");
+    HIP_TRY(ex.gemm(g1), "single: lin1 qkv");
     const int ldy = C + Mh;
     GemmArgs g2 = gemm_args(lna, C, all, offset_rows(s.lin1_w, 3 * (size_t)C, C, es),
                             offset_rows(s.lin1_b, 3 * (size_t)C, 1, es), rows, Mh, C, EPI_BIAS_GELU,
                             at(att, (size_t)C * es), ldy, all);
-    HIP_TRY(gemm(dt, g2, st), "single: lin1 mlp");
+    HIP_TRY(ex.gemm(g2), "single: lin1 mlp");
     RmsArgs rq{qkv, 3 * C, all, rows, m.H, m.d, 0, s.q_g, m.ln_eps};
-    HIP_TRY(rms_heads(dt, rq, st), "single: q norm");
+    HIP_TRY(ex.rms(rq), "single: q norm");
     RmsArgs rk{qkv, 3 * C, all, rows, m.H, m.d, C, s.k_g, m.ln_eps};
-    HIP_TRY(rms_heads(dt, rk, st), "single: k norm");
+    HIP_TRY(ex.rms(rk), "single: k norm");
     aa.out = att; aa.ldo = ldy;
-    HIP_TRY(attention(dt, aa, st), "single: attention");
+    HIP_TRY(ex.attention(aa), "single: attention");
     GemmArgs g3 = gemm_args(att, ldy, all, s.lin2_w, s.lin2_b, rows, C, C + Mh, EPI_GATED, h, C, all);
     g3.resid = u; g3.ldr = C; g3.resid_f32 = 0; g3.gate = mod + 2 * C; g3.ldg = 3 * C;
-    HIP_TRY(gemm(dt, g3, st), "single: lin2");
+    HIP_TRY(ex.gemm(g3), "single: lin2");
     return FF_OK;
   }
 
@@ -234,21 +315,21 @@ ff_status exec_block(const Model& m, int kind, const ff_layer_weights& w, const 
     const int rows = m.B * nseg[si];
     float* ms = mod + 6 * C * si;
     GemvArgs gv{cs, C, 0, s.mod_w, s.mod_b, 6 * C, C, m.B, ms, ldm, 0, nullptr, 0};
-    HIP_TRY(gemv(dt, gv, st), "block: modulation");
+    HIP_TRY(ex.gemv(gv), "block: modulation");
     if (rows == 0) continue;
     LnModArgs ln{u, 0, C, maps[si], rows, C, m.ln_eps, ms, ms + C, ldm, lna, C};
-    HIP_TRY(ln_modulate(dt, ln, st), "block: ln1");
+    HIP_TRY(ex.ln(ln), "block: ln1");
     GemmArgs g = gemm_args(lna, C, maps[si], s.qkv_w, s.qkv_b, rows, 3 * C, C, EPI_BIAS, qkv, 3 * C, maps[si]);
-    HIP_TRY(gemm(dt, g, st), "block: qkv");
+    HIP_TRY(ex.gemm(g), "block: qkv");
     if (kind == FF_MMDIT_DOUBLE) {
       RmsArgs rq{qkv, 3 * C, maps[si], rows, m.H, m.d, 0, s.q_g, m.ln_eps};
-      HIP_TRY(rms_heads(dt, rq, st), "double: q norm");
+      HIP_TRY(ex.rms(rq), "double: q norm");
       RmsArgs rk{qkv, 3 * C, maps[si], rows, m.H, m.d, C, s.k_g, m.ln_eps};
-      HIP_TRY(rms_heads(dt, rk, st), "double: k norm");
+      HIP_TRY(ex.rms(rk), "double: k norm");
     }
   }
   aa.out = att; aa.ldo = C;
-  HIP_TRY(attention(dt, aa, st), "block: attention");
+  HIP_TRY(ex.attention(aa), "block: attention");
   for (int si = 0; si < nstreams; ++si) {
     const ff_stream_weights& s = w.s[si];
     const int rows = m.B * nseg[si];
@@ -256,14 +337,14 @@ ff_status exec_block(const Model& m, int kind, const ff_layer_weights& w, const 
     float* ms = mod + 6 * C * si;
     GemmArgs go = gemm_args(att, C, maps[si], s.o_w, s.o_b, rows, C, C, EPI_GATED, x1f, C, maps[si]);
     go.out_f32 = 1; go.resid = u; go.ldr = C; go.resid_f32 = 0; go.gate = ms + 2 * C; go.ldg = ldm;
-    HIP_TRY(gemm(dt, go, st), "block: proj");
+    HIP_TRY(ex.gemm(go), "block: proj");
     LnModArgs ln{x1f, 1, C, maps[si], rows, C, m.ln_eps, ms + 3 * C, ms + 4 * C, ldm, lna, C};
-    HIP_TRY(ln_modulate(dt, ln, st), "block: ln2");
+    HIP_TRY(ex.ln(ln), "block: ln2");
     GemmArgs g1 = gemm_args(lna, C, maps[si], s.fc1_w, s.fc1_b, rows, Mh, C, EPI_BIAS_GELU, hid, Mh, maps[si]);
-    HIP_TRY(gemm(dt, g1, st), "block: fc1");
+    HIP_TRY(ex.gemm(g1), "block: fc1");
     GemmArgs g2 = gemm_args(hid, Mh, maps[si], s.fc2_w, s.fc2_b, rows, C, Mh, EPI_GATED, h, C, maps[si]);
     g2.resid = x1f; g2.ldr = C; g2.resid_f32 = 1; g2.gate = ms + 5 * C; g2.ldg = ldm;
-    HIP_TRY(gemm(dt, g2, st), "block: fc2");
+    HIP_TRY(ex.gemm(g2), "block: fc2");
   }
   return FF_OK;
 }
@@ -289,6 +370,7 @@ struct ff_ctx {
   int next_step;
   std::vector<uint8_t> written;  // [L * S]: slot holds a refresh of this run
   ff_counts counts;
+  Prof prof;
 };
 
 namespace {
@@ -483,10 +565,10 @@ ff_status ff_block_exact(const ff_model_desc* m, int32_t layer, const ff_layer_w
     const char *pu = (const char*)u, *ph = (const char*)h, *pw = (const char*)ws;
     if ((ph < pu + tb && pu < ph + tb) || (ph < pw + L.total && pw < ph + tb))
       return fail(FF_E_SHAPE, "h overlaps u or the workspace");
-    hipStream_t st = reinterpret_cast<hipStream_t>(stream);
+    Exec ex{reinterpret_cast<hipStream_t>(stream), nullptr, md.dtype, md.es()};
     float* cs = at<float>(ws, L.CS);
-    HIP_TRY(silu_rows(c_t, cs, md.B, md.C, st), "block: silu(c_t)");
-    e = exec_block(md, md.kinds[layer], *w, cs, u, h, ws, st);
+    HIP_TRY(silu_rows(c_t, cs, md.B, md.C, ex.st), "block: silu(c_t)");
+    e = exec_block(md, md.kinds[layer], *w, cs, u, h, ws, ex);
     if (e) return e;
     return ok();
   } catch (...) {
@@ -629,7 +711,8 @@ ff_status ff_denoise_step(ff_ctx* c, int32_t step, float* x, const float* cond, 
         }
       }
     }
-    hipStream_t st = reinterpret_cast<hipStream_t>(stream);
+    Exec ex{reinterpret_cast<hipStream_t>(stream), &c->prof, m.dtype, m.es()};
+    hipStream_t st = ex.st;
     const Ws W = ws_layout(m);
     void* ws = c->ws;
     const int C = m.C, dt = m.dtype;
@@ -641,41 +724,44 @@ ff_status ff_denoise_step(ff_ctx* c, int32_t step, float* x, const float* cond, 
     float* ct = at<float>(ws, W.CT);
     float* cs = at<float>(ws, W.CS);
     // conditioning: c_t = cond + W_t2 SiLU(W_t1 phi(1000 t) + b_t1) + b_t2
-    HIP_TRY(time_embed(1000.0 * t_i, phi, st), "time embedding");
+    HIP_TRY(ex.other(FF_TEMB_DIM * 4.0, [&] { return time_embed(1000.0 * t_i, phi, st); }), "time embedding");
     GemvArgs g1{phi, 0, 0, c->g.t1_w, c->g.t1_b, C, FF_TEMB_DIM, m.B, tmp, C, 1, nullptr, 0};
-    HIP_TRY(gemv(dt, g1, st), "time mlp 1");
+    HIP_TRY(ex.gemv(g1), "time mlp 1");
     GemvArgs g2{tmp, C, 0, c->g.t2_w, c->g.t2_b, C, C, m.B, ct, C, 0, cond, C};
-    HIP_TRY(gemv(dt, g2, st), "time mlp 2");
-    HIP_TRY(silu_rows(ct, cs, m.B, C, st), "silu(c_t)");
+    HIP_TRY(ex.gemv(g2), "time mlp 2");
+    HIP_TRY(ex.other(8.0 * m.B * C, [&] { return silu_rows(ct, cs, m.B, C, st); }), "silu(c_t)");
     // tokens: X = [txt ; patch_embed(patchify(x))]
     PatchGeom pg{m.B, m.lat_c, m.lat_f, m.lat_h, m.lat_w, m.pt, m.ph, m.pw};
     void* patches = at(ws, W.PATCH);
-    HIP_TRY(patchify(dt, x, patches, pg, st), "patchify");
+    const double lat_elems = (double)m.B * m.n_img * m.P;
+    HIP_TRY(ex.other(lat_elems * (4 + es), [&] { return patchify(dt, x, patches, pg, st); }), "patchify");
     void* cur = at(ws, W.X0);
     void* alt = at(ws, W.X1);
     const RowMap img{m.n_img, m.N, m.n_txt};
     const RowMap ident{m.B * m.n_img, m.B * m.n_img, 0};
     GemmArgs pe = gemm_args(patches, m.P, ident, c->g.pe_w, c->g.pe_b, m.B * m.n_img, C, m.P, EPI_BIAS, cur, C, img);
-    HIP_TRY(gemm(dt, pe, st), "patch embed");
-    if (m.n_txt > 0) HIP_TRY(copy_rows(dt, txt, cur, m.B, m.n_txt, m.N, 0, C, st), "text rows");
+    HIP_TRY(ex.gemm(pe), "patch embed");
+    if (m.n_txt > 0)
+      HIP_TRY(ex.other(2.0 * m.B * m.n_txt * C * es, [&] { return copy_rows(dt, txt, cur, m.B, m.n_txt, m.N, 0, C, st); }),
+              "text rows");
     // layers by the plan
     const int mode = s.mode;
     const bool resid = s.feature_mode == FF_RESIDUAL;
     for (int l = 0; l < L; ++l) {
       const int act = p.action[(size_t)i * L + l];
       if (act == FF_ACT_EXACT) {
-        ff_status e = exec_block(m, m.kinds[l], c->lw[l], cs, cur, alt, ws, st);
+        ff_status e = exec_block(m, m.kinds[l], c->lw[l], cs, cur, alt, ws, ex);
         if (e) return e;
         if (mode != FF_VANILLA) {
           const int sl = p.write_slot[i];
           void* dst = (char*)c->cache + ((size_t)l * S + sl) * tb;
-          HIP_TRY(ff::cache_update(dt, dst, resid ? cur : nullptr, alt, E, st), "cache update");
+          HIP_TRY(ex.cache(dst, resid ? cur : nullptr, alt, E), "cache update");
         }
         void* t = cur; cur = alt; alt = t;
         continue;
       }
       if (act == FF_ACT_SITE && mode == FF_EXACT_ONLY) {
-        ff_status e = exec_block(m, m.kinds[l], c->lw[l], cs, cur, alt, ws, st);
+        ff_status e = exec_block(m, m.kinds[l], c->lw[l], cs, cur, alt, ws, ex);
         if (e) return e;
         void* t = cur; cur = alt; alt = t;
         continue;
@@ -688,29 +774,30 @@ ff_status ff_denoise_step(ff_ctx* c, int32_t step, float* x, const float* cond, 
         tm.c[q] = p.coeffs[(size_t)i * (K + 1) + q];
       }
       if (act == FF_ACT_DRAFT) {
-        HIP_TRY(ff::draft(dt, tm, resid ? cur : nullptr, cur, E, st), "draft");
+        HIP_TRY(ex.draft(tm, resid ? cur : nullptr, cur, E), "draft");
         continue;
       }
       // paid site: exact output from the same incoming state, then verify + forward
       void* hf = at(ws, W.HF);
-      ff_status e = exec_block(m, m.kinds[l], c->lw[l], cs, cur, hf, ws, st);
+      ff_status e = exec_block(m, m.kinds[l], c->lw[l], cs, cur, hf, ws, ex);
       if (e) return e;
       float* rel = audit ? audit + ((size_t)i * L + l) * m.B : nullptr;
-      HIP_TRY(ff::verify(dt, tm, resid ? cur : nullptr, hf, cur, mode == FF_FEATFIX ? 1 : 0, m.B, (size_t)m.N * C,
-                         s.eps, rel, at<float>(ws, W.PART), st), "verify");
+      HIP_TRY(ex.verify(tm, resid ? cur : nullptr, hf, cur, mode == FF_FEATFIX ? 1 : 0, m.B, (size_t)m.N * C, s.eps,
+                        rel, at<float>(ws, W.PART)), "verify");
     }
     // final layer on the image rows, unpatchify and Euler
     float* mod = at<float>(ws, W.MOD);
     GemvArgs gf{cs, C, 0, c->g.fmod_w, c->g.fmod_b, 2 * C, C, m.B, mod, 2 * C, 0, nullptr, 0};
-    HIP_TRY(gemv(dt, gf, st), "final modulation");
+    HIP_TRY(ex.gemv(gf), "final modulation");
     void* lna = at(ws, W.LNA);
     LnModArgs ln{cur, 0, C, img, m.B * m.n_img, C, m.ln_eps, mod, mod + C, 2 * C, lna, C};
-    HIP_TRY(ln_modulate(dt, ln, st), "final ln");
+    HIP_TRY(ex.ln(ln), "final ln");
     float* yf = at<float>(ws, W.YF);
     GemmArgs gfl = gemm_args(lna, C, img, c->g.f_w, c->g.f_b, m.B * m.n_img, m.P, C, EPI_BIAS, yf, m.P, ident);
     gfl.out_f32 = 1;
-    HIP_TRY(gemm(dt, gfl, st), "final linear");
-    HIP_TRY(unpatchify_euler(yf, x, (float)(t_n - t_i), pg, st), "unpatchify + euler");
+    HIP_TRY(ex.gemm(gfl), "final linear");
+    HIP_TRY(ex.other(lat_elems * 12.0, [&] { return unpatchify_euler(yf, x, (float)(t_n - t_i), pg, st); }),
+            "unpatchify + euler");
     // bookkeeping after a successful enqueue
     if (p.step_kind[i] == FF_STEP_REFRESH) {
       c->counts.n_full_refresh++;
@@ -728,6 +815,32 @@ ff_status ff_denoise_step(ff_ctx* c, int32_t step, float* x, const float* cond, 
   } catch (...) {
     return fail(FF_E_UNSUPPORTED, "unexpected host exception");
   }
+}
+
+ff_status ff_ctx_profile(ff_ctx* c, int32_t enable) {
+  if (!c) return fail(FF_E_NULL, "ctx is NULL");
+  c->prof.on = enable != 0;
+  c->prof.recs.clear();
+  c->prof.next = 0;
+  return ok();
+}
+
+ff_status ff_ctx_profile_read(ff_ctx* c, ff_prof_stat* out) {
+  if (!c || !out) return fail(FF_E_NULL, "ctx or out is NULL");
+  for (int k = 0; k < FF_PROF_NCLASS; ++k) out[k] = ff_prof_stat{0, 0.0, 0.0, 0.0};
+  for (const Prof::Rec& r : c->prof.recs) {
+    HIP_TRY(hipEventSynchronize(r.b), "profile: event sync");
+    float ms = 0.f;
+    HIP_TRY(hipEventElapsedTime(&ms, r.a, r.b), "profile: elapsed");
+    ff_prof_stat& o = out[r.cls];
+    o.launches++;
+    o.ms += ms;
+    o.flops += r.flops;
+    o.bytes += r.bytes;
+  }
+  c->prof.recs.clear();
+  c->prof.next = 0;
+  return ok();
 }
 
 }  // extern "C"

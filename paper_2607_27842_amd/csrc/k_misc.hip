@@ -107,42 +107,75 @@ __global__ __launch_bounds__(256) void k_rms_heads(RmsArgs a) {
 }
 
 constexpr int kGemvMaxB = 8;
+constexpr int kGemvRows = 4;     // output features per wavefront
+constexpr int kGemvKC = 2048;    // K chunk of the activations staged in LDS
 
-// One wavefront per output feature n; lanes stride over K in 16-byte chunks of W.
+// y[b, n] for 16 consecutive n per workgroup (4 per wavefront).  The activations x[b, k]
+// (after the optional SiLU) are staged in LDS once per K chunk and shared by all rows;
+// each lane streams 16-byte chunks of the weight rows (consecutive lanes -> consecutive
+// chunks) and keeps one accumulator per (row, sample).
 template <int DT>
 __global__ __launch_bounds__(256) void k_gemv(GemvArgs a) {
   using S = St<DT>;
-  const int lane = threadIdx.x % 64;
-  const int n = blockIdx.x * 4 + threadIdx.x / 64;
-  if (n >= a.Nout) return;
-  float acc[kGemvMaxB];
+  extern __shared__ float xs[];   // [B][kGemvKC]
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int n0 = (blockIdx.x * 4 + wave) * kGemvRows;
+  float acc[kGemvRows][kGemvMaxB];
 #pragma unroll
-  for (int b = 0; b < kGemvMaxB; ++b) acc[b] = 0.f;
-  const int chunks = a.K / S::V;
-  for (int c = lane; c < chunks; c += 64) {
-    float w[S::V];
-    S::load(a.W, (size_t)n * a.K + c * S::V, w);
+  for (int r = 0; r < kGemvRows; ++r)
 #pragma unroll
-    for (int b = 0; b < kGemvMaxB; ++b) {
-      if (b < a.B) {
-        const float* xr = a.x + (size_t)b * a.ldx + c * S::V;
+    for (int b = 0; b < kGemvMaxB; ++b) acc[r][b] = 0.f;
+  for (int k0 = 0; k0 < a.K; k0 += kGemvKC) {
+    const int kc = min(kGemvKC, a.K - k0);
+    __syncthreads();
+    for (int i = threadIdx.x; i < a.B * kc; i += 256) {
+      const int b = i / kc, k = i % kc;
+      float v = a.x[(size_t)b * a.ldx + k0 + k];
+      if (a.silu_in) v = silu_f(v);
+      xs[b * kGemvKC + k] = v;
+    }
+    __syncthreads();
+    for (int c = lane; c < kc / S::V; c += 64) {
+      float w[kGemvRows][S::V];
 #pragma unroll
-        for (int j = 0; j < S::V; ++j) {
-          float xv = xr[j];
-          if (a.silu_in) xv = silu_f(xv);
-          acc[b] = fmaf(xv, w[j], acc[b]);
+      for (int r = 0; r < kGemvRows; ++r) {
+        if (n0 + r < a.Nout) {
+          S::load(a.W, (size_t)(n0 + r) * a.K + k0 + c * S::V, w[r]);
+        } else {
+#pragma unroll
+          for (int j = 0; j < S::V; ++j) w[r][j] = 0.f;
+        }
+      }
+#pragma unroll
+      for (int b = 0; b < kGemvMaxB; ++b) {
+        if (b < a.B) {
+          float xv[S::V];
+#pragma unroll
+          for (int j = 0; j < S::V; j += 4) {
+            const float4 q = *reinterpret_cast<const float4*>(&xs[b * kGemvKC + c * S::V + j]);
+            xv[j] = q.x; xv[j + 1] = q.y; xv[j + 2] = q.z; xv[j + 3] = q.w;
+          }
+#pragma unroll
+          for (int r = 0; r < kGemvRows; ++r)
+#pragma unroll
+            for (int j = 0; j < S::V; ++j) acc[r][b] = fmaf(xv[j], w[r][j], acc[r][b]);
         }
       }
     }
   }
-  const float bias = S::ld1(a.bias, n);
 #pragma unroll
-  for (int b = 0; b < kGemvMaxB; ++b) {
-    if (b < a.B) {
-      float y = wave_sum(acc[b]) + bias;
-      if (a.silu_out) y = silu_f(y);
-      if (a.add) y += a.add[(size_t)b * a.ldadd + n];
-      if (lane == 0) a.y[(size_t)b * a.ldy + n] = y;
+  for (int r = 0; r < kGemvRows; ++r) {
+    const int n = n0 + r;
+    if (n >= a.Nout) break;
+    const float bias = S::ld1(a.bias, n);
+#pragma unroll
+    for (int b = 0; b < kGemvMaxB; ++b) {
+      if (b < a.B) {
+        float y = wave_sum(acc[r][b]) + bias;
+        if (a.silu_out) y = silu_f(y);
+        if (a.add) y += a.add[(size_t)b * a.ldadd + n];
+        if (lane == 0) a.y[(size_t)b * a.ldy + n] = y;
+      }
     }
   }
 }
@@ -221,9 +254,10 @@ hipError_t rms_heads(int dtype, const RmsArgs& a, hipStream_t s) {
 }
 
 hipError_t gemv(int dtype, const GemvArgs& a, hipStream_t s) {
-  const int grid = cdiv(a.Nout, 4);
-  if (dtype == DT_BF16) hipLaunchKernelGGL(k_gemv<DT_BF16>, grid, 256, 0, s, a);
-  else hipLaunchKernelGGL(k_gemv<DT_F32>, grid, 256, 0, s, a);
+  const int grid = cdiv(a.Nout, 4 * kGemvRows);
+  const size_t lds = (size_t)a.B * kGemvKC * sizeof(float);
+  if (dtype == DT_BF16) hipLaunchKernelGGL(k_gemv<DT_BF16>, grid, 256, lds, s, a);
+  else hipLaunchKernelGGL(k_gemv<DT_F32>, grid, 256, lds, s, a);
   return hipGetLastError();
 }
 

@@ -119,12 +119,14 @@ def site_mask(cfg: dict, sites=None) -> np.ndarray:
 def to_bf16_values(a: np.ndarray) -> np.ndarray:
     """Round fp32 values to the nearest bf16 (ties to even); returns fp32 holding bf16 values."""
     a = np.ascontiguousarray(a, dtype=np.float32)
-    u = a.view(np.uint32).astype(np.uint64)
-    r = ((u + 0x7FFF + ((u >> 16) & 1)) >> 16) << 16
-    out = r.astype(np.uint32).view(np.float32)
+    u = a.view(np.uint32)
+    r = (u >> 16) & np.uint32(1)          # finite values cannot overflow uint32 below
+    r += np.uint32(0x7FFF)
+    r += u
+    r &= np.uint32(0xFFFF0000)
+    out = r.view(np.float32)
     nan = np.isnan(a)
     if nan.any():
-        out = out.copy()
         out[nan] = np.nan
     return out
 
@@ -134,7 +136,9 @@ def _rng(*key):
 
 
 def _normal(shape, std, *key):
-    return (_rng(*key).standard_normal(shape, dtype=np.float32) * np.float32(std)).astype(np.float32)
+    a = _rng(*key).standard_normal(shape, dtype=np.float32)
+    a *= np.float32(std)
+    return a
 
 
 # Tensor ids inside one layer's weight set; used to seed one PCG64 stream per tensor so a
