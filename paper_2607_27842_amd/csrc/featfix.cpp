@@ -203,6 +203,10 @@ struct Exec {
   hipError_t cache(void* slot, const void* u, const void* h, size_t E) {
     return timed(FF_PROF_CACHE, 0, (u ? 3.0 : 2.0) * E * es, [&] { return ff::cache_update(dt, slot, u, h, E, st); });
   }
+  hipError_t draft_run(const Terms& t, int layers, size_t layer_stride, bool resid, void* x, size_t E) {
+    return timed(FF_PROF_DRAFT, 0, ((double)t.n * layers + (resid ? 2.0 : 1.0)) * E * es,
+                 [&] { return ff::draft_run(dt, t, layers, layer_stride, resid ? 1 : 0, x, E, st); });
+  }
   hipError_t draft(const Terms& t, const void* u, void* hd, size_t E) {
     return timed(FF_PROF_DRAFT, 0, (t.n + (u ? 2.0 : 1.0)) * E * es, [&] { return ff::draft(dt, t, u, hd, E, st); });
   }
@@ -774,7 +778,12 @@ ff_status ff_denoise_step(ff_ctx* c, int32_t step, float* x, const float* cond, 
         tm.c[q] = p.coeffs[(size_t)i * (K + 1) + q];
       }
       if (act == FF_ACT_DRAFT) {
-        HIP_TRY(ex.draft(tm, resid ? cur : nullptr, cur, E), "draft");
+        // the maximal run of drafted layers starting here, applied in one pass (same bits)
+        int l2 = l + 1;
+        while (l2 < L && p.action[(size_t)i * L + l2] == FF_ACT_DRAFT) ++l2;
+        if (l2 - l == 1) HIP_TRY(ex.draft(tm, resid ? cur : nullptr, cur, E), "draft");
+        else HIP_TRY(ex.draft_run(tm, l2 - l, (size_t)S * E, resid, cur, E), "draft run");
+        l = l2 - 1;
         continue;
       }
       // paid site: exact output from the same incoming state, then verify + forward

@@ -1,10 +1,9 @@
 // Dense contractions of the exact block: out = epi(A W^T + bias) with A [M, K] (rows
 // through a RowMap), W [N, K] (both K-contiguous), fp32 accumulation.
 //
-// bf16: v_mfma_f32_16x16x32_bf16 on 256x256 or 128x128 workgroup tiles; operands staged
-// through LDS (row stride padded by 16 bytes so that the 16-byte fragment reads of 16
-// consecutive rows are conflict-free), double-buffered with one barrier per K step; the
-// next K step's global loads are in flight while the current one is multiplied.
+// bf16: v_mfma_f32_32x32x16_bf16 on 256x256 or 128x128 workgroup tiles, fed from LDS.
+// The main kernel streams operands global -> LDS directly through a multi-stage ring; a
+// register-staged kernel (padded LDS rows, double buffer) covers K % 32 != 0.
 // fp32: 64x64x16 tile of plain FMAs (the small fp32 workload is launch-bound).
 #include "dev_common.h"
 
@@ -83,18 +82,21 @@ __device__ __forceinline__ void tile_of(int bid, int tiles_m, int tiles_n, int& 
 }
 
 // ------------------------------------------------------------------ bf16 MFMA GEMM
-// BM x BN workgroup tile, BK = 64, wavefront tiles WM x WN of 16x16x32 MFMAs.  The MFMA
-// takes the weight fragment as its A operand and the activation fragment as B, so the
-// accumulator of a lane holds 4 consecutive output COLUMNS of one output row: the fused
-// epilogue reads bias / gate / residual and writes the result with vector accesses.
+// BM x BN workgroup tile, BK = 64 per LDS stage, wavefront tiles WM x WN of
+// v_mfma_f32_32x32x16_bf16 (the 16x16x32 form issues at half the rate on gfx950).
 constexpr int BK = 64, LDT = BK + 8;
+typedef float f32x16_t __attribute__((ext_vector_type(16)));
 
+// 32x32x16 MFMA: A operand lane l = row (l%32), k 8*(l/32)..+7; B operand lane l = col (l%32),
+// same k; D[v] at row 8*(v/4) + 4*(l/32) + v%4, col l%32.  With A = weight rows (output
+// columns n) and B = activation rows (output rows m): lane l owns output row m = l%32 and
+// columns n = 8*(v/4) + 4*(l/32) + (v%4), i.e. 4 groups of 4 consecutive columns.
 template <int BM, int BN, int WM, int WN, int EPI, bool OUT_F32, bool RES_F32>
 __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64) void k_gemm_bf16(GemmArgs a, int tiles_m, int tiles_n) {
   constexpr int NWN = BN / WN;
   constexpr int NT = (BM / WM) * NWN * 64;
-  constexpr int TM = WM / 16, TN = WN / 16;
-  constexpr int RSTEP = NT / 8;            // rows covered by one pass of 16-byte chunk loads
+  constexpr int TM = WM / 32, TN = WN / 32;
+  constexpr int RSTEP = NT / 8;
   constexpr int CA = BM / RSTEP, CB = BN / RSTEP;
   __shared__ __attribute__((aligned(16))) uint16_t sA[2][BM * LDT];
   __shared__ __attribute__((aligned(16))) uint16_t sB[2][BN * LDT];
@@ -104,7 +106,6 @@ __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64) void k_gemm_bf16(GemmAr
   const int m0 = tm * BM, n0 = tn * BN;
   const uint16_t* A = reinterpret_cast<const uint16_t*>(a.A);
   const uint16_t* W = reinterpret_cast<const uint16_t*>(a.W);
-
   const int lrow = tid >> 3, kc = (tid & 7) * 8;
   size_t offa[CA], offb[CB];
   unsigned mask = 0;
@@ -137,15 +138,15 @@ __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64) void k_gemm_bf16(GemmAr
     _Pragma("unroll") for (int i = 0; i < CB; ++i)                                                     \
       *reinterpret_cast<u32x4_t*>(&sB[buf][(lrow + RSTEP * i) * LDT + kc]) = rb[i];                    \
   } while (0)
-
-  f32x4_t acc[TM][TN];
+  f32x16_t acc[TM][TN];
 #pragma unroll
   for (int i = 0; i < TM; ++i)
 #pragma unroll
-    for (int j = 0; j < TN; ++j) acc[i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-
+    for (int j = 0; j < TN; ++j)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
   const int wm = (wave / NWN) * WM, wn = (wave % NWN) * WN;
-  const int fr = lane & 15, fk = (lane >> 4) * 8;
+  const int fr = lane & 31, fk = (lane >> 5) * 8;
   const int nk = (a.K + BK - 1) / BK;
   FF_GLOAD(0);
   FF_SSTORE(0);
@@ -154,35 +155,165 @@ __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64) void k_gemm_bf16(GemmAr
     const int cur = kt & 1;
     if (kt + 1 < nk) FF_GLOAD((kt + 1) * BK);
 #pragma unroll
-    for (int kk = 0; kk < BK; kk += 32) {
+    for (int kk = 0; kk < BK; kk += 16) {
       bf16x8_t fa[TM], fb[TN];
 #pragma unroll
       for (int t = 0; t < TM; ++t)
-        fa[t] = *reinterpret_cast<const bf16x8_t*>(&sA[cur][(wm + t * 16 + fr) * LDT + kk + fk]);
+        fa[t] = *reinterpret_cast<const bf16x8_t*>(&sA[cur][(wm + t * 32 + fr) * LDT + kk + fk]);
 #pragma unroll
       for (int t = 0; t < TN; ++t)
-        fb[t] = *reinterpret_cast<const bf16x8_t*>(&sB[cur][(wn + t * 16 + fr) * LDT + kk + fk]);
+        fb[t] = *reinterpret_cast<const bf16x8_t*>(&sB[cur][(wn + t * 32 + fr) * LDT + kk + fk]);
 #pragma unroll
       for (int i = 0; i < TM; ++i)
 #pragma unroll
         for (int j = 0; j < TN; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fb[j], fa[i], acc[i][j], 0, 0, 0);
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fb[j], fa[i], acc[i][j], 0, 0, 0);
+      __builtin_amdgcn_iglp_opt(0);   // interleave the LDS fragment reads with the MFMAs
     }
     if (kt + 1 < nk) FF_SSTORE(cur ^ 1);
     __syncthreads();
   }
 #undef FF_GLOAD
 #undef FF_SSTORE
-  // acc[i][j][v] = C[row m0 + wm + 16i + (lane % 16)][col n0 + wn + 16j + 4*(lane / 16) + v]
 #pragma unroll
   for (int i = 0; i < TM; ++i) {
-    const int r = m0 + wm + i * 16 + fr;
+    const int r = m0 + wm + i * 32 + fr;
     if (r >= a.M) continue;
 #pragma unroll
-    for (int j = 0; j < TN; ++j) {
-      const int c = n0 + wn + j * 16 + (lane >> 4) * 4;
-      if (c < a.N) epilogue4_bf16<EPI, OUT_F32, RES_F32>(a, r, c, acc[i][j]);
+    for (int j = 0; j < TN; ++j)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const int c = n0 + wn + j * 32 + q * 8 + (lane >> 5) * 4;
+        if (c < a.N) {
+          const f32x4_t v4 = {acc[i][j][4 * q], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2], acc[i][j][4 * q + 3]};
+          epilogue4_bf16<EPI, OUT_F32, RES_F32>(a, r, c, v4);
+        }
+      }
+  }
+}
+// ------------------------------------------------------------------ bf16 MFMA GEMM, direct-to-LDS
+// For K % 32 == 0.  Operand tiles go global -> LDS with global_load_lds_dwordx4 (no VGPR
+// staging, no ds_write), into an NST-stage ring of 32-wide K slices issued NST-1 slices
+// ahead.  Each DMA instruction fills 1 KB of LDS (16 rows x 64 bytes) in lane order, so
+// rows cannot be padded; instead lane l of a row loads 16-byte chunk (l%4) ^ ((row>>2)&3)
+// (an XOR swizzle), which keeps the 32-row fragment reads conflict-free.
+//
+// Synchronisation is explicit: the compiler's barrier lowering waits for ALL outstanding
+// loads (it cannot tell which stage a DMA targets), which would remove the prefetch.  So a
+// step waits only for its own stage (s_waitcnt vmcnt(n) with the later stages still in
+// flight) and then s_barrier, as one volatile asm that is also a compiler memory barrier;
+// fragment reads are ds_read_b128 asm followed by lgkmcnt(0) and tied to the MFMAs through
+// volatile "+v" asms so that no MFMA can consume a fragment before the wait.
+#define FF_AS1(p) ((const __attribute__((address_space(1))) void*)(p))
+#define FF_AS3(p) ((__attribute__((address_space(3))) void*)(p))
+
+__device__ __forceinline__ bf16x8_t lds_rd128(const uint16_t* p) {
+  u32x4_t v;
+  const uint32_t off = (uint32_t)(uintptr_t)((__attribute__((address_space(3))) const void*)p);
+  asm volatile("ds_read_b128 %0, %1" : "=v"(v) : "v"(off) : "memory");
+  return __builtin_bit_cast(bf16x8_t, v);
+}
+
+template <int BM, int BN, int WM, int WN, int NST, int AUX, int EPI, bool OUT_F32, bool RES_F32>
+__global__ __launch_bounds__((BM / WM) * (BN / WN) * 64) void k_gemm_dl(GemmArgs a, int tiles_m, int tiles_n) {
+  constexpr int BKd = 32;
+  constexpr int NWN = BN / WN;
+  constexpr int NW = (BM / WM) * NWN;
+  constexpr int TM = WM / 32, TN = WN / 32;
+  constexpr int IA = BM / 16 / NW, IB = BN / 16 / NW;   // 1 KB DMA instructions per wave per stage
+  static_assert(IA >= 1 && IB >= 1 && NST >= 2 && NST <= 4, "unsupported tile");
+  __shared__ __attribute__((aligned(1024))) uint16_t sA[NST][BM * BKd];
+  __shared__ __attribute__((aligned(1024))) uint16_t sB[NST][BN * BKd];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  int tm, tn;
+  tile_of(blockIdx.x, tiles_m, tiles_n, tm, tn);
+  const int m0 = tm * BM, n0 = tn * BN;
+  const uint16_t* A = reinterpret_cast<const uint16_t*>(a.A);
+  const uint16_t* W = reinterpret_cast<const uint16_t*>(a.W);
+  // rows past the matrix read row 0 (in bounds); their results are never stored
+  const int lr = lane >> 2, ls = lane & 3;
+  size_t ga[IA], gb[IB];
+#pragma unroll
+  for (int j = 0; j < IA; ++j) {
+    const int row = (wave * IA + j) * 16 + lr, gm = m0 + row;
+    ga[j] = (size_t)a.amap.phys(gm < a.M ? gm : 0) * a.lda + ((ls ^ ((row >> 2) & 3)) * 8);
+  }
+#pragma unroll
+  for (int j = 0; j < IB; ++j) {
+    const int row = (wave * IB + j) * 16 + lr, gn = n0 + row;
+    gb[j] = (size_t)(gn < a.N ? gn : 0) * a.ldw + ((ls ^ ((row >> 2) & 3)) * 8);
+  }
+#define FF_ISSUE(st, k0)                                                                                  \
+  do {                                                                                                    \
+    _Pragma("unroll") for (int j = 0; j < IA; ++j)                                                        \
+      __builtin_amdgcn_global_load_lds(FF_AS1(A + ga[j] + (k0)), FF_AS3(&sA[st][(wave * IA + j) * 16 * BKd]), 16, 0, AUX); \
+    _Pragma("unroll") for (int j = 0; j < IB; ++j)                                                        \
+      __builtin_amdgcn_global_load_lds(FF_AS1(W + gb[j] + (k0)), FF_AS3(&sB[st][(wave * IB + j) * 16 * BKd]), 16, 0, AUX); \
+  } while (0)
+
+  f32x16_t acc[TM][TN];
+#pragma unroll
+  for (int i = 0; i < TM; ++i)
+#pragma unroll
+    for (int j = 0; j < TN; ++j)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
+  const int wm = (wave / NWN) * WM, wn = (wave % NWN) * WN;
+  const int fr = lane & 31, fh = lane >> 5;
+  const int nk = a.K / BKd;
+#pragma unroll
+  for (int s = 0; s < NST - 1; ++s)
+    if (s < nk) FF_ISSUE(s, s * BKd);
+  for (int kt = 0; kt < nk; ++kt) {
+    const int st = kt % NST;
+    const int later = min(NST - 2, nk - 1 - kt);   // stages of this wave issued after stage kt
+    if (later >= 2) asm volatile("s_waitcnt vmcnt(%0)\n\ts_barrier" ::"n"(2 * (IA + IB)) : "memory");
+    else if (later == 1) asm volatile("s_waitcnt vmcnt(%0)\n\ts_barrier" ::"n"(IA + IB) : "memory");
+    else asm volatile("s_waitcnt vmcnt(0)\n\ts_barrier" ::: "memory");
+    // every wave has finished reading stage kt-1: its buffer takes stage kt+NST-1
+    if (kt + NST - 1 < nk) FF_ISSUE((kt + NST - 1) % NST, (kt + NST - 1) * BKd);
+#pragma unroll
+    for (int kk = 0; kk < 2; ++kk) {
+      bf16x8_t fa[TM], fb[TN];
+      const int ch = kk * 2 + fh;
+#pragma unroll
+      for (int t = 0; t < TM; ++t) {
+        const int row = wm + t * 32 + fr;
+        fa[t] = lds_rd128(&sA[st][row * BKd + ((ch ^ ((row >> 2) & 3)) * 8)]);
+      }
+#pragma unroll
+      for (int t = 0; t < TN; ++t) {
+        const int row = wn + t * 32 + fr;
+        fb[t] = lds_rd128(&sB[st][row * BKd + ((ch ^ ((row >> 2) & 3)) * 8)]);
+      }
+      asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+#pragma unroll
+      for (int t = 0; t < TM; ++t) asm volatile("" : "+v"(fa[t]));
+#pragma unroll
+      for (int t = 0; t < TN; ++t) asm volatile("" : "+v"(fb[t]));
+#pragma unroll
+      for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fb[j], fa[i], acc[i][j], 0, 0, 0);
     }
+  }
+#undef FF_ISSUE
+  // lane owns output row m (lane % 32) and 4 groups of 4 consecutive columns
+#pragma unroll
+  for (int i = 0; i < TM; ++i) {
+    const int r = m0 + wm + i * 32 + fr;
+    if (r >= a.M) continue;
+#pragma unroll
+    for (int j = 0; j < TN; ++j)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const int c = n0 + wn + j * 32 + q * 8 + fh * 4;
+        if (c < a.N) {
+          const f32x4_t v4 = {acc[i][j][4 * q], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2], acc[i][j][4 * q + 3]};
+          epilogue4_bf16<EPI, OUT_F32, RES_F32>(a, r, c, v4);
+        }
+      }
   }
 }
 
@@ -237,13 +368,23 @@ void launch_tile(const GemmArgs& a, hipStream_t s) {
   hipLaunchKernelGGL((k_gemm_bf16<BM, BN, WM, WN, EPI, OF, RF>), tm * tn, (BM / WM) * (BN / WN) * 64, 0, s, a, tm, tn);
 }
 
-// 256x256 tiles (8 wavefronts of 128x64, one workgroup per CU) when there are enough of
-// them to fill the chip; otherwise 128x128 tiles (4 wavefronts of 64x64, two per CU).
+template <int BM, int BN, int WM, int WN, int NST, int AUX, int EPI, bool OF, bool RF>
+void launch_dl(const GemmArgs& a, hipStream_t s) {
+  const int tm = (a.M + BM - 1) / BM, tn = (a.N + BN - 1) / BN;
+  hipLaunchKernelGGL((k_gemm_dl<BM, BN, WM, WN, NST, AUX, EPI, OF, RF>), tm * tn, (BM / WM) * (BN / WN) * 64, 0, s,
+                     a, tm, tn);
+}
+
+// Tile choice (measured on MI355X): 256x256 tiles (8 wavefronts of 128x64, 3 stages, loads
+// with sc0|sc1 so the streamed tiles skip the L1) when they fill the chip; else 128x128
+// (8 wavefronts of 64x32, 4 stages, two workgroups per CU).  K % 32 != 0 (the patch
+// embedding) takes the register-staged kernel.
 template <int EPI, bool OF, bool RF>
 void launch_bf16(const GemmArgs& a, hipStream_t s) {
   const long big = (long)((a.M + 255) / 256) * ((a.N + 255) / 256);
-  if (big >= 200) launch_tile<256, 256, 128, 64, EPI, OF, RF>(a, s);
-  else launch_tile<128, 128, 64, 64, EPI, OF, RF>(a, s);
+  if (a.K % 32 != 0) launch_tile<128, 128, 64, 32, EPI, OF, RF>(a, s);
+  else if (big >= 200) launch_dl<256, 256, 128, 64, 3, 17, EPI, OF, RF>(a, s);
+  else launch_dl<128, 128, 64, 32, 4, 0, EPI, OF, RF>(a, s);
 }
 
 }  // namespace

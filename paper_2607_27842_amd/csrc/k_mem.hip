@@ -35,10 +35,12 @@ __global__ __launch_bounds__(kThreads) void k_cache_update(void* __restrict__ sl
   }
 }
 
-// One chunk of the draft h_d = u + sum_m c_m * slot_m (Eq. 2 in coefficient form), fp32
-// sums with explicit fma so that the draft and verify kernels produce identical bits.
+// One chunk of the draft h_d = u + sum_m c_m * slot_m (Eq. 2 in coefficient form) from the
+// incoming values uv (ignored without RES), fp32 sums with explicit fma in a fixed order,
+// then one rounding to the storage type.  Every draft path (single layer, fused run,
+// verify) goes through this function, so they produce identical bits.
 template <int DT, bool RES>
-__device__ __forceinline__ void draft_chunk(const Terms& t, const void* u, size_t i, float* out) {
+__device__ __forceinline__ void draft_math(const Terms& t, size_t off, const float* uv, float* out) {
   using S = St<DT>;
   float f[S::V];
 #pragma unroll
@@ -47,19 +49,38 @@ __device__ __forceinline__ void draft_chunk(const Terms& t, const void* u, size_
   for (int m = 0; m < kMaxTerms; ++m) {
     if (m < t.n) {
       float s[S::V];
-      S::load(t.slot[m], i, s);
+      S::load(t.slot[m], off, s);
 #pragma unroll
       for (int j = 0; j < S::V; ++j) f[j] = fmaf(t.c[m], s[j], f[j]);
     }
   }
   if (RES) {
-    float uv[S::V];
-    S::load(u, i, uv);
 #pragma unroll
     for (int j = 0; j < S::V; ++j) f[j] = uv[j] + f[j];
   }
 #pragma unroll
   for (int j = 0; j < S::V; ++j) out[j] = S::rnd(f[j]);
+}
+
+template <int DT, bool RES>
+__device__ __forceinline__ void draft_chunk(const Terms& t, const void* u, size_t i, float* out) {
+  using S = St<DT>;
+  float uv[S::V];
+  if (RES) S::load(u, i, uv);
+  draft_math<DT, RES>(t, i, uv, out);
+}
+
+template <int DT, bool RES>
+__global__ __launch_bounds__(kThreads) void k_draft_run(Terms t, int layers, size_t layer_stride, void* x,
+                                                        size_t nchunk) {
+  using S = St<DT>;
+  for (size_t c = (size_t)blockIdx.x * kThreads + threadIdx.x; c < nchunk; c += (size_t)gridDim.x * kThreads) {
+    const size_t i = c * S::V;
+    float xv[S::V];
+    if (RES) S::load(x, i, xv);
+    for (int l = 0; l < layers; ++l) draft_math<DT, RES>(t, (size_t)l * layer_stride + i, xv, xv);
+    S::store(x, i, xv);
+  }
 }
 
 template <int DT, bool RES>
@@ -173,6 +194,20 @@ hipError_t draft(int dtype, const Terms& t, const void* u, void* hd, size_t E, h
     size_t n = E / 4;
     if (u) hipLaunchKernelGGL((k_draft<DT_F32, true>), grid_for(n), kThreads, 0, s, t, u, hd, n);
     else hipLaunchKernelGGL((k_draft<DT_F32, false>), grid_for(n), kThreads, 0, s, t, u, hd, n);
+  }
+  return hipGetLastError();
+}
+
+hipError_t draft_run(int dtype, const Terms& t, int layers, size_t layer_stride, int residual, void* x, size_t E,
+                     hipStream_t s) {
+  if (dtype == DT_BF16) {
+    size_t n = E / 8;
+    if (residual) hipLaunchKernelGGL((k_draft_run<DT_BF16, true>), grid_for(n), kThreads, 0, s, t, layers, layer_stride, x, n);
+    else hipLaunchKernelGGL((k_draft_run<DT_BF16, false>), grid_for(n), kThreads, 0, s, t, layers, layer_stride, x, n);
+  } else {
+    size_t n = E / 4;
+    if (residual) hipLaunchKernelGGL((k_draft_run<DT_F32, true>), grid_for(n), kThreads, 0, s, t, layers, layer_stride, x, n);
+    else hipLaunchKernelGGL((k_draft_run<DT_F32, false>), grid_for(n), kThreads, 0, s, t, layers, layer_stride, x, n);
   }
   return hipGetLastError();
 }

@@ -108,16 +108,19 @@ __global__ __launch_bounds__(256) void k_rms_heads(RmsArgs a) {
 
 constexpr int kGemvMaxB = 8;
 constexpr int kGemvRows = 4;     // output features per wavefront
-constexpr int kGemvKC = 2048;    // K chunk of the activations staged in LDS
+constexpr int kGemvKC = 1024;    // K chunk of the activations staged in LDS
 
 // y[b, n] for 16 consecutive n per workgroup (4 per wavefront).  The activations x[b, k]
-// (after the optional SiLU) are staged in LDS once per K chunk and shared by all rows;
-// each lane streams 16-byte chunks of the weight rows (consecutive lanes -> consecutive
-// chunks) and keeps one accumulator per (row, sample).
+// (after the optional SiLU) are staged in LDS once per K chunk and shared by all rows.
+// Every lane first issues all of its 16-byte weight loads for the chunk (consecutive
+// lanes -> consecutive chunks of a row), so a wavefront keeps kGemvRows * kPer loads in
+// flight instead of one dependent round trip per chunk, then accumulates one sum per
+// (row, sample).
 template <int DT>
 __global__ __launch_bounds__(256) void k_gemv(GemvArgs a) {
   using S = St<DT>;
-  extern __shared__ float xs[];   // [B][kGemvKC]
+  constexpr int kPer = kGemvKC / S::V / 64;   // weight chunks per lane per K chunk
+  extern __shared__ float xs[];               // [B][kGemvKC]
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int n0 = (blockIdx.x * 4 + wave) * kGemvRows;
   float acc[kGemvRows][kGemvMaxB];
@@ -128,24 +131,33 @@ __global__ __launch_bounds__(256) void k_gemv(GemvArgs a) {
   for (int k0 = 0; k0 < a.K; k0 += kGemvKC) {
     const int kc = min(kGemvKC, a.K - k0);
     __syncthreads();
-    for (int i = threadIdx.x; i < a.B * kc; i += 256) {
-      const int b = i / kc, k = i % kc;
-      float v = a.x[(size_t)b * a.ldx + k0 + k];
-      if (a.silu_in) v = silu_f(v);
-      xs[b * kGemvKC + k] = v;
+    for (int b = 0; b < a.B; ++b) {
+      const float* xr = a.x + (size_t)b * a.ldx + k0;
+      for (int k = threadIdx.x * 4; k < kc; k += 1024) {
+        float4 v = *reinterpret_cast<const float4*>(xr + k);
+        if (a.silu_in) { v.x = silu_f(v.x); v.y = silu_f(v.y); v.z = silu_f(v.z); v.w = silu_f(v.w); }
+        *reinterpret_cast<float4*>(&xs[b * kGemvKC + k]) = v;
+      }
     }
     __syncthreads();
-    for (int c = lane; c < kc / S::V; c += 64) {
-      float w[kGemvRows][S::V];
+    float w[kPer][kGemvRows][S::V];
+#pragma unroll
+    for (int p = 0; p < kPer; ++p) {
+      const int c = lane + 64 * p;
 #pragma unroll
       for (int r = 0; r < kGemvRows; ++r) {
-        if (n0 + r < a.Nout) {
-          S::load(a.W, (size_t)(n0 + r) * a.K + k0 + c * S::V, w[r]);
+        if (c * S::V < kc && n0 + r < a.Nout) {
+          S::load(a.W, (size_t)(n0 + r) * a.K + k0 + c * S::V, w[p][r]);
         } else {
 #pragma unroll
-          for (int j = 0; j < S::V; ++j) w[r][j] = 0.f;
+          for (int j = 0; j < S::V; ++j) w[p][r][j] = 0.f;
         }
       }
+    }
+#pragma unroll
+    for (int p = 0; p < kPer; ++p) {
+      const int c = lane + 64 * p;
+      if (c * S::V >= kc) break;
 #pragma unroll
       for (int b = 0; b < kGemvMaxB; ++b) {
         if (b < a.B) {
@@ -158,7 +170,7 @@ __global__ __launch_bounds__(256) void k_gemv(GemvArgs a) {
 #pragma unroll
           for (int r = 0; r < kGemvRows; ++r)
 #pragma unroll
-            for (int j = 0; j < S::V; ++j) acc[r][b] = fmaf(xv[j], w[r][j], acc[r][b]);
+            for (int j = 0; j < S::V; ++j) acc[r][b] = fmaf(xv[j], w[p][r][j], acc[r][b]);
         }
       }
     }

@@ -88,6 +88,12 @@ struct Terms {
 hipError_t cache_update(int dtype, void* slot, const void* u, const void* h, size_t E, hipStream_t s);
 // hd = round((u ? u : 0) + sum_m c_m slot_m)
 hipError_t draft(int dtype, const Terms& t, const void* u, void* hd, size_t E, hipStream_t s);
+// A run of consecutive drafted layers l0..l0+layers-1 applied in one pass: for every
+// element, x <- round(x + sum_m c_m slot_{l,m}) (or round(sum_m ...) without u) layer after
+// layer in registers.  slot[m] points at layer l0's m-th slot; layer l's is layer_stride
+// elements further.  Bit-identical to `layers` draft() calls.
+hipError_t draft_run(int dtype, const Terms& t, int layers, size_t layer_stride, int residual, void* x, size_t E,
+                     hipStream_t s);
 // Fused draft rebuild + rel-L1 partial sums + forwarding, then a fixed-order reduction.
 size_t verify_partials_floats(int B);
 hipError_t verify(int dtype, const Terms& t, const void* u, const void* hf, void* hout, int forward_exact,
