@@ -29,6 +29,9 @@ sys.path.insert(0, ROOT)
 METRIC = "denoise steps/sec at DiT-XL/2 & FLUX-like shape; MFMA util %, HBM GB/s %"
 PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
 PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
+CALIB_BYTES = 256 << 20     # plain copy of known size, the scale for FETCH_SIZE / WRITE_SIZE
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_gemm_dit_xl2.json")
+GEMM_SOURCE = os.path.join(ROOT, "paper_2607_27842_amd", "csrc", "k_gemm.hip")
 
 
 def log(*a):
@@ -114,6 +117,31 @@ def profile_loop(loop):
     stats = abi.ff_ctx_profile_read(loop.r.ctx)
     abi.ff_ctx_profile(loop.r.ctx, 0)
     return stats
+
+
+def calibration_copy():
+    """One plain copy kernel of CALIB_BYTES (read) + CALIB_BYTES (write): under rocprofv3
+    --pmc its FETCH_SIZE / WRITE_SIZE give the counters' scale for this machine."""
+    import torch
+    a = torch.ones(CALIB_BYTES // 4, dtype=torch.float32, device="cuda")
+    b = torch.empty_like(a)
+    torch.neg(a, out=b)
+    torch.cuda.synchronize()
+    del a, b
+
+
+def gemm_traffic():
+    """HBM bytes per GEMM launch measured with rocprofv3 counters for the current GEMM
+    source (None if the counters were taken on a different version of the kernel)."""
+    import hashlib
+    try:
+        rec = json.load(open(TRAFFIC_FILE))
+    except (OSError, ValueError):
+        return None
+    sha = hashlib.sha256(open(GEMM_SOURCE, "rb").read()).hexdigest()
+    if rec.get("gemm_source_sha256") != sha:
+        return None
+    return rec.get("bytes_per_launch")
 
 
 def kernel_table(stats):
@@ -219,6 +247,7 @@ def main():
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     abi.lib()
 
+    calibration_copy()
     cfg = synth.get_config("dit_xl2")
     T = cfg["T"]
     warm_loops = max(1, -(-args.warmup // T))
@@ -231,7 +260,7 @@ def main():
     g = kern["gemm"]
     achieved = g["flops"] / (g["ms"] / 1e3) / 1e12
     roof = {"bound": "mfma", "achieved": round(achieved, 1), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
-            "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": None,
+            "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": gemm_traffic(),
             "kernel": "k_gemm_bf16 (all exact-block GEMM launches of one FeatFix loop)",
             "avg_launch_us": round(g["ms"] * 1e3 / g["launches"], 3),
             "flop_per_launch": g["flops"] / g["launches"]}

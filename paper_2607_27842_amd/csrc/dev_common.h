@@ -1,9 +1,23 @@
 // Device-side helpers shared by the gfx950 kernels: bf16 storage conversions and
 // 16-byte vector access.  bf16 values are stored as raw uint16 bit patterns.
 #pragma once
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 #include "kernels.h"
+
+// Launch helper: plain hipLaunchKernelGGL, or hipExtLaunchKernelGGL with the profiler's
+// pending events (then cleared) when a profiled launch is in progress.
+#define FF_LAUNCH(kernel, grid, block, shmem, stream, ...)                                          \
+  do {                                                                                              \
+    ::ff::LaunchEvents& ff_ev_ = ::ff::g_launch_events;                                             \
+    if (ff_ev_.start) {                                                                             \
+      hipExtLaunchKernelGGL(kernel, grid, block, shmem, stream, ff_ev_.start, ff_ev_.stop, 0, __VA_ARGS__); \
+      ff_ev_.start = ff_ev_.stop = nullptr;                                                         \
+    } else {                                                                                        \
+      hipLaunchKernelGGL(kernel, grid, block, shmem, stream, __VA_ARGS__);                          \
+    }                                                                                               \
+  } while (0)
 
 namespace ff {
 

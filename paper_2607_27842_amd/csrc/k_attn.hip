@@ -237,13 +237,13 @@ hipError_t attention(int dtype, const AttnArgs& a, hipStream_t s) {
   if (a.N <= 0) return hipSuccess;
   if (dtype == DT_BF16) {
     dim3 grid((a.N + 127) / 128, a.H, a.B);
-    if (a.d <= 64) hipLaunchKernelGGL(k_attn_bf16<64>, grid, 256, 0, s, a);
-    else if (a.d <= 96) hipLaunchKernelGGL(k_attn_bf16<96>, grid, 256, 0, s, a);
-    else hipLaunchKernelGGL(k_attn_bf16<128>, grid, 256, 0, s, a);
+    if (a.d <= 64) FF_LAUNCH(k_attn_bf16<64>, grid, 256, 0, s, a);
+    else if (a.d <= 96) FF_LAUNCH(k_attn_bf16<96>, grid, 256, 0, s, a);
+    else FF_LAUNCH(k_attn_bf16<128>, grid, 256, 0, s, a);
   } else {
     dim3 grid((a.N + 63) / 64, a.H, a.B);
-    if (a.d <= 64) hipLaunchKernelGGL(k_attn_f32<64>, grid, 64, 0, s, a);
-    else hipLaunchKernelGGL(k_attn_f32<128>, grid, 64, 0, s, a);
+    if (a.d <= 64) FF_LAUNCH(k_attn_f32<64>, grid, 64, 0, s, a);
+    else FF_LAUNCH(k_attn_f32<128>, grid, 64, 0, s, a);
   }
   return hipGetLastError();
 }

@@ -365,13 +365,13 @@ __global__ __launch_bounds__(256) void k_gemm_f32(GemmArgs a) {
 template <int BM, int BN, int WM, int WN, int EPI, bool OF, bool RF>
 void launch_tile(const GemmArgs& a, hipStream_t s) {
   const int tm = (a.M + BM - 1) / BM, tn = (a.N + BN - 1) / BN;
-  hipLaunchKernelGGL((k_gemm_bf16<BM, BN, WM, WN, EPI, OF, RF>), tm * tn, (BM / WM) * (BN / WN) * 64, 0, s, a, tm, tn);
+  FF_LAUNCH((k_gemm_bf16<BM, BN, WM, WN, EPI, OF, RF>), tm * tn, (BM / WM) * (BN / WN) * 64, 0, s, a, tm, tn);
 }
 
 template <int BM, int BN, int WM, int WN, int NST, int AUX, int EPI, bool OF, bool RF>
 void launch_dl(const GemmArgs& a, hipStream_t s) {
   const int tm = (a.M + BM - 1) / BM, tn = (a.N + BN - 1) / BN;
-  hipLaunchKernelGGL((k_gemm_dl<BM, BN, WM, WN, NST, AUX, EPI, OF, RF>), tm * tn, (BM / WM) * (BN / WN) * 64, 0, s,
+  FF_LAUNCH((k_gemm_dl<BM, BN, WM, WN, NST, AUX, EPI, OF, RF>), tm * tn, (BM / WM) * (BN / WN) * 64, 0, s,
                      a, tm, tn);
 }
 
@@ -394,9 +394,9 @@ hipError_t gemm(int dtype, const GemmArgs& a, hipStream_t s) {
   if (dtype == DT_F32) {
     const int grid = ((a.M + 63) / 64) * ((a.N + 63) / 64);
     switch (a.epi) {
-      case EPI_BIAS: hipLaunchKernelGGL(k_gemm_f32<EPI_BIAS>, grid, 256, 0, s, a); break;
-      case EPI_BIAS_GELU: hipLaunchKernelGGL(k_gemm_f32<EPI_BIAS_GELU>, grid, 256, 0, s, a); break;
-      default: hipLaunchKernelGGL(k_gemm_f32<EPI_GATED>, grid, 256, 0, s, a); break;
+      case EPI_BIAS: FF_LAUNCH(k_gemm_f32<EPI_BIAS>, grid, 256, 0, s, a); break;
+      case EPI_BIAS_GELU: FF_LAUNCH(k_gemm_f32<EPI_BIAS_GELU>, grid, 256, 0, s, a); break;
+      default: FF_LAUNCH(k_gemm_f32<EPI_GATED>, grid, 256, 0, s, a); break;
     }
     return hipGetLastError();
   }

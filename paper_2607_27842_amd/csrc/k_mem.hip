@@ -175,12 +175,12 @@ __global__ __launch_bounds__(kThreads) void k_copy_rows(const void* __restrict__
 hipError_t cache_update(int dtype, void* slot, const void* u, const void* h, size_t E, hipStream_t s) {
   if (dtype == DT_BF16) {
     size_t n = E / 8;
-    if (u) hipLaunchKernelGGL((k_cache_update<DT_BF16, true>), grid_for(n), kThreads, 0, s, slot, u, h, n);
-    else hipLaunchKernelGGL((k_cache_update<DT_BF16, false>), grid_for(n), kThreads, 0, s, slot, u, h, n);
+    if (u) FF_LAUNCH((k_cache_update<DT_BF16, true>), grid_for(n), kThreads, 0, s, slot, u, h, n);
+    else FF_LAUNCH((k_cache_update<DT_BF16, false>), grid_for(n), kThreads, 0, s, slot, u, h, n);
   } else {
     size_t n = E / 4;
-    if (u) hipLaunchKernelGGL((k_cache_update<DT_F32, true>), grid_for(n), kThreads, 0, s, slot, u, h, n);
-    else hipLaunchKernelGGL((k_cache_update<DT_F32, false>), grid_for(n), kThreads, 0, s, slot, u, h, n);
+    if (u) FF_LAUNCH((k_cache_update<DT_F32, true>), grid_for(n), kThreads, 0, s, slot, u, h, n);
+    else FF_LAUNCH((k_cache_update<DT_F32, false>), grid_for(n), kThreads, 0, s, slot, u, h, n);
   }
   return hipGetLastError();
 }
@@ -188,12 +188,12 @@ hipError_t cache_update(int dtype, void* slot, const void* u, const void* h, siz
 hipError_t draft(int dtype, const Terms& t, const void* u, void* hd, size_t E, hipStream_t s) {
   if (dtype == DT_BF16) {
     size_t n = E / 8;
-    if (u) hipLaunchKernelGGL((k_draft<DT_BF16, true>), grid_for(n), kThreads, 0, s, t, u, hd, n);
-    else hipLaunchKernelGGL((k_draft<DT_BF16, false>), grid_for(n), kThreads, 0, s, t, u, hd, n);
+    if (u) FF_LAUNCH((k_draft<DT_BF16, true>), grid_for(n), kThreads, 0, s, t, u, hd, n);
+    else FF_LAUNCH((k_draft<DT_BF16, false>), grid_for(n), kThreads, 0, s, t, u, hd, n);
   } else {
     size_t n = E / 4;
-    if (u) hipLaunchKernelGGL((k_draft<DT_F32, true>), grid_for(n), kThreads, 0, s, t, u, hd, n);
-    else hipLaunchKernelGGL((k_draft<DT_F32, false>), grid_for(n), kThreads, 0, s, t, u, hd, n);
+    if (u) FF_LAUNCH((k_draft<DT_F32, true>), grid_for(n), kThreads, 0, s, t, u, hd, n);
+    else FF_LAUNCH((k_draft<DT_F32, false>), grid_for(n), kThreads, 0, s, t, u, hd, n);
   }
   return hipGetLastError();
 }
@@ -202,12 +202,12 @@ hipError_t draft_run(int dtype, const Terms& t, int layers, size_t layer_stride,
                      hipStream_t s) {
   if (dtype == DT_BF16) {
     size_t n = E / 8;
-    if (residual) hipLaunchKernelGGL((k_draft_run<DT_BF16, true>), grid_for(n), kThreads, 0, s, t, layers, layer_stride, x, n);
-    else hipLaunchKernelGGL((k_draft_run<DT_BF16, false>), grid_for(n), kThreads, 0, s, t, layers, layer_stride, x, n);
+    if (residual) FF_LAUNCH((k_draft_run<DT_BF16, true>), grid_for(n), kThreads, 0, s, t, layers, layer_stride, x, n);
+    else FF_LAUNCH((k_draft_run<DT_BF16, false>), grid_for(n), kThreads, 0, s, t, layers, layer_stride, x, n);
   } else {
     size_t n = E / 4;
-    if (residual) hipLaunchKernelGGL((k_draft_run<DT_F32, true>), grid_for(n), kThreads, 0, s, t, layers, layer_stride, x, n);
-    else hipLaunchKernelGGL((k_draft_run<DT_F32, false>), grid_for(n), kThreads, 0, s, t, layers, layer_stride, x, n);
+    if (residual) FF_LAUNCH((k_draft_run<DT_F32, true>), grid_for(n), kThreads, 0, s, t, layers, layer_stride, x, n);
+    else FF_LAUNCH((k_draft_run<DT_F32, false>), grid_for(n), kThreads, 0, s, t, layers, layer_stride, x, n);
   }
   return hipGetLastError();
 }
@@ -223,15 +223,15 @@ hipError_t verify(int dtype, const Terms& t, const void* u, const void* hf, void
   if (nblk < 1) nblk = 1;
   dim3 grid(nblk, B);
   if (dtype == DT_BF16) {
-    if (u) hipLaunchKernelGGL((k_verify<DT_BF16, true>), grid, kThreads, 0, s, t, u, hf, hout, forward_exact, cps, partials);
-    else hipLaunchKernelGGL((k_verify<DT_BF16, false>), grid, kThreads, 0, s, t, u, hf, hout, forward_exact, cps, partials);
+    if (u) FF_LAUNCH((k_verify<DT_BF16, true>), grid, kThreads, 0, s, t, u, hf, hout, forward_exact, cps, partials);
+    else FF_LAUNCH((k_verify<DT_BF16, false>), grid, kThreads, 0, s, t, u, hf, hout, forward_exact, cps, partials);
   } else {
-    if (u) hipLaunchKernelGGL((k_verify<DT_F32, true>), grid, kThreads, 0, s, t, u, hf, hout, forward_exact, cps, partials);
-    else hipLaunchKernelGGL((k_verify<DT_F32, false>), grid, kThreads, 0, s, t, u, hf, hout, forward_exact, cps, partials);
+    if (u) FF_LAUNCH((k_verify<DT_F32, true>), grid, kThreads, 0, s, t, u, hf, hout, forward_exact, cps, partials);
+    else FF_LAUNCH((k_verify<DT_F32, false>), grid, kThreads, 0, s, t, u, hf, hout, forward_exact, cps, partials);
   }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  if (rel_l1) hipLaunchKernelGGL(k_verify_finish, dim3(B), kThreads, 0, s, partials, nblk, eps, rel_l1);
+  if (rel_l1) FF_LAUNCH(k_verify_finish, dim3(B), kThreads, 0, s, partials, nblk, eps, rel_l1);
   return hipGetLastError();
 }
 
@@ -239,8 +239,8 @@ hipError_t copy_rows(int dtype, const void* src, void* dst, int B, int n, int N,
   const int V = dtype == DT_BF16 ? 8 : 4;
   size_t nchunk = (size_t)B * n * (C / V);
   if (nchunk == 0) return hipSuccess;
-  if (dtype == DT_BF16) hipLaunchKernelGGL(k_copy_rows<DT_BF16>, grid_for(nchunk), kThreads, 0, st, src, dst, n, N, off, C, nchunk);
-  else hipLaunchKernelGGL(k_copy_rows<DT_F32>, grid_for(nchunk), kThreads, 0, st, src, dst, n, N, off, C, nchunk);
+  if (dtype == DT_BF16) FF_LAUNCH(k_copy_rows<DT_BF16>, grid_for(nchunk), kThreads, 0, st, src, dst, n, N, off, C, nchunk);
+  else FF_LAUNCH(k_copy_rows<DT_F32>, grid_for(nchunk), kThreads, 0, st, src, dst, n, N, off, C, nchunk);
   return hipGetLastError();
 }
 

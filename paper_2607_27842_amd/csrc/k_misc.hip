@@ -249,10 +249,10 @@ hipError_t ln_modulate(int dtype, const LnModArgs& a, hipStream_t s) {
   if (a.rows == 0) return hipSuccess;
   const int grid = cdiv(a.rows, 4);
   if (dtype == DT_BF16) {
-    if (a.in_f32) hipLaunchKernelGGL((k_ln_modulate<DT_F32, DT_BF16>), grid, 256, 0, s, a);
-    else hipLaunchKernelGGL((k_ln_modulate<DT_BF16, DT_BF16>), grid, 256, 0, s, a);
+    if (a.in_f32) FF_LAUNCH((k_ln_modulate<DT_F32, DT_BF16>), grid, 256, 0, s, a);
+    else FF_LAUNCH((k_ln_modulate<DT_BF16, DT_BF16>), grid, 256, 0, s, a);
   } else {
-    hipLaunchKernelGGL((k_ln_modulate<DT_F32, DT_F32>), grid, 256, 0, s, a);
+    FF_LAUNCH((k_ln_modulate<DT_F32, DT_F32>), grid, 256, 0, s, a);
   }
   return hipGetLastError();
 }
@@ -260,40 +260,40 @@ hipError_t ln_modulate(int dtype, const LnModArgs& a, hipStream_t s) {
 hipError_t rms_heads(int dtype, const RmsArgs& a, hipStream_t s) {
   if (a.rows == 0) return hipSuccess;
   const int grid = cdiv((long)a.rows * a.H, 256);
-  if (dtype == DT_BF16) hipLaunchKernelGGL(k_rms_heads<DT_BF16>, grid, 256, 0, s, a);
-  else hipLaunchKernelGGL(k_rms_heads<DT_F32>, grid, 256, 0, s, a);
+  if (dtype == DT_BF16) FF_LAUNCH(k_rms_heads<DT_BF16>, grid, 256, 0, s, a);
+  else FF_LAUNCH(k_rms_heads<DT_F32>, grid, 256, 0, s, a);
   return hipGetLastError();
 }
 
 hipError_t gemv(int dtype, const GemvArgs& a, hipStream_t s) {
   const int grid = cdiv(a.Nout, 4 * kGemvRows);
   const size_t lds = (size_t)a.B * kGemvKC * sizeof(float);
-  if (dtype == DT_BF16) hipLaunchKernelGGL(k_gemv<DT_BF16>, grid, 256, lds, s, a);
-  else hipLaunchKernelGGL(k_gemv<DT_F32>, grid, 256, lds, s, a);
+  if (dtype == DT_BF16) FF_LAUNCH(k_gemv<DT_BF16>, grid, 256, lds, s, a);
+  else FF_LAUNCH(k_gemv<DT_F32>, grid, 256, lds, s, a);
   return hipGetLastError();
 }
 
 hipError_t time_embed(double sv, float* phi, hipStream_t st) {
-  hipLaunchKernelGGL(k_time_embed, 1, 128, 0, st, sv, phi);
+  FF_LAUNCH(k_time_embed, 1, 128, 0, st, sv, phi);
   return hipGetLastError();
 }
 
 hipError_t silu_rows(const float* x, float* y, int B, int n, hipStream_t st) {
   const long tot = (long)B * n;
-  hipLaunchKernelGGL(k_silu_rows, cdiv(tot, 256), 256, 0, st, x, y, tot);
+  FF_LAUNCH(k_silu_rows, cdiv(tot, 256), 256, 0, st, x, y, tot);
   return hipGetLastError();
 }
 
 hipError_t patchify(int dtype, const float* x, void* patches, const PatchGeom& g, hipStream_t st) {
   const long n = (long)g.B * g.lat_c * g.F * g.H * g.W;
-  if (dtype == DT_BF16) hipLaunchKernelGGL(k_patchify<DT_BF16>, cdiv(n, 256), 256, 0, st, x, patches, g);
-  else hipLaunchKernelGGL(k_patchify<DT_F32>, cdiv(n, 256), 256, 0, st, x, patches, g);
+  if (dtype == DT_BF16) FF_LAUNCH(k_patchify<DT_BF16>, cdiv(n, 256), 256, 0, st, x, patches, g);
+  else FF_LAUNCH(k_patchify<DT_F32>, cdiv(n, 256), 256, 0, st, x, patches, g);
   return hipGetLastError();
 }
 
 hipError_t unpatchify_euler(const float* yv, float* x, float dt, const PatchGeom& g, hipStream_t st) {
   const long n = (long)g.B * g.lat_c * g.F * g.H * g.W;
-  hipLaunchKernelGGL(k_unpatchify_euler, cdiv(n, 256), 256, 0, st, yv, x, dt, g);
+  FF_LAUNCH(k_unpatchify_euler, cdiv(n, 256), 256, 0, st, yv, x, dt, g);
   return hipGetLastError();
 }
 

@@ -8,6 +8,14 @@
 namespace ff {
 
 enum DType { DT_F32 = 0, DT_BF16 = 1 };
+
+// Events for the next kernel launch (set by the host profiler, consumed and cleared by
+// the launch): the kernel is then started with hipExtLaunchKernelGGL, which records
+// `start` / `stop` at the kernel's own execution boundaries.
+struct LaunchEvents {
+  hipEvent_t start = nullptr, stop = nullptr;
+};
+extern thread_local LaunchEvents g_launch_events;
 constexpr int kMaxTerms = 4;  // forecast order K <= 3 -> at most 4 history terms
 
 inline size_t dsize(int dt) { return dt == DT_BF16 ? 2 : 4; }
