@@ -23,6 +23,7 @@ namespace ff {
 
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef float f32x4_t __attribute__((ext_vector_type(4)));
+typedef float f32x16_t __attribute__((ext_vector_type(16)));
 typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));  // 16-byte moves (native vector, not a struct)
 typedef uint32_t u32x2_t __attribute__((ext_vector_type(2)));
 

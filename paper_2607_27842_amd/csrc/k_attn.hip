@@ -2,14 +2,11 @@
 // tiles are staged through LDS and each wavefront keeps a running (max, sum) per query
 // (online softmax), so no N x N matrix is ever stored.
 //
-// bf16 (MFMA): a wavefront owns 32 queries (two 16-query groups); a workgroup of 4
-// wavefronts shares each 64-key tile.  Scores are formed transposed, S^T = K Q^T, with
-// v_mfma_f32_16x16x32_bf16 so that every lane ends up holding the scores of ONE query
-// column for 4 keys per 16-key tile: the softmax statistics need only lane-local work
-// plus two cross-lane steps, and the probabilities are already in the register layout
-// of the B operand of O^T = V^T P^T (no shuffle).  V is transposed into LDS while it is
-// staged so that the A operand of that product is two 8-byte LDS reads.  The head dim
-// is zero-padded to a multiple of 32 for QK^T and of 16 for PV (d = 72 -> 96 / 80).
+// bf16: v_mfma_f32_32x32x16_bf16 (the full-rate gfx950 bf16 MFMA).  A wavefront owns 32
+// queries; a workgroup of 4 or 8 wavefronts shares each 64-key tile.  Scores are formed
+// transposed, S^T = K Q^T, so every lane holds the scores of ONE query: the softmax
+// statistics are lane-local plus one cross-lane step, and the probabilities are already
+// in the register layout of the B operand of O^T = V^T P^T (no shuffle).
 // fp32: one thread per query, 32-key LDS tiles (small fp32 workloads only).
 #include "dev_common.h"
 
@@ -19,158 +16,171 @@ namespace {
 
 constexpr int KT = 64;  // keys per LDS tile
 
-template <int DP>
-__global__ __launch_bounds__(256) void k_attn_bf16(AttnArgs a) {
-  constexpr int LDK = DP + 8;   // K tile row stride (elements)
-  constexpr int LDV = KT + 8;   // V^T tile row stride (elements)
-  constexpr int NKC = DP / 32;  // 32-wide chunks of the head dim for QK^T
-  constexpr int NET = DP / 16;  // 16-wide output tiles of the head dim (upper bound)
+// ---------------------------------------------------------------- bf16, 32x32x16 MFMA
+// NW wavefronts x 32 queries per workgroup; 64-key K/V tiles staged through LDS (K row-
+// major, V transposed), the next tile prefetched into registers during the current one.
+// v_mfma_f32_32x32x16_bf16 layouts (A lane l: row l%32, k 8*(l/32)+0..7; B lane l: col
+// l%32, same k; D[v] at row 8*(v/4) + 4*(l/32) + v%4, col l%32):
+//   S^T = K Q^T : A = K (32 keys x 16 dims), B = Q^T (16 dims x 32 queries) -> lane l holds
+//                 16 scores of query l%32, keys 8*(v/4) + 4*(l/32) + v%4 of a 32-key tile.
+//   O^T += V^T P^T : B = P^T needs, per lane, the probabilities of query l%32 at 8 keys
+//                 for the MFMA k index 8*(l/32)+j; mapping k index j to key
+//                 (j<4 ? 4h+j : 8+4h+j-4) (+16 for the second half of the tile) makes that
+//                 exactly the registers the lane already holds.  A = V^T rows (e) at those
+//                 keys; the transposed V tile stores key k of each 16-key group at column
+//                 vpos(k) (bits 2 and 3 swapped), which makes them one 16-byte LDS read.
+// Head dims are zero-padded: QK^T to a multiple of 16 (DQ), PV to a multiple of 32 (DV).
+__device__ __forceinline__ int vpos(int k) { return (k & ~12) | ((k & 4) << 1) | ((k & 8) >> 1); }
+
+template <int DQ, int DV, int NW>
+__global__ __launch_bounds__(NW * 64) void k_attn32(AttnArgs a) {
+  constexpr int NT = NW * 64;
+  constexpr int LDK = DQ + 8;         // K tile row stride (elements)
+  constexpr int LDV = KT + 8;         // V^T tile row stride
+  constexpr int NQC = DQ / 16;        // 16-wide head-dim chunks of QK^T
+  constexpr int NOT = DV / 32;        // 32-wide output tiles of the head dim
+  constexpr int KCH = KT * (DQ / 8);  // 16-byte chunks of a K tile (DQ >= DV)
+  constexpr int PER = (KCH + NT - 1) / NT;
+  static_assert(DV <= DQ + 16, "layout");
   __shared__ __attribute__((aligned(16))) uint16_t Ks[KT * LDK];
-  __shared__ __attribute__((aligned(16))) uint16_t Vt[DP * LDV];
+  __shared__ __attribute__((aligned(16))) uint16_t Vt[DV * LDV];
 
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int g16 = lane >> 4, c16 = lane & 15;
-  const int b = blockIdx.z, h = blockIdx.y;
-  const int q0 = blockIdx.x * 128 + wave * 32;
+  const int c32 = lane & 31, h = lane >> 5;
+  const int b = blockIdx.z, hd = blockIdx.y;
+  const int q0 = blockIdx.x * (NW * 32) + wave * 32;
   const int N = a.N, d = a.d;
-  const int net = (d + 15) / 16;
   const uint16_t* qkv = reinterpret_cast<const uint16_t*>(a.qkv);
   const size_t rb = (size_t)b * N;
-  const size_t qoff = (size_t)h * d, koff = (size_t)a.C + h * d, voff = 2 * (size_t)a.C + h * d;
+  const size_t qoff = (size_t)hd * d, koff = (size_t)a.C + hd * d, voff = 2 * (size_t)a.C + hd * d;
   const u32x4_t z4 = {0u, 0u, 0u, 0u};
 
-  // Q fragments (B operand of S^T): lane holds Q[q][kc*32 + 8*g16 .. +7] for q = q0 + 16g + c16.
-  bf16x8_t qf[2][NKC];
+  // Q^T fragments: lane holds Q[q0 + c32][16c + 8h .. +7]
+  bf16x8_t qf[NQC];
+  {
+    const int q = q0 + c32;
 #pragma unroll
-  for (int g = 0; g < 2; ++g) {
-    const int q = q0 + 16 * g + c16;
-#pragma unroll
-    for (int kc = 0; kc < NKC; ++kc) {
-      const int e = kc * 32 + 8 * g16;
-      u32x4_t v = (q < N && e < d) ? *reinterpret_cast<const u32x4_t*>(qkv + (rb + q) * a.ldq + qoff + e) : z4;
-      qf[g][kc] = __builtin_bit_cast(bf16x8_t, v);
+    for (int c = 0; c < NQC; ++c) {
+      const int e = 16 * c + 8 * h;
+      const u32x4_t v = (q < N && e < d) ? *reinterpret_cast<const u32x4_t*>(qkv + (rb + q) * a.ldq + qoff + e) : z4;
+      qf[c] = __builtin_bit_cast(bf16x8_t, v);
     }
   }
-
-  f32x4_t o[2][NET];
+  f32x16_t o[NOT];
 #pragma unroll
-  for (int g = 0; g < 2; ++g)
+  for (int t = 0; t < NOT; ++t)
 #pragma unroll
-    for (int t = 0; t < NET; ++t) o[g][t] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-  float mrow[2] = {-INFINITY, -INFINITY}, lrow[2] = {0.f, 0.f};
-  const float sl2 = a.scale * 1.4426950408889634f;  // scores in log2 units
+    for (int v = 0; v < 16; ++v) o[t][v] = 0.f;
+  float mrow = -INFINITY, lrow = 0.f;
+  const float sl2 = a.scale * 1.4426950408889634f;
 
+  // register prefetch of one K/V tile: chunk c -> key c / (DQ/8), dims (c % (DQ/8)) * 8
+  u32x4_t pk[PER], pv[PER];
+  auto fetch = [&](int kv0) {
+#pragma unroll
+    for (int i = 0; i < PER; ++i) {
+      const int c = threadIdx.x + i * NT;
+      const int kr = c / (DQ / 8), e = (c % (DQ / 8)) * 8, key = kv0 + kr;
+      const bool ok = c < KCH && key < N && e < d;
+      pk[i] = ok ? *reinterpret_cast<const u32x4_t*>(qkv + (rb + key) * a.ldq + koff + e) : z4;
+      pv[i] = ok ? *reinterpret_cast<const u32x4_t*>(qkv + (rb + key) * a.ldq + voff + e) : z4;
+    }
+  };
+  auto stage = [&]() {
+#pragma unroll
+    for (int i = 0; i < PER; ++i) {
+      const int c = threadIdx.x + i * NT;
+      if (c < KCH) {
+        const int kr = c / (DQ / 8), e = (c % (DQ / 8)) * 8;
+        *reinterpret_cast<u32x4_t*>(&Ks[kr * LDK + e]) = pk[i];
+        if (e < DV) {
+#pragma unroll
+          for (int j = 0; j < 4; ++j) {
+            Vt[(e + 2 * j) * LDV + vpos(kr)] = (uint16_t)(pv[i][j] & 0xffffu);
+            Vt[(e + 2 * j + 1) * LDV + vpos(kr)] = (uint16_t)(pv[i][j] >> 16);
+          }
+        }
+      }
+    }
+  };
+  fetch(0);
   for (int kv0 = 0; kv0 < N; kv0 += KT) {
+    __syncthreads();           // previous tile fully consumed
+    stage();
     __syncthreads();
-    for (int c = threadIdx.x; c < KT * (DP / 8); c += 256) {
-      const int kr = c / (DP / 8), e = (c % (DP / 8)) * 8, key = kv0 + kr;
-      const bool ok = key < N && e < d;
-      const u32x4_t kv = ok ? *reinterpret_cast<const u32x4_t*>(qkv + (rb + key) * a.ldq + koff + e) : z4;
-      *reinterpret_cast<u32x4_t*>(&Ks[kr * LDK + e]) = kv;
-      const u32x4_t vv = ok ? *reinterpret_cast<const u32x4_t*>(qkv + (rb + key) * a.ldq + voff + e) : z4;
+    if (kv0 + KT < N) fetch(kv0 + KT);   // in flight during this tile's math
+    // scores for two 32-key tiles
+    f32x16_t sc[2];
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        Vt[(e + 2 * i) * LDV + kr] = (uint16_t)(vv[i] & 0xffffu);
-        Vt[(e + 2 * i + 1) * LDV + kr] = (uint16_t)(vv[i] >> 16);
+    for (int t = 0; t < 2; ++t) {
+#pragma unroll
+      for (int v = 0; v < 16; ++v) sc[t][v] = 0.f;
+#pragma unroll
+      for (int c = 0; c < NQC; ++c) {
+        const bf16x8_t kf = *reinterpret_cast<const bf16x8_t*>(&Ks[(t * 32 + c32) * LDK + 16 * c + 8 * h]);
+        sc[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[c], sc[t], 0, 0, 0);
       }
     }
-    __syncthreads();
-
-    // S^T tiles: s[g][t][v] = score(key kv0 + 16t + 4*g16 + v, query q0 + 16g + c16)
-    f32x4_t s[2][4];
+    // online softmax for query q0 + c32 (its 64 scores: 32 in this lane, 32 in lane ^ 32)
+    float mx = -INFINITY;
 #pragma unroll
-    for (int t = 0; t < 4; ++t) {
-      bf16x8_t kf[NKC];
+    for (int t = 0; t < 2; ++t)
 #pragma unroll
-      for (int kc = 0; kc < NKC; ++kc)
-        kf[kc] = *reinterpret_cast<const bf16x8_t*>(&Ks[(t * 16 + c16) * LDK + kc * 32 + 8 * g16]);
-#pragma unroll
-      for (int g = 0; g < 2; ++g) {
-        f32x4_t acc = f32x4_t{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-        for (int kc = 0; kc < NKC; ++kc) acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf[kc], qf[g][kc], acc, 0, 0, 0);
-        s[g][t] = acc;
+      for (int v = 0; v < 16; ++v) {
+        const int key = kv0 + 32 * t + 8 * (v >> 2) + 4 * h + (v & 3);
+        const float x = key < N ? sc[t][v] * sl2 : -INFINITY;
+        sc[t][v] = x;
+        mx = fmaxf(mx, x);
       }
-    }
-
-    bf16x8_t pb[2][2];
+    mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+    const float mnew = fmaxf(mrow, mx);
+    const float alpha = exp2f(mrow - mnew);
+    float ls = 0.f;
 #pragma unroll
-    for (int g = 0; g < 2; ++g) {
-      float mx = -INFINITY;
+    for (int t = 0; t < 2; ++t)
 #pragma unroll
-      for (int t = 0; t < 4; ++t)
-#pragma unroll
-        for (int v = 0; v < 4; ++v) {
-          const int key = kv0 + 16 * t + 4 * g16 + v;
-          const float x = key < N ? s[g][t][v] * sl2 : -INFINITY;
-          s[g][t][v] = x;
-          mx = fmaxf(mx, x);
-        }
-      mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
-      mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
-      const float mnew = fmaxf(mrow[g], mx);
-      const float alpha = exp2f(mrow[g] - mnew);
-      float ls = 0.f;
-#pragma unroll
-      for (int t = 0; t < 4; ++t)
-#pragma unroll
-        for (int v = 0; v < 4; ++v) {
-          const float p = exp2f(s[g][t][v] - mnew);
-          s[g][t][v] = p;
-          ls += p;
-        }
-      ls += __shfl_xor(ls, 16, 64);
-      ls += __shfl_xor(ls, 32, 64);
-      lrow[g] = lrow[g] * alpha + ls;
-      mrow[g] = mnew;
-#pragma unroll
-      for (int t = 0; t < NET; ++t) o[g][t] *= alpha;
-      // B operand of O^T += V^T P^T for key chunk c: keys 32c + 4*g16 + (0..3) and 32c + 16 + 4*g16 + (0..3)
-#pragma unroll
-      for (int c = 0; c < 2; ++c) {
-        bf16x8_t p;
-#pragma unroll
-        for (int v = 0; v < 4; ++v) {
-          p[v] = (__bf16)s[g][2 * c][v];
-          p[4 + v] = (__bf16)s[g][2 * c + 1][v];
-        }
-        pb[g][c] = p;
+      for (int v = 0; v < 16; ++v) {
+        const float pr = exp2f(sc[t][v] - mnew);
+        sc[t][v] = pr;
+        ls += pr;
       }
-    }
+    ls += __shfl_xor(ls, 32, 64);
+    lrow = lrow * alpha + ls;
+    mrow = mnew;
 #pragma unroll
-    for (int c = 0; c < 2; ++c) {
+    for (int t = 0; t < NOT; ++t) o[t] *= alpha;
+    // O^T += V^T P^T over 4 16-key groups (keys 16g + ...)
 #pragma unroll
-      for (int t = 0; t < NET; ++t) {
-        if (t < net) {
-          const uint16_t* vr = &Vt[(t * 16 + c16) * LDV + 32 * c + 4 * g16];
-          const u32x2_t lo = *reinterpret_cast<const u32x2_t*>(vr);
-          const u32x2_t hi = *reinterpret_cast<const u32x2_t*>(vr + 16);
-          const u32x4_t cat = {lo[0], lo[1], hi[0], hi[1]};
-          const bf16x8_t va = __builtin_bit_cast(bf16x8_t, cat);
+    for (int g = 0; g < 4; ++g) {
+      const int t = g >> 1, half = g & 1;   // score tile, and which 16 keys of it
+      bf16x8_t pb;
 #pragma unroll
-          for (int g = 0; g < 2; ++g) o[g][t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(va, pb[g][c], o[g][t], 0, 0, 0);
-        }
+      for (int j = 0; j < 8; ++j) pb[j] = (__bf16)sc[t][8 * half + j];
+      // keys 16g + 4h + {0..3, 8..11} sit at V^T columns 16g + 8h .. +7
+#pragma unroll
+      for (int ot = 0; ot < NOT; ++ot) {
+        const bf16x8_t vf = *reinterpret_cast<const bf16x8_t*>(&Vt[(ot * 32 + c32) * LDV + 16 * g + 8 * h]);
+        o[ot] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pb, o[ot], 0, 0, 0);
       }
     }
   }
-
-  // O^T layout: o[g][t][v] = O[query q0 + 16g + c16][e = 16t + 4*g16 + v]
-  uint16_t* out = reinterpret_cast<uint16_t*>(a.out);
+  // o[ot][v] = O[query q0 + c32][e = 32 ot + 8 (v/4) + 4 h + v%4]
+  const int q = q0 + c32;
+  if (q < N) {
+    uint16_t* out = reinterpret_cast<uint16_t*>(a.out);
+    const float inv = 1.0f / lrow;
 #pragma unroll
-  for (int g = 0; g < 2; ++g) {
-    const int q = q0 + 16 * g + c16;
-    if (q >= N) continue;
-    const float inv = 1.0f / lrow[g];
+    for (int ot = 0; ot < NOT; ++ot)
 #pragma unroll
-    for (int t = 0; t < NET; ++t) {
-      const int e = 16 * t + 4 * g16;
-      if (t < net && e < d) {
-        u32x2_t w;
-        w[0] = (uint32_t)f2bf(o[g][t][0] * inv) | ((uint32_t)f2bf(o[g][t][1] * inv) << 16);
-        w[1] = (uint32_t)f2bf(o[g][t][2] * inv) | ((uint32_t)f2bf(o[g][t][3] * inv) << 16);
-        *reinterpret_cast<u32x2_t*>(out + (rb + q) * a.ldo + (size_t)h * d + e) = w;
+      for (int g = 0; g < 4; ++g) {
+        const int e = 32 * ot + 8 * g + 4 * h;
+        if (e < d) {
+          u32x2_t w;
+          w[0] = (uint32_t)f2bf(o[ot][4 * g] * inv) | ((uint32_t)f2bf(o[ot][4 * g + 1] * inv) << 16);
+          w[1] = (uint32_t)f2bf(o[ot][4 * g + 2] * inv) | ((uint32_t)f2bf(o[ot][4 * g + 3] * inv) << 16);
+          *reinterpret_cast<u32x2_t*>(out + (rb + q) * a.ldo + (size_t)hd * d + e) = w;
+        }
       }
-    }
   }
 }
 
@@ -236,10 +246,19 @@ __global__ __launch_bounds__(64) void k_attn_f32(AttnArgs a) {
 hipError_t attention(int dtype, const AttnArgs& a, hipStream_t s) {
   if (a.N <= 0) return hipSuccess;
   if (dtype == DT_BF16) {
-    dim3 grid((a.N + 127) / 128, a.H, a.B);
-    if (a.d <= 64) FF_LAUNCH(k_attn_bf16<64>, grid, 256, 0, s, a);
-    else if (a.d <= 96) FF_LAUNCH(k_attn_bf16<96>, grid, 256, 0, s, a);
-    else FF_LAUNCH(k_attn_bf16<128>, grid, 256, 0, s, a);
+    // 8 wavefronts (256 queries) per workgroup when that still gives >= 256 workgroups
+    const bool wide = (long)((a.N + 255) / 256) * a.H * a.B >= 256;
+    const dim3 grid((a.N + (wide ? 255 : 127)) / (wide ? 256 : 128), a.H, a.B);
+#define FF_ATTN(DQ, DV)                                                              \
+    do {                                                                             \
+      if (wide) FF_LAUNCH((k_attn32<DQ, DV, 8>), grid, 512, 0, s, a);                \
+      else FF_LAUNCH((k_attn32<DQ, DV, 4>), grid, 256, 0, s, a);                     \
+    } while (0)
+    if (a.d <= 64) FF_ATTN(64, 64);
+    else if (a.d <= 80) FF_ATTN(80, 96);
+    else if (a.d <= 96) FF_ATTN(96, 96);
+    else FF_ATTN(128, 128);
+#undef FF_ATTN
   } else {
     dim3 grid((a.N + 63) / 64, a.H, a.B);
     if (a.d <= 64) FF_LAUNCH(k_attn_f32<64>, grid, 64, 0, s, a);

@@ -85,7 +85,6 @@ __device__ __forceinline__ void tile_of(int bid, int tiles_m, int tiles_n, int& 
 // BM x BN workgroup tile, BK = 64 per LDS stage, wavefront tiles WM x WN of
 // v_mfma_f32_32x32x16_bf16 (the 16x16x32 form issues at half the rate on gfx950).
 constexpr int BK = 64, LDT = BK + 8;
-typedef float f32x16_t __attribute__((ext_vector_type(16)));
 
 // 32x32x16 MFMA: A operand lane l = row (l%32), k 8*(l/32)..+7; B operand lane l = col (l%32),
 // same k; D[v] at row 8*(v/4) + 4*(l/32) + v%4, col l%32.  With A = weight rows (output

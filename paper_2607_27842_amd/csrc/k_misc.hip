@@ -112,10 +112,9 @@ constexpr int kGemvKC = 1024;    // K chunk of the activations staged in LDS
 
 // y[b, n] for 16 consecutive n per workgroup (4 per wavefront).  The activations x[b, k]
 // (after the optional SiLU) are staged in LDS once per K chunk and shared by all rows.
-// Every lane first issues all of its 16-byte weight loads for the chunk (consecutive
-// lanes -> consecutive chunks of a row), so a wavefront keeps kGemvRows * kPer loads in
-// flight instead of one dependent round trip per chunk, then accumulates one sum per
-// (row, sample).
+// Per chunk, every lane first issues all of its 16-byte weight loads (consecutive lanes
+// -> consecutive chunks of a row) and every thread all of its activation loads, so the
+// chunk costs one memory round trip; then one sum per (row, sample) is accumulated.
 template <int DT>
 __global__ __launch_bounds__(256) void k_gemv(GemvArgs a) {
   using S = St<DT>;
@@ -130,16 +129,7 @@ __global__ __launch_bounds__(256) void k_gemv(GemvArgs a) {
     for (int b = 0; b < kGemvMaxB; ++b) acc[r][b] = 0.f;
   for (int k0 = 0; k0 < a.K; k0 += kGemvKC) {
     const int kc = min(kGemvKC, a.K - k0);
-    __syncthreads();
-    for (int b = 0; b < a.B; ++b) {
-      const float* xr = a.x + (size_t)b * a.ldx + k0;
-      for (int k = threadIdx.x * 4; k < kc; k += 1024) {
-        float4 v = *reinterpret_cast<const float4*>(xr + k);
-        if (a.silu_in) { v.x = silu_f(v.x); v.y = silu_f(v.y); v.z = silu_f(v.z); v.w = silu_f(v.w); }
-        *reinterpret_cast<float4*>(&xs[b * kGemvKC + k]) = v;
-      }
-    }
-    __syncthreads();
+    // weight loads first (they do not depend on the activations) ...
     float w[kPer][kGemvRows][S::V];
 #pragma unroll
     for (int p = 0; p < kPer; ++p) {
@@ -154,6 +144,23 @@ __global__ __launch_bounds__(256) void k_gemv(GemvArgs a) {
         }
       }
     }
+    // ... then every sample's activation chunk (one float4 per thread and sample, all
+    // loads issued before any is stored) into LDS
+    float4 xv4[kGemvMaxB];
+    const int k4 = threadIdx.x * 4;   // 256 threads x 4 = kGemvKC
+#pragma unroll
+    for (int b = 0; b < kGemvMaxB; ++b)
+      if (b < a.B && k4 < kc) xv4[b] = *reinterpret_cast<const float4*>(a.x + (size_t)b * a.ldx + k0 + k4);
+    __syncthreads();   // the previous chunk's LDS reads are done
+#pragma unroll
+    for (int b = 0; b < kGemvMaxB; ++b) {
+      if (b < a.B && k4 < kc) {
+        float4 v = xv4[b];
+        if (a.silu_in) { v.x = silu_f(v.x); v.y = silu_f(v.y); v.z = silu_f(v.z); v.w = silu_f(v.w); }
+        *reinterpret_cast<float4*>(&xs[b * kGemvKC + k4]) = v;
+      }
+    }
+    __syncthreads();
 #pragma unroll
     for (int p = 0; p < kPer; ++p) {
       const int c = lane + 64 * p;
@@ -175,19 +182,24 @@ __global__ __launch_bounds__(256) void k_gemv(GemvArgs a) {
       }
     }
   }
+  // Cross-lane sums of the kGemvRows * B partials: one transposed pass through LDS (each
+  // lane writes its partials, lane v then adds column v over the 64 lanes in order) instead
+  // of one 6-step butterfly per value.
+  __shared__ float red[4][kGemvRows * kGemvMaxB][65];
 #pragma unroll
-  for (int r = 0; r < kGemvRows; ++r) {
-    const int n = n0 + r;
-    if (n >= a.Nout) break;
-    const float bias = S::ld1(a.bias, n);
+  for (int r = 0; r < kGemvRows; ++r)
 #pragma unroll
-    for (int b = 0; b < kGemvMaxB; ++b) {
-      if (b < a.B) {
-        float y = wave_sum(acc[r][b]) + bias;
-        if (a.silu_out) y = silu_f(y);
-        if (a.add) y += a.add[(size_t)b * a.ldadd + n];
-        if (lane == 0) a.y[(size_t)b * a.ldy + n] = y;
-      }
+    for (int b = 0; b < kGemvMaxB; ++b) red[wave][r * kGemvMaxB + b][lane] = acc[r][b];
+  __syncthreads();
+  if (lane < kGemvRows * kGemvMaxB) {
+    const int r = lane / kGemvMaxB, b = lane % kGemvMaxB, n = n0 + r;
+    if (b < a.B && n < a.Nout) {
+      float sum = 0.f;
+      for (int l = 0; l < 64; ++l) sum += red[wave][lane][l];
+      float y = sum + S::ld1(a.bias, n);
+      if (a.silu_out) y = silu_f(y);
+      if (a.add) y += a.add[(size_t)b * a.ldadd + n];
+      a.y[(size_t)b * a.ldy + n] = y;
     }
   }
 }
