@@ -107,8 +107,18 @@ ff_status check_model(const ff_model_desc* m, Model* out) {
 
 // ---------------------------------------------------------------- workspace layout
 struct Ws {
-  size_t X0, X1, HF, LNA, QKV, ATT, X1F, HID, MOD, CT, CS, TMP, PHI, PATCH, YF, PART, total;
+  size_t X0, X1, HF, LNA, QKV, ATT, X1F, HID, MOD, CT, CS, TMP, PHI, PATCH, YF, PART, MODS, total;
+  size_t mod_slot;   // floats per layer slot of MODS
 };
+
+// Modulation vectors per layer kind: 6C (DiT), 2 x 6C (MMDiT double), 3C (MMDiT single).
+int mod_floats(int kind, int C) { return kind == FF_MMDIT_DOUBLE ? 12 * C : kind == FF_MMDIT_SINGLE ? 3 * C : 6 * C; }
+int mod_width(const Model& m) {
+  int w = 0;
+  for (int k : m.kinds) w = std::max(w, mod_floats(k, m.C));
+  return w;
+}
+constexpr int kModLayers = kGemvJobs / 2;   // layers whose modulation one batched launch computes
 
 Ws ws_layout(const Model& m) {
   Ws w{};
@@ -131,6 +141,8 @@ Ws ws_layout(const Model& m) {
   w.PATCH = take((size_t)m.B * m.n_img * m.P * es);
   w.YF = take((size_t)m.B * m.n_img * m.P * 4);
   w.PART = take(verify_partials_floats(m.B) * 4);
+  w.mod_slot = (size_t)m.B * mod_width(m);
+  w.MODS = take(kModLayers * w.mod_slot * 4);
   w.total = off;
   return w;
 }
@@ -197,6 +209,14 @@ struct Exec {
     return timed(FF_PROF_ATTN, 4.0 * a.B * (double)a.N * a.N * a.H * a.d, rows * 4.0 * a.C * es,
                  [&] { return ff::attention(dt, a, st); });
   }
+  hipError_t gemv_batch(const GemvBatch& b) {
+    double fl = 0, by = 0;
+    for (int i = 0; i < b.njobs; ++i) {
+      fl += 2.0 * b.B * b.job[i].Nout * b.K;
+      by += (double)b.job[i].Nout * b.K * es;
+    }
+    return timed(FF_PROF_GEMV, fl, by, [&] { return ff::gemv_batch(dt, b, st); });
+  }
   hipError_t gemv(const GemvArgs& a) {
     return timed(FF_PROF_GEMV, 2.0 * a.B * a.Nout * a.K, (double)a.Nout * a.K * es, [&] { return ff::gemv(dt, a, st); });
   }
@@ -204,8 +224,8 @@ struct Exec {
     return timed(FF_PROF_NORM, 0, (double)a.rows * a.C * ((a.in_f32 ? 4 : es) + es),
                  [&] { return ff::ln_modulate(dt, a, st); });
   }
-  hipError_t rms(const RmsArgs& a) {
-    return timed(FF_PROF_NORM, 0, 2.0 * a.rows * a.H * a.d * es, [&] { return ff::rms_heads(dt, a, st); });
+  hipError_t rms_qk(const RmsQKArgs& a) {
+    return timed(FF_PROF_NORM, 0, 4.0 * a.rows * a.H * a.d * es, [&] { return ff::rms_qk(dt, a, st); });
   }
   hipError_t cache(void* slot, const void* u, const void* h, size_t E) {
     return timed(FF_PROF_CACHE, 0, (u ? 3.0 : 2.0) * E * es, [&] { return ff::cache_update(dt, slot, u, h, E, st); });
@@ -268,7 +288,7 @@ const void* offset_rows(const void* p, size_t rows, size_t cols, size_t es) {
 
 // h = B_l(u; c_t) with cs = SiLU(c_t) [B, C] fp32 already in the workspace.
 ff_status exec_block(const Model& m, int kind, const ff_layer_weights& w, const float* cs, const void* u,
-                     void* h, void* ws, Exec& ex) {
+                     void* h, void* ws, Exec& ex, const float* mod_pre = nullptr) {
   const Ws L = ws_layout(m);
   const int C = m.C, Mh = m.M, dt = m.dtype;
   const size_t es = m.es();
@@ -277,7 +297,8 @@ ff_status exec_block(const Model& m, int kind, const ff_layer_weights& w, const 
   void* att = at(ws, L.ATT);
   float* x1f = at<float>(ws, L.X1F);
   void* hid = at(ws, L.HID);
-  float* mod = at<float>(ws, L.MOD);
+  // modulation: precomputed by the caller (batched over the layers of a step) or here
+  float* mod = mod_pre ? const_cast<float*>(mod_pre) : at<float>(ws, L.MOD);
   const float scale = 1.0f / sqrtf((float)m.d);
 
   AttnArgs aa{};
@@ -287,8 +308,10 @@ ff_status exec_block(const Model& m, int kind, const ff_layer_weights& w, const 
     const ff_stream_weights& s = w.s[0];
     const RowMap all = whole(m);
     const int rows = m.B * m.N;
-    GemvArgs gv{cs, C, 0, s.mod_w, s.mod_b, 3 * C, C, m.B, mod, 3 * C, 0, nullptr, 0};
-    HIP_TRY(ex.gemv(gv), "single: modulation");
+    if (!mod_pre) {
+      GemvArgs gv{cs, C, 0, s.mod_w, s.mod_b, 3 * C, C, m.B, mod, 3 * C, 0, nullptr, 0};
+      HIP_TRY(ex.gemv(gv), "single: modulation");
+    }
     LnModArgs ln{u, 0, C, all, rows, C, m.ln_eps, mod, mod + C, 3 * C, lna, C};
     HIP_TRY(ex.ln(ln), "single: ln");
     GemmArgs g1 = gemm_args(lna, C, all, s.lin1_w, s.lin1_b, rows, 3 * C, C, EPI_BIAS, qkv, 3 * C, all);
@@ -298,10 +321,8 @@ ff_status exec_block(const Model& m, int kind, const ff_layer_weights& w, const 
                             offset_rows(s.lin1_b, 3 * (size_t)C, 1, es), rows, Mh, C, EPI_BIAS_GELU,
                             at(att, (size_t)C * es), ldy, all);
     HIP_TRY(ex.gemm(g2), "single: lin1 mlp");
-    RmsArgs rq{qkv, 3 * C, all, rows, m.H, m.d, 0, s.q_g, m.ln_eps};
-    HIP_TRY(ex.rms(rq), "single: q norm");
-    RmsArgs rk{qkv, 3 * C, all, rows, m.H, m.d, C, s.k_g, m.ln_eps};
-    HIP_TRY(ex.rms(rk), "single: k norm");
+    RmsQKArgs rn{qkv, 3 * C, all, rows, m.H, m.d, s.q_g, s.k_g, m.ln_eps};
+    HIP_TRY(ex.rms_qk(rn), "single: q/k norm");
     aa.out = att; aa.ldo = ldy;
     HIP_TRY(ex.attention(aa), "single: attention");
     GemmArgs g3 = gemm_args(att, ldy, all, s.lin2_w, s.lin2_b, rows, C, C + Mh, EPI_GATED, h, C, all);
@@ -325,18 +346,18 @@ ff_status exec_block(const Model& m, int kind, const ff_layer_weights& w, const 
     const ff_stream_weights& s = w.s[si];
     const int rows = m.B * nseg[si];
     float* ms = mod + 6 * C * si;
-    GemvArgs gv{cs, C, 0, s.mod_w, s.mod_b, 6 * C, C, m.B, ms, ldm, 0, nullptr, 0};
-    HIP_TRY(ex.gemv(gv), "block: modulation");
+    if (!mod_pre) {
+      GemvArgs gv{cs, C, 0, s.mod_w, s.mod_b, 6 * C, C, m.B, ms, ldm, 0, nullptr, 0};
+      HIP_TRY(ex.gemv(gv), "block: modulation");
+    }
     if (rows == 0) continue;
     LnModArgs ln{u, 0, C, maps[si], rows, C, m.ln_eps, ms, ms + C, ldm, lna, C};
     HIP_TRY(ex.ln(ln), "block: ln1");
     GemmArgs g = gemm_args(lna, C, maps[si], s.qkv_w, s.qkv_b, rows, 3 * C, C, EPI_BIAS, qkv, 3 * C, maps[si]);
     HIP_TRY(ex.gemm(g), "block: qkv");
     if (kind == FF_MMDIT_DOUBLE) {
-      RmsArgs rq{qkv, 3 * C, maps[si], rows, m.H, m.d, 0, s.q_g, m.ln_eps};
-      HIP_TRY(ex.rms(rq), "double: q norm");
-      RmsArgs rk{qkv, 3 * C, maps[si], rows, m.H, m.d, C, s.k_g, m.ln_eps};
-      HIP_TRY(ex.rms(rk), "double: k norm");
+      RmsQKArgs rn{qkv, 3 * C, maps[si], rows, m.H, m.d, s.q_g, s.k_g, m.ln_eps};
+      HIP_TRY(ex.rms_qk(rn), "double: q/k norm");
     }
   }
   aa.out = att; aa.ldo = C;
@@ -741,6 +762,38 @@ ff_status ff_denoise_step(ff_ctx* c, int32_t step, float* x, const float* cond, 
     GemvArgs g2{tmp, C, 0, c->g.t2_w, c->g.t2_b, C, C, m.B, ct, C, 0, cond, C};
     HIP_TRY(ex.gemv(g2), "time mlp 2");
     HIP_TRY(ex.other(8.0 * m.B * C, [&] { return silu_rows(ct, cs, m.B, C, st); }), "silu(c_t)");
+    // Modulation of the layers that run exact this step, computed kModLayers layers at a
+    // time in one batched GEMV launch each; mod_of[l] = that layer's vectors.
+    auto runs_exact = [&](int l) {
+      const int a = p.action[(size_t)i * L + l];
+      return a == FF_ACT_EXACT || a == FF_ACT_SITE;
+    };
+    float* mods = at<float>(ws, W.MODS);
+    std::vector<const float*> mod_of(L, nullptr);
+    auto ensure_mod = [&](int l) -> ff_status {
+      if (mod_of[l]) return FF_OK;
+      GemvBatch bt{};
+      bt.x = cs; bt.ldx = C; bt.silu_in = 0; bt.K = C; bt.B = m.B;
+      int slot = 0;
+      for (int l2 = l; l2 < L && slot < kModLayers; ++l2) {
+        if (!runs_exact(l2)) continue;
+        float* dst = mods + (size_t)slot * W.mod_slot;
+        const int kind = m.kinds[l2];
+        const ff_stream_weights* sw = c->lw[l2].s;
+        if (kind == FF_MMDIT_SINGLE) {
+          bt.job[bt.njobs++] = GemvJob{sw[0].mod_w, sw[0].mod_b, dst, 3 * C, 3 * C};
+        } else if (kind == FF_MMDIT_DOUBLE) {
+          bt.job[bt.njobs++] = GemvJob{sw[0].mod_w, sw[0].mod_b, dst, 6 * C, 12 * C};
+          bt.job[bt.njobs++] = GemvJob{sw[1].mod_w, sw[1].mod_b, dst + 6 * C, 6 * C, 12 * C};
+        } else {
+          bt.job[bt.njobs++] = GemvJob{sw[0].mod_w, sw[0].mod_b, dst, 6 * C, 6 * C};
+        }
+        mod_of[l2] = dst;
+        ++slot;
+      }
+      HIP_TRY(ex.gemv_batch(bt), "batched modulation");
+      return FF_OK;
+    };
     // tokens: X = [txt ; patch_embed(patchify(x))]
     PatchGeom pg{m.B, m.lat_c, m.lat_f, m.lat_h, m.lat_w, m.pt, m.ph, m.pw};
     void* patches = at(ws, W.PATCH);
@@ -761,7 +814,9 @@ ff_status ff_denoise_step(ff_ctx* c, int32_t step, float* x, const float* cond, 
     for (int l = 0; l < L; ++l) {
       const int act = p.action[(size_t)i * L + l];
       if (act == FF_ACT_EXACT) {
-        ff_status e = exec_block(m, m.kinds[l], c->lw[l], cs, cur, alt, ws, ex);
+        ff_status e = ensure_mod(l);
+        if (e) return e;
+        e = exec_block(m, m.kinds[l], c->lw[l], cs, cur, alt, ws, ex, mod_of[l]);
         if (e) return e;
         if (mode != FF_VANILLA) {
           const int sl = p.write_slot[i];
@@ -772,7 +827,9 @@ ff_status ff_denoise_step(ff_ctx* c, int32_t step, float* x, const float* cond, 
         continue;
       }
       if (act == FF_ACT_SITE && mode == FF_EXACT_ONLY) {
-        ff_status e = exec_block(m, m.kinds[l], c->lw[l], cs, cur, alt, ws, ex);
+        ff_status e = ensure_mod(l);
+        if (e) return e;
+        e = exec_block(m, m.kinds[l], c->lw[l], cs, cur, alt, ws, ex, mod_of[l]);
         if (e) return e;
         void* t = cur; cur = alt; alt = t;
         continue;
@@ -795,7 +852,9 @@ ff_status ff_denoise_step(ff_ctx* c, int32_t step, float* x, const float* cond, 
       }
       // paid site: exact output from the same incoming state, then verify + forward
       void* hf = at(ws, W.HF);
-      ff_status e = exec_block(m, m.kinds[l], c->lw[l], cs, cur, hf, ws, ex);
+      ff_status e = ensure_mod(l);
+      if (e) return e;
+      e = exec_block(m, m.kinds[l], c->lw[l], cs, cur, hf, ws, ex, mod_of[l]);
       if (e) return e;
       float* rel = audit ? audit + ((size_t)i * L + l) * m.B : nullptr;
       HIP_TRY(ex.verify(tm, resid ? cur : nullptr, hf, cur, mode == FF_FEATFIX ? 1 : 0, m.B, (size_t)m.N * C, s.eps,

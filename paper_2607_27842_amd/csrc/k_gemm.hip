@@ -200,10 +200,19 @@ __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64) void k_gemm_bf16(GemmAr
 // Synchronisation is explicit: the compiler's barrier lowering waits for ALL outstanding
 // loads (it cannot tell which stage a DMA targets), which would remove the prefetch.  So a
 // step waits only for its own stage (s_waitcnt vmcnt(n) with the later stages still in
-// flight) and then s_barrier, as one volatile asm that is also a compiler memory barrier;
-// fragment reads are ds_read_b128 asm followed by lgkmcnt(0) and tied to the MFMAs through
-// volatile "+v" asms so that no MFMA can consume a fragment before the wait.
+// flight) and then s_barrier, as one volatile asm that is also a compiler memory barrier.
+// Fragments are double-buffered in registers across the two 16-wide k steps of a stage:
+// the reads of the next step (ds_read_b128 asm) are in flight while the MFMAs of the
+// current one run, each step waits with lgkmcnt(TM+TN) for the older reads only, and
+// volatile "+v" asms tie the fragments to the MFMAs so that none is consumed before its
+// wait.  The one barrier per stage sits between the two k steps.
 #define FF_AS1(p) ((const __attribute__((address_space(1))) void*)(p))
+#define FF_WAIT_STAGE(later)                                                                            \
+  do {                                                                                                  \
+    if ((later) >= 2) asm volatile("s_waitcnt vmcnt(%0)\n\ts_barrier" ::"n"(2 * (IA + IB)) : "memory");  \
+    else if ((later) == 1) asm volatile("s_waitcnt vmcnt(%0)\n\ts_barrier" ::"n"(IA + IB) : "memory");  \
+    else asm volatile("s_waitcnt vmcnt(0)\n\ts_barrier" ::: "memory");                                \
+  } while (0)
 #define FF_AS3(p) ((__attribute__((address_space(3))) void*)(p))
 
 __device__ __forceinline__ bf16x8_t lds_rd128(const uint16_t* p) {
@@ -220,7 +229,7 @@ __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64) void k_gemm_dl(GemmArgs
   constexpr int NW = (BM / WM) * NWN;
   constexpr int TM = WM / 32, TN = WN / 32;
   constexpr int IA = BM / 16 / NW, IB = BN / 16 / NW;   // 1 KB DMA instructions per wave per stage
-  static_assert(IA >= 1 && IB >= 1 && NST >= 2 && NST <= 4, "unsupported tile");
+  static_assert(IA >= 1 && IB >= 1 && NST >= 3 && NST <= 4 && TM + TN <= 15, "unsupported tile");
   __shared__ __attribute__((aligned(1024))) uint16_t sA[NST][BM * BKd];
   __shared__ __attribute__((aligned(1024))) uint16_t sB[NST][BN * BKd];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -259,43 +268,70 @@ __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64) void k_gemm_dl(GemmArgs
       for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
   const int wm = (wave / NWN) * WM, wn = (wave % NWN) * WN;
   const int fr = lane & 31, fh = lane >> 5;
+  // fragment offsets within a stage for the two 16-wide k steps
+  int offa[2][TM], offb[2][TN];
+#pragma unroll
+  for (int kk = 0; kk < 2; ++kk) {
+#pragma unroll
+    for (int t = 0; t < TM; ++t) {
+      const int row = wm + t * 32 + fr;
+      offa[kk][t] = row * BKd + (((kk * 2 + fh) ^ ((row >> 2) & 3)) * 8);
+    }
+#pragma unroll
+    for (int t = 0; t < TN; ++t) {
+      const int row = wn + t * 32 + fr;
+      offb[kk][t] = row * BKd + (((kk * 2 + fh) ^ ((row >> 2) & 3)) * 8);
+    }
+  }
   const int nk = a.K / BKd;
 #pragma unroll
   for (int s = 0; s < NST - 1; ++s)
     if (s < nk) FF_ISSUE(s, s * BKd);
+  FF_WAIT_STAGE(min(NST - 2, nk - 1));
+  bf16x8_t fa0[TM], fb0[TN], fa1[TM], fb1[TN];
+#pragma unroll
+  for (int t = 0; t < TM; ++t) fa0[t] = lds_rd128(&sA[0][offa[0][t]]);
+#pragma unroll
+  for (int t = 0; t < TN; ++t) fb0[t] = lds_rd128(&sB[0][offb[0][t]]);
   for (int kt = 0; kt < nk; ++kt) {
     const int st = kt % NST;
-    const int later = min(NST - 2, nk - 1 - kt);   // stages of this wave issued after stage kt
-    if (later >= 2) asm volatile("s_waitcnt vmcnt(%0)\n\ts_barrier" ::"n"(2 * (IA + IB)) : "memory");
-    else if (later == 1) asm volatile("s_waitcnt vmcnt(%0)\n\ts_barrier" ::"n"(IA + IB) : "memory");
-    else asm volatile("s_waitcnt vmcnt(0)\n\ts_barrier" ::: "memory");
-    // every wave has finished reading stage kt-1: its buffer takes stage kt+NST-1
-    if (kt + NST - 1 < nk) FF_ISSUE((kt + NST - 1) % NST, (kt + NST - 1) * BKd);
+    // second k step of stage kt in flight while the first one's MFMAs run
 #pragma unroll
-    for (int kk = 0; kk < 2; ++kk) {
-      bf16x8_t fa[TM], fb[TN];
-      const int ch = kk * 2 + fh;
+    for (int t = 0; t < TM; ++t) fa1[t] = lds_rd128(&sA[st][offa[1][t]]);
 #pragma unroll
-      for (int t = 0; t < TM; ++t) {
-        const int row = wm + t * 32 + fr;
-        fa[t] = lds_rd128(&sA[st][row * BKd + ((ch ^ ((row >> 2) & 3)) * 8)]);
-      }
+    for (int t = 0; t < TN; ++t) fb1[t] = lds_rd128(&sB[st][offb[1][t]]);
+    asm volatile("s_waitcnt lgkmcnt(%0)" ::"n"(TM + TN) : "memory");
 #pragma unroll
-      for (int t = 0; t < TN; ++t) {
-        const int row = wn + t * 32 + fr;
-        fb[t] = lds_rd128(&sB[st][row * BKd + ((ch ^ ((row >> 2) & 3)) * 8)]);
-      }
+    for (int t = 0; t < TM; ++t) asm volatile("" : "+v"(fa0[t]));
+#pragma unroll
+    for (int t = 0; t < TN; ++t) asm volatile("" : "+v"(fb0[t]));
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+      for (int j = 0; j < TN; ++j) acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fb0[j], fa0[i], acc[i][j], 0, 0, 0);
+    if (kt + 1 < nk) {
+      // stage kt+1 complete everywhere, and every wave is past its reads of stage kt-1,
+      // whose buffer now takes stage kt+NST-1; then the first k step of stage kt+1 is
+      // read while the second one of stage kt computes
+      FF_WAIT_STAGE(min(NST - 3, nk - 2 - kt));
+      if (kt + NST - 1 < nk) FF_ISSUE((kt + NST - 1) % NST, (kt + NST - 1) * BKd);
+      const int sn = (kt + 1) % NST;
+#pragma unroll
+      for (int t = 0; t < TM; ++t) fa0[t] = lds_rd128(&sA[sn][offa[0][t]]);
+#pragma unroll
+      for (int t = 0; t < TN; ++t) fb0[t] = lds_rd128(&sB[sn][offb[0][t]]);
+      asm volatile("s_waitcnt lgkmcnt(%0)" ::"n"(TM + TN) : "memory");
+    } else {
       asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
-#pragma unroll
-      for (int t = 0; t < TM; ++t) asm volatile("" : "+v"(fa[t]));
-#pragma unroll
-      for (int t = 0; t < TN; ++t) asm volatile("" : "+v"(fb[t]));
-#pragma unroll
-      for (int i = 0; i < TM; ++i)
-#pragma unroll
-        for (int j = 0; j < TN; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fb[j], fa[i], acc[i][j], 0, 0, 0);
     }
+#pragma unroll
+    for (int t = 0; t < TM; ++t) asm volatile("" : "+v"(fa1[t]));
+#pragma unroll
+    for (int t = 0; t < TN; ++t) asm volatile("" : "+v"(fb1[t]));
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+      for (int j = 0; j < TN; ++j) acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fb1[j], fa1[i], acc[i][j], 0, 0, 0);
   }
 #undef FF_ISSUE
   // lane owns output row m (lane % 32) and 4 groups of 4 consecutive columns
@@ -374,15 +410,16 @@ void launch_dl(const GemmArgs& a, hipStream_t s) {
                      a, tm, tn);
 }
 
-// Tile choice (measured on MI355X): 256x256 tiles (8 wavefronts of 128x64, 3 stages, loads
-// with sc0|sc1 so the streamed tiles skip the L1) when they fill the chip; else 128x128
-// (8 wavefronts of 64x32, 4 stages, two workgroups per CU).  K % 32 != 0 (the patch
+// Tile choice (measured on MI355X): 256x256 tiles (8 wavefronts of 128x64, 4 stages, loads
+// with sc0|sc1 so the streamed tiles skip the L1) from 160 such tiles on (below that the
+// 256 CUs are underfilled); else 128x128 (8 wavefronts of 64x32, 4 stages, two workgroups
+// per CU).  K % 32 != 0 (the patch
 // embedding) takes the register-staged kernel.
 template <int EPI, bool OF, bool RF>
 void launch_bf16(const GemmArgs& a, hipStream_t s) {
   const long big = (long)((a.M + 255) / 256) * ((a.N + 255) / 256);
   if (a.K % 32 != 0) launch_tile<128, 128, 64, 32, EPI, OF, RF>(a, s);
-  else if (big >= 200) launch_dl<256, 256, 128, 64, 3, 17, EPI, OF, RF>(a, s);
+  else if (big >= 160) launch_dl<256, 256, 128, 64, 4, 17, EPI, OF, RF>(a, s);
   else launch_dl<128, 128, 64, 32, 4, 0, EPI, OF, RF>(a, s);
 }
 

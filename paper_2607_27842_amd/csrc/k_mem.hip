@@ -78,7 +78,14 @@ __global__ __launch_bounds__(kThreads) void k_draft_run(Terms t, int layers, siz
     const size_t i = c * S::V;
     float xv[S::V];
     if (RES) S::load(x, i, xv);
-    for (int l = 0; l < layers; ++l) draft_math<DT, RES>(t, (size_t)l * layer_stride + i, xv, xv);
+    // four layers per pass: their history loads do not depend on the running value, so
+    // all of them are in flight together
+    int l = 0;
+    for (; l + 4 <= layers; l += 4) {
+#pragma unroll
+      for (int q = 0; q < 4; ++q) draft_math<DT, RES>(t, (size_t)(l + q) * layer_stride + i, xv, xv);
+    }
+    for (; l < layers; ++l) draft_math<DT, RES>(t, (size_t)l * layer_stride + i, xv, xv);
     S::store(x, i, xv);
   }
 }
@@ -109,7 +116,7 @@ __device__ __forceinline__ void block_sum2(float& a, float& b) {
   }
 }
 
-constexpr int kMaxVerifyBlocks = 256;  // partial-sum blocks per sample
+constexpr int kMaxVerifyBlocks = 2048;  // partial-sum blocks per sample
 
 // Verify + replace (Eq. 3-5): rebuild the draft from the same incoming u, accumulate
 // sum|h_d - h_f| and sum|h_f| for this sample, and forward h_f (FeatFix) or h_d (Verify).
@@ -218,7 +225,7 @@ hipError_t verify(int dtype, const Terms& t, const void* u, const void* hf, void
                   int B, size_t Eb, float eps, float* rel_l1, float* partials, hipStream_t s) {
   const int V = dtype == DT_BF16 ? 8 : 4;
   const size_t cps = Eb / V;
-  int nblk = cdiv((long)cps, kThreads * 4);
+  int nblk = cdiv((long)cps, kThreads);
   if (nblk > kMaxVerifyBlocks) nblk = kMaxVerifyBlocks;
   if (nblk < 1) nblk = 1;
   dim3 grid(nblk, B);

@@ -106,6 +106,40 @@ __global__ __launch_bounds__(256) void k_rms_heads(RmsArgs a) {
   }
 }
 
+// q and k of a row in one pass: each lane owns one 16-byte chunk of the row's [q | k]
+// columns, the LPH = d / V lanes of a head add their sums of squares with xor shuffles
+// (fixed order), and every lane rescales its own chunk.  One wavefront covers 64 chunks.
+template <int DT, int LPH>
+__global__ __launch_bounds__(256) void k_rms_qk(RmsQKArgs a) {
+  using S = St<DT>;
+  const int lane = threadIdx.x & 63;
+  const long wv = (long)blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int span = 2 * a.H * a.d;                 // q and k columns
+  const int nseg = (span + 64 * S::V - 1) / (64 * S::V);
+  const long r = wv / nseg;
+  if (r >= a.rows) return;                        // whole wavefront, no barrier below
+  const int col = (int)(wv % nseg) * 64 * S::V + lane * S::V;
+  const bool on = col < span;
+  const size_t base = (size_t)a.map.phys((int)r) * a.ld;
+  float v[S::V];
+  float ss = 0.f;
+  if (on) {
+    S::load(a.x, base + col, v);
+#pragma unroll
+    for (int j = 0; j < S::V; ++j) ss = fmaf(v[j], v[j], ss);
+  }
+#pragma unroll
+  for (int o = LPH / 2; o >= 1; o /= 2) ss += __shfl_xor(ss, o, 64);
+  if (!on) return;
+  const float inv = 1.0f / sqrtf(ss / (float)a.d + a.eps);
+  const int qk = col >= a.H * a.d;
+  const int e = (col - qk * a.H * a.d) % a.d;
+  const void* g = qk ? a.gk : a.gq;
+#pragma unroll
+  for (int j = 0; j < S::V; ++j) v[j] = v[j] * inv * S::ld1(g, e + j);
+  S::store(a.x, base + col, v);
+}
+
 constexpr int kGemvMaxB = 8;
 constexpr int kGemvRows = 4;     // output features per wavefront
 constexpr int kGemvKC = 1024;    // K chunk of the activations staged in LDS
@@ -116,12 +150,12 @@ constexpr int kGemvKC = 1024;    // K chunk of the activations staged in LDS
 // -> consecutive chunks of a row) and every thread all of its activation loads, so the
 // chunk costs one memory round trip; then one sum per (row, sample) is accumulated.
 template <int DT>
-__global__ __launch_bounds__(256) void k_gemv(GemvArgs a) {
+__device__ __forceinline__ void gemv_tile(const GemvArgs a, int blk) {
   using S = St<DT>;
   constexpr int kPer = kGemvKC / S::V / 64;   // weight chunks per lane per K chunk
   extern __shared__ float xs[];               // [B][kGemvKC]
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int n0 = (blockIdx.x * 4 + wave) * kGemvRows;
+  const int n0 = (blk * 4 + wave) * kGemvRows;
   float acc[kGemvRows][kGemvMaxB];
 #pragma unroll
   for (int r = 0; r < kGemvRows; ++r)
@@ -204,6 +238,20 @@ __global__ __launch_bounds__(256) void k_gemv(GemvArgs a) {
   }
 }
 
+template <int DT>
+__global__ __launch_bounds__(256) void k_gemv(GemvArgs a) { gemv_tile<DT>(a, blockIdx.x); }
+
+// Several independent GEMVs over the same activations in one launch (blockIdx.y = job):
+// the modulation vectors of every exact layer of a step, so that the weight streams of
+// all of them share one grid instead of one small launch each.
+template <int DT>
+__global__ __launch_bounds__(256) void k_gemv_batch(GemvBatch bt) {
+  const GemvJob j = bt.job[blockIdx.y];
+  if ((int)blockIdx.x * 4 * kGemvRows >= j.Nout) return;   // whole workgroup: no barrier skipped
+  const GemvArgs a{bt.x, bt.ldx, bt.silu_in, j.W, j.bias, j.Nout, bt.K, bt.B, j.y, j.ldy, 0, nullptr, 0};
+  gemv_tile<DT>(a, blockIdx.x);
+}
+
 __global__ void k_time_embed(double s, float* phi) {
   const int k = threadIdx.x;  // 0..127
   const double f = exp(-log(10000.0) * (double)k / 128.0);
@@ -277,11 +325,48 @@ hipError_t rms_heads(int dtype, const RmsArgs& a, hipStream_t s) {
   return hipGetLastError();
 }
 
+hipError_t rms_qk(int dtype, const RmsQKArgs& a, hipStream_t s) {
+  if (a.rows == 0) return hipSuccess;
+  const int V = dtype == DT_BF16 ? 8 : 4;
+  const int lph = a.d / V;
+  const bool fast = a.d % V == 0 && (lph == 8 || lph == 16 || lph == 32) && (64 * V) % a.d == 0;
+  if (!fast) {   // per-head thread kernel, q then k
+    RmsArgs q{a.x, a.ld, a.map, a.rows, a.H, a.d, 0, a.gq, a.eps};
+    hipError_t e = rms_heads(dtype, q, s);
+    if (e != hipSuccess) return e;
+    RmsArgs k{a.x, a.ld, a.map, a.rows, a.H, a.d, a.H * a.d, a.gk, a.eps};
+    return rms_heads(dtype, k, s);
+  }
+  const int nseg = cdiv(2 * a.H * a.d, 64 * V);
+  const int grid = cdiv((long)a.rows * nseg, 4);
+#define FF_RMS(LPH)                                                            \
+  do {                                                                         \
+    if (dtype == DT_BF16) FF_LAUNCH((k_rms_qk<DT_BF16, LPH>), grid, 256, 0, s, a); \
+    else FF_LAUNCH((k_rms_qk<DT_F32, LPH>), grid, 256, 0, s, a);              \
+  } while (0)
+  if (lph == 8) FF_RMS(8);
+  else if (lph == 16) FF_RMS(16);
+  else FF_RMS(32);
+#undef FF_RMS
+  return hipGetLastError();
+}
+
 hipError_t gemv(int dtype, const GemvArgs& a, hipStream_t s) {
   const int grid = cdiv(a.Nout, 4 * kGemvRows);
   const size_t lds = (size_t)a.B * kGemvKC * sizeof(float);
   if (dtype == DT_BF16) FF_LAUNCH(k_gemv<DT_BF16>, grid, 256, lds, s, a);
   else FF_LAUNCH(k_gemv<DT_F32>, grid, 256, lds, s, a);
+  return hipGetLastError();
+}
+
+hipError_t gemv_batch(int dtype, const GemvBatch& bt, hipStream_t s) {
+  if (bt.njobs <= 0) return hipSuccess;
+  int nmax = 0;
+  for (int i = 0; i < bt.njobs; ++i) nmax = max(nmax, bt.job[i].Nout);
+  const dim3 grid(cdiv(nmax, 4 * kGemvRows), bt.njobs);
+  const size_t lds = (size_t)bt.B * kGemvKC * sizeof(float);
+  if (dtype == DT_BF16) FF_LAUNCH(k_gemv_batch<DT_BF16>, grid, 256, lds, s, bt);
+  else FF_LAUNCH(k_gemv_batch<DT_F32>, grid, 256, lds, s, bt);
   return hipGetLastError();
 }
 

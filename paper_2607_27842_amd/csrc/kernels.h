@@ -56,6 +56,19 @@ struct GemvArgs {
   const float* add; int ldadd;
 };
 hipError_t gemv(int dtype, const GemvArgs& a, hipStream_t s);
+// Up to kGemvJobs GEMVs sharing x (and K, B, SiLU on input) in one launch; no add term,
+// no SiLU on output.  B <= 8.
+constexpr int kGemvJobs = 32;
+struct GemvJob {
+  const void* W; const void* bias; float* y;
+  int Nout, ldy;
+};
+struct GemvBatch {
+  const float* x; int ldx; int silu_in;
+  int K, B, njobs;
+  GemvJob job[kGemvJobs];
+};
+hipError_t gemv_batch(int dtype, const GemvBatch& bt, hipStream_t s);
 
 // ---------------------------------------------------------------- normalisation
 // out[phys(r), :C] = LN(in[phys(r), :C]) * (1 + scale[b*ldm + :]) + shift[b*ldm + :]
@@ -74,6 +87,13 @@ struct RmsArgs {
   const void* g; float eps;
 };
 hipError_t rms_heads(int dtype, const RmsArgs& a, hipStream_t s);
+// Both per-head RMSNorms of a qkv row block: q at columns [0, H*d) with gain gq, k at
+// [H*d, 2*H*d) with gain gk (in place).
+struct RmsQKArgs {
+  void* x; int ld; RowMap map; int rows, H, d;
+  const void* gq; const void* gk; float eps;
+};
+hipError_t rms_qk(int dtype, const RmsQKArgs& a, hipStream_t s);
 
 // ---------------------------------------------------------------- attention
 // out[b*N + i, h*d + e] = softmax_j(q_i . k_j * scale) v_j,  q/k/v read from
