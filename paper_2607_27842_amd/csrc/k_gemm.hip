@@ -26,41 +26,77 @@ __device__ __forceinline__ void epilogue_store(const GemmArgs a, int r, int c, f
   else St<DT>::st1(a.out, pr * a.ldo + c, v);
 }
 
-// Epilogue for 4 consecutive output columns c..c+3 of row r (N % 8 == 0, so all four are
-// in range when c is): 8/16-byte loads of bias, gate and residual and one vector store.
-template <int EPI, bool OUT_F32, bool RES_F32>
-__device__ __forceinline__ void epilogue4_bf16(const GemmArgs a, int r, int c, f32x4_t acc) {
+// Epilogue of one wavefront's TM x TN block of 32x32 MFMA tiles (acc), whose rows start at
+// rbase and columns at cbase: lane l owns row rbase + 32 i + l%32 and, per 32-column tile,
+// 4 groups of 4 consecutive columns (8 q + 4 (l/32)).  All loads of a row block (bias,
+// gate, residual) are issued before any is used, from clamped in-range addresses rather
+// than behind per-group branches, so the block costs one memory round trip; only the
+// stores are predicated (N % 8 == 0: a group is in range as a whole).
+template <int TM, int TN, int EPI, bool OUT_F32, bool RES_F32>
+__device__ __forceinline__ void epilogue_block(const GemmArgs a, int rbase, int cbase, const f32x16_t (&acc)[TM][TN]) {
+  const int lane = threadIdx.x & 63, fr = lane & 31, fh = lane >> 5;
   const uint16_t* bias = reinterpret_cast<const uint16_t*>(a.bias);
-  const u32x2_t bw = *reinterpret_cast<const u32x2_t*>(bias + c);
-  float v[4] = {acc[0] + __uint_as_float(bw[0] << 16), acc[1] + __uint_as_float(bw[0] & 0xffff0000u),
-                acc[2] + __uint_as_float(bw[1] << 16), acc[3] + __uint_as_float(bw[1] & 0xffff0000u)};
-  if (EPI == EPI_BIAS_GELU) {
+  int col[TN][4];
+  u32x2_t bw[TN][4];
 #pragma unroll
-    for (int j = 0; j < 4; ++j) v[j] = gelu_tanh_f(v[j]);
-  }
-  const size_t pr = (size_t)a.omap.phys(r);
-  if (EPI == EPI_GATED) {
-    float res[4];
-    if (RES_F32) {
-      const f32x4_t q = *reinterpret_cast<const f32x4_t*>(reinterpret_cast<const float*>(a.resid) + pr * a.ldr + c);
-      res[0] = q[0]; res[1] = q[1]; res[2] = q[2]; res[3] = q[3];
-    } else {
-      const u32x2_t q = *reinterpret_cast<const u32x2_t*>(reinterpret_cast<const uint16_t*>(a.resid) + pr * a.ldr + c);
-      res[0] = __uint_as_float(q[0] << 16); res[1] = __uint_as_float(q[0] & 0xffff0000u);
-      res[2] = __uint_as_float(q[1] << 16); res[3] = __uint_as_float(q[1] & 0xffff0000u);
+  for (int j = 0; j < TN; ++j)
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      col[j][q] = cbase + j * 32 + q * 8 + fh * 4;
+      bw[j][q] = *reinterpret_cast<const u32x2_t*>(bias + (col[j][q] < a.N ? col[j][q] : 0));
     }
-    const f32x4_t g = *reinterpret_cast<const f32x4_t*>(a.gate + (size_t)a.omap.sample(r) * a.ldg + c);
 #pragma unroll
-    for (int j = 0; j < 4; ++j) v[j] = res[j] + g[j] * v[j];
-  }
-  if (OUT_F32) {
-    const f32x4_t o = {v[0], v[1], v[2], v[3]};
-    *reinterpret_cast<f32x4_t*>(reinterpret_cast<float*>(a.out) + pr * a.ldo + c) = o;
-  } else {
-    u32x2_t o;
-    o[0] = (uint32_t)f2bf(v[0]) | ((uint32_t)f2bf(v[1]) << 16);
-    o[1] = (uint32_t)f2bf(v[2]) | ((uint32_t)f2bf(v[3]) << 16);
-    *reinterpret_cast<u32x2_t*>(reinterpret_cast<uint16_t*>(a.out) + pr * a.ldo + c) = o;
+  for (int i = 0; i < TM; ++i) {
+    const int r = rbase + i * 32 + fr;
+    const bool rok = r < a.M;
+    const size_t pr = (size_t)a.omap.phys(rok ? r : 0);
+    f32x4_t gt[TN][4], rs[TN][4];
+    if (EPI == EPI_GATED) {
+      const float* grow = a.gate + (size_t)a.omap.sample(rok ? r : 0) * a.ldg;
+#pragma unroll
+      for (int j = 0; j < TN; ++j)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const int c = col[j][q] < a.N ? col[j][q] : 0;
+          gt[j][q] = *reinterpret_cast<const f32x4_t*>(grow + c);
+          if (RES_F32) {
+            rs[j][q] = *reinterpret_cast<const f32x4_t*>(reinterpret_cast<const float*>(a.resid) + pr * a.ldr + c);
+          } else {
+            const u32x2_t w = *reinterpret_cast<const u32x2_t*>(reinterpret_cast<const uint16_t*>(a.resid) + pr * a.ldr + c);
+            rs[j][q][0] = __uint_as_float(w[0] << 16); rs[j][q][1] = __uint_as_float(w[0] & 0xffff0000u);
+            rs[j][q][2] = __uint_as_float(w[1] << 16); rs[j][q][3] = __uint_as_float(w[1] & 0xffff0000u);
+          }
+        }
+    }
+#pragma unroll
+    for (int j = 0; j < TN; ++j)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        float v[4] = {acc[i][j][4 * q] + __uint_as_float(bw[j][q][0] << 16),
+                      acc[i][j][4 * q + 1] + __uint_as_float(bw[j][q][0] & 0xffff0000u),
+                      acc[i][j][4 * q + 2] + __uint_as_float(bw[j][q][1] << 16),
+                      acc[i][j][4 * q + 3] + __uint_as_float(bw[j][q][1] & 0xffff0000u)};
+        if (EPI == EPI_BIAS_GELU) {
+#pragma unroll
+          for (int e = 0; e < 4; ++e) v[e] = gelu_tanh_f(v[e]);
+        }
+        if (EPI == EPI_GATED) {
+#pragma unroll
+          for (int e = 0; e < 4; ++e) v[e] = rs[j][q][e] + gt[j][q][e] * v[e];
+        }
+        if (rok && col[j][q] < a.N) {
+          const int c = col[j][q];
+          if (OUT_F32) {
+            const f32x4_t o = {v[0], v[1], v[2], v[3]};
+            *reinterpret_cast<f32x4_t*>(reinterpret_cast<float*>(a.out) + pr * a.ldo + c) = o;
+          } else {
+            u32x2_t o;
+            o[0] = (uint32_t)f2bf(v[0]) | ((uint32_t)f2bf(v[1]) << 16);
+            o[1] = (uint32_t)f2bf(v[2]) | ((uint32_t)f2bf(v[3]) << 16);
+            *reinterpret_cast<u32x2_t*>(reinterpret_cast<uint16_t*>(a.out) + pr * a.ldo + c) = o;
+          }
+        }
+      }
   }
 }
 
@@ -174,21 +210,7 @@ __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64) void k_gemm_bf16(GemmAr
   }
 #undef FF_GLOAD
 #undef FF_SSTORE
-#pragma unroll
-  for (int i = 0; i < TM; ++i) {
-    const int r = m0 + wm + i * 32 + fr;
-    if (r >= a.M) continue;
-#pragma unroll
-    for (int j = 0; j < TN; ++j)
-#pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        const int c = n0 + wn + j * 32 + q * 8 + (lane >> 5) * 4;
-        if (c < a.N) {
-          const f32x4_t v4 = {acc[i][j][4 * q], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2], acc[i][j][4 * q + 3]};
-          epilogue4_bf16<EPI, OUT_F32, RES_F32>(a, r, c, v4);
-        }
-      }
-  }
+  epilogue_block<TM, TN, EPI, OUT_F32, RES_F32>(a, m0 + wm, n0 + wn, acc);
 }
 // ------------------------------------------------------------------ bf16 MFMA GEMM, direct-to-LDS
 // For K % 32 == 0.  Operand tiles go global -> LDS with global_load_lds_dwordx4 (no VGPR
@@ -334,22 +356,7 @@ __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64) void k_gemm_dl(GemmArgs
       for (int j = 0; j < TN; ++j) acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fb1[j], fa1[i], acc[i][j], 0, 0, 0);
   }
 #undef FF_ISSUE
-  // lane owns output row m (lane % 32) and 4 groups of 4 consecutive columns
-#pragma unroll
-  for (int i = 0; i < TM; ++i) {
-    const int r = m0 + wm + i * 32 + fr;
-    if (r >= a.M) continue;
-#pragma unroll
-    for (int j = 0; j < TN; ++j)
-#pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        const int c = n0 + wn + j * 32 + q * 8 + fh * 4;
-        if (c < a.N) {
-          const f32x4_t v4 = {acc[i][j][4 * q], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2], acc[i][j][4 * q + 3]};
-          epilogue4_bf16<EPI, OUT_F32, RES_F32>(a, r, c, v4);
-        }
-      }
-  }
+  epilogue_block<TM, TN, EPI, OUT_F32, RES_F32>(a, m0 + wm, n0 + wn, acc);
 }
 
 // ------------------------------------------------------------------ fp32 FMA GEMM

@@ -238,6 +238,91 @@ __device__ __forceinline__ void gemv_tile(const GemvArgs a, int blk) {
   }
 }
 
+// bf16 weights, B <= 8: y[b, n0..n0+15] on v_mfma_f32_16x16x32_bf16.  The fp32 activations
+// are split once (k_gemv_split) into bf16 hi + lo parts (x = hi + lo to ~2^-17 relative);
+// MFMA rows 0-7 carry hi of samples 0-7 and rows 8-15 lo, so one instruction covers both
+// halves and output rows b and b+8 are added at the end.  The four wavefronts take
+// interleaved 32-wide K steps and their 16x16 partial tiles are summed through LDS in
+// wavefront order.  16x16x32 layouts: A lane l holds row l%16, k = 8*(l/16)+0..7; B lane
+// l holds column l%16, same k; D lane l holds column l%16, rows 4*(l/16)+0..3.
+constexpr int kMvU = 4;   // K steps per wavefront whose loads are issued together
+
+__global__ __launch_bounds__(256) void k_gemv_split(const float* __restrict__ x, int ldx, int silu_in, int K, int B,
+                                                    uint16_t* __restrict__ xs) {
+  const int t = blockIdx.x * 256 + threadIdx.x;   // one 8-wide chunk of one sample
+  const int kc = K / 8;
+  if (t >= B * kc) return;
+  const int b = t / kc, k = (t % kc) * 8;
+  const f32x4_t v0 = *reinterpret_cast<const f32x4_t*>(x + (size_t)b * ldx + k);
+  const f32x4_t v1 = *reinterpret_cast<const f32x4_t*>(x + (size_t)b * ldx + k + 4);
+  u32x4_t hi, lo;
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    float a0 = j < 2 ? v0[2 * j] : v1[2 * j - 4], a1 = j < 2 ? v0[2 * j + 1] : v1[2 * j - 3];
+    if (silu_in) { a0 = silu_f(a0); a1 = silu_f(a1); }
+    const uint16_t h0 = f2bf(a0), h1 = f2bf(a1);
+    const uint16_t l0 = f2bf(a0 - bf2f(h0)), l1 = f2bf(a1 - bf2f(h1));
+    hi[j] = (uint32_t)h0 | ((uint32_t)h1 << 16);
+    lo[j] = (uint32_t)l0 | ((uint32_t)l1 << 16);
+  }
+  *reinterpret_cast<u32x4_t*>(xs + (size_t)b * K + k) = hi;
+  *reinterpret_cast<u32x4_t*>(xs + (size_t)(8 + b) * K + k) = lo;
+}
+
+__device__ __forceinline__ void gemv_mfma_tile(const GemvArgs a, int blk) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int n0 = blk * 16;
+  const int rc = lane & 15, kq = (lane >> 4) * 8;
+  const int n = n0 + rc;
+  const bool nok = n < a.Nout, bok = (rc & 7) < a.B;
+  const uint16_t* wrow = reinterpret_cast<const uint16_t*>(a.W) + (size_t)(nok ? n : 0) * a.K;
+  const uint16_t* xrow = a.xs + (size_t)rc * a.K;
+  const int nks = (a.K + 31) / 32;
+  const u32x4_t z4 = {0u, 0u, 0u, 0u};
+  f32x4_t acc = {0.f, 0.f, 0.f, 0.f};
+  for (int ks0 = wave; ks0 < nks; ks0 += 4 * kMvU) {
+    u32x4_t wv[kMvU], xv[kMvU];
+#pragma unroll
+    for (int u = 0; u < kMvU; ++u) {
+      const int k = (ks0 + 4 * u) * 32 + kq;
+      const bool kin = ks0 + 4 * u < nks && k < a.K;   // K % 8 == 0: a lane's 8 are all in or out
+      wv[u] = (kin && nok) ? *reinterpret_cast<const u32x4_t*>(wrow + k) : z4;
+      xv[u] = (kin && bok) ? *reinterpret_cast<const u32x4_t*>(xrow + k) : z4;
+    }
+#pragma unroll
+    for (int u = 0; u < kMvU; ++u)
+      acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, xv[u]), __builtin_bit_cast(bf16x8_t, wv[u]),
+                                                   acc, 0, 0, 0);
+  }
+  __shared__ float red[4][64][4];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) red[wave][lane][j] = acc[j];
+  __syncthreads();
+  if (threadIdx.x < 128) {
+    const int ob = threadIdx.x >> 4, on = threadIdx.x & 15;   // output (sample, column)
+    const int lh = (ob >> 2) * 16 + on, ll = ((ob >> 2) + 2) * 16 + on, j = ob & 3;
+    float hi = 0.f, lw = 0.f;
+#pragma unroll
+    for (int w = 0; w < 4; ++w) { hi += red[w][lh][j]; lw += red[w][ll][j]; }
+    const int nn = n0 + on;
+    if (ob < a.B && nn < a.Nout) {
+      float y = (hi + lw) + St<DT_BF16>::ld1(a.bias, nn);
+      if (a.silu_out) y = silu_f(y);
+      if (a.add) y += a.add[(size_t)ob * a.ldadd + nn];
+      a.y[(size_t)ob * a.ldy + nn] = y;
+    }
+  }
+}
+
+__global__ __launch_bounds__(256) void k_gemv_mfma(GemvArgs a) { gemv_mfma_tile(a, blockIdx.x); }
+
+__global__ __launch_bounds__(256) void k_gemv_mfma_batch(GemvBatch bt) {
+  const GemvJob j = bt.job[blockIdx.y];
+  if ((int)blockIdx.x * 16 >= j.Nout) return;   // whole workgroup: no barrier skipped
+  const GemvArgs a{bt.x, bt.ldx, bt.silu_in, j.W, j.bias, j.Nout, bt.K, bt.B, j.y, j.ldy, 0, nullptr, 0, bt.xs};
+  gemv_mfma_tile(a, blockIdx.x);
+}
+
 template <int DT>
 __global__ __launch_bounds__(256) void k_gemv(GemvArgs a) { gemv_tile<DT>(a, blockIdx.x); }
 
@@ -248,7 +333,7 @@ template <int DT>
 __global__ __launch_bounds__(256) void k_gemv_batch(GemvBatch bt) {
   const GemvJob j = bt.job[blockIdx.y];
   if ((int)blockIdx.x * 4 * kGemvRows >= j.Nout) return;   // whole workgroup: no barrier skipped
-  const GemvArgs a{bt.x, bt.ldx, bt.silu_in, j.W, j.bias, j.Nout, bt.K, bt.B, j.y, j.ldy, 0, nullptr, 0};
+  const GemvArgs a{bt.x, bt.ldx, bt.silu_in, j.W, j.bias, j.Nout, bt.K, bt.B, j.y, j.ldy, 0, nullptr, 0, nullptr};
   gemv_tile<DT>(a, blockIdx.x);
 }
 
@@ -352,6 +437,10 @@ hipError_t rms_qk(int dtype, const RmsQKArgs& a, hipStream_t s) {
 }
 
 hipError_t gemv(int dtype, const GemvArgs& a, hipStream_t s) {
+  if (dtype == DT_BF16 && a.xs) {
+    FF_LAUNCH(k_gemv_mfma, cdiv(a.Nout, 16), 256, 0, s, a);
+    return hipGetLastError();
+  }
   const int grid = cdiv(a.Nout, 4 * kGemvRows);
   const size_t lds = (size_t)a.B * kGemvKC * sizeof(float);
   if (dtype == DT_BF16) FF_LAUNCH(k_gemv<DT_BF16>, grid, 256, lds, s, a);
@@ -359,10 +448,19 @@ hipError_t gemv(int dtype, const GemvArgs& a, hipStream_t s) {
   return hipGetLastError();
 }
 
+hipError_t gemv_split(const float* x, int ldx, int silu_in, int K, int B, uint16_t* xs, hipStream_t s) {
+  FF_LAUNCH(k_gemv_split, cdiv((long)B * (K / 8), 256), 256, 0, s, x, ldx, silu_in, K, B, xs);
+  return hipGetLastError();
+}
+
 hipError_t gemv_batch(int dtype, const GemvBatch& bt, hipStream_t s) {
   if (bt.njobs <= 0) return hipSuccess;
   int nmax = 0;
   for (int i = 0; i < bt.njobs; ++i) nmax = max(nmax, bt.job[i].Nout);
+  if (dtype == DT_BF16 && bt.xs) {
+    FF_LAUNCH(k_gemv_mfma_batch, dim3(cdiv(nmax, 16), bt.njobs), 256, 0, s, bt);
+    return hipGetLastError();
+  }
   const dim3 grid(cdiv(nmax, 4 * kGemvRows), bt.njobs);
   const size_t lds = (size_t)bt.B * kGemvKC * sizeof(float);
   if (dtype == DT_BF16) FF_LAUNCH(k_gemv_batch<DT_BF16>, grid, 256, lds, s, bt);

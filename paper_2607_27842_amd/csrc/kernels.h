@@ -48,14 +48,19 @@ hipError_t gemm(int dtype, const GemmArgs& a, hipStream_t s);
 
 // y[b, n] = (add ? add[b*ldadd + n] : 0) + act( sum_k f(x[b*ldx + k]) * W[n, k] + bias[n] )
 // x, y, add fp32; W, bias model dtype; f = SiLU if silu_in; act = SiLU if silu_out.
+// bf16 weights with xs set run on MFMA and read the activations from xs ([16, K] bf16,
+// 16-byte aligned), which gemv_split must have filled from the same x first: f(x) split
+// into bf16 hi (rows 0..B-1) and lo (rows 8..8+B-1) parts, f(x) = hi + lo to ~2^-17.
 struct GemvArgs {
   const float* x; int ldx; int silu_in;
   const void* W; const void* bias;
   int Nout, K, B;
   float* y; int ldy; int silu_out;
   const float* add; int ldadd;
+  uint16_t* xs;
 };
 hipError_t gemv(int dtype, const GemvArgs& a, hipStream_t s);
+hipError_t gemv_split(const float* x, int ldx, int silu_in, int K, int B, uint16_t* xs, hipStream_t s);
 // Up to kGemvJobs GEMVs sharing x (and K, B, SiLU on input) in one launch; no add term,
 // no SiLU on output.  B <= 8.
 constexpr int kGemvJobs = 32;
@@ -66,8 +71,10 @@ struct GemvJob {
 struct GemvBatch {
   const float* x; int ldx; int silu_in;
   int K, B, njobs;
+  uint16_t* xs;   // as GemvArgs::xs (bf16 only)
   GemvJob job[kGemvJobs];
 };
+inline size_t gemv_split_bytes(int K) { return (size_t)16 * K * 2; }
 hipError_t gemv_batch(int dtype, const GemvBatch& bt, hipStream_t s);
 
 // ---------------------------------------------------------------- normalisation
