@@ -31,7 +31,8 @@ PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
 PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
 CALIB_BYTES = 256 << 20     # plain copy of known size, the scale for FETCH_SIZE / WRITE_SIZE
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_gemm_dit_xl2.json")
-GEMM_SOURCE = os.path.join(ROOT, "paper_2607_27842_amd", "csrc", "k_gemm.hip")
+# the GEMM kernels and the device helpers their epilogue uses: traffic counters belong to these exact sources
+GEMM_SOURCES = [os.path.join(ROOT, "paper_2607_27842_amd", "csrc", f) for f in ("k_gemm.hip", "dev_common.h")]
 
 
 def log(*a):
@@ -138,7 +139,10 @@ def gemm_traffic():
         rec = json.load(open(TRAFFIC_FILE))
     except (OSError, ValueError):
         return None
-    sha = hashlib.sha256(open(GEMM_SOURCE, "rb").read()).hexdigest()
+    h = hashlib.sha256()
+    for f in GEMM_SOURCES:
+        h.update(open(f, "rb").read())
+    sha = h.hexdigest()
     if rec.get("gemm_source_sha256") != sha:
         return None
     return rec.get("bytes_per_launch")
@@ -261,7 +265,7 @@ def main():
     achieved = g["flops"] / (g["ms"] / 1e3) / 1e12
     roof = {"bound": "mfma", "achieved": round(achieved, 1), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
             "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": gemm_traffic(),
-            "kernel": "k_gemm_bf16 (all exact-block GEMM launches of one FeatFix loop)",
+            "kernel": "k_gemm_dl / k_gemm_bf16 (all exact-block GEMM launches of one FeatFix loop)",
             "avg_launch_us": round(g["ms"] * 1e3 / g["launches"], 3),
             "flop_per_launch": g["flops"] / g["launches"]}
     hbm = {}
