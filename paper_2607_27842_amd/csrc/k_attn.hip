@@ -39,11 +39,13 @@ __global__ __launch_bounds__(NW * 64) void k_attn32(AttnArgs a) {
   constexpr int LDV = KT + 8;         // V^T tile row stride
   constexpr int NQC = DQ / 16;        // 16-wide head-dim chunks of QK^T
   constexpr int NOT = DV / 32;        // 32-wide output tiles of the head dim
-  constexpr int KCH = KT * (DQ / 8);  // 16-byte chunks of a K tile (DQ >= DV)
-  constexpr int PER = (KCH + NT - 1) / NT;
+  constexpr int KCH = KT * (DQ / 8);  // 16-byte chunks of a K tile
+  constexpr int PK = (KCH + NT - 1) / NT;
+  constexpr int VG = (KT / 4) * (DV / 8);   // V groups: 4 consecutive keys x 8 head dims
+  constexpr int PV = (VG + NT - 1) / NT;
   static_assert(DV <= DQ + 16, "layout");
-  __shared__ __attribute__((aligned(16))) uint16_t Ks[KT * LDK];
-  __shared__ __attribute__((aligned(16))) uint16_t Vt[DV * LDV];
+  __shared__ __attribute__((aligned(16))) uint16_t Ks[2][KT * LDK];
+  __shared__ __attribute__((aligned(16))) uint16_t Vt[2][DV * LDV];
 
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int c32 = lane & 31, h = lane >> 5;
@@ -74,41 +76,68 @@ __global__ __launch_bounds__(NW * 64) void k_attn32(AttnArgs a) {
   float mrow = -INFINITY, lrow = 0.f;
   const float sl2 = a.scale * 1.4426950408889634f;
 
-  // register prefetch of one K/V tile: chunk c -> key c / (DQ/8), dims (c % (DQ/8)) * 8
-  u32x4_t pk[PER], pv[PER];
+  // Register prefetch of one K/V tile.  K: chunk c -> key c / (DQ/8), dims (c % (DQ/8))*8.
+  // V: group g -> keys 4 (g / (DV/8)) + 0..3, dims (g % (DV/8))*8, so that each transposed
+  // row piece (4 keys of one dim) is one 8-byte LDS store.
+  u32x4_t pk[PK], pv[PV][4];
   auto fetch = [&](int kv0) {
 #pragma unroll
-    for (int i = 0; i < PER; ++i) {
+    for (int i = 0; i < PK; ++i) {
       const int c = threadIdx.x + i * NT;
       const int kr = c / (DQ / 8), e = (c % (DQ / 8)) * 8, key = kv0 + kr;
-      const bool ok = c < KCH && key < N && e < d;
-      pk[i] = ok ? *reinterpret_cast<const u32x4_t*>(qkv + (rb + key) * a.ldq + koff + e) : z4;
-      pv[i] = ok ? *reinterpret_cast<const u32x4_t*>(qkv + (rb + key) * a.ldq + voff + e) : z4;
+      pk[i] = (c < KCH && key < N && e < d) ? *reinterpret_cast<const u32x4_t*>(qkv + (rb + key) * a.ldq + koff + e) : z4;
+    }
+#pragma unroll
+    for (int i = 0; i < PV; ++i) {
+      const int g = threadIdx.x + i * NT;
+      const int k4 = (g / (DV / 8)) * 4, e = (g % (DV / 8)) * 8;
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int key = kv0 + k4 + r;
+        pv[i][r] = (g < VG && key < N && e < d) ? *reinterpret_cast<const u32x4_t*>(qkv + (rb + key) * a.ldq + voff + e) : z4;
+      }
     }
   };
-  auto stage = [&]() {
+  auto stage = [&](int buf) {
 #pragma unroll
-    for (int i = 0; i < PER; ++i) {
+    for (int i = 0; i < PK; ++i) {
       const int c = threadIdx.x + i * NT;
       if (c < KCH) {
         const int kr = c / (DQ / 8), e = (c % (DQ / 8)) * 8;
-        *reinterpret_cast<u32x4_t*>(&Ks[kr * LDK + e]) = pk[i];
-        if (e < DV) {
+        *reinterpret_cast<u32x4_t*>(&Ks[buf][kr * LDK + e]) = pk[i];
+      }
+    }
 #pragma unroll
-          for (int j = 0; j < 4; ++j) {
-            Vt[(e + 2 * j) * LDV + vpos(kr)] = (uint16_t)(pv[i][j] & 0xffffu);
-            Vt[(e + 2 * j + 1) * LDV + vpos(kr)] = (uint16_t)(pv[i][j] >> 16);
-          }
+    for (int i = 0; i < PV; ++i) {
+      const int g = threadIdx.x + i * NT;
+      if (g < VG) {
+        const int k4 = (g / (DV / 8)) * 4, e = (g % (DV / 8)) * 8;
+        uint16_t* dst = &Vt[buf][e * LDV + vpos(k4)];   // keys k4..k4+3 stay consecutive under vpos
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          u32x2_t lo, hi;   // dims e + 2j and e + 2j + 1 of the four keys
+          lo[0] = (pv[i][0][j] & 0xffffu) | (pv[i][1][j] << 16);
+          lo[1] = (pv[i][2][j] & 0xffffu) | (pv[i][3][j] << 16);
+          hi[0] = (pv[i][0][j] >> 16) | (pv[i][1][j] & 0xffff0000u);
+          hi[1] = (pv[i][2][j] >> 16) | (pv[i][3][j] & 0xffff0000u);
+          *reinterpret_cast<u32x2_t*>(dst + (2 * j) * LDV) = lo;
+          *reinterpret_cast<u32x2_t*>(dst + (2 * j + 1) * LDV) = hi;
         }
       }
     }
   };
+  // LDS writes done, then barrier; the global prefetch of the tile after next stays in flight
+  // (the compiler's barrier would also wait for it)
+#define FF_LDS_BARRIER() asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory")
+  const int ntiles = (N + KT - 1) / KT;
   fetch(0);
-  for (int kv0 = 0; kv0 < N; kv0 += KT) {
-    __syncthreads();           // previous tile fully consumed
-    stage();
-    __syncthreads();
-    if (kv0 + KT < N) fetch(kv0 + KT);   // in flight during this tile's math
+  stage(0);
+  if (ntiles > 1) fetch(KT);
+  FF_LDS_BARRIER();
+  for (int kt = 0; kt < ntiles; ++kt) {
+    const int kv0 = kt * KT, buf = kt & 1;
+    const uint16_t* K_ = Ks[buf];
+    const uint16_t* V_ = Vt[buf];
     // scores for two 32-key tiles
     f32x16_t sc[2];
 #pragma unroll
@@ -117,30 +146,39 @@ __global__ __launch_bounds__(NW * 64) void k_attn32(AttnArgs a) {
       for (int v = 0; v < 16; ++v) sc[t][v] = 0.f;
 #pragma unroll
       for (int c = 0; c < NQC; ++c) {
-        const bf16x8_t kf = *reinterpret_cast<const bf16x8_t*>(&Ks[(t * 32 + c32) * LDK + 16 * c + 8 * h]);
+        const bf16x8_t kf = *reinterpret_cast<const bf16x8_t*>(&K_[(t * 32 + c32) * LDK + 16 * c + 8 * h]);
         sc[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[c], sc[t], 0, 0, 0);
       }
     }
     // online softmax for query q0 + c32 (its 64 scores: 32 in this lane, 32 in lane ^ 32)
     float mx = -INFINITY;
+    if (kv0 + KT <= N) {
 #pragma unroll
-    for (int t = 0; t < 2; ++t)
+      for (int t = 0; t < 2; ++t)
 #pragma unroll
-      for (int v = 0; v < 16; ++v) {
-        const int key = kv0 + 32 * t + 8 * (v >> 2) + 4 * h + (v & 3);
-        const float x = key < N ? sc[t][v] * sl2 : -INFINITY;
-        sc[t][v] = x;
-        mx = fmaxf(mx, x);
-      }
+        for (int v = 0; v < 16; ++v) {
+          sc[t][v] *= sl2;
+          mx = fmaxf(mx, sc[t][v]);
+        }
+    } else {   // last, partial tile: keys past N get probability 0
+#pragma unroll
+      for (int t = 0; t < 2; ++t)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+          const int key = kv0 + 32 * t + 8 * (v >> 2) + 4 * h + (v & 3);
+          sc[t][v] = key < N ? sc[t][v] * sl2 : -INFINITY;
+          mx = fmaxf(mx, sc[t][v]);
+        }
+    }
     mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
     const float mnew = fmaxf(mrow, mx);
-    const float alpha = exp2f(mrow - mnew);
+    const float alpha = __builtin_amdgcn_exp2f(mrow - mnew);   // v_exp_f32: exp2(-inf) = 0
     float ls = 0.f;
 #pragma unroll
     for (int t = 0; t < 2; ++t)
 #pragma unroll
       for (int v = 0; v < 16; ++v) {
-        const float pr = exp2f(sc[t][v] - mnew);
+        const float pr = __builtin_amdgcn_exp2f(sc[t][v] - mnew);
         sc[t][v] = pr;
         ls += pr;
       }
@@ -159,11 +197,18 @@ __global__ __launch_bounds__(NW * 64) void k_attn32(AttnArgs a) {
       // keys 16g + 4h + {0..3, 8..11} sit at V^T columns 16g + 8h .. +7
 #pragma unroll
       for (int ot = 0; ot < NOT; ++ot) {
-        const bf16x8_t vf = *reinterpret_cast<const bf16x8_t*>(&Vt[(ot * 32 + c32) * LDV + 16 * g + 8 * h]);
+        const bf16x8_t vf = *reinterpret_cast<const bf16x8_t*>(&V_[(ot * 32 + c32) * LDV + 16 * g + 8 * h]);
         o[ot] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pb, o[ot], 0, 0, 0);
       }
     }
+    // the other buffer held tile kt-1, which every wave finished before the last barrier
+    if (kt + 1 < ntiles) {
+      stage(buf ^ 1);
+      if (kt + 2 < ntiles) fetch(kv0 + 2 * KT);
+    }
+    FF_LDS_BARRIER();
   }
+#undef FF_LDS_BARRIER
   // o[ot][v] = O[query q0 + c32][e = 32 ot + 8 (v/4) + 4 h + v%4]
   const int q = q0 + c32;
   if (q < N) {
