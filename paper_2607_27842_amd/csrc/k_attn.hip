@@ -15,6 +15,7 @@ namespace ff {
 namespace {
 
 constexpr int KT = 64;  // keys per LDS tile
+constexpr float kLazy = 8.0f;  // log2 headroom before the running max is raised
 
 // ---------------------------------------------------------------- bf16, 32x32x16 MFMA
 // NW wavefronts x 32 queries per workgroup; 64-key K/V tiles staged through LDS (K row-
@@ -77,8 +78,9 @@ __global__ __launch_bounds__(NW * 64) void k_attn32(AttnArgs a) {
   const float sl2 = a.scale * 1.4426950408889634f;
 
   // Register prefetch of one K/V tile.  K: chunk c -> key c / (DQ/8), dims (c % (DQ/8))*8.
-  // V: group g -> keys 4 (g / (DV/8)) + 0..3, dims (g % (DV/8))*8, so that each transposed
-  // row piece (4 keys of one dim) is one 8-byte LDS store.
+  // V: group g -> keys 4 (g % (KT/4)) + 0..3, dims (g / (KT/4))*8: each transposed row piece
+  // (4 keys of one dim) is one 8-byte LDS store, and the 16 consecutive lanes of a store
+  // fill one 128-byte V^T row segment (no bank conflicts).
   u32x4_t pk[PK], pv[PV][4];
   auto fetch = [&](int kv0) {
 #pragma unroll
@@ -90,7 +92,7 @@ __global__ __launch_bounds__(NW * 64) void k_attn32(AttnArgs a) {
 #pragma unroll
     for (int i = 0; i < PV; ++i) {
       const int g = threadIdx.x + i * NT;
-      const int k4 = (g / (DV / 8)) * 4, e = (g % (DV / 8)) * 8;
+      const int k4 = (g % (KT / 4)) * 4, e = (g / (KT / 4)) * 8;
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
         const int key = kv0 + k4 + r;
@@ -111,7 +113,7 @@ __global__ __launch_bounds__(NW * 64) void k_attn32(AttnArgs a) {
     for (int i = 0; i < PV; ++i) {
       const int g = threadIdx.x + i * NT;
       if (g < VG) {
-        const int k4 = (g / (DV / 8)) * 4, e = (g % (DV / 8)) * 8;
+        const int k4 = (g % (KT / 4)) * 4, e = (g / (KT / 4)) * 8;
         uint16_t* dst = &Vt[buf][e * LDV + vpos(k4)];   // keys k4..k4+3 stay consecutive under vpos
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
@@ -150,43 +152,43 @@ __global__ __launch_bounds__(NW * 64) void k_attn32(AttnArgs a) {
         sc[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[c], sc[t], 0, 0, 0);
       }
     }
-    // online softmax for query q0 + c32 (its 64 scores: 32 in this lane, 32 in lane ^ 32)
+    // online softmax for query q0 + c32 (its 64 scores: 32 in this lane, 32 in lane ^ 32).
+    // The running max m is kept in log2 units of the scaled scores; it is raised (and O, l
+    // rescaled) only when the tile's max exceeds it by more than kLazy, so most tiles skip
+    // the rescale.  The shift cancels in O / l, and p <= 2^kLazy stays well inside fp32.
     float mx = -INFINITY;
-    if (kv0 + KT <= N) {
-#pragma unroll
-      for (int t = 0; t < 2; ++t)
-#pragma unroll
-        for (int v = 0; v < 16; ++v) {
-          sc[t][v] *= sl2;
-          mx = fmaxf(mx, sc[t][v]);
-        }
-    } else {   // last, partial tile: keys past N get probability 0
+    if (kv0 + KT > N) {   // last, partial tile: keys past N get probability 0
 #pragma unroll
       for (int t = 0; t < 2; ++t)
 #pragma unroll
         for (int v = 0; v < 16; ++v) {
           const int key = kv0 + 32 * t + 8 * (v >> 2) + 4 * h + (v & 3);
-          sc[t][v] = key < N ? sc[t][v] * sl2 : -INFINITY;
-          mx = fmaxf(mx, sc[t][v]);
+          if (key >= N) sc[t][v] = -INFINITY;
         }
     }
-    mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
-    const float mnew = fmaxf(mrow, mx);
-    const float alpha = __builtin_amdgcn_exp2f(mrow - mnew);   // v_exp_f32: exp2(-inf) = 0
+#pragma unroll
+    for (int t = 0; t < 2; ++t)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) mx = fmaxf(mx, sc[t][v]);
+    mx = fmaxf(mx, __shfl_xor(mx, 32, 64)) * sl2;   // scale > 0: max commutes with it
+    if (mx > mrow + kLazy) {
+      const float alpha = __builtin_amdgcn_exp2f(mrow - mx);   // v_exp_f32: exp2(-inf) = 0
+      lrow *= alpha;
+#pragma unroll
+      for (int t = 0; t < NOT; ++t) o[t] *= alpha;
+      mrow = mx;
+    }
     float ls = 0.f;
 #pragma unroll
     for (int t = 0; t < 2; ++t)
 #pragma unroll
       for (int v = 0; v < 16; ++v) {
-        const float pr = __builtin_amdgcn_exp2f(sc[t][v] - mnew);
+        const float pr = __builtin_amdgcn_exp2f(fmaf(sc[t][v], sl2, -mrow));
         sc[t][v] = pr;
         ls += pr;
       }
     ls += __shfl_xor(ls, 32, 64);
-    lrow = lrow * alpha + ls;
-    mrow = mnew;
-#pragma unroll
-    for (int t = 0; t < NOT; ++t) o[t] *= alpha;
+    lrow += ls;
     // O^T += V^T P^T over 4 16-key groups (keys 16g + ...)
 #pragma unroll
     for (int g = 0; g < 4; ++g) {
