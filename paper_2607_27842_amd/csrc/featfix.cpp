@@ -296,8 +296,12 @@ const void* offset_rows(const void* p, size_t rows, size_t cols, size_t es) {
 }
 
 // h = B_l(u; c_t) with cs = SiLU(c_t) [B, C] fp32 already in the workspace.
+// cache_slot (bf16 only): the history refresh of this layer (slot = h - u, or h when
+// !cache_resid) is written by the epilogue of the block's last GEMM, from the same rounded
+// h that the separate cache kernel would read back.
 ff_status exec_block(const Model& m, int kind, const ff_layer_weights& w, const float* cs, const void* u,
-                     void* h, void* ws, Exec& ex, const float* mod_pre = nullptr) {
+                     void* h, void* ws, Exec& ex, const float* mod_pre = nullptr, void* cache_slot = nullptr,
+                     bool cache_resid = true) {
   const Ws L = ws_layout(m);
   const int C = m.C, Mh = m.M, dt = m.dtype;
   const size_t es = m.es();
@@ -336,6 +340,7 @@ ff_status exec_block(const Model& m, int kind, const ff_layer_weights& w, const 
     HIP_TRY(ex.attention(aa), "single: attention");
     GemmArgs g3 = gemm_args(att, ldy, all, s.lin2_w, s.lin2_b, rows, C, C + Mh, EPI_GATED, h, C, all);
     g3.resid = u; g3.ldr = C; g3.resid_f32 = 0; g3.gate = mod + 2 * C; g3.ldg = 3 * C;
+    g3.cache_out = cache_slot; g3.cache_u = cache_resid ? u : nullptr;
     HIP_TRY(ex.gemm(g3), "single: lin2");
     return FF_OK;
   }
@@ -385,6 +390,7 @@ ff_status exec_block(const Model& m, int kind, const ff_layer_weights& w, const 
     HIP_TRY(ex.gemm(g1), "block: fc1");
     GemmArgs g2 = gemm_args(hid, Mh, maps[si], s.fc2_w, s.fc2_b, rows, C, Mh, EPI_GATED, h, C, maps[si]);
     g2.resid = x1f; g2.ldr = C; g2.resid_f32 = 1; g2.gate = ms + 5 * C; g2.ldg = ldm;
+    g2.cache_out = cache_slot; g2.cache_u = cache_resid ? u : nullptr;
     HIP_TRY(ex.gemm(g2), "block: fc2");
   }
   return FF_OK;
@@ -826,13 +832,12 @@ ff_status ff_denoise_step(ff_ctx* c, int32_t step, float* x, const float* cond, 
       if (act == FF_ACT_EXACT) {
         ff_status e = ensure_mod(l);
         if (e) return e;
-        e = exec_block(m, m.kinds[l], c->lw[l], cs, cur, alt, ws, ex, mod_of[l]);
+        // bf16: the refresh is fused into the block's last GEMM; fp32: a separate pass
+        void* dst = mode != FF_VANILLA ? (char*)c->cache + ((size_t)l * S + p.write_slot[i]) * tb : nullptr;
+        const bool fuse = dst && dt == FF_BF16;
+        e = exec_block(m, m.kinds[l], c->lw[l], cs, cur, alt, ws, ex, mod_of[l], fuse ? dst : nullptr, resid);
         if (e) return e;
-        if (mode != FF_VANILLA) {
-          const int sl = p.write_slot[i];
-          void* dst = (char*)c->cache + ((size_t)l * S + sl) * tb;
-          HIP_TRY(ex.cache(dst, resid ? cur : nullptr, alt, E), "cache update");
-        }
+        if (dst && !fuse) HIP_TRY(ex.cache(dst, resid ? cur : nullptr, alt, E), "cache update");
         void* t = cur; cur = alt; alt = t;
         continue;
       }

@@ -51,6 +51,17 @@ __device__ __forceinline__ void epilogue_block(const GemmArgs a, int rbase, int 
     const bool rok = r < a.M;
     const size_t pr = (size_t)a.omap.phys(rok ? r : 0);
     f32x4_t gt[TN][4], rs[TN][4];
+    constexpr bool kCache = EPI == EPI_GATED && !OUT_F32;
+    const bool cache = kCache && a.cache_out != nullptr;
+    u32x2_t uw[TN][4];
+    if (kCache && cache && a.cache_u) {
+#pragma unroll
+      for (int j = 0; j < TN; ++j)
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+          uw[j][q] = *reinterpret_cast<const u32x2_t*>(reinterpret_cast<const uint16_t*>(a.cache_u) + pr * a.ldo +
+                                                       (col[j][q] < a.N ? col[j][q] : 0));
+    }
     if (EPI == EPI_GATED) {
       const float* grow = a.gate + (size_t)a.omap.sample(rok ? r : 0) * a.ldg;
 #pragma unroll
@@ -94,6 +105,19 @@ __device__ __forceinline__ void epilogue_block(const GemmArgs a, int rbase, int 
             o[0] = (uint32_t)f2bf(v[0]) | ((uint32_t)f2bf(v[1]) << 16);
             o[1] = (uint32_t)f2bf(v[2]) | ((uint32_t)f2bf(v[3]) << 16);
             *reinterpret_cast<u32x2_t*>(reinterpret_cast<uint16_t*>(a.out) + pr * a.ldo + c) = o;
+            if (kCache && cache) {
+              // history refresh from the stored (rounded) output, as the separate kernel does
+              u32x2_t dlt = o;
+              if (a.cache_u) {
+                const float h0 = __uint_as_float(o[0] << 16), h1 = __uint_as_float(o[0] & 0xffff0000u);
+                const float h2 = __uint_as_float(o[1] << 16), h3 = __uint_as_float(o[1] & 0xffff0000u);
+                const float u0 = __uint_as_float(uw[j][q][0] << 16), u1 = __uint_as_float(uw[j][q][0] & 0xffff0000u);
+                const float u2 = __uint_as_float(uw[j][q][1] << 16), u3 = __uint_as_float(uw[j][q][1] & 0xffff0000u);
+                dlt[0] = (uint32_t)f2bf(h0 - u0) | ((uint32_t)f2bf(h1 - u1) << 16);
+                dlt[1] = (uint32_t)f2bf(h2 - u2) | ((uint32_t)f2bf(h3 - u3) << 16);
+              }
+              *reinterpret_cast<u32x2_t*>(reinterpret_cast<uint16_t*>(a.cache_out) + pr * a.ldo + c) = dlt;
+            }
           }
         }
       }

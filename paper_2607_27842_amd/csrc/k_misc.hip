@@ -29,10 +29,12 @@ template <> __device__ __forceinline__ void st4<DT_BF16>(void* p, size_t i, cons
   *reinterpret_cast<uint2*>(reinterpret_cast<uint16_t*>(p) + i) = w;
 }
 
-constexpr int kLnMaxUnits = 16;  // 4-element units per lane: C <= 64 * 16 * 4 = 4096
+// LayerNorm rows: at most 16 4-element units per lane, C <= 64 * 16 * 4 = 4096 (host check)
 
 // One wavefront per row: LN over C (biased variance, no affine), then adaLN modulation.
-template <int DT_IN, int DT_OUT>
+// The row and its shift / scale vectors are all loaded up front, so the two reductions
+// (mean, then variance about it) are the only waits between the loads and the stores.
+template <int DT_IN, int DT_OUT, int U>   // U: 4-element units per lane, C <= 256 U
 __global__ __launch_bounds__(256) void k_ln_modulate(LnModArgs a) {
   const int lane = threadIdx.x % 64;
   const int r = blockIdx.x * 4 + threadIdx.x / 64;
@@ -40,20 +42,27 @@ __global__ __launch_bounds__(256) void k_ln_modulate(LnModArgs a) {
   const size_t pr = (size_t)a.map.phys(r);
   const int b = a.map.sample(r);
   const int units = a.C / 4;
-  float v[kLnMaxUnits][4];
+  const float* sh = a.shift + (size_t)b * a.ldm;
+  const float* sc = a.scale + (size_t)b * a.ldm;
+  float v[U][4];
+  float4 s4[U], c4[U];
   float s = 0.f;
 #pragma unroll
-  for (int k = 0; k < kLnMaxUnits; ++k) {
+  for (int k = 0; k < U; ++k) {
     const int u = k * 64 + lane;
     if (u < units) {
       ld4<DT_IN>(a.in, pr * a.ldi + u * 4, v[k]);
-      s += (v[k][0] + v[k][1]) + (v[k][2] + v[k][3]);
+      s4[k] = *reinterpret_cast<const float4*>(sh + u * 4);
+      c4[k] = *reinterpret_cast<const float4*>(sc + u * 4);
     }
   }
+#pragma unroll
+  for (int k = 0; k < U; ++k)
+    if (k * 64 + lane < units) s += (v[k][0] + v[k][1]) + (v[k][2] + v[k][3]);
   const float mean = wave_sum(s) / (float)a.C;
   float q = 0.f;
 #pragma unroll
-  for (int k = 0; k < kLnMaxUnits; ++k) {
+  for (int k = 0; k < U; ++k) {
     const int u = k * 64 + lane;
     if (u < units) {
 #pragma unroll
@@ -64,19 +73,15 @@ __global__ __launch_bounds__(256) void k_ln_modulate(LnModArgs a) {
     }
   }
   const float rstd = 1.0f / sqrtf(wave_sum(q) / (float)a.C + a.eps);
-  const float* sh = a.shift + (size_t)b * a.ldm;
-  const float* sc = a.scale + (size_t)b * a.ldm;
 #pragma unroll
-  for (int k = 0; k < kLnMaxUnits; ++k) {
+  for (int k = 0; k < U; ++k) {
     const int u = k * 64 + lane;
     if (u < units) {
-      const float4 s4 = *reinterpret_cast<const float4*>(sh + u * 4);
-      const float4 c4 = *reinterpret_cast<const float4*>(sc + u * 4);
       float o[4];
-      o[0] = (v[k][0] - mean) * rstd * (1.0f + c4.x) + s4.x;
-      o[1] = (v[k][1] - mean) * rstd * (1.0f + c4.y) + s4.y;
-      o[2] = (v[k][2] - mean) * rstd * (1.0f + c4.z) + s4.z;
-      o[3] = (v[k][3] - mean) * rstd * (1.0f + c4.w) + s4.w;
+      o[0] = (v[k][0] - mean) * rstd * (1.0f + c4[k].x) + s4[k].x;
+      o[1] = (v[k][1] - mean) * rstd * (1.0f + c4[k].y) + s4[k].y;
+      o[2] = (v[k][2] - mean) * rstd * (1.0f + c4[k].z) + s4[k].z;
+      o[3] = (v[k][3] - mean) * rstd * (1.0f + c4[k].w) + s4[k].w;
       st4<DT_OUT>(a.out, pr * a.ldo + u * 4, o);
     }
   }
@@ -393,12 +398,22 @@ __global__ __launch_bounds__(256) void k_unpatchify_euler(const float* __restric
 hipError_t ln_modulate(int dtype, const LnModArgs& a, hipStream_t s) {
   if (a.rows == 0) return hipSuccess;
   const int grid = cdiv(a.rows, 4);
-  if (dtype == DT_BF16) {
-    if (a.in_f32) FF_LAUNCH((k_ln_modulate<DT_F32, DT_BF16>), grid, 256, 0, s, a);
-    else FF_LAUNCH((k_ln_modulate<DT_BF16, DT_BF16>), grid, 256, 0, s, a);
-  } else {
-    FF_LAUNCH((k_ln_modulate<DT_F32, DT_F32>), grid, 256, 0, s, a);
-  }
+  const int units = cdiv(a.C / 4, 64);   // 4-element units per lane (C <= 4096 checked on the host)
+#define FF_LN(U)                                                                          \
+  do {                                                                                    \
+    if (dtype == DT_BF16) {                                                               \
+      if (a.in_f32) FF_LAUNCH((k_ln_modulate<DT_F32, DT_BF16, U>), grid, 256, 0, s, a);   \
+      else FF_LAUNCH((k_ln_modulate<DT_BF16, DT_BF16, U>), grid, 256, 0, s, a);           \
+    } else {                                                                              \
+      FF_LAUNCH((k_ln_modulate<DT_F32, DT_F32, U>), grid, 256, 0, s, a);                  \
+    }                                                                                     \
+  } while (0)
+  if (units <= 2) FF_LN(2);
+  else if (units <= 5) FF_LN(5);
+  else if (units <= 8) FF_LN(8);
+  else if (units <= 12) FF_LN(12);
+  else FF_LN(16);
+#undef FF_LN
   return hipGetLastError();
 }
 

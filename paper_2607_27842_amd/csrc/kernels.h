@@ -43,6 +43,9 @@ struct GemmArgs {
   // EPI_GATED: out = resid[omap.phys(r), n] + gate[sample(r) * ldg + n] * (acc + bias[n])
   const void* resid; int ldr; int resid_f32;
   const float* gate; int ldg;
+  // bf16 EPI_GATED with a bf16 output only: also refresh a history slot laid out like out,
+  // cache_out[phys(r), n] = round(out - cache_u[phys(r), n]) (cache_u == NULL: = out)
+  void* cache_out; const void* cache_u;
 };
 hipError_t gemm(int dtype, const GemmArgs& a, hipStream_t s);
 
