@@ -383,6 +383,103 @@ __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64) void k_gemm_dl(GemmArgs
   epilogue_block<TM, TN, EPI, OUT_F32, RES_F32>(a, m0 + wm, n0 + wn, acc);
 }
 
+// ------------------------------------------------------------------ bf16 MFMA GEMM, 64-wide K stages
+// For K % 64 == 0 on grids that keep the MFMAs busy for a whole stage (see launch_bf16).
+// Two LDS buffers of 64-wide K stages: 128-byte rows (full cache lines per DMA row, 8 rows
+// per 1 KB instruction), XOR swizzle chunk ^ (row & 7).  The DMA of stage kt+1 is issued
+// right after the barrier that ends stage kt-1 (its buffer is free then) and lands during
+// stage kt's four 16-wide k steps, whose fragments are double-buffered in registers as in
+// k_gemm_dl; one wait + barrier per stage.
+template <int BM, int BN, int WM, int WN, int AUX, int EPI, bool OUT_F32, bool RES_F32>
+__global__ __launch_bounds__((BM / WM) * (BN / WN) * 64) void k_gemm_dl64(GemmArgs a, int tiles_m, int tiles_n) {
+  constexpr int BKd = 64, CH = 8, RPI = 8, KS = 4;
+  constexpr int NWN = BN / WN;
+  constexpr int NW = (BM / WM) * NWN;
+  constexpr int TM = WM / 32, TN = WN / 32;
+  constexpr int IA = BM / RPI / NW, IB = BN / RPI / NW;
+  static_assert(IA >= 1 && IB >= 1 && TM + TN <= 15, "unsupported tile");
+  __shared__ __attribute__((aligned(1024))) uint16_t sA[2][BM * BKd];
+  __shared__ __attribute__((aligned(1024))) uint16_t sB[2][BN * BKd];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  int tm, tn;
+  tile_of(blockIdx.x, tiles_m, tiles_n, tm, tn);
+  const int m0 = tm * BM, n0 = tn * BN;
+  const uint16_t* A = reinterpret_cast<const uint16_t*>(a.A);
+  const uint16_t* W = reinterpret_cast<const uint16_t*>(a.W);
+  const int lr = lane / CH, ls = lane % CH;
+  size_t ga[IA], gb[IB];
+#pragma unroll
+  for (int j = 0; j < IA; ++j) {
+    const int row = (wave * IA + j) * RPI + lr, gm = m0 + row;
+    ga[j] = (size_t)a.amap.phys(gm < a.M ? gm : 0) * a.lda + ((ls ^ (row & 7)) * 8);
+  }
+#pragma unroll
+  for (int j = 0; j < IB; ++j) {
+    const int row = (wave * IB + j) * RPI + lr, gn = n0 + row;
+    gb[j] = (size_t)(gn < a.N ? gn : 0) * a.ldw + ((ls ^ (row & 7)) * 8);
+  }
+#define FF_ISSUE(st, k0)                                                                                  \
+  do {                                                                                                    \
+    _Pragma("unroll") for (int j = 0; j < IA; ++j)                                                        \
+      __builtin_amdgcn_global_load_lds(FF_AS1(A + ga[j] + (k0)), FF_AS3(&sA[st][(wave * IA + j) * RPI * BKd]), 16, 0, AUX); \
+    _Pragma("unroll") for (int j = 0; j < IB; ++j)                                                        \
+      __builtin_amdgcn_global_load_lds(FF_AS1(W + gb[j] + (k0)), FF_AS3(&sB[st][(wave * IB + j) * RPI * BKd]), 16, 0, AUX); \
+  } while (0)
+  f32x16_t acc[TM][TN];
+#pragma unroll
+  for (int i = 0; i < TM; ++i)
+#pragma unroll
+    for (int j = 0; j < TN; ++j)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
+  const int wm = (wave / NWN) * WM, wn = (wave % NWN) * WN;
+  const int fr = lane & 31, fh = lane >> 5;
+  int rowa[TM], rowb[TN];
+#pragma unroll
+  for (int t = 0; t < TM; ++t) rowa[t] = wm + t * 32 + fr;
+#pragma unroll
+  for (int t = 0; t < TN; ++t) rowb[t] = wn + t * 32 + fr;
+  const int nk = a.K / BKd;
+  FF_ISSUE(0, 0);
+  asm volatile("s_waitcnt vmcnt(0)\n\ts_barrier" ::: "memory");
+  bf16x8_t fa[2][TM], fb[2][TN];
+  for (int kt = 0; kt < nk; ++kt) {
+    const int st = kt & 1;
+    if (kt + 1 < nk) FF_ISSUE(st ^ 1, (kt + 1) * BKd);   // buffer of stage kt-1: free after the last barrier
+#pragma unroll
+    for (int t = 0; t < TM; ++t) fa[0][t] = lds_rd128(&sA[st][rowa[t] * BKd + ((fh ^ (rowa[t] & 7)) * 8)]);
+#pragma unroll
+    for (int t = 0; t < TN; ++t) fb[0][t] = lds_rd128(&sB[st][rowb[t] * BKd + ((fh ^ (rowb[t] & 7)) * 8)]);
+#pragma unroll
+    for (int s = 0; s < KS; ++s) {
+      const int cur = s & 1, nxt = cur ^ 1;
+      if (s + 1 < KS) {
+        const int ch = (s + 1) * 2 + fh;
+#pragma unroll
+        for (int t = 0; t < TM; ++t) fa[nxt][t] = lds_rd128(&sA[st][rowa[t] * BKd + ((ch ^ (rowa[t] & 7)) * 8)]);
+#pragma unroll
+        for (int t = 0; t < TN; ++t) fb[nxt][t] = lds_rd128(&sB[st][rowb[t] * BKd + ((ch ^ (rowb[t] & 7)) * 8)]);
+        asm volatile("s_waitcnt lgkmcnt(%0)" ::"n"(TM + TN) : "memory");
+      } else {
+        asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+      }
+#pragma unroll
+      for (int t = 0; t < TM; ++t) asm volatile("" : "+v"(fa[cur][t]));
+#pragma unroll
+      for (int t = 0; t < TN; ++t) asm volatile("" : "+v"(fb[cur][t]));
+#pragma unroll
+      for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j) acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fb[cur][j], fa[cur][i], acc[i][j], 0, 0, 0);
+    }
+    // stage kt+1 landed everywhere, and every wave is done reading stage kt
+    asm volatile("s_waitcnt vmcnt(0)\n\ts_barrier" ::: "memory");
+  }
+#undef FF_ISSUE
+  epilogue_block<TM, TN, EPI, OUT_F32, RES_F32>(a, m0 + wm, n0 + wn, acc);
+}
+
+
 // ------------------------------------------------------------------ fp32 FMA GEMM
 template <int EPI>
 __global__ __launch_bounds__(256) void k_gemm_f32(GemmArgs a) {
@@ -441,16 +538,27 @@ void launch_dl(const GemmArgs& a, hipStream_t s) {
                      a, tm, tn);
 }
 
-// Tile choice (measured on MI355X): 256x256 tiles (8 wavefronts of 128x64, 4 stages, loads
-// with sc0|sc1 so the streamed tiles skip the L1) from 160 such tiles on (below that the
-// 256 CUs are underfilled); else 128x128 (8 wavefronts of 64x32, 4 stages, two workgroups
-// per CU).  K % 32 != 0 (the patch
+// Tile choice (measured on MI355X): 256x256 tiles (8 wavefronts of 128x64, loads with
+// sc0|sc1 so the streamed tiles skip the L1) from 160 such tiles on (below that the 256 CUs
+// are underfilled); else 128x128 (8 wavefronts of 64x32).  64-wide K stages (two buffers)
+// where a stage keeps the CU's MFMAs busy long enough to hide the next stage's loads: the
+// 256x256 tiles, and 128x128 tiles when there are more than 256 of them (two per CU).  With
+// one 128x128 tile per CU the 4-stage ring of 32-wide stages is faster.  K % 32 != 0 (the patch
 // embedding) takes the register-staged kernel.
+template <int BM, int BN, int WM, int WN, int AUX, int EPI, bool OF, bool RF>
+void launch_dl64(const GemmArgs& a, hipStream_t s) {
+  const int tm = (a.M + BM - 1) / BM, tn = (a.N + BN - 1) / BN;
+  FF_LAUNCH((k_gemm_dl64<BM, BN, WM, WN, AUX, EPI, OF, RF>), tm * tn, (BM / WM) * (BN / WN) * 64, 0, s, a, tm, tn);
+}
+
 template <int EPI, bool OF, bool RF>
 void launch_bf16(const GemmArgs& a, hipStream_t s) {
   const long big = (long)((a.M + 255) / 256) * ((a.N + 255) / 256);
+  const long small = (long)((a.M + 127) / 128) * ((a.N + 127) / 128);
   if (a.K % 32 != 0) launch_tile<128, 128, 64, 32, EPI, OF, RF>(a, s);
+  else if (a.K % 64 == 0 && big >= 160) launch_dl64<256, 256, 128, 64, 17, EPI, OF, RF>(a, s);
   else if (big >= 160) launch_dl<256, 256, 128, 64, 4, 17, EPI, OF, RF>(a, s);
+  else if (a.K % 64 == 0 && small > 256) launch_dl64<128, 128, 64, 32, 0, EPI, OF, RF>(a, s);
   else launch_dl<128, 128, 64, 32, 4, 0, EPI, OF, RF>(a, s);
 }
 
