@@ -126,3 +126,14 @@ def test_mmdit_block_full_shape_sampled_rows(name, kind):
     W = synth.make_layer_weights(cfg, 0, bias_std=0.02, gain_std=0.1)
     say(f"{name} full block kind={kind} N={cfg['n_img'] + cfg['n_txt']} (sampled rows)")
     check_block(cfg, W, rows=np.array(SAMPLE_ROWS[name]))
+
+
+def test_dit_block_gemm_tile_paths():
+    """A DiT block whose GEMMs take every bf16 tile path: qkv and fc1 256x256 tiles with
+    32-wide K stages (K = 2080 is not a multiple of 64), proj 128x128 with 32-wide stages,
+    fc2 128x128 with 64-wide stages (K = 8320, 272 tiles); attention with head dim 104."""
+    need_gpu()
+    cfg = ragged_cfg(synth.DIT, synth.BF16, d=104, H=20, B=2, lat=(4, 1, 64, 64), mlp_ratio=4)
+    W = boosted(synth.make_layer_weights(cfg, 0, bias_std=0.02, gain_std=0.1), synth.DIT)
+    say("dit block C=2080 d=104 N=1024 B=2 (sampled rows)")
+    check_block(cfg, W, rows=np.array([0, 1, 255, 256, 511, 700, 1022, 1023]))
