@@ -33,9 +33,9 @@ constexpr float kLazy = 8.0f;  // log2 headroom before the running max is raised
 // Head dims are zero-padded: QK^T to a multiple of 16 (DQ), PV to a multiple of 32 (DV).
 __device__ __forceinline__ int vpos(int k) { return (k & ~12) | ((k & 4) << 1) | ((k & 8) >> 1); }
 
-template <int DQ, int DV, int NW>
-__global__ __launch_bounds__(NW * 64) void k_attn32(AttnArgs a) {
-  constexpr int NT = NW * 64;
+template <int DQ, int DV, int NW, int SPLIT>
+__global__ __launch_bounds__(NW * SPLIT * 64) void k_attn32(AttnArgs a) {
+  constexpr int NT = NW * 64;   // threads of one group
   constexpr int LDK = DQ + 8;         // K tile row stride (elements)
   constexpr int LDV = KT + 8;         // V^T tile row stride
   constexpr int NQC = DQ / 16;        // 16-wide head-dim chunks of QK^T
@@ -45,10 +45,15 @@ __global__ __launch_bounds__(NW * 64) void k_attn32(AttnArgs a) {
   constexpr int VG = (KT / 4) * (DV / 8);   // V groups: 4 consecutive keys x 8 head dims
   constexpr int PV = (VG + NT - 1) / NT;
   static_assert(DV <= DQ + 16, "layout");
-  __shared__ __attribute__((aligned(16))) uint16_t Ks[2][KT * LDK];
-  __shared__ __attribute__((aligned(16))) uint16_t Vt[2][DV * LDV];
+  // per group: two K tiles [KT][LDK] and two V^T tiles [DV][LDV]
+  constexpr int KSZ = KT * LDK, VSZ = DV * LDV;
+  __shared__ __attribute__((aligned(16))) uint16_t smem[SPLIT * 2 * (KSZ + VSZ)];
+  auto Ks = [&](int g, int b) { return smem + (g * 2 + b) * KSZ; };
+  auto Vt = [&](int g, int b) { return smem + SPLIT * 2 * KSZ + (g * 2 + b) * VSZ; };
 
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  // SPLIT groups of NW wavefronts take the same queries over disjoint key ranges
+  const int grp = threadIdx.x / NT, gtid = threadIdx.x % NT;
+  const int lane = threadIdx.x & 63, wave = (threadIdx.x >> 6) % NW;
   const int c32 = lane & 31, h = lane >> 5;
   const int b = blockIdx.z, hd = blockIdx.y;
   const int q0 = blockIdx.x * (NW * 32) + wave * 32;
@@ -85,13 +90,13 @@ __global__ __launch_bounds__(NW * 64) void k_attn32(AttnArgs a) {
   auto fetch = [&](int kv0) {
 #pragma unroll
     for (int i = 0; i < PK; ++i) {
-      const int c = threadIdx.x + i * NT;
+      const int c = gtid + i * NT;
       const int kr = c / (DQ / 8), e = (c % (DQ / 8)) * 8, key = kv0 + kr;
       pk[i] = (c < KCH && key < N && e < d) ? *reinterpret_cast<const u32x4_t*>(qkv + (rb + key) * a.ldq + koff + e) : z4;
     }
 #pragma unroll
     for (int i = 0; i < PV; ++i) {
-      const int g = threadIdx.x + i * NT;
+      const int g = gtid + i * NT;
       const int k4 = (g % (KT / 4)) * 4, e = (g / (KT / 4)) * 8;
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
@@ -103,18 +108,18 @@ __global__ __launch_bounds__(NW * 64) void k_attn32(AttnArgs a) {
   auto stage = [&](int buf) {
 #pragma unroll
     for (int i = 0; i < PK; ++i) {
-      const int c = threadIdx.x + i * NT;
+      const int c = gtid + i * NT;
       if (c < KCH) {
         const int kr = c / (DQ / 8), e = (c % (DQ / 8)) * 8;
-        *reinterpret_cast<u32x4_t*>(&Ks[buf][kr * LDK + e]) = pk[i];
+        *reinterpret_cast<u32x4_t*>(Ks(grp, buf) + kr * LDK + e) = pk[i];
       }
     }
 #pragma unroll
     for (int i = 0; i < PV; ++i) {
-      const int g = threadIdx.x + i * NT;
+      const int g = gtid + i * NT;
       if (g < VG) {
         const int k4 = (g % (KT / 4)) * 4, e = (g / (KT / 4)) * 8;
-        uint16_t* dst = &Vt[buf][e * LDV + vpos(k4)];   // keys k4..k4+3 stay consecutive under vpos
+        uint16_t* dst = Vt(grp, buf) + e * LDV + vpos(k4);   // keys k4..k4+3 stay consecutive under vpos
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
           u32x2_t lo, hi;   // dims e + 2j and e + 2j + 1 of the four keys
@@ -131,15 +136,19 @@ __global__ __launch_bounds__(NW * 64) void k_attn32(AttnArgs a) {
   // LDS writes done, then barrier; the global prefetch of the tile after next stays in flight
   // (the compiler's barrier would also wait for it)
 #define FF_LDS_BARRIER() asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory")
+  // this group's tiles: [t0, t0 + nt) of the ntiles key tiles (every group runs the same
+  // number of iterations, so the workgroup barriers line up; a group past the end has
+  // kv0 >= N, all its keys masked, and contributes nothing)
   const int ntiles = (N + KT - 1) / KT;
-  fetch(0);
+  const int nt = (ntiles + SPLIT - 1) / SPLIT, t0 = grp * nt;
+  fetch(t0 * KT);
   stage(0);
-  if (ntiles > 1) fetch(KT);
+  if (nt > 1) fetch((t0 + 1) * KT);
   FF_LDS_BARRIER();
-  for (int kt = 0; kt < ntiles; ++kt) {
-    const int kv0 = kt * KT, buf = kt & 1;
-    const uint16_t* K_ = Ks[buf];
-    const uint16_t* V_ = Vt[buf];
+  for (int kt = 0; kt < nt; ++kt) {
+    const int kv0 = (t0 + kt) * KT, buf = kt & 1;
+    const uint16_t* K_ = Ks(grp, buf);
+    const uint16_t* V_ = Vt(grp, buf);
     // scores for two 32-key tiles
     f32x16_t sc[2];
 #pragma unroll
@@ -204,13 +213,45 @@ __global__ __launch_bounds__(NW * 64) void k_attn32(AttnArgs a) {
       }
     }
     // the other buffer held tile kt-1, which every wave finished before the last barrier
-    if (kt + 1 < ntiles) {
+    if (kt + 1 < nt) {
       stage(buf ^ 1);
-      if (kt + 2 < ntiles) fetch(kv0 + 2 * KT);
+      if (kt + 2 < nt) fetch(kv0 + 2 * KT);
     }
     FF_LDS_BARRIER();
   }
 #undef FF_LDS_BARRIER
+  if (SPLIT > 1) {
+    // merge the groups' (m, l, O) through LDS (the tile buffers are free after the last
+    // barrier): group g > 0 writes, group 0 combines in group order, exactly:
+    // m = max m_g, O = sum_g O_g 2^(m_g - m), l = sum_g l_g 2^(m_g - m)
+    constexpr int PF = NOT * 16 + 2;   // floats per lane
+    float* xch = reinterpret_cast<float*>(smem);
+    static_assert(sizeof(smem) >= (size_t)(SPLIT - 1) * NW * 64 * PF * 4, "exchange space");
+    if (grp > 0) {
+      float* p = xch + (((size_t)(grp - 1) * NW + wave) * PF) * 64 + lane;
+#pragma unroll
+      for (int t = 0; t < NOT; ++t)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) p[(t * 16 + v) * 64] = o[t][v];
+      p[(NOT * 16) * 64] = mrow;
+      p[(NOT * 16 + 1) * 64] = lrow;
+    }
+    __syncthreads();
+    if (grp > 0) return;
+#pragma unroll
+    for (int g2 = 1; g2 < SPLIT; ++g2) {
+      const float* p = xch + (((size_t)(g2 - 1) * NW + wave) * PF) * 64 + lane;
+      const float m2 = p[(NOT * 16) * 64], l2 = p[(NOT * 16 + 1) * 64];
+      const float mm = fmaxf(mrow, m2);
+      const float a1 = __builtin_amdgcn_exp2f(mrow - mm), a2 = __builtin_amdgcn_exp2f(m2 - mm);
+#pragma unroll
+      for (int t = 0; t < NOT; ++t)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) o[t][v] = o[t][v] * a1 + p[(t * 16 + v) * 64] * a2;
+      lrow = lrow * a1 + l2 * a2;
+      mrow = mm;
+    }
+  }
   // o[ot][v] = O[query q0 + c32][e = 32 ot + 8 (v/4) + 4 h + v%4]
   const int q = q0 + c32;
   if (q < N) {
@@ -293,13 +334,17 @@ __global__ __launch_bounds__(64) void k_attn_f32(AttnArgs a) {
 hipError_t attention(int dtype, const AttnArgs& a, hipStream_t s) {
   if (a.N <= 0) return hipSuccess;
   if (dtype == DT_BF16) {
-    // 8 wavefronts (256 queries) per workgroup when that still gives >= 256 workgroups
+    // 8 wavefronts (256 queries) per workgroup when that still gives >= 256 workgroups;
+    // else 4 wavefronts (128 queries), and when even those are fewer than 2 per CU on
+    // average, two groups of 4 over the two halves of the keys
     const bool wide = (long)((a.N + 255) / 256) * a.H * a.B >= 256;
+    const bool split = !wide && (long)((a.N + 127) / 128) * a.H * a.B < 512 && a.N > KT;
     const dim3 grid((a.N + (wide ? 255 : 127)) / (wide ? 256 : 128), a.H, a.B);
 #define FF_ATTN(DQ, DV)                                                              \
     do {                                                                             \
-      if (wide) FF_LAUNCH((k_attn32<DQ, DV, 8>), grid, 512, 0, s, a);                \
-      else FF_LAUNCH((k_attn32<DQ, DV, 4>), grid, 256, 0, s, a);                     \
+      if (wide) FF_LAUNCH((k_attn32<DQ, DV, 8, 1>), grid, 512, 0, s, a);             \
+      else if (split) FF_LAUNCH((k_attn32<DQ, DV, 4, 2>), grid, 512, 0, s, a);       \
+      else FF_LAUNCH((k_attn32<DQ, DV, 4, 1>), grid, 256, 0, s, a);                  \
     } while (0)
     if (a.d <= 64) FF_ATTN(64, 64);
     else if (a.d <= 80) FF_ATTN(80, 96);
