@@ -232,12 +232,22 @@ def cpu_baseline(steps=5, layers=8):
                       f"host affinity {cores} cores, BLAS threads {blas_threads}"}
 
 
+WORKLOAD_TEXT = {
+    "dit_xl2": "DiT-XL/2-shaped FeatFix loop: 28 DiT blocks, hidden 1152, 16x72 heads, MLP 4608, 256 tokens, "
+               "batch 8, bf16, T=50, R=5, K=2, S=3, sites {13,27}",
+    "flux": "FLUX-like MMDiT FeatFix loop: 19 double + 38 single blocks, hidden 3072, 24x128 heads, MLP 12288, "
+            "4096 image + 512 text tokens, batch 1, bf16, T=50, R=6, K=1, S=2, sites {18,37,56}",
+}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=100)
     ap.add_argument("--warmup", type=int, default=50)
-    ap.add_argument("--no-flux", action="store_true")
+    ap.add_argument("--no-flux", action="store_true", help="skip the FLUX-like loops reported in extra")
+    ap.add_argument("--no-dit", action="store_true",
+                    help="time the FLUX-like loop as the primary workload instead of DiT-XL/2 (profiling)")
     ap.add_argument("--no-vanilla", action="store_true")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     args = ap.parse_args()
@@ -252,20 +262,21 @@ def main():
     abi.lib()
 
     calibration_copy()
-    cfg = synth.get_config("dit_xl2")
+    name = "flux" if args.no_dit else "dit_xl2"
+    cfg = synth.get_config(name)
     T = cfg["T"]
     warm_loops = max(1, -(-args.warmup // T))
     modes = ["featfix"] + ([] if args.no_vanilla else ["vanilla"])
-    dit = run_workload("dit_xl2", modes, warm_loops, args.steps, with_profile=True)
-    ff = dit["featfix"]
+    prim = run_workload(name, modes, warm_loops, args.steps, with_profile=True)
+    ff = prim["featfix"]
     ms_step = ff["ms"] / ff["steps"]
     value = ff["steps"] / (ff["ms"] / 1e3)
     kern = ff.pop("kernels")
     g = kern["gemm"]
     achieved = g["flops"] / (g["ms"] / 1e3) / 1e12
     roof = {"bound": "mfma", "achieved": round(achieved, 1), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
-            "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": gemm_traffic(),
-            "kernel": "k_gemm_dl / k_gemm_bf16 (all exact-block GEMM launches of one FeatFix loop)",
+            "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": gemm_traffic() if name == "dit_xl2" else None,
+            "kernel": "k_gemm_dl64 / k_gemm_dl / k_gemm_bf16 (all exact-block GEMM launches of one FeatFix loop)",
             "avg_launch_us": round(g["ms"] * 1e3 / g["launches"], 3),
             "flop_per_launch": g["flops"] / g["launches"]}
     hbm = {}
@@ -276,10 +287,11 @@ def main():
             hbm[k] = {"achieved_gbs": round(gbs, 1), "frac": round(gbs / PEAK_HBM_GBS, 4),
                       "avg_launch_us": round(s["ms"] * 1e3 / s["launches"], 3),
                       "bytes_per_launch": s["bytes"] / s["launches"]}
-    extra = {"dit_xl2": dit, "dit_kernels": kernel_table(kern), "hbm_roofline": hbm}
-    if "vanilla" in dit:
-        extra["dit_featfix_over_vanilla"] = round(value / dit["vanilla"]["steps_per_s"], 3)
-    if not args.no_flux:
+    key = "dit" if name == "dit_xl2" else "flux"
+    extra = {name: prim, f"{key}_kernels": kernel_table(kern), "hbm_roofline": hbm}
+    if "vanilla" in prim:
+        extra[f"{key}_featfix_over_vanilla"] = round(value / prim["vanilla"]["steps_per_s"], 3)
+    if name == "dit_xl2" and not args.no_flux:
         flux = run_workload("flux", ["featfix"] + ([] if args.no_vanilla else ["vanilla"]), 1, 0,
                             with_profile=True)
         fk = flux["featfix"].pop("kernels")
@@ -290,12 +302,11 @@ def main():
     out = {"metric": METRIC, "value": round(value, 3), "unit": "steps/s", "n_gpus": 1, "steps": ff["steps"],
            "warmup": warm_loops * T, "ms_per_step": round(ms_step, 4), "higher_is_better": True, "scaling": "weak",
            "vs_baseline": None, "dtype": "bf16",
-           "data": "synthetic: seeded N(0,1) latent and class vector, random-init N(0,0.02) weights",
-           "config": {"workload": "DiT-XL/2-shaped FeatFix loop: 28 DiT blocks, hidden 1152, 16x72 heads, "
-                                  "MLP 4608, 256 tokens, batch 8, bf16, T=50, R=5, K=2, S=3, sites {13,27}",
-                      "global_batch": cfg["B"], "seq_len": cfg["n_img"], "parallelism": "none (1 GPU)"},
+           "data": "synthetic: seeded N(0,1) latent and class/text vectors, random-init N(0,0.02) weights",
+           "config": {"workload": WORKLOAD_TEXT[name], "global_batch": cfg["B"],
+                      "seq_len": cfg["n_img"] + cfg["n_txt"], "parallelism": "none (1 GPU)"},
            "roofline": roof}
-    if not args.no_cpu_baseline:
+    if not args.no_cpu_baseline and name == "dit_xl2":
         log("[bench] timing the CPU oracle sample ...")
         out["cpu_baseline"] = cpu_baseline()
     out["extra"] = extra
