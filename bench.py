@@ -199,7 +199,7 @@ def run_workload(name, mode_names, warmup_loops, timed_steps_n, with_profile):
     return res
 
 
-def cpu_baseline(steps=5, layers=8):
+def cpu_baseline(steps=5, layers=10):
     """The oracle on the host, on a bounded sample of the DiT-XL/2 FeatFix loop: the first
     R=5 steps (1 refresh + 4 cached steps) at full width, tokens and batch but `layers`
     blocks with sites at the middle (L/2 - 1) and last block, the rule that gives {13, 27}

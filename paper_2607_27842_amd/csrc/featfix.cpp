@@ -205,6 +205,13 @@ struct Exec {
     const double bytes = ((double)a.M * a.K + (double)a.N * a.K) * es + (double)a.M * a.N * (a.out_f32 ? 4 : es);
     return timed(FF_PROF_GEMM, 2.0 * a.M * a.N * a.K, bytes, [&] { return ff::gemm(dt, a, st); });
   }
+  hipError_t gemm2(const GemmArgs& a0, const GemmArgs& a1) {
+    auto fl = [](const GemmArgs& a) { return 2.0 * a.M * a.N * a.K; };
+    auto by = [&](const GemmArgs& a) {
+      return ((double)a.M * a.K + (double)a.N * a.K) * es + (double)a.M * a.N * (a.out_f32 ? 4 : es);
+    };
+    return timed(FF_PROF_GEMM, fl(a0) + fl(a1), by(a0) + by(a1), [&] { return ff::gemm2(dt, a0, a1, st); });
+  }
   hipError_t attention(const AttnArgs& a) {
     const double rows = (double)a.B * a.N;
     return timed(FF_PROF_ATTN, 4.0 * a.B * (double)a.N * a.N * a.H * a.d, rows * 4.0 * a.C * es,
@@ -345,7 +352,10 @@ ff_status exec_block(const Model& m, int kind, const ff_layer_weights& w, const 
     return FF_OK;
   }
 
-  // DiT block (one stream) or MMDiT double block (text rows, then image rows).
+  // DiT block (one stream) or MMDiT double block (text rows, then image rows).  The two
+  // streams of a double block write disjoint rows of the shared buffers, so each stage runs
+  // for both streams before the next one, and every projection of the two streams (same
+  // N, K and epilogue, different weights and rows) is one grouped GEMM launch.
   const int nstreams = kind == FF_MMDIT_DOUBLE ? 2 : 1;
   RowMap maps[2];
   int nseg[2];
@@ -356,6 +366,18 @@ ff_status exec_block(const Model& m, int kind, const ff_layer_weights& w, const 
     maps[0] = whole(m); nseg[0] = m.N;
   }
   const int ldm = 6 * C * nstreams;
+  // the stream GEMMs of one stage: grouped when both streams have rows
+  auto run2 = [&](GemmArgs* g, const char* what) -> ff_status {
+    const bool has0 = nstreams > 1 && m.B * nseg[0] > 0, has1 = m.B * nseg[nstreams - 1] > 0;
+    if (nstreams > 1 && has0 && has1) {
+      HIP_TRY(ex.gemm2(g[0], g[1]), what);
+    } else {
+      for (int si = 0; si < nstreams; ++si)
+        if (m.B * nseg[si] > 0) HIP_TRY(ex.gemm(g[si]), what);
+    }
+    return FF_OK;
+  };
+  GemmArgs gs[2];
   for (int si = 0; si < nstreams; ++si) {
     const ff_stream_weights& s = w.s[si];
     const int rows = m.B * nseg[si];
@@ -367,32 +389,45 @@ ff_status exec_block(const Model& m, int kind, const ff_layer_weights& w, const 
     if (rows == 0) continue;
     LnModArgs ln{u, 0, C, maps[si], rows, C, m.ln_eps, ms, ms + C, ldm, lna, C};
     HIP_TRY(ex.ln(ln), "block: ln1");
-    GemmArgs g = gemm_args(lna, C, maps[si], s.qkv_w, s.qkv_b, rows, 3 * C, C, EPI_BIAS, qkv, 3 * C, maps[si]);
-    HIP_TRY(ex.gemm(g), "block: qkv");
-    if (kind == FF_MMDIT_DOUBLE) {
-      RmsQKArgs rn{qkv, 3 * C, maps[si], rows, m.H, m.d, s.q_g, s.k_g, m.ln_eps};
+  }
+  for (int si = 0; si < nstreams; ++si)
+    gs[si] = gemm_args(lna, C, maps[si], w.s[si].qkv_w, w.s[si].qkv_b, m.B * nseg[si], 3 * C, C, EPI_BIAS, qkv, 3 * C,
+                       maps[si]);
+  if (ff_status e = run2(gs, "block: qkv")) return e;
+  if (kind == FF_MMDIT_DOUBLE) {
+    for (int si = 0; si < nstreams; ++si) {
+      const int rows = m.B * nseg[si];
+      if (rows == 0) continue;
+      RmsQKArgs rn{qkv, 3 * C, maps[si], rows, m.H, m.d, w.s[si].q_g, w.s[si].k_g, m.ln_eps};
       HIP_TRY(ex.rms_qk(rn), "double: q/k norm");
     }
   }
   aa.out = att; aa.ldo = C;
   HIP_TRY(ex.attention(aa), "block: attention");
   for (int si = 0; si < nstreams; ++si) {
-    const ff_stream_weights& s = w.s[si];
+    float* ms = mod + 6 * C * si;
+    gs[si] = gemm_args(att, C, maps[si], w.s[si].o_w, w.s[si].o_b, m.B * nseg[si], C, C, EPI_GATED, x1f, C, maps[si]);
+    gs[si].out_f32 = 1; gs[si].resid = u; gs[si].ldr = C; gs[si].resid_f32 = 0; gs[si].gate = ms + 2 * C; gs[si].ldg = ldm;
+  }
+  if (ff_status e = run2(gs, "block: proj")) return e;
+  for (int si = 0; si < nstreams; ++si) {
     const int rows = m.B * nseg[si];
     if (rows == 0) continue;
     float* ms = mod + 6 * C * si;
-    GemmArgs go = gemm_args(att, C, maps[si], s.o_w, s.o_b, rows, C, C, EPI_GATED, x1f, C, maps[si]);
-    go.out_f32 = 1; go.resid = u; go.ldr = C; go.resid_f32 = 0; go.gate = ms + 2 * C; go.ldg = ldm;
-    HIP_TRY(ex.gemm(go), "block: proj");
     LnModArgs ln{x1f, 1, C, maps[si], rows, C, m.ln_eps, ms + 3 * C, ms + 4 * C, ldm, lna, C};
     HIP_TRY(ex.ln(ln), "block: ln2");
-    GemmArgs g1 = gemm_args(lna, C, maps[si], s.fc1_w, s.fc1_b, rows, Mh, C, EPI_BIAS_GELU, hid, Mh, maps[si]);
-    HIP_TRY(ex.gemm(g1), "block: fc1");
-    GemmArgs g2 = gemm_args(hid, Mh, maps[si], s.fc2_w, s.fc2_b, rows, C, Mh, EPI_GATED, h, C, maps[si]);
-    g2.resid = x1f; g2.ldr = C; g2.resid_f32 = 1; g2.gate = ms + 5 * C; g2.ldg = ldm;
-    g2.cache_out = cache_slot; g2.cache_u = cache_resid ? u : nullptr;
-    HIP_TRY(ex.gemm(g2), "block: fc2");
   }
+  for (int si = 0; si < nstreams; ++si)
+    gs[si] = gemm_args(lna, C, maps[si], w.s[si].fc1_w, w.s[si].fc1_b, m.B * nseg[si], Mh, C, EPI_BIAS_GELU, hid, Mh,
+                       maps[si]);
+  if (ff_status e = run2(gs, "block: fc1")) return e;
+  for (int si = 0; si < nstreams; ++si) {
+    float* ms = mod + 6 * C * si;
+    gs[si] = gemm_args(hid, Mh, maps[si], w.s[si].fc2_w, w.s[si].fc2_b, m.B * nseg[si], C, Mh, EPI_GATED, h, C, maps[si]);
+    gs[si].resid = x1f; gs[si].ldr = C; gs[si].resid_f32 = 1; gs[si].gate = ms + 5 * C; gs[si].ldg = ldm;
+    gs[si].cache_out = cache_slot; gs[si].cache_u = cache_resid ? u : nullptr;
+  }
+  if (ff_status e = run2(gs, "block: fc2")) return e;
   return FF_OK;
 }
 

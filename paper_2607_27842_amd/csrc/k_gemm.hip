@@ -36,114 +36,122 @@ template <int TM, int TN, int EPI, bool OUT_F32, bool RES_F32>
 __device__ __forceinline__ void epilogue_block(const GemmArgs a, int rbase, int cbase, const f32x16_t (&acc)[TM][TN]) {
   const int lane = threadIdx.x & 63, fr = lane & 31, fh = lane >> 5;
   const uint16_t* bias = reinterpret_cast<const uint16_t*>(a.bias);
-  int col[TN][4];
-  u32x2_t bw[TN][4];
-#pragma unroll
-  for (int j = 0; j < TN; ++j)
-#pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      col[j][q] = cbase + j * 32 + q * 8 + fh * 4;
-      bw[j][q] = *reinterpret_cast<const u32x2_t*>(bias + (col[j][q] < a.N ? col[j][q] : 0));
-    }
+  // column tiles whose loads are staged together: all TN, or one at a time for the gated
+  // epilogue of wide tiles (gate, residual and history input would not fit the registers)
+  constexpr int JB = (EPI == EPI_GATED && TN > 1) ? 1 : TN;
+  constexpr bool kCache = EPI == EPI_GATED && !OUT_F32;
+  const bool cache = kCache && a.cache_out != nullptr;
 #pragma unroll
   for (int i = 0; i < TM; ++i) {
     const int r = rbase + i * 32 + fr;
     const bool rok = r < a.M;
     const size_t pr = (size_t)a.omap.phys(rok ? r : 0);
-    f32x4_t gt[TN][4], rs[TN][4];
-    constexpr bool kCache = EPI == EPI_GATED && !OUT_F32;
-    const bool cache = kCache && a.cache_out != nullptr;
-    u32x2_t uw[TN][4];
-    if (kCache && cache && a.cache_u) {
+    const float* grow = a.gate + (size_t)a.omap.sample(rok ? r : 0) * a.ldg;
 #pragma unroll
-      for (int j = 0; j < TN; ++j)
+    for (int jb = 0; jb < TN; jb += JB) {
+      int col[JB][4];
+      u32x2_t bw[JB][4], uw[JB][4];
+      f32x4_t gt[JB][4], rs[JB][4];
 #pragma unroll
-        for (int q = 0; q < 4; ++q)
-          uw[j][q] = *reinterpret_cast<const u32x2_t*>(reinterpret_cast<const uint16_t*>(a.cache_u) + pr * a.ldo +
-                                                       (col[j][q] < a.N ? col[j][q] : 0));
-    }
-    if (EPI == EPI_GATED) {
-      const float* grow = a.gate + (size_t)a.omap.sample(rok ? r : 0) * a.ldg;
-#pragma unroll
-      for (int j = 0; j < TN; ++j)
+      for (int jj = 0; jj < JB; ++jj)
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
-          const int c = col[j][q] < a.N ? col[j][q] : 0;
-          gt[j][q] = *reinterpret_cast<const f32x4_t*>(grow + c);
-          if (RES_F32) {
-            rs[j][q] = *reinterpret_cast<const f32x4_t*>(reinterpret_cast<const float*>(a.resid) + pr * a.ldr + c);
-          } else {
-            const u32x2_t w = *reinterpret_cast<const u32x2_t*>(reinterpret_cast<const uint16_t*>(a.resid) + pr * a.ldr + c);
-            rs[j][q][0] = __uint_as_float(w[0] << 16); rs[j][q][1] = __uint_as_float(w[0] & 0xffff0000u);
-            rs[j][q][2] = __uint_as_float(w[1] << 16); rs[j][q][3] = __uint_as_float(w[1] & 0xffff0000u);
+          col[jj][q] = cbase + (jb + jj) * 32 + q * 8 + fh * 4;
+          const int c = col[jj][q] < a.N ? col[jj][q] : 0;
+          bw[jj][q] = *reinterpret_cast<const u32x2_t*>(bias + c);
+          if (EPI == EPI_GATED) {
+            gt[jj][q] = *reinterpret_cast<const f32x4_t*>(grow + c);
+            if (RES_F32) {
+              rs[jj][q] = *reinterpret_cast<const f32x4_t*>(reinterpret_cast<const float*>(a.resid) + pr * a.ldr + c);
+            } else {
+              const u32x2_t w = *reinterpret_cast<const u32x2_t*>(reinterpret_cast<const uint16_t*>(a.resid) + pr * a.ldr + c);
+              rs[jj][q][0] = __uint_as_float(w[0] << 16); rs[jj][q][1] = __uint_as_float(w[0] & 0xffff0000u);
+              rs[jj][q][2] = __uint_as_float(w[1] << 16); rs[jj][q][3] = __uint_as_float(w[1] & 0xffff0000u);
+            }
           }
+          if (kCache && cache && a.cache_u)
+            uw[jj][q] = *reinterpret_cast<const u32x2_t*>(reinterpret_cast<const uint16_t*>(a.cache_u) + pr * a.ldo + c);
         }
-    }
 #pragma unroll
-    for (int j = 0; j < TN; ++j)
+      for (int jj = 0; jj < JB; ++jj)
 #pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        float v[4] = {acc[i][j][4 * q] + __uint_as_float(bw[j][q][0] << 16),
-                      acc[i][j][4 * q + 1] + __uint_as_float(bw[j][q][0] & 0xffff0000u),
-                      acc[i][j][4 * q + 2] + __uint_as_float(bw[j][q][1] << 16),
-                      acc[i][j][4 * q + 3] + __uint_as_float(bw[j][q][1] & 0xffff0000u)};
-        if (EPI == EPI_BIAS_GELU) {
+        for (int q = 0; q < 4; ++q) {
+          const int j = jb + jj;
+          float v[4] = {acc[i][j][4 * q] + __uint_as_float(bw[jj][q][0] << 16),
+                        acc[i][j][4 * q + 1] + __uint_as_float(bw[jj][q][0] & 0xffff0000u),
+                        acc[i][j][4 * q + 2] + __uint_as_float(bw[jj][q][1] << 16),
+                        acc[i][j][4 * q + 3] + __uint_as_float(bw[jj][q][1] & 0xffff0000u)};
+          if (EPI == EPI_BIAS_GELU) {
 #pragma unroll
-          for (int e = 0; e < 4; ++e) v[e] = gelu_tanh_f(v[e]);
-        }
-        if (EPI == EPI_GATED) {
+            for (int e = 0; e < 4; ++e) v[e] = gelu_tanh_f(v[e]);
+          }
+          if (EPI == EPI_GATED) {
 #pragma unroll
-          for (int e = 0; e < 4; ++e) v[e] = rs[j][q][e] + gt[j][q][e] * v[e];
-        }
-        if (rok && col[j][q] < a.N) {
-          const int c = col[j][q];
-          if (OUT_F32) {
-            const f32x4_t o = {v[0], v[1], v[2], v[3]};
-            *reinterpret_cast<f32x4_t*>(reinterpret_cast<float*>(a.out) + pr * a.ldo + c) = o;
-          } else {
-            u32x2_t o;
-            o[0] = (uint32_t)f2bf(v[0]) | ((uint32_t)f2bf(v[1]) << 16);
-            o[1] = (uint32_t)f2bf(v[2]) | ((uint32_t)f2bf(v[3]) << 16);
-            *reinterpret_cast<u32x2_t*>(reinterpret_cast<uint16_t*>(a.out) + pr * a.ldo + c) = o;
-            if (kCache && cache) {
-              // history refresh from the stored (rounded) output, as the separate kernel does
-              u32x2_t dlt = o;
-              if (a.cache_u) {
-                const float h0 = __uint_as_float(o[0] << 16), h1 = __uint_as_float(o[0] & 0xffff0000u);
-                const float h2 = __uint_as_float(o[1] << 16), h3 = __uint_as_float(o[1] & 0xffff0000u);
-                const float u0 = __uint_as_float(uw[j][q][0] << 16), u1 = __uint_as_float(uw[j][q][0] & 0xffff0000u);
-                const float u2 = __uint_as_float(uw[j][q][1] << 16), u3 = __uint_as_float(uw[j][q][1] & 0xffff0000u);
-                dlt[0] = (uint32_t)f2bf(h0 - u0) | ((uint32_t)f2bf(h1 - u1) << 16);
-                dlt[1] = (uint32_t)f2bf(h2 - u2) | ((uint32_t)f2bf(h3 - u3) << 16);
+            for (int e = 0; e < 4; ++e) v[e] = rs[jj][q][e] + gt[jj][q][e] * v[e];
+          }
+          if (rok && col[jj][q] < a.N) {
+            const int c = col[jj][q];
+            if (OUT_F32) {
+              const f32x4_t o = {v[0], v[1], v[2], v[3]};
+              *reinterpret_cast<f32x4_t*>(reinterpret_cast<float*>(a.out) + pr * a.ldo + c) = o;
+            } else {
+              u32x2_t o;
+              o[0] = (uint32_t)f2bf(v[0]) | ((uint32_t)f2bf(v[1]) << 16);
+              o[1] = (uint32_t)f2bf(v[2]) | ((uint32_t)f2bf(v[3]) << 16);
+              *reinterpret_cast<u32x2_t*>(reinterpret_cast<uint16_t*>(a.out) + pr * a.ldo + c) = o;
+              if (kCache && cache) {
+                // history refresh from the stored (rounded) output, as the separate kernel does
+                u32x2_t dlt = o;
+                if (a.cache_u) {
+                  const float h0 = __uint_as_float(o[0] << 16), h1 = __uint_as_float(o[0] & 0xffff0000u);
+                  const float h2 = __uint_as_float(o[1] << 16), h3 = __uint_as_float(o[1] & 0xffff0000u);
+                  const float u0 = __uint_as_float(uw[jj][q][0] << 16), u1 = __uint_as_float(uw[jj][q][0] & 0xffff0000u);
+                  const float u2 = __uint_as_float(uw[jj][q][1] << 16), u3 = __uint_as_float(uw[jj][q][1] & 0xffff0000u);
+                  dlt[0] = (uint32_t)f2bf(h0 - u0) | ((uint32_t)f2bf(h1 - u1) << 16);
+                  dlt[1] = (uint32_t)f2bf(h2 - u2) | ((uint32_t)f2bf(h3 - u3) << 16);
+                }
+                *reinterpret_cast<u32x2_t*>(reinterpret_cast<uint16_t*>(a.cache_out) + pr * a.ldo + c) = dlt;
               }
-              *reinterpret_cast<u32x2_t*>(reinterpret_cast<uint16_t*>(a.cache_out) + pr * a.ldo + c) = dlt;
             }
           }
         }
-      }
+    }
   }
 }
 
-// Workgroup -> output tile.  Workgroups are dispatched round-robin over the 8 XCDs (each
-// with its own L2); the first floor(n/8)*8 of them are renumbered so that every XCD owns
-// a contiguous range of tiles, and tiles are ordered in groups of kGroupM tile-rows so
-// that an XCD's concurrent tiles share A rows and W columns in its L2.
+// Up to two GEMMs of the same epilogue in one launch (the text and image streams of an
+// MMDiT block): workgroups [0, n0) take problem 0's tiles, the rest problem 1's.
+struct GemmGroup {
+  GemmArgs g[2];
+  int tm[2], tn[2];   // tile rows / columns per problem
+  int n;              // problems (1 or 2)
+};
+
+// Workgroup -> (problem, output tile).  Workgroups are dispatched round-robin over the 8
+// XCDs (each with its own L2); the first floor(n/8)*8 of them are renumbered so that every
+// XCD owns a contiguous range of tiles, and within a problem tiles are ordered in groups
+// of kGroupM tile-rows so that an XCD's concurrent tiles share A rows and W columns in its
+// L2.
 constexpr int kGroupM = 8;
-__device__ __forceinline__ void tile_of(int bid, int tiles_m, int tiles_n, int& tm, int& tn) {
-  const int nwg = tiles_m * tiles_n;
+__device__ __forceinline__ int tile_of(int bid, int tm0, int tn0, int tm1, int tn1, int np, int& tm, int& tn) {
+  const int n0 = tm0 * tn0;
+  const int nwg = n0 + (np > 1 ? tm1 * tn1 : 0);
   const int full = (nwg / 8) * 8;
-  const int id = bid < full ? (bid % 8) * (full / 8) + bid / 8 : bid;
+  int id = bid < full ? (bid % 8) * (full / 8) + bid / 8 : bid;
+  int p = 0, tiles_m = tm0, tiles_n = tn0;
+  if (id >= n0) { p = 1; id -= n0; tiles_m = tm1; tiles_n = tn1; }
   const int per_group = kGroupM * tiles_n;
   const int first_m = (id / per_group) * kGroupM;
   const int gsz = min(tiles_m - first_m, kGroupM);
   const int in_group = id % per_group;
   tm = first_m + in_group % gsz;
   tn = in_group / gsz;
+  return p;
 }
 
 // ------------------------------------------------------------------ bf16 MFMA GEMM
-// BM x BN workgroup tile, BK = 64 per LDS stage, wavefront tiles WM x WN of
-// v_mfma_f32_32x32x16_bf16 (the 16x16x32 form issues at half the rate on gfx950).
+// Register-staged fallback (K % 32 != 0): BM x BN workgroup tile, BK = 64 per LDS stage
+// with padded rows, wavefront tiles WM x WN of v_mfma_f32_32x32x16_bf16.
 constexpr int BK = 64, LDT = BK + 8;
 
 // 32x32x16 MFMA: A operand lane l = row (l%32), k 8*(l/32)..+7; B operand lane l = col (l%32),
@@ -151,7 +159,7 @@ constexpr int BK = 64, LDT = BK + 8;
 // columns n) and B = activation rows (output rows m): lane l owns output row m = l%32 and
 // columns n = 8*(v/4) + 4*(l/32) + (v%4), i.e. 4 groups of 4 consecutive columns.
 template <int BM, int BN, int WM, int WN, int EPI, bool OUT_F32, bool RES_F32>
-__global__ __launch_bounds__((BM / WM) * (BN / WN) * 64) void k_gemm_bf16(GemmArgs a, int tiles_m, int tiles_n) {
+__global__ __launch_bounds__((BM / WM) * (BN / WN) * 64) void k_gemm_bf16(GemmGroup G) {
   constexpr int NWN = BN / WN;
   constexpr int NT = (BM / WM) * NWN * 64;
   constexpr int TM = WM / 32, TN = WN / 32;
@@ -161,7 +169,11 @@ __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64) void k_gemm_bf16(GemmAr
   __shared__ __attribute__((aligned(16))) uint16_t sB[2][BN * LDT];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   int tm, tn;
-  tile_of(blockIdx.x, tiles_m, tiles_n, tm, tn);
+  // workgroup-uniform: keep the problem select and tile origin in scalar registers
+  const int prob = __builtin_amdgcn_readfirstlane(tile_of(blockIdx.x, G.tm[0], G.tn[0], G.tm[1], G.tn[1], G.n, tm, tn));
+  tm = __builtin_amdgcn_readfirstlane(tm);
+  tn = __builtin_amdgcn_readfirstlane(tn);
+  const GemmArgs a = prob ? G.g[1] : G.g[0];
   const int m0 = tm * BM, n0 = tn * BN;
   const uint16_t* A = reinterpret_cast<const uint16_t*>(a.A);
   const uint16_t* W = reinterpret_cast<const uint16_t*>(a.W);
@@ -269,7 +281,7 @@ __device__ __forceinline__ bf16x8_t lds_rd128(const uint16_t* p) {
 }
 
 template <int BM, int BN, int WM, int WN, int NST, int AUX, int EPI, bool OUT_F32, bool RES_F32>
-__global__ __launch_bounds__((BM / WM) * (BN / WN) * 64) void k_gemm_dl(GemmArgs a, int tiles_m, int tiles_n) {
+__global__ __launch_bounds__((BM / WM) * (BN / WN) * 64) void k_gemm_dl(GemmGroup G) {
   constexpr int BKd = 32;
   constexpr int NWN = BN / WN;
   constexpr int NW = (BM / WM) * NWN;
@@ -280,7 +292,11 @@ __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64) void k_gemm_dl(GemmArgs
   __shared__ __attribute__((aligned(1024))) uint16_t sB[NST][BN * BKd];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   int tm, tn;
-  tile_of(blockIdx.x, tiles_m, tiles_n, tm, tn);
+  // workgroup-uniform: keep the problem select and tile origin in scalar registers
+  const int prob = __builtin_amdgcn_readfirstlane(tile_of(blockIdx.x, G.tm[0], G.tn[0], G.tm[1], G.tn[1], G.n, tm, tn));
+  tm = __builtin_amdgcn_readfirstlane(tm);
+  tn = __builtin_amdgcn_readfirstlane(tn);
+  const GemmArgs a = prob ? G.g[1] : G.g[0];
   const int m0 = tm * BM, n0 = tn * BN;
   const uint16_t* A = reinterpret_cast<const uint16_t*>(a.A);
   const uint16_t* W = reinterpret_cast<const uint16_t*>(a.W);
@@ -391,7 +407,7 @@ __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64) void k_gemm_dl(GemmArgs
 // stage kt's four 16-wide k steps, whose fragments are double-buffered in registers as in
 // k_gemm_dl; one wait + barrier per stage.
 template <int BM, int BN, int WM, int WN, int AUX, int EPI, bool OUT_F32, bool RES_F32>
-__global__ __launch_bounds__((BM / WM) * (BN / WN) * 64) void k_gemm_dl64(GemmArgs a, int tiles_m, int tiles_n) {
+__global__ __launch_bounds__((BM / WM) * (BN / WN) * 64) void k_gemm_dl64(GemmGroup G) {
   constexpr int BKd = 64, CH = 8, RPI = 8, KS = 4;
   constexpr int NWN = BN / WN;
   constexpr int NW = (BM / WM) * NWN;
@@ -402,7 +418,11 @@ __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64) void k_gemm_dl64(GemmAr
   __shared__ __attribute__((aligned(1024))) uint16_t sB[2][BN * BKd];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   int tm, tn;
-  tile_of(blockIdx.x, tiles_m, tiles_n, tm, tn);
+  // workgroup-uniform: keep the problem select and tile origin in scalar registers
+  const int prob = __builtin_amdgcn_readfirstlane(tile_of(blockIdx.x, G.tm[0], G.tn[0], G.tm[1], G.tn[1], G.n, tm, tn));
+  tm = __builtin_amdgcn_readfirstlane(tm);
+  tn = __builtin_amdgcn_readfirstlane(tn);
+  const GemmArgs a = prob ? G.g[1] : G.g[0];
   const int m0 = tm * BM, n0 = tn * BN;
   const uint16_t* A = reinterpret_cast<const uint16_t*>(a.A);
   const uint16_t* W = reinterpret_cast<const uint16_t*>(a.W);
@@ -525,17 +545,39 @@ __global__ __launch_bounds__(256) void k_gemm_f32(GemmArgs a) {
     }
 }
 
+template <int BM, int BN>
+GemmGroup make_group(const GemmArgs* a, int n, int& nwg) {
+  GemmGroup G{};
+  G.n = n;
+  nwg = 0;
+  for (int i = 0; i < n; ++i) {
+    G.g[i] = a[i];
+    G.tm[i] = (a[i].M + BM - 1) / BM;
+    G.tn[i] = (a[i].N + BN - 1) / BN;
+    nwg += G.tm[i] * G.tn[i];
+  }
+  return G;
+}
+
 template <int BM, int BN, int WM, int WN, int EPI, bool OF, bool RF>
-void launch_tile(const GemmArgs& a, hipStream_t s) {
-  const int tm = (a.M + BM - 1) / BM, tn = (a.N + BN - 1) / BN;
-  FF_LAUNCH((k_gemm_bf16<BM, BN, WM, WN, EPI, OF, RF>), tm * tn, (BM / WM) * (BN / WN) * 64, 0, s, a, tm, tn);
+void launch_tile(const GemmArgs* a, int n, hipStream_t s) {
+  int nwg;
+  const GemmGroup G = make_group<BM, BN>(a, n, nwg);
+  FF_LAUNCH((k_gemm_bf16<BM, BN, WM, WN, EPI, OF, RF>), nwg, (BM / WM) * (BN / WN) * 64, 0, s, G);
 }
 
 template <int BM, int BN, int WM, int WN, int NST, int AUX, int EPI, bool OF, bool RF>
-void launch_dl(const GemmArgs& a, hipStream_t s) {
-  const int tm = (a.M + BM - 1) / BM, tn = (a.N + BN - 1) / BN;
-  FF_LAUNCH((k_gemm_dl<BM, BN, WM, WN, NST, AUX, EPI, OF, RF>), tm * tn, (BM / WM) * (BN / WN) * 64, 0, s,
-                     a, tm, tn);
+void launch_dl(const GemmArgs* a, int n, hipStream_t s) {
+  int nwg;
+  const GemmGroup G = make_group<BM, BN>(a, n, nwg);
+  FF_LAUNCH((k_gemm_dl<BM, BN, WM, WN, NST, AUX, EPI, OF, RF>), nwg, (BM / WM) * (BN / WN) * 64, 0, s, G);
+}
+
+template <int BM, int BN, int WM, int WN, int AUX, int EPI, bool OF, bool RF>
+void launch_dl64(const GemmArgs* a, int n, hipStream_t s) {
+  int nwg;
+  const GemmGroup G = make_group<BM, BN>(a, n, nwg);
+  FF_LAUNCH((k_gemm_dl64<BM, BN, WM, WN, AUX, EPI, OF, RF>), nwg, (BM / WM) * (BN / WN) * 64, 0, s, G);
 }
 
 // Tile choice (measured on MI355X): 256x256 tiles (8 wavefronts of 128x64, loads with
@@ -543,23 +585,49 @@ void launch_dl(const GemmArgs& a, hipStream_t s) {
 // are underfilled); else 128x128 (8 wavefronts of 64x32).  64-wide K stages (two buffers)
 // where a stage keeps the CU's MFMAs busy long enough to hide the next stage's loads: the
 // 256x256 tiles, and 128x128 tiles when there are more than 256 of them (two per CU).  With
-// one 128x128 tile per CU the 4-stage ring of 32-wide stages is faster.  K % 32 != 0 (the patch
-// embedding) takes the register-staged kernel.
-template <int BM, int BN, int WM, int WN, int AUX, int EPI, bool OF, bool RF>
-void launch_dl64(const GemmArgs& a, hipStream_t s) {
-  const int tm = (a.M + BM - 1) / BM, tn = (a.N + BN - 1) / BN;
-  FF_LAUNCH((k_gemm_dl64<BM, BN, WM, WN, AUX, EPI, OF, RF>), tm * tn, (BM / WM) * (BN / WN) * 64, 0, s, a, tm, tn);
+// one 128x128 tile per CU the 4-stage ring of 32-wide stages is faster.  A group is sized
+// by its total tile count; every problem of it must meet the K condition of the kernel.
+template <int EPI, bool OF, bool RF>
+void launch_bf16(const GemmArgs* a, int n, hipStream_t s) {
+  long big = 0, small = 0;
+  bool k32 = true, k64 = true;
+  for (int i = 0; i < n; ++i) {
+    big += (long)((a[i].M + 255) / 256) * ((a[i].N + 255) / 256);
+    small += (long)((a[i].M + 127) / 128) * ((a[i].N + 127) / 128);
+    k32 = k32 && a[i].K % 32 == 0;
+    k64 = k64 && a[i].K % 64 == 0;
+  }
+  if (!k32) launch_tile<128, 128, 64, 32, EPI, OF, RF>(a, n, s);
+  else if (k64 && big >= 160) launch_dl64<256, 256, 128, 64, 17, EPI, OF, RF>(a, n, s);
+  else if (big >= 160) launch_dl<256, 256, 128, 64, 4, 17, EPI, OF, RF>(a, n, s);
+  else if (k64 && small > 256) launch_dl64<128, 128, 64, 32, 0, EPI, OF, RF>(a, n, s);
+  else launch_dl<128, 128, 64, 32, 4, 0, EPI, OF, RF>(a, n, s);
 }
 
-template <int EPI, bool OF, bool RF>
-void launch_bf16(const GemmArgs& a, hipStream_t s) {
-  const long big = (long)((a.M + 255) / 256) * ((a.N + 255) / 256);
-  const long small = (long)((a.M + 127) / 128) * ((a.N + 127) / 128);
-  if (a.K % 32 != 0) launch_tile<128, 128, 64, 32, EPI, OF, RF>(a, s);
-  else if (a.K % 64 == 0 && big >= 160) launch_dl64<256, 256, 128, 64, 17, EPI, OF, RF>(a, s);
-  else if (big >= 160) launch_dl<256, 256, 128, 64, 4, 17, EPI, OF, RF>(a, s);
-  else if (a.K % 64 == 0 && small > 256) launch_dl64<128, 128, 64, 32, 0, EPI, OF, RF>(a, s);
-  else launch_dl<128, 128, 64, 32, 4, 0, EPI, OF, RF>(a, s);
+}  // namespace
+
+namespace {
+
+// bf16 dispatch of n (1 or 2) problems that share epilogue, output and residual types
+hipError_t gemm_bf16(const GemmArgs* a, int n, hipStream_t s) {
+  const bool of = a[0].out_f32 != 0, rf = a[0].resid_f32 != 0;
+  switch (a[0].epi) {
+    case EPI_BIAS:
+      if (of) launch_bf16<EPI_BIAS, true, false>(a, n, s);
+      else launch_bf16<EPI_BIAS, false, false>(a, n, s);
+      break;
+    case EPI_BIAS_GELU:
+      if (of) launch_bf16<EPI_BIAS_GELU, true, false>(a, n, s);
+      else launch_bf16<EPI_BIAS_GELU, false, false>(a, n, s);
+      break;
+    default:
+      if (of && rf) launch_bf16<EPI_GATED, true, true>(a, n, s);
+      else if (of) launch_bf16<EPI_GATED, true, false>(a, n, s);
+      else if (rf) launch_bf16<EPI_GATED, false, true>(a, n, s);
+      else launch_bf16<EPI_GATED, false, false>(a, n, s);
+      break;
+  }
+  return hipGetLastError();
 }
 
 }  // namespace
@@ -575,24 +643,18 @@ hipError_t gemm(int dtype, const GemmArgs& a, hipStream_t s) {
     }
     return hipGetLastError();
   }
-  const bool of = a.out_f32 != 0, rf = a.resid_f32 != 0;
-  switch (a.epi) {
-    case EPI_BIAS:
-      if (of) launch_bf16<EPI_BIAS, true, false>(a, s);
-      else launch_bf16<EPI_BIAS, false, false>(a, s);
-      break;
-    case EPI_BIAS_GELU:
-      if (of) launch_bf16<EPI_BIAS_GELU, true, false>(a, s);
-      else launch_bf16<EPI_BIAS_GELU, false, false>(a, s);
-      break;
-    default:
-      if (of && rf) launch_bf16<EPI_GATED, true, true>(a, s);
-      else if (of) launch_bf16<EPI_GATED, true, false>(a, s);
-      else if (rf) launch_bf16<EPI_GATED, false, true>(a, s);
-      else launch_bf16<EPI_GATED, false, false>(a, s);
-      break;
+  return gemm_bf16(&a, 1, s);
+}
+
+hipError_t gemm2(int dtype, const GemmArgs& a0, const GemmArgs& a1, hipStream_t s) {
+  const bool e0 = a0.M > 0 && a0.N > 0, e1 = a1.M > 0 && a1.N > 0;
+  const bool same = a0.epi == a1.epi && a0.out_f32 == a1.out_f32 && a0.resid_f32 == a1.resid_f32;
+  if (dtype == DT_F32 || !same || !e0 || !e1) {
+    hipError_t e = gemm(dtype, a0, s);
+    return e != hipSuccess ? e : gemm(dtype, a1, s);
   }
-  return hipGetLastError();
+  const GemmArgs both[2] = {a0, a1};
+  return gemm_bf16(both, 2, s);
 }
 
 }  // namespace ff

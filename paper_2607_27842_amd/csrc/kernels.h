@@ -48,6 +48,9 @@ struct GemmArgs {
   void* cache_out; const void* cache_u;
 };
 hipError_t gemm(int dtype, const GemmArgs& a, hipStream_t s);
+// Two GEMMs in one launch when they share epi, out_f32 and resid_f32 (bf16); otherwise two
+// launches.  Same results as two gemm() calls.
+hipError_t gemm2(int dtype, const GemmArgs& a0, const GemmArgs& a1, hipStream_t s);
 
 // y[b, n] = (add ? add[b*ldadd + n] : 0) + act( sum_k f(x[b*ldx + k]) * W[n, k] + bias[n] )
 // x, y, add fp32; W, bias model dtype; f = SiLU if silu_in; act = SiLU if silu_out.
