@@ -334,13 +334,13 @@ ff_status exec_block(const Model& m, int kind, const ff_layer_weights& w, const 
     }
     LnModArgs ln{u, 0, C, all, rows, C, m.ln_eps, mod, mod + C, 3 * C, lna, C};
     HIP_TRY(ex.ln(ln), "single: ln");
+    // lin1 = [qkv | MLP] over the same input: the two parts (bias, bias + GELU) in one launch
     GemmArgs g1 = gemm_args(lna, C, all, s.lin1_w, s.lin1_b, rows, 3 * C, C, EPI_BIAS, qkv, 3 * C, all);
-    HIP_TRY(ex.gemm(g1), "single: lin1 qkv");
     const int ldy = C + Mh;
     GemmArgs g2 = gemm_args(lna, C, all, offset_rows(s.lin1_w, 3 * (size_t)C, C, es),
                             offset_rows(s.lin1_b, 3 * (size_t)C, 1, es), rows, Mh, C, EPI_BIAS_GELU,
                             at(att, (size_t)C * es), ldy, all);
-    HIP_TRY(ex.gemm(g2), "single: lin1 mlp");
+    HIP_TRY(ex.gemm2(g1, g2), "single: lin1");
     RmsQKArgs rn{qkv, 3 * C, all, rows, m.H, m.d, s.q_g, s.k_g, m.ln_eps};
     HIP_TRY(ex.rms_qk(rn), "single: q/k norm");
     aa.out = att; aa.ldo = ldy;

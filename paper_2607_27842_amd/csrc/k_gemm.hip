@@ -11,6 +11,11 @@ namespace ff {
 
 namespace {
 
+// Template-only epilogue value: bias, plus GELU where the problem's own a.epi asks for it
+// (a uniform branch per tile), so that a bias GEMM and a bias+GELU GEMM can share a launch.
+constexpr int EPI_BIAS_OR_GELU = 3;
+
+
 template <int EPI, bool OUT_F32, bool RES_F32, int DT>
 __device__ __forceinline__ void epilogue_store(const GemmArgs a, int r, int c, float acc) {
   float v = acc + St<DT>::ld1(a.bias, c);
@@ -41,6 +46,16 @@ __device__ __forceinline__ void epilogue_block(const GemmArgs a, int rbase, int 
   constexpr int JB = (EPI == EPI_GATED && TN > 1) ? 1 : TN;
   constexpr bool kCache = EPI == EPI_GATED && !OUT_F32;
   const bool cache = kCache && a.cache_out != nullptr;
+  // columns and bias depend on the column only: loaded once for all row blocks
+  int col[TN][4];
+  u32x2_t bw[TN][4];
+#pragma unroll
+  for (int j = 0; j < TN; ++j)
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      col[j][q] = cbase + j * 32 + q * 8 + fh * 4;
+      bw[j][q] = *reinterpret_cast<const u32x2_t*>(bias + (col[j][q] < a.N ? col[j][q] : 0));
+    }
 #pragma unroll
   for (int i = 0; i < TM; ++i) {
     const int r = rbase + i * 32 + fr;
@@ -49,16 +64,13 @@ __device__ __forceinline__ void epilogue_block(const GemmArgs a, int rbase, int 
     const float* grow = a.gate + (size_t)a.omap.sample(rok ? r : 0) * a.ldg;
 #pragma unroll
     for (int jb = 0; jb < TN; jb += JB) {
-      int col[JB][4];
-      u32x2_t bw[JB][4], uw[JB][4];
+      u32x2_t uw[JB][4];
       f32x4_t gt[JB][4], rs[JB][4];
 #pragma unroll
       for (int jj = 0; jj < JB; ++jj)
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
-          col[jj][q] = cbase + (jb + jj) * 32 + q * 8 + fh * 4;
-          const int c = col[jj][q] < a.N ? col[jj][q] : 0;
-          bw[jj][q] = *reinterpret_cast<const u32x2_t*>(bias + c);
+          const int c = col[jb + jj][q] < a.N ? col[jb + jj][q] : 0;
           if (EPI == EPI_GATED) {
             gt[jj][q] = *reinterpret_cast<const f32x4_t*>(grow + c);
             if (RES_F32) {
@@ -77,11 +89,11 @@ __device__ __forceinline__ void epilogue_block(const GemmArgs a, int rbase, int 
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
           const int j = jb + jj;
-          float v[4] = {acc[i][j][4 * q] + __uint_as_float(bw[jj][q][0] << 16),
-                        acc[i][j][4 * q + 1] + __uint_as_float(bw[jj][q][0] & 0xffff0000u),
-                        acc[i][j][4 * q + 2] + __uint_as_float(bw[jj][q][1] << 16),
-                        acc[i][j][4 * q + 3] + __uint_as_float(bw[jj][q][1] & 0xffff0000u)};
-          if (EPI == EPI_BIAS_GELU) {
+          float v[4] = {acc[i][j][4 * q] + __uint_as_float(bw[j][q][0] << 16),
+                        acc[i][j][4 * q + 1] + __uint_as_float(bw[j][q][0] & 0xffff0000u),
+                        acc[i][j][4 * q + 2] + __uint_as_float(bw[j][q][1] << 16),
+                        acc[i][j][4 * q + 3] + __uint_as_float(bw[j][q][1] & 0xffff0000u)};
+          if (EPI == EPI_BIAS_GELU || (EPI == EPI_BIAS_OR_GELU && a.epi == EPI_BIAS_GELU)) {
 #pragma unroll
             for (int e = 0; e < 4; ++e) v[e] = gelu_tanh_f(v[e]);
           }
@@ -89,8 +101,8 @@ __device__ __forceinline__ void epilogue_block(const GemmArgs a, int rbase, int 
 #pragma unroll
             for (int e = 0; e < 4; ++e) v[e] = rs[jj][q][e] + gt[jj][q][e] * v[e];
           }
-          if (rok && col[jj][q] < a.N) {
-            const int c = col[jj][q];
+          if (rok && col[j][q] < a.N) {
+            const int c = col[j][q];
             if (OUT_F32) {
               const f32x4_t o = {v[0], v[1], v[2], v[3]};
               *reinterpret_cast<f32x4_t*>(reinterpret_cast<float*>(a.out) + pr * a.ldo + c) = o;
@@ -121,10 +133,10 @@ __device__ __forceinline__ void epilogue_block(const GemmArgs a, int rbase, int 
 
 // Up to two GEMMs of the same epilogue in one launch (the text and image streams of an
 // MMDiT block): workgroups [0, n0) take problem 0's tiles, the rest problem 1's.
+template <int NP>
 struct GemmGroup {
-  GemmArgs g[2];
-  int tm[2], tn[2];   // tile rows / columns per problem
-  int n;              // problems (1 or 2)
+  GemmArgs g[NP];
+  int tm[NP], tn[NP];   // tile rows / columns per problem
 };
 
 // Workgroup -> (problem, output tile).  Workgroups are dispatched round-robin over the 8
@@ -158,8 +170,8 @@ constexpr int BK = 64, LDT = BK + 8;
 // same k; D[v] at row 8*(v/4) + 4*(l/32) + v%4, col l%32.  With A = weight rows (output
 // columns n) and B = activation rows (output rows m): lane l owns output row m = l%32 and
 // columns n = 8*(v/4) + 4*(l/32) + (v%4), i.e. 4 groups of 4 consecutive columns.
-template <int BM, int BN, int WM, int WN, int EPI, bool OUT_F32, bool RES_F32>
-__global__ __launch_bounds__((BM / WM) * (BN / WN) * 64) void k_gemm_bf16(GemmGroup G) {
+template <int BM, int BN, int WM, int WN, int EPI, bool OUT_F32, bool RES_F32, int NP>
+__global__ __launch_bounds__((BM / WM) * (BN / WN) * 64) void k_gemm_bf16(GemmGroup<NP> G) {
   constexpr int NWN = BN / WN;
   constexpr int NT = (BM / WM) * NWN * 64;
   constexpr int TM = WM / 32, TN = WN / 32;
@@ -170,10 +182,10 @@ __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64) void k_gemm_bf16(GemmGr
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   int tm, tn;
   // workgroup-uniform: keep the problem select and tile origin in scalar registers
-  const int prob = __builtin_amdgcn_readfirstlane(tile_of(blockIdx.x, G.tm[0], G.tn[0], G.tm[1], G.tn[1], G.n, tm, tn));
+  const int prob = __builtin_amdgcn_readfirstlane(tile_of(blockIdx.x, G.tm[0], G.tn[0], G.tm[NP - 1], G.tn[NP - 1], NP, tm, tn));
   tm = __builtin_amdgcn_readfirstlane(tm);
   tn = __builtin_amdgcn_readfirstlane(tn);
-  const GemmArgs a = prob ? G.g[1] : G.g[0];
+  const GemmArgs a = (NP > 1 && prob) ? G.g[NP - 1] : G.g[0];
   const int m0 = tm * BM, n0 = tn * BN;
   const uint16_t* A = reinterpret_cast<const uint16_t*>(a.A);
   const uint16_t* W = reinterpret_cast<const uint16_t*>(a.W);
@@ -280,8 +292,8 @@ __device__ __forceinline__ bf16x8_t lds_rd128(const uint16_t* p) {
   return __builtin_bit_cast(bf16x8_t, v);
 }
 
-template <int BM, int BN, int WM, int WN, int NST, int AUX, int EPI, bool OUT_F32, bool RES_F32>
-__global__ __launch_bounds__((BM / WM) * (BN / WN) * 64) void k_gemm_dl(GemmGroup G) {
+template <int BM, int BN, int WM, int WN, int NST, int AUX, int EPI, bool OUT_F32, bool RES_F32, int NP>
+__global__ __launch_bounds__((BM / WM) * (BN / WN) * 64) void k_gemm_dl(GemmGroup<NP> G) {
   constexpr int BKd = 32;
   constexpr int NWN = BN / WN;
   constexpr int NW = (BM / WM) * NWN;
@@ -293,10 +305,10 @@ __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64) void k_gemm_dl(GemmGrou
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   int tm, tn;
   // workgroup-uniform: keep the problem select and tile origin in scalar registers
-  const int prob = __builtin_amdgcn_readfirstlane(tile_of(blockIdx.x, G.tm[0], G.tn[0], G.tm[1], G.tn[1], G.n, tm, tn));
+  const int prob = __builtin_amdgcn_readfirstlane(tile_of(blockIdx.x, G.tm[0], G.tn[0], G.tm[NP - 1], G.tn[NP - 1], NP, tm, tn));
   tm = __builtin_amdgcn_readfirstlane(tm);
   tn = __builtin_amdgcn_readfirstlane(tn);
-  const GemmArgs a = prob ? G.g[1] : G.g[0];
+  const GemmArgs a = (NP > 1 && prob) ? G.g[NP - 1] : G.g[0];
   const int m0 = tm * BM, n0 = tn * BN;
   const uint16_t* A = reinterpret_cast<const uint16_t*>(a.A);
   const uint16_t* W = reinterpret_cast<const uint16_t*>(a.W);
@@ -406,8 +418,8 @@ __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64) void k_gemm_dl(GemmGrou
 // right after the barrier that ends stage kt-1 (its buffer is free then) and lands during
 // stage kt's four 16-wide k steps, whose fragments are double-buffered in registers as in
 // k_gemm_dl; one wait + barrier per stage.
-template <int BM, int BN, int WM, int WN, int AUX, int EPI, bool OUT_F32, bool RES_F32>
-__global__ __launch_bounds__((BM / WM) * (BN / WN) * 64) void k_gemm_dl64(GemmGroup G) {
+template <int BM, int BN, int WM, int WN, int AUX, int EPI, bool OUT_F32, bool RES_F32, int NP>
+__global__ __launch_bounds__((BM / WM) * (BN / WN) * 64) void k_gemm_dl64(GemmGroup<NP> G) {
   constexpr int BKd = 64, CH = 8, RPI = 8, KS = 4;
   constexpr int NWN = BN / WN;
   constexpr int NW = (BM / WM) * NWN;
@@ -419,10 +431,10 @@ __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64) void k_gemm_dl64(GemmGr
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   int tm, tn;
   // workgroup-uniform: keep the problem select and tile origin in scalar registers
-  const int prob = __builtin_amdgcn_readfirstlane(tile_of(blockIdx.x, G.tm[0], G.tn[0], G.tm[1], G.tn[1], G.n, tm, tn));
+  const int prob = __builtin_amdgcn_readfirstlane(tile_of(blockIdx.x, G.tm[0], G.tn[0], G.tm[NP - 1], G.tn[NP - 1], NP, tm, tn));
   tm = __builtin_amdgcn_readfirstlane(tm);
   tn = __builtin_amdgcn_readfirstlane(tn);
-  const GemmArgs a = prob ? G.g[1] : G.g[0];
+  const GemmArgs a = (NP > 1 && prob) ? G.g[NP - 1] : G.g[0];
   const int m0 = tm * BM, n0 = tn * BN;
   const uint16_t* A = reinterpret_cast<const uint16_t*>(a.A);
   const uint16_t* W = reinterpret_cast<const uint16_t*>(a.W);
@@ -545,12 +557,11 @@ __global__ __launch_bounds__(256) void k_gemm_f32(GemmArgs a) {
     }
 }
 
-template <int BM, int BN>
-GemmGroup make_group(const GemmArgs* a, int n, int& nwg) {
-  GemmGroup G{};
-  G.n = n;
+template <int BM, int BN, int NP>
+GemmGroup<NP> make_group(const GemmArgs* a, int& nwg) {
+  GemmGroup<NP> G{};
   nwg = 0;
-  for (int i = 0; i < n; ++i) {
+  for (int i = 0; i < NP; ++i) {
     G.g[i] = a[i];
     G.tm[i] = (a[i].M + BM - 1) / BM;
     G.tn[i] = (a[i].N + BN - 1) / BN;
@@ -562,22 +573,37 @@ GemmGroup make_group(const GemmArgs* a, int n, int& nwg) {
 template <int BM, int BN, int WM, int WN, int EPI, bool OF, bool RF>
 void launch_tile(const GemmArgs* a, int n, hipStream_t s) {
   int nwg;
-  const GemmGroup G = make_group<BM, BN>(a, n, nwg);
-  FF_LAUNCH((k_gemm_bf16<BM, BN, WM, WN, EPI, OF, RF>), nwg, (BM / WM) * (BN / WN) * 64, 0, s, G);
+  if (n == 1) {
+    const GemmGroup<1> G = make_group<BM, BN, 1>(a, nwg);
+    FF_LAUNCH((k_gemm_bf16<BM, BN, WM, WN, EPI, OF, RF, 1>), nwg, (BM / WM) * (BN / WN) * 64, 0, s, G);
+  } else {
+    const GemmGroup<2> G = make_group<BM, BN, 2>(a, nwg);
+    FF_LAUNCH((k_gemm_bf16<BM, BN, WM, WN, EPI, OF, RF, 2>), nwg, (BM / WM) * (BN / WN) * 64, 0, s, G);
+  }
 }
 
 template <int BM, int BN, int WM, int WN, int NST, int AUX, int EPI, bool OF, bool RF>
 void launch_dl(const GemmArgs* a, int n, hipStream_t s) {
   int nwg;
-  const GemmGroup G = make_group<BM, BN>(a, n, nwg);
-  FF_LAUNCH((k_gemm_dl<BM, BN, WM, WN, NST, AUX, EPI, OF, RF>), nwg, (BM / WM) * (BN / WN) * 64, 0, s, G);
+  if (n == 1) {
+    const GemmGroup<1> G = make_group<BM, BN, 1>(a, nwg);
+    FF_LAUNCH((k_gemm_dl<BM, BN, WM, WN, NST, AUX, EPI, OF, RF, 1>), nwg, (BM / WM) * (BN / WN) * 64, 0, s, G);
+  } else {
+    const GemmGroup<2> G = make_group<BM, BN, 2>(a, nwg);
+    FF_LAUNCH((k_gemm_dl<BM, BN, WM, WN, NST, AUX, EPI, OF, RF, 2>), nwg, (BM / WM) * (BN / WN) * 64, 0, s, G);
+  }
 }
 
 template <int BM, int BN, int WM, int WN, int AUX, int EPI, bool OF, bool RF>
 void launch_dl64(const GemmArgs* a, int n, hipStream_t s) {
   int nwg;
-  const GemmGroup G = make_group<BM, BN>(a, n, nwg);
-  FF_LAUNCH((k_gemm_dl64<BM, BN, WM, WN, AUX, EPI, OF, RF>), nwg, (BM / WM) * (BN / WN) * 64, 0, s, G);
+  if (n == 1) {
+    const GemmGroup<1> G = make_group<BM, BN, 1>(a, nwg);
+    FF_LAUNCH((k_gemm_dl64<BM, BN, WM, WN, AUX, EPI, OF, RF, 1>), nwg, (BM / WM) * (BN / WN) * 64, 0, s, G);
+  } else {
+    const GemmGroup<2> G = make_group<BM, BN, 2>(a, nwg);
+    FF_LAUNCH((k_gemm_dl64<BM, BN, WM, WN, AUX, EPI, OF, RF, 2>), nwg, (BM / WM) * (BN / WN) * 64, 0, s, G);
+  }
 }
 
 // Tile choice (measured on MI355X): 256x256 tiles (8 wavefronts of 128x64, loads with
@@ -611,6 +637,11 @@ namespace {
 // bf16 dispatch of n (1 or 2) problems that share epilogue, output and residual types
 hipError_t gemm_bf16(const GemmArgs* a, int n, hipStream_t s) {
   const bool of = a[0].out_f32 != 0, rf = a[0].resid_f32 != 0;
+  if (n == 2 && a[0].epi != a[1].epi) {   // bias with bias+GELU (gemm2 admits no other mix)
+    if (of) launch_bf16<EPI_BIAS_OR_GELU, true, false>(a, n, s);
+    else launch_bf16<EPI_BIAS_OR_GELU, false, false>(a, n, s);
+    return hipGetLastError();
+  }
   switch (a[0].epi) {
     case EPI_BIAS:
       if (of) launch_bf16<EPI_BIAS, true, false>(a, n, s);
@@ -648,8 +679,15 @@ hipError_t gemm(int dtype, const GemmArgs& a, hipStream_t s) {
 
 hipError_t gemm2(int dtype, const GemmArgs& a0, const GemmArgs& a1, hipStream_t s) {
   const bool e0 = a0.M > 0 && a0.N > 0, e1 = a1.M > 0 && a1.N > 0;
-  const bool same = a0.epi == a1.epi && a0.out_f32 == a1.out_f32 && a0.resid_f32 == a1.resid_f32;
-  if (dtype == DT_F32 || !same || !e0 || !e1) {
+  const bool ungated = a0.epi != EPI_GATED && a1.epi != EPI_GATED;
+  const bool same = (a0.epi == a1.epi || ungated) && a0.out_f32 == a1.out_f32 && a0.resid_f32 == a1.resid_f32;
+  // Grouping pays when the 256x256 grid it forms needs no more rounds over the 256 CUs
+  // than the larger problem alone (the other one rides along), or when both are large and
+  // it saves a partial round.
+  const long t0 = (long)((a0.M + 255) / 256) * ((a0.N + 255) / 256), t1 = (long)((a1.M + 255) / 256) * ((a1.N + 255) / 256);
+  const long rg = (t0 + t1 + 255) / 256, r0 = (t0 + 255) / 256, r1 = (t1 + 255) / 256;
+  const bool pays = t0 + t1 < 160 || rg <= (r0 > r1 ? r0 : r1) || ((t0 < t1 ? t0 : t1) >= 160 && rg < r0 + r1);
+  if (dtype == DT_F32 || !same || !e0 || !e1 || !pays) {
     hipError_t e = gemm(dtype, a0, s);
     return e != hipSuccess ? e : gemm(dtype, a1, s);
   }

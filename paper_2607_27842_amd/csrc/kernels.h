@@ -48,8 +48,9 @@ struct GemmArgs {
   void* cache_out; const void* cache_u;
 };
 hipError_t gemm(int dtype, const GemmArgs& a, hipStream_t s);
-// Two GEMMs in one launch when they share epi, out_f32 and resid_f32 (bf16); otherwise two
-// launches.  Same results as two gemm() calls.
+// Two GEMMs in one launch (bf16) when they share out_f32 and resid_f32 and either share epi
+// or mix EPI_BIAS with EPI_BIAS_GELU, and when the combined grid does not take more rounds
+// over the CUs; otherwise two launches.  Same results as two gemm() calls.
 hipError_t gemm2(int dtype, const GemmArgs& a0, const GemmArgs& a1, hipStream_t s);
 
 // y[b, n] = (add ? add[b*ldadd + n] : 0) + act( sum_k f(x[b*ldx + k]) * W[n, k] + bias[n] )
