@@ -33,20 +33,21 @@ constexpr float kLazy = 8.0f;  // log2 headroom before the running max is raised
 // Head dims are zero-padded: QK^T to a multiple of 16 (DQ), PV to a multiple of 32 (DV).
 __device__ __forceinline__ int vpos(int k) { return (k & ~12) | ((k & 4) << 1) | ((k & 8) >> 1); }
 
-template <int DQ, int DV, int NW, int SPLIT>
+template <int DQ, int DV, int NW, int SPLIT, int KTL>   // KTL: keys per LDS tile (64 or 128)
 __global__ __launch_bounds__(NW * SPLIT * 64) void k_attn32(AttnArgs a) {
+  constexpr int NS = KTL / 32;        // 32-key score tiles per LDS tile
   constexpr int NT = NW * 64;   // threads of one group
   constexpr int LDK = DQ + 8;         // K tile row stride (elements)
-  constexpr int LDV = KT + 8;         // V^T tile row stride
+  constexpr int LDV = KTL + 8;        // V^T tile row stride
   constexpr int NQC = DQ / 16;        // 16-wide head-dim chunks of QK^T
   constexpr int NOT = DV / 32;        // 32-wide output tiles of the head dim
-  constexpr int KCH = KT * (DQ / 8);  // 16-byte chunks of a K tile
+  constexpr int KCH = KTL * (DQ / 8); // 16-byte chunks of a K tile
   constexpr int PK = (KCH + NT - 1) / NT;
-  constexpr int VG = (KT / 4) * (DV / 8);   // V groups: 4 consecutive keys x 8 head dims
+  constexpr int VG = (KTL / 4) * (DV / 8);  // V groups: 4 consecutive keys x 8 head dims
   constexpr int PV = (VG + NT - 1) / NT;
   static_assert(DV <= DQ + 16, "layout");
-  // per group: two K tiles [KT][LDK] and two V^T tiles [DV][LDV]
-  constexpr int KSZ = KT * LDK, VSZ = DV * LDV;
+  // per group: two K tiles [KTL][LDK] and two V^T tiles [DV][LDV]
+  constexpr int KSZ = KTL * LDK, VSZ = DV * LDV;
   __shared__ __attribute__((aligned(16))) uint16_t smem[SPLIT * 2 * (KSZ + VSZ)];
   auto Ks = [&](int g, int b) { return smem + (g * 2 + b) * KSZ; };
   auto Vt = [&](int g, int b) { return smem + SPLIT * 2 * KSZ + (g * 2 + b) * VSZ; };
@@ -83,7 +84,7 @@ __global__ __launch_bounds__(NW * SPLIT * 64) void k_attn32(AttnArgs a) {
   const float sl2 = a.scale * 1.4426950408889634f;
 
   // Register prefetch of one K/V tile.  K: chunk c -> key c / (DQ/8), dims (c % (DQ/8))*8.
-  // V: group g -> keys 4 (g % (KT/4)) + 0..3, dims (g / (KT/4))*8: each transposed row piece
+  // V: group g -> keys 4 (g % (KTL/4)) + 0..3, dims (g / (KTL/4))*8: each transposed row piece
   // (4 keys of one dim) is one 8-byte LDS store, and the 16 consecutive lanes of a store
   // fill one 128-byte V^T row segment (no bank conflicts).
   u32x4_t pk[PK], pv[PV][4];
@@ -97,7 +98,7 @@ __global__ __launch_bounds__(NW * SPLIT * 64) void k_attn32(AttnArgs a) {
 #pragma unroll
     for (int i = 0; i < PV; ++i) {
       const int g = gtid + i * NT;
-      const int k4 = (g % (KT / 4)) * 4, e = (g / (KT / 4)) * 8;
+      const int k4 = (g % (KTL / 4)) * 4, e = (g / (KTL / 4)) * 8;
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
         const int key = kv0 + k4 + r;
@@ -118,7 +119,7 @@ __global__ __launch_bounds__(NW * SPLIT * 64) void k_attn32(AttnArgs a) {
     for (int i = 0; i < PV; ++i) {
       const int g = gtid + i * NT;
       if (g < VG) {
-        const int k4 = (g % (KT / 4)) * 4, e = (g / (KT / 4)) * 8;
+        const int k4 = (g % (KTL / 4)) * 4, e = (g / (KTL / 4)) * 8;
         uint16_t* dst = Vt(grp, buf) + e * LDV + vpos(k4);   // keys k4..k4+3 stay consecutive under vpos
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
@@ -139,20 +140,20 @@ __global__ __launch_bounds__(NW * SPLIT * 64) void k_attn32(AttnArgs a) {
   // this group's tiles: [t0, t0 + nt) of the ntiles key tiles (every group runs the same
   // number of iterations, so the workgroup barriers line up; a group past the end has
   // kv0 >= N, all its keys masked, and contributes nothing)
-  const int ntiles = (N + KT - 1) / KT;
+  const int ntiles = (N + KTL - 1) / KTL;
   const int nt = (ntiles + SPLIT - 1) / SPLIT, t0 = grp * nt;
-  fetch(t0 * KT);
+  fetch(t0 * KTL);
   stage(0);
-  if (nt > 1) fetch((t0 + 1) * KT);
+  if (nt > 1) fetch((t0 + 1) * KTL);
   FF_LDS_BARRIER();
   for (int kt = 0; kt < nt; ++kt) {
-    const int kv0 = (t0 + kt) * KT, buf = kt & 1;
+    const int kv0 = (t0 + kt) * KTL, buf = kt & 1;
     const uint16_t* K_ = Ks(grp, buf);
     const uint16_t* V_ = Vt(grp, buf);
-    // scores for two 32-key tiles
-    f32x16_t sc[2];
+    // scores for NS 32-key tiles
+    f32x16_t sc[NS];
 #pragma unroll
-    for (int t = 0; t < 2; ++t) {
+    for (int t = 0; t < NS; ++t) {
 #pragma unroll
       for (int v = 0; v < 16; ++v) sc[t][v] = 0.f;
 #pragma unroll
@@ -161,14 +162,14 @@ __global__ __launch_bounds__(NW * SPLIT * 64) void k_attn32(AttnArgs a) {
         sc[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[c], sc[t], 0, 0, 0);
       }
     }
-    // online softmax for query q0 + c32 (its 64 scores: 32 in this lane, 32 in lane ^ 32).
+    // online softmax for query q0 + c32 (its KTL scores: half in this lane, half in lane ^ 32).
     // The running max m is kept in log2 units of the scaled scores; it is raised (and O, l
     // rescaled) only when the tile's max exceeds it by more than kLazy, so most tiles skip
     // the rescale.  The shift cancels in O / l, and p <= 2^kLazy stays well inside fp32.
     float mx = -INFINITY;
-    if (kv0 + KT > N) {   // last, partial tile: keys past N get probability 0
+    if (kv0 + KTL > N) {   // last, partial tile: keys past N get probability 0
 #pragma unroll
-      for (int t = 0; t < 2; ++t)
+      for (int t = 0; t < NS; ++t)
 #pragma unroll
         for (int v = 0; v < 16; ++v) {
           const int key = kv0 + 32 * t + 8 * (v >> 2) + 4 * h + (v & 3);
@@ -176,7 +177,7 @@ __global__ __launch_bounds__(NW * SPLIT * 64) void k_attn32(AttnArgs a) {
         }
     }
 #pragma unroll
-    for (int t = 0; t < 2; ++t)
+    for (int t = 0; t < NS; ++t)
 #pragma unroll
       for (int v = 0; v < 16; ++v) mx = fmaxf(mx, sc[t][v]);
     mx = fmaxf(mx, __shfl_xor(mx, 32, 64)) * sl2;   // scale > 0: max commutes with it
@@ -189,7 +190,7 @@ __global__ __launch_bounds__(NW * SPLIT * 64) void k_attn32(AttnArgs a) {
     }
     float ls = 0.f;
 #pragma unroll
-    for (int t = 0; t < 2; ++t)
+    for (int t = 0; t < NS; ++t)
 #pragma unroll
       for (int v = 0; v < 16; ++v) {
         const float pr = __builtin_amdgcn_exp2f(fmaf(sc[t][v], sl2, -mrow));
@@ -198,9 +199,9 @@ __global__ __launch_bounds__(NW * SPLIT * 64) void k_attn32(AttnArgs a) {
       }
     ls += __shfl_xor(ls, 32, 64);
     lrow += ls;
-    // O^T += V^T P^T over 4 16-key groups (keys 16g + ...)
+    // O^T += V^T P^T over the 16-key groups (keys 16g + ...)
 #pragma unroll
-    for (int g = 0; g < 4; ++g) {
+    for (int g = 0; g < 2 * NS; ++g) {
       const int t = g >> 1, half = g & 1;   // score tile, and which 16 keys of it
       bf16x8_t pb;
 #pragma unroll
@@ -215,7 +216,7 @@ __global__ __launch_bounds__(NW * SPLIT * 64) void k_attn32(AttnArgs a) {
     // the other buffer held tile kt-1, which every wave finished before the last barrier
     if (kt + 1 < nt) {
       stage(buf ^ 1);
-      if (kt + 2 < nt) fetch(kv0 + 2 * KT);
+      if (kt + 2 < nt) fetch(kv0 + 2 * KTL);
     }
     FF_LDS_BARRIER();
   }
@@ -342,9 +343,9 @@ hipError_t attention(int dtype, const AttnArgs& a, hipStream_t s) {
     const dim3 grid((a.N + (wide ? 255 : 127)) / (wide ? 256 : 128), a.H, a.B);
 #define FF_ATTN(DQ, DV)                                                              \
     do {                                                                             \
-      if (wide) FF_LAUNCH((k_attn32<DQ, DV, 8, 1>), grid, 512, 0, s, a);             \
-      else if (split) FF_LAUNCH((k_attn32<DQ, DV, 4, 2>), grid, 512, 0, s, a);       \
-      else FF_LAUNCH((k_attn32<DQ, DV, 4, 1>), grid, 256, 0, s, a);                  \
+      if (wide) FF_LAUNCH((k_attn32<DQ, DV, 8, 1, 128>), grid, 512, 0, s, a);        \
+      else if (split) FF_LAUNCH((k_attn32<DQ, DV, 4, 2, 64>), grid, 512, 0, s, a);   \
+      else FF_LAUNCH((k_attn32<DQ, DV, 4, 1, 64>), grid, 256, 0, s, a);              \
     } while (0)
     if (a.d <= 64) FF_ATTN(64, 64);
     else if (a.d <= 80) FF_ATTN(80, 96);
