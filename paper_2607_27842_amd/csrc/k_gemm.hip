@@ -261,29 +261,37 @@ __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64) void k_gemm_bf16(GemmGr
   epilogue_block<TM, TN, EPI, OUT_F32, RES_F32>(a, m0 + wm, n0 + wn, acc);
 }
 // ------------------------------------------------------------------ bf16 MFMA GEMM, direct-to-LDS
-// For K % 32 == 0.  Operand tiles go global -> LDS with global_load_lds_dwordx4 (no VGPR
-// staging, no ds_write), into an NST-stage ring of 32-wide K slices issued NST-1 slices
-// ahead.  Each DMA instruction fills 1 KB of LDS (16 rows x 64 bytes) in lane order, so
-// rows cannot be padded; instead lane l of a row loads 16-byte chunk (l%4) ^ ((row>>2)&3)
-// (an XOR swizzle), which keeps the 32-row fragment reads conflict-free.
+// For K % BKd == 0 (BKd = 32 or 64).  Operand tiles go global -> LDS with
+// global_load_lds_dwordx4 (no VGPR staging, no ds_write), into an NST-stage ring of
+// BKd-wide K slices issued NST-1 slices ahead.  Each DMA instruction fills 1 KB of LDS in
+// lane order (16 rows x 64 bytes, or 8 rows x 128 bytes), so rows cannot be padded;
+// instead lane l of a row loads a 16-byte chunk XOR-swizzled by the row ((l%4) ^
+// ((row>>2)&3), or (l%8) ^ (row&7)), which keeps the 32-row fragment reads conflict-free.
 //
 // Synchronisation is explicit: the compiler's barrier lowering waits for ALL outstanding
 // loads (it cannot tell which stage a DMA targets), which would remove the prefetch.  So a
-// step waits only for its own stage (s_waitcnt vmcnt(n) with the later stages still in
-// flight) and then s_barrier, as one volatile asm that is also a compiler memory barrier.
-// Fragments are double-buffered in registers across the two 16-wide k steps of a stage:
-// the reads of the next step (ds_read_b128 asm) are in flight while the MFMAs of the
-// current one run, each step waits with lgkmcnt(TM+TN) for the older reads only, and
-// volatile "+v" asms tie the fragments to the MFMAs so that none is consumed before its
-// wait.  The one barrier per stage sits between the two k steps.
+// stage boundary waits only for the next stage (s_waitcnt vmcnt(n) with the later stages
+// still in flight) and then s_barrier, as one volatile asm that is also a compiler memory
+// barrier.  Fragments are double-buffered in registers across the 16-wide k steps: the
+// reads of the next step (ds_read_b128 asm) are in flight while the MFMAs of the current
+// one run, each step waits with lgkmcnt(TM+TN) for the older reads only, and volatile "+v"
+// asms tie the fragments to the MFMAs so that none is consumed before its wait.  The one
+// barrier per stage sits between its last k step and the next stage's first.
 #define FF_AS1(p) ((const __attribute__((address_space(1))) void*)(p))
-#define FF_WAIT_STAGE(later)                                                                            \
-  do {                                                                                                  \
-    if ((later) >= 2) asm volatile("s_waitcnt vmcnt(%0)\n\ts_barrier" ::"n"(2 * (IA + IB)) : "memory");  \
-    else if ((later) == 1) asm volatile("s_waitcnt vmcnt(%0)\n\ts_barrier" ::"n"(IA + IB) : "memory");  \
-    else asm volatile("s_waitcnt vmcnt(0)\n\ts_barrier" ::: "memory");                                \
-  } while (0)
 #define FF_AS3(p) ((__attribute__((address_space(3))) void*)(p))
+
+// Wait until at most later * PER of this wave's DMA instructions are outstanding, then
+// barrier.  A later beyond the cases waits for more than needed, which is safe.
+template <int PER>
+__device__ __forceinline__ void wait_stage(int later) {
+  static_assert(3 * PER <= 63, "vmcnt field");
+  switch (later) {
+    case 0: asm volatile("s_waitcnt vmcnt(0)\n\ts_barrier" ::: "memory"); break;
+    case 1: asm volatile("s_waitcnt vmcnt(%0)\n\ts_barrier" ::"n"(PER) : "memory"); break;
+    case 2: asm volatile("s_waitcnt vmcnt(%0)\n\ts_barrier" ::"n"(2 * PER) : "memory"); break;
+    default: asm volatile("s_waitcnt vmcnt(%0)\n\ts_barrier" ::"n"(3 * PER) : "memory"); break;
+  }
+}
 
 __device__ __forceinline__ bf16x8_t lds_rd128(const uint16_t* p) {
   u32x4_t v;
@@ -292,14 +300,16 @@ __device__ __forceinline__ bf16x8_t lds_rd128(const uint16_t* p) {
   return __builtin_bit_cast(bf16x8_t, v);
 }
 
-template <int BM, int BN, int WM, int WN, int NST, int AUX, int EPI, bool OUT_F32, bool RES_F32, int NP>
+template <int BM, int BN, int WM, int WN, int NST, int BKd, int AUX, int EPI, bool OUT_F32, bool RES_F32, int NP>
 __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64) void k_gemm_dl(GemmGroup<NP> G) {
-  constexpr int BKd = 32;
   constexpr int NWN = BN / WN;
   constexpr int NW = (BM / WM) * NWN;
   constexpr int TM = WM / 32, TN = WN / 32;
-  constexpr int IA = BM / 16 / NW, IB = BN / 16 / NW;   // 1 KB DMA instructions per wave per stage
-  static_assert(IA >= 1 && IB >= 1 && NST >= 3 && NST <= 4 && TM + TN <= 15, "unsupported tile");
+  constexpr int CH = BKd / 8, RPI = 64 / CH, KS = BKd / 16;   // chunks per row, rows per DMA, k steps
+  constexpr int IA = BM / RPI / NW, IB = BN / RPI / NW;        // DMA instructions per wave per stage
+  static_assert(BKd == 32 || BKd == 64, "stage width");
+  static_assert(IA * RPI * NW == BM && IB * RPI * NW == BN, "every tile row loaded by one DMA lane");
+  static_assert(NST >= 3 && NST <= 5 && TM + TN <= 15, "unsupported tile");
   __shared__ __attribute__((aligned(1024))) uint16_t sA[NST][BM * BKd];
   __shared__ __attribute__((aligned(1024))) uint16_t sB[NST][BN * BKd];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -312,25 +322,26 @@ __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64) void k_gemm_dl(GemmGrou
   const int m0 = tm * BM, n0 = tn * BN;
   const uint16_t* A = reinterpret_cast<const uint16_t*>(a.A);
   const uint16_t* W = reinterpret_cast<const uint16_t*>(a.W);
+  auto swz = [](int ch, int row) { return BKd == 64 ? (ch ^ (row & 7)) : (ch ^ ((row >> 2) & 3)); };
   // rows past the matrix read row 0 (in bounds); their results are never stored
-  const int lr = lane >> 2, ls = lane & 3;
+  const int lr = lane / CH, ls = lane % CH;
   size_t ga[IA], gb[IB];
 #pragma unroll
   for (int j = 0; j < IA; ++j) {
-    const int row = (wave * IA + j) * 16 + lr, gm = m0 + row;
-    ga[j] = (size_t)a.amap.phys(gm < a.M ? gm : 0) * a.lda + ((ls ^ ((row >> 2) & 3)) * 8);
+    const int row = (wave * IA + j) * RPI + lr, gm = m0 + row;
+    ga[j] = (size_t)a.amap.phys(gm < a.M ? gm : 0) * a.lda + swz(ls, row) * 8;
   }
 #pragma unroll
   for (int j = 0; j < IB; ++j) {
-    const int row = (wave * IB + j) * 16 + lr, gn = n0 + row;
-    gb[j] = (size_t)(gn < a.N ? gn : 0) * a.ldw + ((ls ^ ((row >> 2) & 3)) * 8);
+    const int row = (wave * IB + j) * RPI + lr, gn = n0 + row;
+    gb[j] = (size_t)(gn < a.N ? gn : 0) * a.ldw + swz(ls, row) * 8;
   }
 #define FF_ISSUE(st, k0)                                                                                  \
   do {                                                                                                    \
     _Pragma("unroll") for (int j = 0; j < IA; ++j)                                                        \
-      __builtin_amdgcn_global_load_lds(FF_AS1(A + ga[j] + (k0)), FF_AS3(&sA[st][(wave * IA + j) * 16 * BKd]), 16, 0, AUX); \
+      __builtin_amdgcn_global_load_lds(FF_AS1(A + ga[j] + (k0)), FF_AS3(&sA[st][(wave * IA + j) * RPI * BKd]), 16, 0, AUX); \
     _Pragma("unroll") for (int j = 0; j < IB; ++j)                                                        \
-      __builtin_amdgcn_global_load_lds(FF_AS1(W + gb[j] + (k0)), FF_AS3(&sB[st][(wave * IB + j) * 16 * BKd]), 16, 0, AUX); \
+      __builtin_amdgcn_global_load_lds(FF_AS1(W + gb[j] + (k0)), FF_AS3(&sB[st][(wave * IB + j) * RPI * BKd]), 16, 0, AUX); \
   } while (0)
 
   f32x16_t acc[TM][TN];
@@ -342,70 +353,66 @@ __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64) void k_gemm_dl(GemmGrou
       for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
   const int wm = (wave / NWN) * WM, wn = (wave % NWN) * WN;
   const int fr = lane & 31, fh = lane >> 5;
-  // fragment offsets within a stage for the two 16-wide k steps
-  int offa[2][TM], offb[2][TN];
+  // fragment offsets within a stage for its 16-wide k steps
+  int offa[KS][TM], offb[KS][TN];
 #pragma unroll
-  for (int kk = 0; kk < 2; ++kk) {
+  for (int kk = 0; kk < KS; ++kk) {
 #pragma unroll
     for (int t = 0; t < TM; ++t) {
       const int row = wm + t * 32 + fr;
-      offa[kk][t] = row * BKd + (((kk * 2 + fh) ^ ((row >> 2) & 3)) * 8);
+      offa[kk][t] = row * BKd + swz(kk * 2 + fh, row) * 8;
     }
 #pragma unroll
     for (int t = 0; t < TN; ++t) {
       const int row = wn + t * 32 + fr;
-      offb[kk][t] = row * BKd + (((kk * 2 + fh) ^ ((row >> 2) & 3)) * 8);
+      offb[kk][t] = row * BKd + swz(kk * 2 + fh, row) * 8;
     }
   }
   const int nk = a.K / BKd;
 #pragma unroll
   for (int s = 0; s < NST - 1; ++s)
     if (s < nk) FF_ISSUE(s, s * BKd);
-  FF_WAIT_STAGE(min(NST - 2, nk - 1));
-  bf16x8_t fa0[TM], fb0[TN], fa1[TM], fb1[TN];
+  wait_stage<IA + IB>(min(NST - 2, nk - 1));   // stage 0 landed
+  bf16x8_t fa[2][TM], fb[2][TN];
 #pragma unroll
-  for (int t = 0; t < TM; ++t) fa0[t] = lds_rd128(&sA[0][offa[0][t]]);
+  for (int t = 0; t < TM; ++t) fa[0][t] = lds_rd128(&sA[0][offa[0][t]]);
 #pragma unroll
-  for (int t = 0; t < TN; ++t) fb0[t] = lds_rd128(&sB[0][offb[0][t]]);
+  for (int t = 0; t < TN; ++t) fb[0][t] = lds_rd128(&sB[0][offb[0][t]]);
   for (int kt = 0; kt < nk; ++kt) {
     const int st = kt % NST;
-    // second k step of stage kt in flight while the first one's MFMAs run
 #pragma unroll
-    for (int t = 0; t < TM; ++t) fa1[t] = lds_rd128(&sA[st][offa[1][t]]);
+    for (int s = 0; s < KS; ++s) {
+      const int cur = s & 1, nxt = cur ^ 1;   // KS is even: stage k step 0 is always buffer 0
+      if (s + 1 < KS) {
 #pragma unroll
-    for (int t = 0; t < TN; ++t) fb1[t] = lds_rd128(&sB[st][offb[1][t]]);
-    asm volatile("s_waitcnt lgkmcnt(%0)" ::"n"(TM + TN) : "memory");
+        for (int t = 0; t < TM; ++t) fa[nxt][t] = lds_rd128(&sA[st][offa[s + 1][t]]);
 #pragma unroll
-    for (int t = 0; t < TM; ++t) asm volatile("" : "+v"(fa0[t]));
+        for (int t = 0; t < TN; ++t) fb[nxt][t] = lds_rd128(&sB[st][offb[s + 1][t]]);
+        asm volatile("s_waitcnt lgkmcnt(%0)" ::"n"(TM + TN) : "memory");
+      } else if (kt + 1 < nk) {
+        // stage kt+1 complete everywhere, and every wave is past its reads of stage kt-1,
+        // whose buffer now takes stage kt+NST-1; then the first k step of stage kt+1 is
+        // read while the last one of stage kt computes
+        wait_stage<IA + IB>(min(NST - 3, nk - 2 - kt));
+        if (kt + NST - 1 < nk) FF_ISSUE((kt + NST - 1) % NST, (kt + NST - 1) * BKd);
+        const int sn = (kt + 1) % NST;
 #pragma unroll
-    for (int t = 0; t < TN; ++t) asm volatile("" : "+v"(fb0[t]));
+        for (int t = 0; t < TM; ++t) fa[nxt][t] = lds_rd128(&sA[sn][offa[0][t]]);
 #pragma unroll
-    for (int i = 0; i < TM; ++i)
+        for (int t = 0; t < TN; ++t) fb[nxt][t] = lds_rd128(&sB[sn][offb[0][t]]);
+        asm volatile("s_waitcnt lgkmcnt(%0)" ::"n"(TM + TN) : "memory");
+      } else {
+        asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+      }
 #pragma unroll
-      for (int j = 0; j < TN; ++j) acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fb0[j], fa0[i], acc[i][j], 0, 0, 0);
-    if (kt + 1 < nk) {
-      // stage kt+1 complete everywhere, and every wave is past its reads of stage kt-1,
-      // whose buffer now takes stage kt+NST-1; then the first k step of stage kt+1 is
-      // read while the second one of stage kt computes
-      FF_WAIT_STAGE(min(NST - 3, nk - 2 - kt));
-      if (kt + NST - 1 < nk) FF_ISSUE((kt + NST - 1) % NST, (kt + NST - 1) * BKd);
-      const int sn = (kt + 1) % NST;
+      for (int t = 0; t < TM; ++t) asm volatile("" : "+v"(fa[cur][t]));
 #pragma unroll
-      for (int t = 0; t < TM; ++t) fa0[t] = lds_rd128(&sA[sn][offa[0][t]]);
+      for (int t = 0; t < TN; ++t) asm volatile("" : "+v"(fb[cur][t]));
 #pragma unroll
-      for (int t = 0; t < TN; ++t) fb0[t] = lds_rd128(&sB[sn][offb[0][t]]);
-      asm volatile("s_waitcnt lgkmcnt(%0)" ::"n"(TM + TN) : "memory");
-    } else {
-      asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+      for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j) acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fb[cur][j], fa[cur][i], acc[i][j], 0, 0, 0);
     }
-#pragma unroll
-    for (int t = 0; t < TM; ++t) asm volatile("" : "+v"(fa1[t]));
-#pragma unroll
-    for (int t = 0; t < TN; ++t) asm volatile("" : "+v"(fb1[t]));
-#pragma unroll
-    for (int i = 0; i < TM; ++i)
-#pragma unroll
-      for (int j = 0; j < TN; ++j) acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fb1[j], fa1[i], acc[i][j], 0, 0, 0);
   }
 #undef FF_ISSUE
   epilogue_block<TM, TN, EPI, OUT_F32, RES_F32>(a, m0 + wm, n0 + wn, acc);
@@ -582,15 +589,15 @@ void launch_tile(const GemmArgs* a, int n, hipStream_t s) {
   }
 }
 
-template <int BM, int BN, int WM, int WN, int NST, int AUX, int EPI, bool OF, bool RF>
+template <int BM, int BN, int WM, int WN, int NST, int BKd, int AUX, int EPI, bool OF, bool RF>
 void launch_dl(const GemmArgs* a, int n, hipStream_t s) {
   int nwg;
   if (n == 1) {
     const GemmGroup<1> G = make_group<BM, BN, 1>(a, nwg);
-    FF_LAUNCH((k_gemm_dl<BM, BN, WM, WN, NST, AUX, EPI, OF, RF, 1>), nwg, (BM / WM) * (BN / WN) * 64, 0, s, G);
+    FF_LAUNCH((k_gemm_dl<BM, BN, WM, WN, NST, BKd, AUX, EPI, OF, RF, 1>), nwg, (BM / WM) * (BN / WN) * 64, 0, s, G);
   } else {
     const GemmGroup<2> G = make_group<BM, BN, 2>(a, nwg);
-    FF_LAUNCH((k_gemm_dl<BM, BN, WM, WN, NST, AUX, EPI, OF, RF, 2>), nwg, (BM / WM) * (BN / WN) * 64, 0, s, G);
+    FF_LAUNCH((k_gemm_dl<BM, BN, WM, WN, NST, BKd, AUX, EPI, OF, RF, 2>), nwg, (BM / WM) * (BN / WN) * 64, 0, s, G);
   }
 }
 
@@ -606,28 +613,62 @@ void launch_dl64(const GemmArgs* a, int n, hipStream_t s) {
   }
 }
 
-// Tile choice (measured on MI355X): 256x256 tiles (8 wavefronts of 128x64, loads with
-// sc0|sc1 so the streamed tiles skip the L1) from 160 such tiles on (below that the 256 CUs
-// are underfilled); else 128x128 (8 wavefronts of 64x32).  64-wide K stages (two buffers)
-// where a stage keeps the CU's MFMAs busy long enough to hide the next stage's loads: the
-// 256x256 tiles, and 128x128 tiles when there are more than 256 of them (two per CU).  With
-// one 128x128 tile per CU the 4-stage ring of 32-wide stages is faster.  A group is sized
-// by its total tile count; every problem of it must meet the K condition of the kernel.
+// Tile choice for K % 64 == 0: the candidate minimising (rounds of workgroups over the
+// 256 CUs) x (time of one round of that candidate), measured on MI355X with random bf16
+// data and expressed relative to a round of 256x256 tiles.  The round time scales with K
+// alike for all candidates, so the choice depends on the tile counts only.
+//   kTile256     256x256, 8 waves of 128x64, 2 x 64-wide stages, 1 per CU          1.00
+//   kTile256x160 256x160, 4 waves of 64x160, 2 x 64-wide stages, 1 per CU          0.96
+//   kTile128x2   128x128, 8 waves of 64x32, 2 x 64-wide stages, 2 per CU (512/round) 0.80
+//   kTile128     128x128, 8 waves of 64x32, 4 x 64-wide stages, 1 per CU          0.43
+// Larger tiles need fewer operand bytes per MFMA (LDS traffic per MFMA limits the 128x128
+// tiles), smaller ones fill the CUs on small grids (M = 2048 shapes).  Operands of the
+// 256-row tiles load with sc0|sc1 (they skip the L1; each tile streams its panels once).
+// A group is costed by its total tile count.  K % 32 == 0 only: 4 x 32-wide stages,
+// 256x256 from 160 such tiles on, else 128x128; otherwise the register-staged kernel.
+enum { kTile256, kTile256x160, kTile128x2, kTile128, kTileCount };
+struct TilePlan { int tile; double cost; };
+
+long tiles_of(const GemmArgs* a, int n, int bm, int bn) {
+  long t = 0;
+  for (int i = 0; i < n; ++i) t += (long)((a[i].M + bm - 1) / bm) * ((a[i].N + bn - 1) / bn);
+  return t;
+}
+
+TilePlan plan_k64(const GemmArgs* a, int n) {
+  static const double kRound[kTileCount] = {1.00, 0.96, 0.80, 0.43};
+  const long t[kTileCount] = {tiles_of(a, n, 256, 256), tiles_of(a, n, 256, 160), tiles_of(a, n, 128, 128),
+                              tiles_of(a, n, 128, 128)};
+  const long per_round[kTileCount] = {256, 256, 512, 256};
+  TilePlan best{kTile256, 1e300};
+  for (int c = 0; c < kTileCount; ++c) {
+    const double cost = (double)((t[c] + per_round[c] - 1) / per_round[c]) * kRound[c];
+    if (cost < best.cost) best = TilePlan{c, cost};
+  }
+  return best;
+}
+
+bool all_k(const GemmArgs* a, int n, int m) {
+  for (int i = 0; i < n; ++i)
+    if (a[i].K % m) return false;
+  return true;
+}
+
 template <int EPI, bool OF, bool RF>
 void launch_bf16(const GemmArgs* a, int n, hipStream_t s) {
-  long big = 0, small = 0;
-  bool k32 = true, k64 = true;
-  for (int i = 0; i < n; ++i) {
-    big += (long)((a[i].M + 255) / 256) * ((a[i].N + 255) / 256);
-    small += (long)((a[i].M + 127) / 128) * ((a[i].N + 127) / 128);
-    k32 = k32 && a[i].K % 32 == 0;
-    k64 = k64 && a[i].K % 64 == 0;
+  if (!all_k(a, n, 32)) {
+    launch_tile<128, 128, 64, 32, EPI, OF, RF>(a, n, s);
+  } else if (!all_k(a, n, 64)) {
+    if (tiles_of(a, n, 256, 256) >= 160) launch_dl<256, 256, 128, 64, 4, 32, 17, EPI, OF, RF>(a, n, s);
+    else launch_dl<128, 128, 64, 32, 4, 32, 0, EPI, OF, RF>(a, n, s);
+  } else {
+    switch (plan_k64(a, n).tile) {
+      case kTile256: launch_dl64<256, 256, 128, 64, 17, EPI, OF, RF>(a, n, s); break;
+      case kTile256x160: launch_dl64<256, 160, 64, 160, 17, EPI, OF, RF>(a, n, s); break;
+      case kTile128x2: launch_dl64<128, 128, 64, 32, 0, EPI, OF, RF>(a, n, s); break;
+      default: launch_dl<128, 128, 64, 32, 4, 64, 17, EPI, OF, RF>(a, n, s); break;
+    }
   }
-  if (!k32) launch_tile<128, 128, 64, 32, EPI, OF, RF>(a, n, s);
-  else if (k64 && big >= 160) launch_dl64<256, 256, 128, 64, 17, EPI, OF, RF>(a, n, s);
-  else if (big >= 160) launch_dl<256, 256, 128, 64, 4, 17, EPI, OF, RF>(a, n, s);
-  else if (k64 && small > 256) launch_dl64<128, 128, 64, 32, 0, EPI, OF, RF>(a, n, s);
-  else launch_dl<128, 128, 64, 32, 4, 0, EPI, OF, RF>(a, n, s);
 }
 
 }  // namespace
@@ -681,17 +722,21 @@ hipError_t gemm2(int dtype, const GemmArgs& a0, const GemmArgs& a1, hipStream_t 
   const bool e0 = a0.M > 0 && a0.N > 0, e1 = a1.M > 0 && a1.N > 0;
   const bool ungated = a0.epi != EPI_GATED && a1.epi != EPI_GATED;
   const bool same = (a0.epi == a1.epi || ungated) && a0.out_f32 == a1.out_f32 && a0.resid_f32 == a1.resid_f32;
-  // Grouping pays when the 256x256 grid it forms needs no more rounds over the 256 CUs
-  // than the larger problem alone (the other one rides along), or when both are large and
-  // it saves a partial round.
-  const long t0 = (long)((a0.M + 255) / 256) * ((a0.N + 255) / 256), t1 = (long)((a1.M + 255) / 256) * ((a1.N + 255) / 256);
-  const long rg = (t0 + t1 + 255) / 256, r0 = (t0 + 255) / 256, r1 = (t1 + 255) / 256;
-  const bool pays = t0 + t1 < 160 || rg <= (r0 > r1 ? r0 : r1) || ((t0 < t1 ? t0 : t1) >= 160 && rg < r0 + r1);
+  // Grouping pays when the combined launch costs no more rounds than the two launches
+  // (same cost model as the tile choice; with K % 64 != 0, by 256x256 rounds).
+  const GemmArgs both[2] = {a0, a1};
+  bool pays;
+  if (all_k(both, 2, 64)) {
+    pays = plan_k64(both, 2).cost <= plan_k64(&a0, 1).cost + plan_k64(&a1, 1).cost;
+  } else {
+    const long t0 = tiles_of(&a0, 1, 256, 256), t1 = tiles_of(&a1, 1, 256, 256);
+    const long rg = (t0 + t1 + 255) / 256, r0 = (t0 + 255) / 256, r1 = (t1 + 255) / 256;
+    pays = t0 + t1 < 160 || rg <= (r0 > r1 ? r0 : r1) || ((t0 < t1 ? t0 : t1) >= 160 && rg < r0 + r1);
+  }
   if (dtype == DT_F32 || !same || !e0 || !e1 || !pays) {
     hipError_t e = gemm(dtype, a0, s);
     return e != hipSuccess ? e : gemm(dtype, a1, s);
   }
-  const GemmArgs both[2] = {a0, a1};
   return gemm_bf16(both, 2, s);
 }
 
