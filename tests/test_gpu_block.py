@@ -141,11 +141,22 @@ def test_dit_block_gemm_tile_paths():
 
 def test_dit_block_ragged_wide_tiles():
     """A DiT block with 2000 token rows (ragged against both the 256- and 128-row tiles):
-    fc1 (N = 4608) takes 256x160 tiles with a ragged last column tile, proj and fc2 one
-    128x128 tile per CU with four 64-wide K stages, qkv two 128x128 tiles per CU."""
+    fc1 (N = 4608) takes 256x160 tiles with a ragged last column tile, proj and fc2
+    128x96 tiles with four 64-wide K stages, qkv two 128x128 tiles per CU."""
     need_gpu()
     cfg = ragged_cfg(synth.DIT, synth.BF16, d=72, H=16, B=4, lat=(4, 1, 50, 40), mlp_ratio=4)
     W = boosted(synth.make_layer_weights(cfg, 0, bias_std=0.02, gain_std=0.1), synth.DIT)
     say("dit block C=1152 d=72 N=500 B=4 (sampled rows)")
     check_block(cfg, W, rows=np.array([0, 1, 127, 128, 255, 256, 420, 450, 498, 499]))
+
+
+def test_dit_block_c2048_tiles():
+    """A DiT block with C = 2048 (16 heads of 128) and 2048 rows: qkv and fc1 take 256x256
+    tiles with 64-wide stages, proj and fc2 (N = 2048, 256 tiles) one 128x128 tile per CU
+    with four 64-wide stages; attention with head dim 128."""
+    need_gpu()
+    cfg = ragged_cfg(synth.DIT, synth.BF16, d=128, H=16, B=2, lat=(4, 1, 64, 64), mlp_ratio=4)
+    W = boosted(synth.make_layer_weights(cfg, 0, bias_std=0.02, gain_std=0.1), synth.DIT)
+    say("dit block C=2048 d=128 N=1024 B=2 (sampled rows)")
+    check_block(cfg, W, rows=np.array([0, 1, 127, 128, 511, 777, 1023]))
 
