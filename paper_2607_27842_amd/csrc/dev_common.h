@@ -29,13 +29,16 @@ typedef uint32_t u32x2_t __attribute__((ext_vector_type(2)));
 
 __device__ __forceinline__ float bf2f(uint16_t b) { return __uint_as_float((uint32_t)b << 16); }
 
-// fp32 -> bf16, round to nearest even (NaN stays NaN).
-__device__ __forceinline__ uint16_t f2bf(float f) {
-  uint32_t u = __float_as_uint(f);
-  if ((u & 0x7fffffffu) > 0x7f800000u) return (uint16_t)((u >> 16) | 0x40u);
-  u += 0x7fffu + ((u >> 16) & 1u);
-  return (uint16_t)(u >> 16);
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+typedef float f32x2_t __attribute__((ext_vector_type(2)));
+
+// fp32 -> bf16, round to nearest even (NaN stays NaN): gfx950's v_cvt_pk_bf16_f32, one
+// instruction per pair instead of the integer rounding sequence per value.
+__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
+  const f32x2_t v = {lo, hi};
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, bf16x2_t));
 }
+__device__ __forceinline__ uint16_t f2bf(float f) { return __builtin_bit_cast(uint16_t, (__bf16)f); }
 
 // Storage traits: 8 elements per 16-byte chunk for bf16, 4 for fp32.
 template <int DT> struct St;
@@ -53,7 +56,7 @@ template <> struct St<DT_BF16> {
   __device__ __forceinline__ static void store(void* p, size_t i, const float* v) {
     uint32_t a[4];
 #pragma unroll
-    for (int j = 0; j < 4; ++j) a[j] = (uint32_t)f2bf(v[2 * j]) | ((uint32_t)f2bf(v[2 * j + 1]) << 16);
+    for (int j = 0; j < 4; ++j) a[j] = pack_bf16x2(v[2 * j], v[2 * j + 1]);
     *reinterpret_cast<uint4*>(reinterpret_cast<uint16_t*>(p) + i) = make_uint4(a[0], a[1], a[2], a[3]);
   }
   __device__ __forceinline__ static float rnd(float x) { return bf2f(f2bf(x)); }

@@ -265,8 +265,8 @@ __global__ __launch_bounds__(NW * SPLIT * 64) void k_attn32(AttnArgs a) {
         const int e = 32 * ot + 8 * g + 4 * h;
         if (e < d) {
           u32x2_t w;
-          w[0] = (uint32_t)f2bf(o[ot][4 * g] * inv) | ((uint32_t)f2bf(o[ot][4 * g + 1] * inv) << 16);
-          w[1] = (uint32_t)f2bf(o[ot][4 * g + 2] * inv) | ((uint32_t)f2bf(o[ot][4 * g + 3] * inv) << 16);
+          w[0] = pack_bf16x2(o[ot][4 * g] * inv, o[ot][4 * g + 1] * inv);
+          w[1] = pack_bf16x2(o[ot][4 * g + 2] * inv, o[ot][4 * g + 3] * inv);
           *reinterpret_cast<u32x2_t*>(out + (rb + q) * a.ldo + (size_t)hd * d + e) = w;
         }
       }

@@ -31,102 +31,109 @@ __device__ __forceinline__ void epilogue_store(const GemmArgs a, int r, int c, f
   else St<DT>::st1(a.out, pr * a.ldo + c, v);
 }
 
+// Elements (uint16) of LDS the epilogue stages per workgroup: each wave owns 32 rows of
+// its WN columns in fp32 (the worst case), rows padded by 4 floats.
+template <int NW, int WN>
+constexpr int epi_lds_elems() { return NW * 32 * (WN + 4) * 2; }
+
 // Epilogue of one wavefront's TM x TN block of 32x32 MFMA tiles (acc), whose rows start at
-// rbase and columns at cbase: lane l owns row rbase + 32 i + l%32 and, per 32-column tile,
-// 4 groups of 4 consecutive columns (8 q + 4 (l/32)).  All loads of a row block (bias,
-// gate, residual) are issued before any is used, from clamped in-range addresses rather
-// than behind per-group branches, so the block costs one memory round trip; only the
-// stores are predicated (N % 8 == 0: a group is in range as a whole).
+// rbase and columns at cbase.  In the MFMA layout lane l owns row rbase + 32 i + l%32 and,
+// per 32-column tile, 4 groups of 4 consecutive columns (8 q + 4 (l/32)): a store
+// instruction there writes 8 bytes to each of 32 rows, which costs the memory pipeline one
+// request per row.  So each 32-row block goes through the wave's own LDS region (lds):
+// values are finished as far as the MFMA layout allows (bias, GELU) and staged as rows,
+// as rounded bf16 when that is the output, else in fp32 (the gated residual is added to
+// the unrounded value).  They are read back with consecutive lanes on consecutive
+// 8-column pieces of a row, so every residual, gate and history load and every store is
+// a 16-byte access and one instruction covers whole row segments.  The physical row (and
+// sample) of each row is computed once by the lane that owns it in the MFMA layout and
+// fetched by the storing lanes with a lane shuffle.  N % 8 == 0: a piece is in range as a
+// whole.  LDS use is wave-private: the caller must have retired the main loop's LDS reads
+// of all waves (barrier) before the first call.
 template <int TM, int TN, int EPI, bool OUT_F32, bool RES_F32>
-__device__ __forceinline__ void epilogue_block(const GemmArgs a, int rbase, int cbase, const f32x16_t (&acc)[TM][TN]) {
+__device__ __forceinline__ void epilogue_block(const GemmArgs a, int rbase, int cbase, const f32x16_t (&acc)[TM][TN], uint16_t* lds) {
+  constexpr bool kF32 = OUT_F32 || EPI == EPI_GATED;
+  constexpr int WN = TN * 32, CPR = WN / 8, RPP = 64 / CPR, NPASS = (32 + RPP - 1) / RPP;
+  constexpr int LDW = kF32 ? WN + 4 : WN + 8;   // row pitch in staged elements
+  static_assert(CPR <= 64, "row wider than a wavefront's pieces");
+  constexpr bool kCache = EPI == EPI_GATED && !OUT_F32;
   const int lane = threadIdx.x & 63, fr = lane & 31, fh = lane >> 5;
   const uint16_t* bias = reinterpret_cast<const uint16_t*>(a.bias);
-  // column tiles whose loads are staged together: all TN, or one at a time for the gated
-  // epilogue of wide tiles (gate, residual and history input would not fit the registers)
-  constexpr int JB = (EPI == EPI_GATED && TN > 1) ? 1 : TN;
-  constexpr bool kCache = EPI == EPI_GATED && !OUT_F32;
-  const bool cache = kCache && a.cache_out != nullptr;
-  // columns and bias depend on the column only: loaded once for all row blocks
-  int col[TN][4];
-  u32x2_t bw[TN][4];
-#pragma unroll
-  for (int j = 0; j < TN; ++j)
-#pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      col[j][q] = cbase + j * 32 + q * 8 + fh * 4;
-      bw[j][q] = *reinterpret_cast<const u32x2_t*>(bias + (col[j][q] < a.N ? col[j][q] : 0));
-    }
+  const bool gelu = EPI == EPI_BIAS_GELU || (EPI == EPI_BIAS_OR_GELU && a.epi == EPI_BIAS_GELU);
+  float* lf = reinterpret_cast<float*>(lds);
 #pragma unroll
   for (int i = 0; i < TM; ++i) {
-    const int r = rbase + i * 32 + fr;
-    const bool rok = r < a.M;
-    const size_t pr = (size_t)a.omap.phys(rok ? r : 0);
-    const float* grow = a.gate + (size_t)a.omap.sample(rok ? r : 0) * a.ldg;
+    const int rmine = rbase + i * 32 + fr;
+    const int prow = a.omap.phys(rmine < a.M ? rmine : 0);
+    const int srow = EPI == EPI_GATED ? a.omap.sample(rmine < a.M ? rmine : 0) : 0;
 #pragma unroll
-    for (int jb = 0; jb < TN; jb += JB) {
-      u32x2_t uw[JB][4];
-      f32x4_t gt[JB][4], rs[JB][4];
+    for (int j = 0; j < TN; ++j)
 #pragma unroll
-      for (int jj = 0; jj < JB; ++jj)
+      for (int q = 0; q < 4; ++q) {
+        const int c = cbase + j * 32 + q * 8 + fh * 4;
+        const u32x2_t bw = *reinterpret_cast<const u32x2_t*>(bias + (c < a.N ? c : 0));
+        float v[4] = {acc[i][j][4 * q] + __uint_as_float(bw[0] << 16), acc[i][j][4 * q + 1] + __uint_as_float(bw[0] & 0xffff0000u),
+                      acc[i][j][4 * q + 2] + __uint_as_float(bw[1] << 16), acc[i][j][4 * q + 3] + __uint_as_float(bw[1] & 0xffff0000u)};
+        if (gelu) {
 #pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          const int c = col[jb + jj][q] < a.N ? col[jb + jj][q] : 0;
-          if (EPI == EPI_GATED) {
-            gt[jj][q] = *reinterpret_cast<const f32x4_t*>(grow + c);
-            if (RES_F32) {
-              rs[jj][q] = *reinterpret_cast<const f32x4_t*>(reinterpret_cast<const float*>(a.resid) + pr * a.ldr + c);
-            } else {
-              const u32x2_t w = *reinterpret_cast<const u32x2_t*>(reinterpret_cast<const uint16_t*>(a.resid) + pr * a.ldr + c);
-              rs[jj][q][0] = __uint_as_float(w[0] << 16); rs[jj][q][1] = __uint_as_float(w[0] & 0xffff0000u);
-              rs[jj][q][2] = __uint_as_float(w[1] << 16); rs[jj][q][3] = __uint_as_float(w[1] & 0xffff0000u);
-            }
-          }
-          if (kCache && cache && a.cache_u)
-            uw[jj][q] = *reinterpret_cast<const u32x2_t*>(reinterpret_cast<const uint16_t*>(a.cache_u) + pr * a.ldo + c);
+          for (int e = 0; e < 4; ++e) v[e] = gelu_tanh_f(v[e]);
         }
-#pragma unroll
-      for (int jj = 0; jj < JB; ++jj)
-#pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          const int j = jb + jj;
-          float v[4] = {acc[i][j][4 * q] + __uint_as_float(bw[j][q][0] << 16),
-                        acc[i][j][4 * q + 1] + __uint_as_float(bw[j][q][0] & 0xffff0000u),
-                        acc[i][j][4 * q + 2] + __uint_as_float(bw[j][q][1] << 16),
-                        acc[i][j][4 * q + 3] + __uint_as_float(bw[j][q][1] & 0xffff0000u)};
-          if (EPI == EPI_BIAS_GELU || (EPI == EPI_BIAS_OR_GELU && a.epi == EPI_BIAS_GELU)) {
-#pragma unroll
-            for (int e = 0; e < 4; ++e) v[e] = gelu_tanh_f(v[e]);
-          }
-          if (EPI == EPI_GATED) {
-#pragma unroll
-            for (int e = 0; e < 4; ++e) v[e] = rs[jj][q][e] + gt[jj][q][e] * v[e];
-          }
-          if (rok && col[j][q] < a.N) {
-            const int c = col[j][q];
-            if (OUT_F32) {
-              const f32x4_t o = {v[0], v[1], v[2], v[3]};
-              *reinterpret_cast<f32x4_t*>(reinterpret_cast<float*>(a.out) + pr * a.ldo + c) = o;
-            } else {
-              u32x2_t o;
-              o[0] = (uint32_t)f2bf(v[0]) | ((uint32_t)f2bf(v[1]) << 16);
-              o[1] = (uint32_t)f2bf(v[2]) | ((uint32_t)f2bf(v[3]) << 16);
-              *reinterpret_cast<u32x2_t*>(reinterpret_cast<uint16_t*>(a.out) + pr * a.ldo + c) = o;
-              if (kCache && cache) {
-                // history refresh from the stored (rounded) output, as the separate kernel does
-                u32x2_t dlt = o;
-                if (a.cache_u) {
-                  const float h0 = __uint_as_float(o[0] << 16), h1 = __uint_as_float(o[0] & 0xffff0000u);
-                  const float h2 = __uint_as_float(o[1] << 16), h3 = __uint_as_float(o[1] & 0xffff0000u);
-                  const float u0 = __uint_as_float(uw[jj][q][0] << 16), u1 = __uint_as_float(uw[jj][q][0] & 0xffff0000u);
-                  const float u2 = __uint_as_float(uw[jj][q][1] << 16), u3 = __uint_as_float(uw[jj][q][1] & 0xffff0000u);
-                  dlt[0] = (uint32_t)f2bf(h0 - u0) | ((uint32_t)f2bf(h1 - u1) << 16);
-                  dlt[1] = (uint32_t)f2bf(h2 - u2) | ((uint32_t)f2bf(h3 - u3) << 16);
-                }
-                *reinterpret_cast<u32x2_t*>(reinterpret_cast<uint16_t*>(a.cache_out) + pr * a.ldo + c) = dlt;
-              }
-            }
-          }
+        const int off = fr * LDW + j * 32 + q * 8 + fh * 4;
+        if (kF32) {
+          *reinterpret_cast<f32x4_t*>(lf + off) = f32x4_t{v[0], v[1], v[2], v[3]};
+        } else {
+          *reinterpret_cast<u32x2_t*>(lds + off) = u32x2_t{pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3])};
         }
+      }
+#pragma unroll
+    for (int p = 0; p < NPASS; ++p) {
+      const int rr = p * RPP + lane / CPR, cc = (lane % CPR) * 8;
+      const int src = rr < 32 ? rr : 0;
+      const size_t pr = (size_t)__shfl(prow, src, 64);
+      const int sr = EPI == EPI_GATED ? __shfl(srow, src, 64) : 0;
+      const int r = rbase + i * 32 + rr, c = cbase + cc;
+      if (lane >= RPP * CPR || rr >= 32 || r >= a.M || c >= a.N) continue;
+      if (!kF32) {
+        *reinterpret_cast<u32x4_t*>(reinterpret_cast<uint16_t*>(a.out) + pr * a.ldo + c) =
+            *reinterpret_cast<const u32x4_t*>(lds + rr * LDW + cc);
+        continue;
+      }
+      const f32x4_t x0 = *reinterpret_cast<const f32x4_t*>(lf + rr * LDW + cc);
+      const f32x4_t x1 = *reinterpret_cast<const f32x4_t*>(lf + rr * LDW + cc + 4);
+      float v[8] = {x0[0], x0[1], x0[2], x0[3], x1[0], x1[1], x1[2], x1[3]};
+      if (EPI == EPI_GATED) {
+        float rs[8], g[8];
+        if (RES_F32) {
+          St<DT_F32>::load(a.resid, pr * a.ldr + c, rs);
+          St<DT_F32>::load(a.resid, pr * a.ldr + c + 4, rs + 4);
+        } else {
+          St<DT_BF16>::load(a.resid, pr * a.ldr + c, rs);
+        }
+        const float* gp = a.gate + (size_t)sr * a.ldg + c;
+        St<DT_F32>::load(gp, 0, g);
+        St<DT_F32>::load(gp, 4, g + 4);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) v[e] = rs[e] + g[e] * v[e];
+      }
+      if (OUT_F32) {
+        St<DT_F32>::store(a.out, pr * a.ldo + c, v);
+        St<DT_F32>::store(a.out, pr * a.ldo + c + 4, v + 4);
+        continue;
+      }
+      St<DT_BF16>::store(a.out, pr * a.ldo + c, v);
+      if (kCache && a.cache_out) {
+        // history refresh from the stored (rounded) output, as the separate kernel does
+        float h[8];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) h[e] = St<DT_BF16>::rnd(v[e]);
+        if (a.cache_u) {
+          float u[8];
+          St<DT_BF16>::load(a.cache_u, pr * a.ldo + c, u);
+#pragma unroll
+          for (int e = 0; e < 8; ++e) h[e] -= u[e];
+        }
+        St<DT_BF16>::store(a.cache_out, pr * a.ldo + c, h);
+      }
     }
   }
 }
@@ -177,8 +184,10 @@ __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64) void k_gemm_bf16(GemmGr
   constexpr int TM = WM / 32, TN = WN / 32;
   constexpr int RSTEP = NT / 8;
   constexpr int CA = BM / RSTEP, CB = BN / RSTEP;
-  __shared__ __attribute__((aligned(16))) uint16_t sA[2][BM * LDT];
-  __shared__ __attribute__((aligned(16))) uint16_t sB[2][BN * LDT];
+  constexpr int kMain = 2 * (BM + BN) * LDT, kEpi = epi_lds_elems<(BM / WM) * NWN, WN>();
+  __shared__ __attribute__((aligned(1024))) uint16_t smem[kMain > kEpi ? kMain : kEpi];
+  uint16_t (*sA)[BM * LDT] = reinterpret_cast<uint16_t (*)[BM * LDT]>(smem);
+  uint16_t (*sB)[BN * LDT] = reinterpret_cast<uint16_t (*)[BN * LDT]>(smem + 2 * BM * LDT);
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   int tm, tn;
   // workgroup-uniform: keep the problem select and tile origin in scalar registers
@@ -258,7 +267,8 @@ __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64) void k_gemm_bf16(GemmGr
   }
 #undef FF_GLOAD
 #undef FF_SSTORE
-  epilogue_block<TM, TN, EPI, OUT_F32, RES_F32>(a, m0 + wm, n0 + wn, acc);
+  // the loop ends with a barrier after every wave's last LDS read
+  epilogue_block<TM, TN, EPI, OUT_F32, RES_F32>(a, m0 + wm, n0 + wn, acc, smem + wave * 32 * (WN + 4) * 2);
 }
 // ------------------------------------------------------------------ bf16 MFMA GEMM, direct-to-LDS
 // For K % BKd == 0 (BKd = 32 or 64).  Operand tiles go global -> LDS with
@@ -310,8 +320,10 @@ __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64) void k_gemm_dl(GemmGrou
   static_assert(BKd == 32 || BKd == 64, "stage width");
   static_assert(IA * RPI * NW == BM && IB * RPI * NW == BN, "every tile row loaded by one DMA lane");
   static_assert(NST >= 3 && NST <= 5 && TM + TN <= 15, "unsupported tile");
-  __shared__ __attribute__((aligned(1024))) uint16_t sA[NST][BM * BKd];
-  __shared__ __attribute__((aligned(1024))) uint16_t sB[NST][BN * BKd];
+  constexpr int kMain = NST * (BM + BN) * BKd, kEpi = epi_lds_elems<NW, WN>();
+  __shared__ __attribute__((aligned(1024))) uint16_t smem[kMain > kEpi ? kMain : kEpi];
+  uint16_t (*sA)[BM * BKd] = reinterpret_cast<uint16_t (*)[BM * BKd]>(smem);
+  uint16_t (*sB)[BN * BKd] = reinterpret_cast<uint16_t (*)[BN * BKd]>(smem + NST * BM * BKd);
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   int tm, tn;
   // workgroup-uniform: keep the problem select and tile origin in scalar registers
@@ -415,7 +427,8 @@ __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64) void k_gemm_dl(GemmGrou
     }
   }
 #undef FF_ISSUE
-  epilogue_block<TM, TN, EPI, OUT_F32, RES_F32>(a, m0 + wm, n0 + wn, acc);
+  __syncthreads();   // every wave's last fragment reads retired before LDS is reused
+  epilogue_block<TM, TN, EPI, OUT_F32, RES_F32>(a, m0 + wm, n0 + wn, acc, smem + wave * 32 * (WN + 4) * 2);
 }
 
 // ------------------------------------------------------------------ bf16 MFMA GEMM, 64-wide K stages
@@ -433,8 +446,10 @@ __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64) void k_gemm_dl64(GemmGr
   constexpr int TM = WM / 32, TN = WN / 32;
   constexpr int IA = BM / RPI / NW, IB = BN / RPI / NW;
   static_assert(IA >= 1 && IB >= 1 && TM + TN <= 15, "unsupported tile");
-  __shared__ __attribute__((aligned(1024))) uint16_t sA[2][BM * BKd];
-  __shared__ __attribute__((aligned(1024))) uint16_t sB[2][BN * BKd];
+  constexpr int kMain = 2 * (BM + BN) * BKd, kEpi = epi_lds_elems<NW, WN>();
+  __shared__ __attribute__((aligned(1024))) uint16_t smem[kMain > kEpi ? kMain : kEpi];
+  uint16_t (*sA)[BM * BKd] = reinterpret_cast<uint16_t (*)[BM * BKd]>(smem);
+  uint16_t (*sB)[BN * BKd] = reinterpret_cast<uint16_t (*)[BN * BKd]>(smem + 2 * BM * BKd);
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   int tm, tn;
   // workgroup-uniform: keep the problem select and tile origin in scalar registers
@@ -515,7 +530,8 @@ __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64) void k_gemm_dl64(GemmGr
     asm volatile("s_waitcnt vmcnt(0)\n\ts_barrier" ::: "memory");
   }
 #undef FF_ISSUE
-  epilogue_block<TM, TN, EPI, OUT_F32, RES_F32>(a, m0 + wm, n0 + wn, acc);
+  // the loop ends with a barrier after every wave's last LDS read
+  epilogue_block<TM, TN, EPI, OUT_F32, RES_F32>(a, m0 + wm, n0 + wn, acc, smem + wave * 32 * (WN + 4) * 2);
 }
 
 

@@ -24,8 +24,8 @@ template <> __device__ __forceinline__ void st4<DT_F32>(void* p, size_t i, const
 }
 template <> __device__ __forceinline__ void st4<DT_BF16>(void* p, size_t i, const float* v) {
   uint2 w;
-  w.x = (uint32_t)f2bf(v[0]) | ((uint32_t)f2bf(v[1]) << 16);
-  w.y = (uint32_t)f2bf(v[2]) | ((uint32_t)f2bf(v[3]) << 16);
+  w.x = pack_bf16x2(v[0], v[1]);
+  w.y = pack_bf16x2(v[2], v[3]);
   *reinterpret_cast<uint2*>(reinterpret_cast<uint16_t*>(p) + i) = w;
 }
 
