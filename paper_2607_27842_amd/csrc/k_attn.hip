@@ -188,12 +188,15 @@ __global__ __launch_bounds__(NW * SPLIT * 64) void k_attn32(AttnArgs a) {
       for (int t = 0; t < NOT; ++t) o[t] *= alpha;
       mrow = mx;
     }
+    // mrow is still -inf only if every score so far is -inf (all keys masked, as for a
+    // group whose keys start past N): those probabilities are exp2(-inf) = 0, not NaN
+    const float moff = mrow == -INFINITY ? 0.f : mrow;
     float ls = 0.f;
 #pragma unroll
     for (int t = 0; t < NS; ++t)
 #pragma unroll
       for (int v = 0; v < 16; ++v) {
-        const float pr = __builtin_amdgcn_exp2f(fmaf(sc[t][v], sl2, -mrow));
+        const float pr = __builtin_amdgcn_exp2f(fmaf(sc[t][v], sl2, -moff));
         sc[t][v] = pr;
         ls += pr;
       }
