@@ -276,7 +276,10 @@ __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64) void k_gemm_bf16(GemmGr
 // BKd-wide K slices issued NST-1 slices ahead.  Each DMA instruction fills 1 KB of LDS in
 // lane order (16 rows x 64 bytes, or 8 rows x 128 bytes), so rows cannot be padded;
 // instead lane l of a row loads a 16-byte chunk XOR-swizzled by the row ((l%4) ^
-// ((row>>2)&3), or (l%8) ^ (row&7)), which keeps the 32-row fragment reads conflict-free.
+// ((row>>2)&3), or (l%8) ^ ((row>>1)&7)), which keeps the fragment reads free of bank
+// conflicts: a 16-row group of a read spreads over all 64 banks.  (With 128-byte rows, even
+// rows sit on banks 0-31 and odd rows on 32-63, so the 64-wide swizzle takes row/2; the
+// first version used row&7, which put rows r and r+8 on the same banks.)
 //
 // Synchronisation is explicit: the compiler's barrier lowering waits for ALL outstanding
 // loads (it cannot tell which stage a DMA targets), which would remove the prefetch.  So a
@@ -334,7 +337,7 @@ __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64) void k_gemm_dl(GemmGrou
   const int m0 = tm * BM, n0 = tn * BN;
   const uint16_t* A = reinterpret_cast<const uint16_t*>(a.A);
   const uint16_t* W = reinterpret_cast<const uint16_t*>(a.W);
-  auto swz = [](int ch, int row) { return BKd == 64 ? (ch ^ (row & 7)) : (ch ^ ((row >> 2) & 3)); };
+  auto swz = [](int ch, int row) { return BKd == 64 ? (ch ^ ((row >> 1) & 7)) : (ch ^ ((row >> 2) & 3)); };
   // rows past the matrix read row 0 (in bounds); their results are never stored
   const int lr = lane / CH, ls = lane % CH;
   size_t ga[IA], gb[IB];
@@ -434,7 +437,7 @@ __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64) void k_gemm_dl(GemmGrou
 // ------------------------------------------------------------------ bf16 MFMA GEMM, 64-wide K stages
 // For K % 64 == 0 on grids that keep the MFMAs busy for a whole stage (see launch_bf16).
 // Two LDS buffers of 64-wide K stages: 128-byte rows (full cache lines per DMA row, 8 rows
-// per 1 KB instruction), XOR swizzle chunk ^ (row & 7).  The DMA of stage kt+1 is issued
+// per 1 KB instruction), XOR swizzle chunk ^ ((row >> 1) & 7).  The DMA of stage kt+1 is issued
 // right after the barrier that ends stage kt-1 (its buffer is free then) and lands during
 // stage kt's four 16-wide k steps, whose fragments are double-buffered in registers as in
 // k_gemm_dl; one wait + barrier per stage.
@@ -465,12 +468,12 @@ __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64) void k_gemm_dl64(GemmGr
 #pragma unroll
   for (int j = 0; j < IA; ++j) {
     const int row = (wave * IA + j) * RPI + lr, gm = m0 + row;
-    ga[j] = (size_t)a.amap.phys(gm < a.M ? gm : 0) * a.lda + ((ls ^ (row & 7)) * 8);
+    ga[j] = (size_t)a.amap.phys(gm < a.M ? gm : 0) * a.lda + ((ls ^ ((row >> 1) & 7)) * 8);
   }
 #pragma unroll
   for (int j = 0; j < IB; ++j) {
     const int row = (wave * IB + j) * RPI + lr, gn = n0 + row;
-    gb[j] = (size_t)(gn < a.N ? gn : 0) * a.ldw + ((ls ^ (row & 7)) * 8);
+    gb[j] = (size_t)(gn < a.N ? gn : 0) * a.ldw + ((ls ^ ((row >> 1) & 7)) * 8);
   }
 #define FF_ISSUE(st, k0)                                                                                  \
   do {                                                                                                    \
@@ -501,18 +504,18 @@ __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64) void k_gemm_dl64(GemmGr
     const int st = kt & 1;
     if (kt + 1 < nk) FF_ISSUE(st ^ 1, (kt + 1) * BKd);   // buffer of stage kt-1: free after the last barrier
 #pragma unroll
-    for (int t = 0; t < TM; ++t) fa[0][t] = lds_rd128(&sA[st][rowa[t] * BKd + ((fh ^ (rowa[t] & 7)) * 8)]);
+    for (int t = 0; t < TM; ++t) fa[0][t] = lds_rd128(&sA[st][rowa[t] * BKd + ((fh ^ ((rowa[t] >> 1) & 7)) * 8)]);
 #pragma unroll
-    for (int t = 0; t < TN; ++t) fb[0][t] = lds_rd128(&sB[st][rowb[t] * BKd + ((fh ^ (rowb[t] & 7)) * 8)]);
+    for (int t = 0; t < TN; ++t) fb[0][t] = lds_rd128(&sB[st][rowb[t] * BKd + ((fh ^ ((rowb[t] >> 1) & 7)) * 8)]);
 #pragma unroll
     for (int s = 0; s < KS; ++s) {
       const int cur = s & 1, nxt = cur ^ 1;
       if (s + 1 < KS) {
         const int ch = (s + 1) * 2 + fh;
 #pragma unroll
-        for (int t = 0; t < TM; ++t) fa[nxt][t] = lds_rd128(&sA[st][rowa[t] * BKd + ((ch ^ (rowa[t] & 7)) * 8)]);
+        for (int t = 0; t < TM; ++t) fa[nxt][t] = lds_rd128(&sA[st][rowa[t] * BKd + ((ch ^ ((rowa[t] >> 1) & 7)) * 8)]);
 #pragma unroll
-        for (int t = 0; t < TN; ++t) fb[nxt][t] = lds_rd128(&sB[st][rowb[t] * BKd + ((ch ^ (rowb[t] & 7)) * 8)]);
+        for (int t = 0; t < TN; ++t) fb[nxt][t] = lds_rd128(&sB[st][rowb[t] * BKd + ((ch ^ ((rowb[t] >> 1) & 7)) * 8)]);
         asm volatile("s_waitcnt lgkmcnt(%0)" ::"n"(TM + TN) : "memory");
       } else {
         asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
