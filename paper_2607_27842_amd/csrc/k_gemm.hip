@@ -188,7 +188,9 @@ __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64) void k_gemm_bf16(GemmGr
   __shared__ __attribute__((aligned(1024))) uint16_t smem[kMain > kEpi ? kMain : kEpi];
   uint16_t (*sA)[BM * LDT] = reinterpret_cast<uint16_t (*)[BM * LDT]>(smem);
   uint16_t (*sB)[BN * LDT] = reinterpret_cast<uint16_t (*)[BN * LDT]>(smem + 2 * BM * LDT);
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  // wave index in a scalar register: the per-wave LDS addresses of the DMA (M0) are then
+  // computed on the scalar unit instead of with a v_readfirstlane per instruction
+  const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   int tm, tn;
   // workgroup-uniform: keep the problem select and tile origin in scalar registers
   const int prob = __builtin_amdgcn_readfirstlane(tile_of(blockIdx.x, G.tm[0], G.tn[0], G.tm[NP - 1], G.tn[NP - 1], NP, tm, tn));
@@ -327,7 +329,9 @@ __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64) void k_gemm_dl(GemmGrou
   __shared__ __attribute__((aligned(1024))) uint16_t smem[kMain > kEpi ? kMain : kEpi];
   uint16_t (*sA)[BM * BKd] = reinterpret_cast<uint16_t (*)[BM * BKd]>(smem);
   uint16_t (*sB)[BN * BKd] = reinterpret_cast<uint16_t (*)[BN * BKd]>(smem + NST * BM * BKd);
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  // wave index in a scalar register: the per-wave LDS addresses of the DMA (M0) are then
+  // computed on the scalar unit instead of with a v_readfirstlane per instruction
+  const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   int tm, tn;
   // workgroup-uniform: keep the problem select and tile origin in scalar registers
   const int prob = __builtin_amdgcn_readfirstlane(tile_of(blockIdx.x, G.tm[0], G.tn[0], G.tm[NP - 1], G.tn[NP - 1], NP, tm, tn));
@@ -453,7 +457,9 @@ __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64) void k_gemm_dl64(GemmGr
   __shared__ __attribute__((aligned(1024))) uint16_t smem[kMain > kEpi ? kMain : kEpi];
   uint16_t (*sA)[BM * BKd] = reinterpret_cast<uint16_t (*)[BM * BKd]>(smem);
   uint16_t (*sB)[BN * BKd] = reinterpret_cast<uint16_t (*)[BN * BKd]>(smem + 2 * BM * BKd);
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  // wave index in a scalar register: the per-wave LDS addresses of the DMA (M0) are then
+  // computed on the scalar unit instead of with a v_readfirstlane per instruction
+  const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   int tm, tn;
   // workgroup-uniform: keep the problem select and tile origin in scalar registers
   const int prob = __builtin_amdgcn_readfirstlane(tile_of(blockIdx.x, G.tm[0], G.tn[0], G.tm[NP - 1], G.tn[NP - 1], NP, tm, tn));
