@@ -59,6 +59,15 @@ template <> struct St<DT_BF16> {
     for (int j = 0; j < 4; ++j) a[j] = pack_bf16x2(v[2 * j], v[2 * j + 1]);
     *reinterpret_cast<uint4*>(reinterpret_cast<uint16_t*>(p) + i) = make_uint4(a[0], a[1], a[2], a[3]);
   }
+  // the same 16-byte load with the non-temporal hint, for data read once (history slots)
+  __device__ __forceinline__ static void load_nt(const void* p, size_t i, float* v) {
+    const u32x4_t w = __builtin_nontemporal_load(reinterpret_cast<const u32x4_t*>(reinterpret_cast<const uint16_t*>(p) + i));
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      v[2 * j] = __uint_as_float(w[j] << 16);
+      v[2 * j + 1] = __uint_as_float(w[j] & 0xffff0000u);
+    }
+  }
   __device__ __forceinline__ static float rnd(float x) { return bf2f(f2bf(x)); }
   __device__ __forceinline__ static float ld1(const void* p, size_t i) {
     return bf2f(reinterpret_cast<const uint16_t*>(p)[i]);
@@ -75,6 +84,10 @@ template <> struct St<DT_F32> {
   }
   __device__ __forceinline__ static void store(void* p, size_t i, const float* v) {
     *reinterpret_cast<float4*>(reinterpret_cast<float*>(p) + i) = make_float4(v[0], v[1], v[2], v[3]);
+  }
+  __device__ __forceinline__ static void load_nt(const void* p, size_t i, float* v) {
+    const f32x4_t w = __builtin_nontemporal_load(reinterpret_cast<const f32x4_t*>(reinterpret_cast<const float*>(p) + i));
+    v[0] = w[0]; v[1] = w[1]; v[2] = w[2]; v[3] = w[3];
   }
   __device__ __forceinline__ static float rnd(float x) { return x; }
   __device__ __forceinline__ static float ld1(const void* p, size_t i) {

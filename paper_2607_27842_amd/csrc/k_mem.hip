@@ -49,7 +49,7 @@ __device__ __forceinline__ void draft_math(const Terms& t, size_t off, const flo
   for (int m = 0; m < kMaxTerms; ++m) {
     if (m < t.n) {
       float s[S::V];
-      S::load(t.slot[m], off, s);
+      S::load_nt(t.slot[m], off, s);   // each history value is read once per step
 #pragma unroll
       for (int j = 0; j < S::V; ++j) f[j] = fmaf(t.c[m], s[j], f[j]);
     }
