@@ -849,11 +849,11 @@ ff_status ff_denoise_step(ff_ctx* c, int32_t step, float* x, const float* cond, 
     PatchGeom pg{m.B, m.lat_c, m.lat_f, m.lat_h, m.lat_w, m.pt, m.ph, m.pw};
     void* patches = at(ws, W.PATCH);
     const double lat_elems = (double)m.B * m.n_img * m.P;
-    HIP_TRY(ex.other(lat_elems * (4 + es), [&] { return patchify(dt, x, patches, pg, st); }), "patchify");
     void* cur = at(ws, W.X0);
     void* alt = at(ws, W.X1);
     const RowMap img{m.n_img, m.N, m.n_txt};
     const RowMap ident{m.B * m.n_img, m.B * m.n_img, 0};
+    HIP_TRY(ex.other(lat_elems * (4 + es), [&] { return patchify(dt, x, patches, pg, st); }), "patchify");
     GemmArgs pe = gemm_args(patches, m.P, ident, c->g.pe_w, c->g.pe_b, m.B * m.n_img, C, m.P, EPI_BIAS, cur, C, img);
     HIP_TRY(ex.gemm(pe), "patch embed");
     if (m.n_txt > 0)
@@ -914,15 +914,24 @@ ff_status ff_denoise_step(ff_ctx* c, int32_t step, float* x, const float* cond, 
     float* mod = at<float>(ws, W.MOD);
     GemvArgs gf{cs, C, 0, c->g.fmod_w, c->g.fmod_b, 2 * C, C, m.B, mod, 2 * C, 0, nullptr, 0, xsplit};
     HIP_TRY(ex.gemv(gf), "final modulation");
-    void* lna = at(ws, W.LNA);
-    LnModArgs ln{cur, 0, C, img, m.B * m.n_img, C, m.ln_eps, mod, mod + C, 2 * C, lna, C};
-    HIP_TRY(ex.ln(ln), "final ln");
-    float* yf = at<float>(ws, W.YF);
-    GemmArgs gfl = gemm_args(lna, C, img, c->g.f_w, c->g.f_b, m.B * m.n_img, m.P, C, EPI_BIAS, yf, m.P, ident);
-    gfl.out_f32 = 1;
-    HIP_TRY(ex.gemm(gfl), "final linear");
-    HIP_TRY(ex.other(lat_elems * 12.0, [&] { return unpatchify_euler(yf, x, (float)(t_n - t_i), pg, st); }),
-            "unpatchify + euler");
+    if (final_layer_ok(dt, m.P, C)) {
+      // LN + modulation + final linear + unpatchify + Euler in one launch, one wavefront
+      // per image token (small final weights only)
+      const FinalArgs fa{cur, C, img, m.B * m.n_img, C, m.ln_eps, mod, mod + C, 2 * C, c->g.f_w, c->g.f_b,
+                         x, (float)(t_n - t_i), pg};
+      HIP_TRY(ex.other((double)m.B * m.n_img * C * es + lat_elems * 8.0, [&] { return final_layer(dt, fa, st); }),
+              "final layer");
+    } else {
+      void* lna = at(ws, W.LNA);
+      LnModArgs ln{cur, 0, C, img, m.B * m.n_img, C, m.ln_eps, mod, mod + C, 2 * C, lna, C};
+      HIP_TRY(ex.ln(ln), "final ln");
+      float* yf = at<float>(ws, W.YF);
+      GemmArgs gfl = gemm_args(lna, C, img, c->g.f_w, c->g.f_b, m.B * m.n_img, m.P, C, EPI_BIAS, yf, m.P, ident);
+      gfl.out_f32 = 1;
+      HIP_TRY(ex.gemm(gfl), "final linear");
+      HIP_TRY(ex.other(lat_elems * 12.0, [&] { return unpatchify_euler(yf, x, (float)(t_n - t_i), pg, st); }),
+              "unpatchify + euler");
+    }
     // bookkeeping after a successful enqueue
     if (p.step_kind[i] == FF_STEP_REFRESH) {
       c->counts.n_full_refresh++;

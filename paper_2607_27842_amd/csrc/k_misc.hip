@@ -393,6 +393,123 @@ __global__ __launch_bounds__(256) void k_unpatchify_euler(const float* __restric
   x[i] = x[i] + dt * yv[((long)b * n_img + tok) * P + feat];
 }
 
+
+// Sum of NP per-lane values over the 64 lanes of a wavefront, by recursive halving: at the
+// step with stride s, a lane keeps one half of its values (the upper half if lane & s),
+// adds the partner's copy of that half, and hands over the other half.  After log2(NP)
+// steps every lane holds one output, o = lane / (64 / NP); the remaining strides sum the
+// lanes that share it.  63 shuffles for NP = 64 instead of 6 NP.
+template <int NP>
+__device__ __forceinline__ float wave_reduce_outputs(float (&v)[NP], int lane) {
+  static_assert(NP >= 1 && NP <= 64 && (NP & (NP - 1)) == 0, "power of two");
+#pragma unroll
+  for (int n = NP, s = 32; n > 1; n /= 2, s /= 2) {
+    const bool upper = (lane & s) != 0;
+#pragma unroll
+    for (int k = 0; k < n / 2; ++k) {
+      const float send = upper ? v[k] : v[k + n / 2];
+      const float recv = __shfl_xor(send, s, 64);
+      v[k] = (upper ? v[k + n / 2] : v[k]) + recv;
+    }
+  }
+  float r = v[0];
+#pragma unroll
+  for (int s = 32 / NP; s > 0; s /= 2) r += __shfl_xor(r, s, 64);
+  return r;
+}
+
+// Final weights up to this size are read straight from the caches by every wavefront;
+// larger ones (FLUX-like: 384 KB) make that L2-bound, and the GEMM path, which reuses the
+// weight across a tile, is faster there.
+constexpr size_t kFinalMaxWeightBytes = 64 * 1024;
+
+template <int DT, int U, int NP>   // U: 4-element units per lane, NP: outputs per token
+__global__ __launch_bounds__(256) void k_final_layer(FinalArgs a) {
+  using S = St<DT>;
+  const int lane = threadIdx.x % 64;
+  const int r = blockIdx.x * 4 + threadIdx.x / 64;
+  if (r >= a.rows) return;   // r is per wavefront: the whole wave leaves together
+  const size_t pr = (size_t)a.map.phys(r);
+  const int b = a.map.sample(r);
+  const int units = a.C / 4;
+  const float* sh = a.shift + (size_t)b * a.ldm;
+  const float* sc = a.scale + (size_t)b * a.ldm;
+  float v[U][4];
+  float s = 0.f;
+#pragma unroll
+  for (int k = 0; k < U; ++k) {
+    const int u = k * 64 + lane;
+    if (u < units) ld4<DT>(a.in, pr * a.ldi + u * 4, v[k]);
+  }
+#pragma unroll
+  for (int k = 0; k < U; ++k)
+    if (k * 64 + lane < units) s += (v[k][0] + v[k][1]) + (v[k][2] + v[k][3]);
+  const float mean = wave_sum(s) / (float)a.C;
+  float q = 0.f;
+#pragma unroll
+  for (int k = 0; k < U; ++k)
+    if (k * 64 + lane < units) {
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const float dlt = v[k][j] - mean;
+        q += dlt * dlt;
+      }
+    }
+  const float rstd = 1.0f / sqrtf(wave_sum(q) / (float)a.C + a.eps);
+  // the modulated row, rounded to the model dtype as ln_modulate stores it
+#pragma unroll
+  for (int k = 0; k < U; ++k) {
+    const int u = k * 64 + lane;
+    if (u < units) {
+      const float4 s4 = *reinterpret_cast<const float4*>(sh + u * 4);
+      const float4 c4 = *reinterpret_cast<const float4*>(sc + u * 4);
+      v[k][0] = St<DT>::rnd((v[k][0] - mean) * rstd * (1.0f + c4.x) + s4.x);
+      v[k][1] = St<DT>::rnd((v[k][1] - mean) * rstd * (1.0f + c4.y) + s4.y);
+      v[k][2] = St<DT>::rnd((v[k][2] - mean) * rstd * (1.0f + c4.z) + s4.z);
+      v[k][3] = St<DT>::rnd((v[k][3] - mean) * rstd * (1.0f + c4.w) + s4.w);
+    }
+  }
+  // outputs in groups of at most 32 (register budget), each reduced over the wavefront
+  constexpr int NG = NP > 32 ? 32 : NP;
+  constexpr int LPO = 64 / NG;   // lanes per output after the reduction
+  const PatchGeom& g = a.g;
+  const int Hp = g.H / g.ph, Wp = g.W / g.pw;
+  const int n_img = (g.F / g.pt) * Hp * Wp;
+  const int tok = r - b * n_img;
+  const int wx = tok % Wp, hy = (tok / Wp) % Hp, f = tok / (Wp * Hp);
+#pragma unroll
+  for (int og = 0; og < NP; og += NG) {
+    float acc[NG];
+#pragma unroll
+    for (int o = 0; o < NG; ++o) acc[o] = 0.f;
+#pragma unroll
+    for (int k = 0; k < U; ++k) {
+      const int u = k * 64 + lane;
+      if (u < units) {
+#pragma unroll
+        for (int o = 0; o < NG; ++o) {
+          float w[4];
+          ld4<DT>(a.W, (size_t)(og + o) * a.C + u * 4, w);
+#pragma unroll
+          for (int j = 0; j < 4; ++j) acc[o] = fmaf(v[k][j], w[j], acc[o]);
+        }
+      }
+    }
+    const float sum = wave_reduce_outputs<NG>(acc, lane);
+    if (lane % LPO == 0) {
+      const int o = og + lane / LPO;
+      const float val = sum + S::ld1(a.bias, o);
+      // unpatchify: output o of token (b, tok) is latent pixel (ch, f pt + da, hy ph + dy, wx pw + dx)
+      const int ch = o % g.lat_c, dx = (o / g.lat_c) % g.pw, dy = (o / (g.lat_c * g.pw)) % g.ph;
+      const int da = o / (g.lat_c * g.pw * g.ph);
+      const size_t idx = ((((size_t)b * g.lat_c + ch) * g.F + (f * g.pt + da)) * g.H + (hy * g.ph + dy)) * g.W +
+                         (wx * g.pw + dx);
+      a.x[idx] = a.x[idx] + a.dt * val;
+    }
+  }
+}
+
+
 }  // namespace
 
 hipError_t ln_modulate(int dtype, const LnModArgs& a, hipStream_t s) {
@@ -504,6 +621,38 @@ hipError_t patchify(int dtype, const float* x, void* patches, const PatchGeom& g
 hipError_t unpatchify_euler(const float* yv, float* x, float dt, const PatchGeom& g, hipStream_t st) {
   const long n = (long)g.B * g.lat_c * g.F * g.H * g.W;
   FF_LAUNCH(k_unpatchify_euler, cdiv(n, 256), 256, 0, st, yv, x, dt, g);
+  return hipGetLastError();
+}
+
+
+bool final_layer_ok(int dtype, int P, int C) {
+  return (P == 16 || P == 32 || P == 64) && C % 4 == 0 && C <= 4096 && (size_t)P * C * dsize(dtype) <= kFinalMaxWeightBytes;
+}
+
+hipError_t final_layer(int dtype, const FinalArgs& a, hipStream_t s) {
+  if (a.rows == 0) return hipSuccess;
+  const int P = a.g.pt * a.g.ph * a.g.pw * a.g.lat_c;
+  if (!final_layer_ok(dtype, P, a.C)) return hipErrorInvalidValue;
+  const int grid = cdiv(a.rows, 4);
+  const int units = cdiv(a.C / 4, 64);
+#define FF_FIN(U, NP)                                                                   \
+  do {                                                                                  \
+    if (dtype == DT_BF16) FF_LAUNCH((k_final_layer<DT_BF16, U, NP>), grid, 256, 0, s, a); \
+    else FF_LAUNCH((k_final_layer<DT_F32, U, NP>), grid, 256, 0, s, a);                 \
+  } while (0)
+#define FF_FIN_U(NP)                          \
+  do {                                        \
+    if (units <= 2) FF_FIN(2, NP);            \
+    else if (units <= 5) FF_FIN(5, NP);       \
+    else if (units <= 8) FF_FIN(8, NP);       \
+    else if (units <= 12) FF_FIN(12, NP);     \
+    else FF_FIN(16, NP);                      \
+  } while (0)
+  if (P == 16) FF_FIN_U(16);
+  else if (P == 32) FF_FIN_U(32);
+  else FF_FIN_U(64);
+#undef FF_FIN_U
+#undef FF_FIN
   return hipGetLastError();
 }
 

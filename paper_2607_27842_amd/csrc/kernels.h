@@ -151,6 +151,22 @@ struct PatchGeom { int B, lat_c, F, H, W, pt, ph, pw; };
 hipError_t patchify(int dtype, const float* x, void* patches, const PatchGeom& g, hipStream_t st);
 // x[b, ch, f, y, x] += dt * yv[(b*n_img + tok), feat], feat order (dt, dy, dx, ch)
 hipError_t unpatchify_euler(const float* yv, float* x, float dt, const PatchGeom& g, hipStream_t st);
+// Fused final layer of the image rows + unpatchify + Euler, one wavefront per token:
+// a = round(LN(in[phys(r)]) (1 + scale[b]) + shift[b]) (model dtype, as ln_modulate),
+// v = a W^T + bias (fp32, P = pt*ph*pw*lat_c outputs, W [P, C] model dtype), then
+// x[pixel of (r, o)] += dt * v[o] with feature order (dt, dy, dx, ch) as unpatchify_euler.
+// The same values as ln_modulate -> gemm (fp32 out) -> unpatchify_euler up to fp32
+// summation order.  Every wavefront reads the whole final weight from the caches, so this
+// pays only for small weights: final_layer_ok(dtype, P, C); the caller uses the three-
+// kernel path otherwise (there a GEMM reuses the weight across its tiles).
+struct FinalArgs {
+  const void* in; int ldi; RowMap map; int rows, C; float eps;
+  const float* shift; const float* scale; int ldm;
+  const void* W; const void* bias;
+  float* x; float dt; PatchGeom g;
+};
+bool final_layer_ok(int dtype, int P, int C);
+hipError_t final_layer(int dtype, const FinalArgs& a, hipStream_t st);
 // dst[(b*N + off + i) * C + :] = src[(b*n + i) * C + :]  (model dtype rows)
 hipError_t copy_rows(int dtype, const void* src, void* dst, int B, int n, int N, int off, int C, hipStream_t st);
 
