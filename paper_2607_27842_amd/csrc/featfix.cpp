@@ -217,8 +217,11 @@ struct Exec {
     return timed(FF_PROF_ATTN, 4.0 * a.B * (double)a.N * a.N * a.H * a.d, rows * 4.0 * a.C * es,
                  [&] { return ff::attention(dt, a, st); });
   }
+  hipError_t split(const float* x, int ldx, int K, int B, uint16_t* xs) {
+    return timed(FF_PROF_OTHER, 0, (double)B * K * 8, [&] { return ff::gemv_split(x, ldx, 0, K, B, xs, st); });
+  }
   hipError_t gemv_batch(const GemvBatch& b) {
-    if (dt == DT_BF16 && b.xs) {
+    if (dt == DT_BF16 && b.xs && !b.xs_ready) {
       hipError_t e = timed(FF_PROF_OTHER, 0, (double)b.B * b.K * 8, [&] { return ff::gemv_split(b.x, b.ldx, b.silu_in, b.K, b.B, b.xs, st); });
       if (e != hipSuccess) return e;
     }
@@ -230,7 +233,7 @@ struct Exec {
     return timed(FF_PROF_GEMV, fl, by, [&] { return ff::gemv_batch(dt, b, st); });
   }
   hipError_t gemv(const GemvArgs& a) {
-    if (dt == DT_BF16 && a.xs) {
+    if (dt == DT_BF16 && a.xs && !a.xs_ready) {
       hipError_t e = timed(FF_PROF_OTHER, 0, (double)a.B * a.K * 8, [&] { return ff::gemv_split(a.x, a.ldx, a.silu_in, a.K, a.B, a.xs, st); });
       if (e != hipSuccess) return e;
     }
@@ -813,6 +816,10 @@ ff_status ff_denoise_step(ff_ctx* c, int32_t step, float* x, const float* cond, 
     GemvArgs g2{tmp, C, 0, c->g.t2_w, c->g.t2_b, C, C, m.B, ct, C, 0, cond, C, xsplit};
     HIP_TRY(ex.gemv(g2), "time mlp 2");
     HIP_TRY(ex.other(8.0 * m.B * C, [&] { return silu_rows(ct, cs, m.B, C, st); }), "silu(c_t)");
+    // bf16: the MFMA GEMVs of this step that read SiLU(c_t) (modulation batches, final
+    // modulation) share one hi/lo split of it, made here; xsplit is not reused until then
+    const int cs_split = dt == FF_BF16;
+    if (cs_split) HIP_TRY(ex.split(cs, C, C, m.B, xsplit), "split silu(c_t)");
     // Modulation of the layers that run exact this step, computed kModLayers layers at a
     // time in one batched GEMV launch each; mod_of[l] = that layer's vectors.
     auto runs_exact = [&](int l) {
@@ -824,7 +831,7 @@ ff_status ff_denoise_step(ff_ctx* c, int32_t step, float* x, const float* cond, 
     auto ensure_mod = [&](int l) -> ff_status {
       if (mod_of[l]) return FF_OK;
       GemvBatch bt{};
-      bt.x = cs; bt.ldx = C; bt.silu_in = 0; bt.K = C; bt.B = m.B; bt.xs = xsplit;
+      bt.x = cs; bt.ldx = C; bt.silu_in = 0; bt.K = C; bt.B = m.B; bt.xs = xsplit; bt.xs_ready = cs_split;
       int slot = 0;
       for (int l2 = l; l2 < L && slot < kModLayers; ++l2) {
         if (!runs_exact(l2)) continue;
@@ -912,7 +919,7 @@ ff_status ff_denoise_step(ff_ctx* c, int32_t step, float* x, const float* cond, 
     }
     // final layer on the image rows, unpatchify and Euler
     float* mod = at<float>(ws, W.MOD);
-    GemvArgs gf{cs, C, 0, c->g.fmod_w, c->g.fmod_b, 2 * C, C, m.B, mod, 2 * C, 0, nullptr, 0, xsplit};
+    GemvArgs gf{cs, C, 0, c->g.fmod_w, c->g.fmod_b, 2 * C, C, m.B, mod, 2 * C, 0, nullptr, 0, xsplit, cs_split};
     HIP_TRY(ex.gemv(gf), "final modulation");
     if (final_layer_ok(dt, m.P, C)) {
       // LN + modulation + final linear + unpatchify + Euler in one launch, one wavefront

@@ -65,6 +65,7 @@ struct GemvArgs {
   float* y; int ldy; int silu_out;
   const float* add; int ldadd;
   uint16_t* xs;
+  int xs_ready;   // xs already holds gemv_split of this x (the caller skips the split)
 };
 hipError_t gemv(int dtype, const GemvArgs& a, hipStream_t s);
 hipError_t gemv_split(const float* x, int ldx, int silu_in, int K, int B, uint16_t* xs, hipStream_t s);
@@ -79,6 +80,7 @@ struct GemvBatch {
   const float* x; int ldx; int silu_in;
   int K, B, njobs;
   uint16_t* xs;   // as GemvArgs::xs (bf16 only)
+  int xs_ready;   // as GemvArgs::xs_ready
   GemvJob job[kGemvJobs];
 };
 inline size_t gemv_split_bytes(int K) { return (size_t)16 * K * 2; }
