@@ -643,7 +643,7 @@ void launch_dl64(const GemmArgs* a, int n, hipStream_t s) {
 // data and expressed relative to a round of 256x256 tiles.  The round time scales with K
 // alike for all candidates, so the choice depends on the tile counts only.
 //   kTile256     256x256, 8 waves of 128x64, 2 x 64-wide stages, 1 per CU          1.00
-//   kTile256x160 256x160, 4 waves of 64x160, 2 x 64-wide stages, 1 per CU          0.96
+//   kTile256x192 256x192, 8 waves of 64x96,  2 x 64-wide stages, 1 per CU          0.91
 //   kTile128x2   128x128, 8 waves of 64x32, 2 x 64-wide stages, 2 per CU (512/round) 0.80
 //   kTile128     128x128, 8 waves of 64x32, 4 x 64-wide stages, 1 per CU          0.43
 //   kTile128x96  128x96,  4 waves of 32x96, 4 x 64-wide stages, 1 per CU           0.40
@@ -653,7 +653,7 @@ void launch_dl64(const GemmArgs* a, int n, hipStream_t s) {
 // 256-row tiles load with sc0|sc1 (they skip the L1; each tile streams its panels once).
 // A group is costed by its total tile count.  K % 32 == 0 only: 4 x 32-wide stages,
 // 256x256 from 160 such tiles on, else 128x128; otherwise the register-staged kernel.
-enum { kTile256, kTile256x160, kTile128x2, kTile128, kTile128x96, kTile128x64, kTileCount };
+enum { kTile256, kTile256x192, kTile128x2, kTile128, kTile128x96, kTile128x64, kTileCount };
 struct TilePlan { int tile; double cost; };
 
 long tiles_of(const GemmArgs* a, int n, int bm, int bn) {
@@ -663,8 +663,8 @@ long tiles_of(const GemmArgs* a, int n, int bm, int bn) {
 }
 
 TilePlan plan_k64(const GemmArgs* a, int n) {
-  static const double kRound[kTileCount] = {1.00, 0.96, 0.80, 0.43, 0.40, 0.38};
-  const long t[kTileCount] = {tiles_of(a, n, 256, 256), tiles_of(a, n, 256, 160), tiles_of(a, n, 128, 128),
+  static const double kRound[kTileCount] = {1.00, 0.91, 0.80, 0.43, 0.40, 0.38};
+  const long t[kTileCount] = {tiles_of(a, n, 256, 256), tiles_of(a, n, 256, 192), tiles_of(a, n, 128, 128),
                               tiles_of(a, n, 128, 128), tiles_of(a, n, 128, 96), tiles_of(a, n, 128, 64)};
   const long per_round[kTileCount] = {256, 256, 512, 256, 256, 256};
   TilePlan best{kTile256, 1e300};
@@ -691,7 +691,7 @@ void launch_bf16(const GemmArgs* a, int n, hipStream_t s) {
   } else {
     switch (plan_k64(a, n).tile) {
       case kTile256: launch_dl64<256, 256, 128, 64, 17, EPI, OF, RF>(a, n, s); break;
-      case kTile256x160: launch_dl64<256, 160, 64, 160, 17, EPI, OF, RF>(a, n, s); break;
+      case kTile256x192: launch_dl64<256, 192, 64, 96, 17, EPI, OF, RF>(a, n, s); break;
       case kTile128x2: launch_dl64<128, 128, 64, 32, 0, EPI, OF, RF>(a, n, s); break;
       case kTile128: launch_dl<128, 128, 64, 32, 4, 64, 17, EPI, OF, RF>(a, n, s); break;
       case kTile128x96: launch_dl<128, 96, 32, 96, 4, 64, 17, EPI, OF, RF>(a, n, s); break;

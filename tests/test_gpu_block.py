@@ -141,8 +141,8 @@ def test_dit_block_gemm_tile_paths():
 
 def test_dit_block_ragged_wide_tiles():
     """A DiT block with 2000 token rows (ragged against both the 256- and 128-row tiles):
-    fc1 (N = 4608) takes 256x160 tiles with a ragged last column tile, proj and fc2
-    128x96 tiles with four 64-wide K stages, qkv two 128x128 tiles per CU."""
+    fc1 (N = 4608) takes 256x192 tiles, proj and fc2 128x96 tiles with four 64-wide K
+    stages, qkv two 128x128 tiles per CU."""
     need_gpu()
     cfg = ragged_cfg(synth.DIT, synth.BF16, d=72, H=16, B=4, lat=(4, 1, 50, 40), mlp_ratio=4)
     W = boosted(synth.make_layer_weights(cfg, 0, bias_std=0.02, gain_std=0.1), synth.DIT)
