@@ -34,31 +34,43 @@ template <> __device__ __forceinline__ void st4<DT_BF16>(void* p, size_t i, cons
 // One wavefront per row: LN over C (biased variance, no affine), then adaLN modulation.
 // The row and its shift / scale vectors are all loaded up front, so the two reductions
 // (mean, then variance about it) are the only waits between the loads and the stores.
-template <int DT_IN, int DT_OUT, int U>   // U: 4-element units per lane, C <= 256 U
+// 8-element access: one 16-byte load / store for bf16, two for fp32
+template <int DT> __device__ __forceinline__ void ld8(const void* p, size_t i, float* v) {
+  St<DT>::load(p, i, v);
+  if (St<DT>::V == 4) St<DT>::load(p, i + 4, v + 4);
+}
+template <int DT> __device__ __forceinline__ void st8(void* p, size_t i, const float* v) {
+  St<DT>::store(p, i, v);
+  if (St<DT>::V == 4) St<DT>::store(p, i + 4, v + 4);
+}
+
+template <int DT_IN, int DT_OUT, int U>   // U: 8-element units per lane, C <= 512 U
 __global__ __launch_bounds__(256) void k_ln_modulate(LnModArgs a) {
   const int lane = threadIdx.x % 64;
   const int r = blockIdx.x * 4 + threadIdx.x / 64;
   if (r >= a.rows) return;
   const size_t pr = (size_t)a.map.phys(r);
   const int b = a.map.sample(r);
-  const int units = a.C / 4;
+  const int units = a.C / 8;
   const float* sh = a.shift + (size_t)b * a.ldm;
   const float* sc = a.scale + (size_t)b * a.ldm;
-  float v[U][4];
-  float4 s4[U], c4[U];
+  float v[U][8], s8[U][8], c8[U][8];
   float s = 0.f;
 #pragma unroll
   for (int k = 0; k < U; ++k) {
     const int u = k * 64 + lane;
     if (u < units) {
-      ld4<DT_IN>(a.in, pr * a.ldi + u * 4, v[k]);
-      s4[k] = *reinterpret_cast<const float4*>(sh + u * 4);
-      c4[k] = *reinterpret_cast<const float4*>(sc + u * 4);
+      ld8<DT_IN>(a.in, pr * a.ldi + u * 8, v[k]);
+      ld8<DT_F32>(sh, u * 8, s8[k]);
+      ld8<DT_F32>(sc, u * 8, c8[k]);
     }
   }
 #pragma unroll
   for (int k = 0; k < U; ++k)
-    if (k * 64 + lane < units) s += (v[k][0] + v[k][1]) + (v[k][2] + v[k][3]);
+    if (k * 64 + lane < units) {
+#pragma unroll
+      for (int j = 0; j < 8; j += 2) s += v[k][j] + v[k][j + 1];
+    }
   const float mean = wave_sum(s) / (float)a.C;
   float q = 0.f;
 #pragma unroll
@@ -66,7 +78,7 @@ __global__ __launch_bounds__(256) void k_ln_modulate(LnModArgs a) {
     const int u = k * 64 + lane;
     if (u < units) {
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
+      for (int j = 0; j < 8; ++j) {
         const float dlt = v[k][j] - mean;
         q += dlt * dlt;
       }
@@ -77,12 +89,10 @@ __global__ __launch_bounds__(256) void k_ln_modulate(LnModArgs a) {
   for (int k = 0; k < U; ++k) {
     const int u = k * 64 + lane;
     if (u < units) {
-      float o[4];
-      o[0] = (v[k][0] - mean) * rstd * (1.0f + c4[k].x) + s4[k].x;
-      o[1] = (v[k][1] - mean) * rstd * (1.0f + c4[k].y) + s4[k].y;
-      o[2] = (v[k][2] - mean) * rstd * (1.0f + c4[k].z) + s4[k].z;
-      o[3] = (v[k][3] - mean) * rstd * (1.0f + c4[k].w) + s4[k].w;
-      st4<DT_OUT>(a.out, pr * a.ldo + u * 4, o);
+      float o[8];
+#pragma unroll
+      for (int j = 0; j < 8; ++j) o[j] = (v[k][j] - mean) * rstd * (1.0f + c8[k][j]) + s8[k][j];
+      st8<DT_OUT>(a.out, pr * a.ldo + u * 8, o);
     }
   }
 }
@@ -515,7 +525,7 @@ __global__ __launch_bounds__(256) void k_final_layer(FinalArgs a) {
 hipError_t ln_modulate(int dtype, const LnModArgs& a, hipStream_t s) {
   if (a.rows == 0) return hipSuccess;
   const int grid = cdiv(a.rows, 4);
-  const int units = cdiv(a.C / 4, 64);   // 4-element units per lane (C <= 4096 checked on the host)
+  const int units = cdiv(a.C / 8, 64);   // 8-element units per lane (C % 8 == 0, C <= 4096 checked on the host)
 #define FF_LN(U)                                                                          \
   do {                                                                                    \
     if (dtype == DT_BF16) {                                                               \
@@ -525,11 +535,11 @@ hipError_t ln_modulate(int dtype, const LnModArgs& a, hipStream_t s) {
       FF_LAUNCH((k_ln_modulate<DT_F32, DT_F32, U>), grid, 256, 0, s, a);                  \
     }                                                                                     \
   } while (0)
-  if (units <= 2) FF_LN(2);
-  else if (units <= 5) FF_LN(5);
-  else if (units <= 8) FF_LN(8);
-  else if (units <= 12) FF_LN(12);
-  else FF_LN(16);
+  if (units <= 1) FF_LN(1);
+  else if (units <= 3) FF_LN(3);
+  else if (units <= 4) FF_LN(4);
+  else if (units <= 6) FF_LN(6);
+  else FF_LN(8);
 #undef FF_LN
   return hipGetLastError();
 }
