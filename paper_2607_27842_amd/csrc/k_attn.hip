@@ -256,23 +256,39 @@ __global__ __launch_bounds__(NW * SPLIT * 64) void k_attn32(AttnArgs a) {
       mrow = mm;
     }
   }
-  // o[ot][v] = O[query q0 + c32][e = 32 ot + 8 (v/4) + 4 h + v%4]
-  const int q = q0 + c32;
-  if (q < N) {
-    uint16_t* out = reinterpret_cast<uint16_t*>(a.out);
+  // o[ot][v] = O[query q0 + c32][e = 32 ot + 8 (v/4) + 4 h + v%4].  In that layout a store
+  // instruction writes 8 bytes to each of 32 rows (a memory request per row), so the
+  // normalised tile goes through the wave's own LDS region as rows of bf16 and is stored
+  // as 16-byte row pieces, consecutive lanes on consecutive pieces.  The region is free:
+  // every tile read ended before the last barrier, and with SPLIT > 1 it is this wave's
+  // own merge entry, which it has finished reading (LDS ops of a wave complete in order).
+  constexpr int LDO = DV + 8;                              // staged row pitch (elements)
+  constexpr int PFX = SPLIT > 1 ? (NOT * 16 + 2) * 64 * 2 : 0;   // merge entry (elements)
+  constexpr int RW = 32 * LDO > PFX ? 32 * LDO : PFX;
+  static_assert(sizeof(smem) >= (size_t)NW * RW * 2, "output staging space");
+  uint16_t* stg = smem + wave * RW;
+  {
     const float inv = 1.0f / lrow;
 #pragma unroll
     for (int ot = 0; ot < NOT; ++ot)
 #pragma unroll
       for (int g = 0; g < 4; ++g) {
         const int e = 32 * ot + 8 * g + 4 * h;
-        if (e < d) {
-          u32x2_t w;
-          w[0] = pack_bf16x2(o[ot][4 * g] * inv, o[ot][4 * g + 1] * inv);
-          w[1] = pack_bf16x2(o[ot][4 * g + 2] * inv, o[ot][4 * g + 3] * inv);
-          *reinterpret_cast<u32x2_t*>(out + (rb + q) * a.ldo + (size_t)hd * d + e) = w;
-        }
+        u32x2_t w;
+        w[0] = pack_bf16x2(o[ot][4 * g] * inv, o[ot][4 * g + 1] * inv);
+        w[1] = pack_bf16x2(o[ot][4 * g + 2] * inv, o[ot][4 * g + 3] * inv);
+        *reinterpret_cast<u32x2_t*>(stg + c32 * LDO + e) = w;
       }
+  }
+  // d % 8 == 0 (host check): d/8 pieces per query row
+  uint16_t* out = reinterpret_cast<uint16_t*>(a.out);
+  const int ppr = d / 8;
+  for (int idx = lane; idx < 32 * ppr; idx += 64) {
+    const int row = idx / ppr, pc = idx - row * ppr;
+    const int qq = q0 + row;
+    if (qq < N)
+      *reinterpret_cast<u32x4_t*>(out + (rb + qq) * a.ldo + (size_t)hd * d + pc * 8) =
+          *reinterpret_cast<const u32x4_t*>(stg + row * LDO + pc * 8);
   }
 }
 
