@@ -292,6 +292,13 @@ __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64) void k_gemm_bf16(GemmGr
 // one run, each step waits with lgkmcnt(TM+TN) for the older reads only, and volatile "+v"
 // asms tie the fragments to the MFMAs so that none is consumed before its wait.  The one
 // barrier per stage sits between its last k step and the next stage's first.
+//
+// KG = 2 doubles the waves without growing the tile: waves w and w + NW accumulate the
+// same output block, the first over k steps 0-1 of every 64-wide stage and the second
+// over steps 2-3 (only the first issues the DMA; the second's vmcnt waits pass at once and
+// the stage barrier orders it).  With two waves per SIMD, one wave's LDS reads and barrier
+// waits hide behind the other's MFMAs.  After the loop the second k group hands its fp32
+// sums to the first through LDS (a fixed order: group 0 + group 1), which runs the epilogue.
 #define FF_AS1(p) ((const __attribute__((address_space(1))) void*)(p))
 #define FF_AS3(p) ((__attribute__((address_space(3))) void*)(p))
 
@@ -315,23 +322,29 @@ __device__ __forceinline__ bf16x8_t lds_rd128(const uint16_t* p) {
   return __builtin_bit_cast(bf16x8_t, v);
 }
 
-template <int BM, int BN, int WM, int WN, int NST, int BKd, int AUX, int EPI, bool OUT_F32, bool RES_F32, int NP>
-__global__ __launch_bounds__((BM / WM) * (BN / WN) * 64) void k_gemm_dl(GemmGroup<NP> G) {
+template <int BM, int BN, int WM, int WN, int NST, int BKd, int KG, int AUX, int EPI, bool OUT_F32, bool RES_F32, int NP>
+__global__ __launch_bounds__(KG * (BM / WM) * (BN / WN) * 64) void k_gemm_dl(GemmGroup<NP> G) {
   constexpr int NWN = BN / WN;
-  constexpr int NW = (BM / WM) * NWN;
+  constexpr int NW = (BM / WM) * NWN;                            // output blocks (waves per k group)
   constexpr int TM = WM / 32, TN = WN / 32;
   constexpr int CH = BKd / 8, RPI = 64 / CH, KS = BKd / 16;   // chunks per row, rows per DMA, k steps
+  constexpr int KPG = KS / KG;                                   // k steps per stage of one k group
   constexpr int IA = BM / RPI / NW, IB = BN / RPI / NW;        // DMA instructions per wave per stage
   static_assert(BKd == 32 || BKd == 64, "stage width");
+  static_assert((KG == 1 || KG == 2) && KPG % 2 == 0, "k groups take an even number of k steps");
   static_assert(IA * RPI * NW == BM && IB * RPI * NW == BN, "every tile row loaded by one DMA lane");
   static_assert(NST >= 3 && NST <= 5 && TM + TN <= 15, "unsupported tile");
   constexpr int kMain = NST * (BM + BN) * BKd, kEpi = epi_lds_elems<NW, WN>();
-  __shared__ __attribute__((aligned(1024))) uint16_t smem[kMain > kEpi ? kMain : kEpi];
+  constexpr int kRed = KG > 1 ? NW * TM * TN * 16 * 64 * 2 : 0;   // k group 1's partial sums (fp32)
+  __shared__ __attribute__((aligned(1024))) uint16_t smem[kMain > kEpi + kRed ? kMain : kEpi + kRed];
   uint16_t (*sA)[BM * BKd] = reinterpret_cast<uint16_t (*)[BM * BKd]>(smem);
   uint16_t (*sB)[BN * BKd] = reinterpret_cast<uint16_t (*)[BN * BKd]>(smem + NST * BM * BKd);
   // wave index in a scalar register: the per-wave LDS addresses of the DMA (M0) are then
-  // computed on the scalar unit instead of with a v_readfirstlane per instruction
+  // computed on the scalar unit instead of with a v_readfirstlane per instruction.  With
+  // KG = 2, waves w and w + NW own the same output block (cw) and split every stage's k
+  // steps between them (k group grp); only k group 0 issues the DMA.
   const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int grp = KG > 1 ? wave / NW : 0, cw = KG > 1 ? wave % NW : wave;
   int tm, tn;
   // workgroup-uniform: keep the problem select and tile origin in scalar registers
   const int prob = __builtin_amdgcn_readfirstlane(tile_of(blockIdx.x, G.tm[0], G.tn[0], G.tm[NP - 1], G.tn[NP - 1], NP, tm, tn));
@@ -347,20 +360,22 @@ __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64) void k_gemm_dl(GemmGrou
   size_t ga[IA], gb[IB];
 #pragma unroll
   for (int j = 0; j < IA; ++j) {
-    const int row = (wave * IA + j) * RPI + lr, gm = m0 + row;
+    const int row = (cw * IA + j) * RPI + lr, gm = m0 + row;
     ga[j] = (size_t)a.amap.phys(gm < a.M ? gm : 0) * a.lda + swz(ls, row) * 8;
   }
 #pragma unroll
   for (int j = 0; j < IB; ++j) {
-    const int row = (wave * IB + j) * RPI + lr, gn = n0 + row;
+    const int row = (cw * IB + j) * RPI + lr, gn = n0 + row;
     gb[j] = (size_t)(gn < a.N ? gn : 0) * a.ldw + swz(ls, row) * 8;
   }
 #define FF_ISSUE(st, k0)                                                                                  \
   do {                                                                                                    \
-    _Pragma("unroll") for (int j = 0; j < IA; ++j)                                                        \
-      __builtin_amdgcn_global_load_lds(FF_AS1(A + ga[j] + (k0)), FF_AS3(&sA[st][(wave * IA + j) * RPI * BKd]), 16, 0, AUX); \
-    _Pragma("unroll") for (int j = 0; j < IB; ++j)                                                        \
-      __builtin_amdgcn_global_load_lds(FF_AS1(W + gb[j] + (k0)), FF_AS3(&sB[st][(wave * IB + j) * RPI * BKd]), 16, 0, AUX); \
+    if (KG == 1 || grp == 0) {                                                                            \
+      _Pragma("unroll") for (int j = 0; j < IA; ++j)                                                      \
+        __builtin_amdgcn_global_load_lds(FF_AS1(A + ga[j] + (k0)), FF_AS3(&sA[st][(cw * IA + j) * RPI * BKd]), 16, 0, AUX); \
+      _Pragma("unroll") for (int j = 0; j < IB; ++j)                                                      \
+        __builtin_amdgcn_global_load_lds(FF_AS1(W + gb[j] + (k0)), FF_AS3(&sB[st][(cw * IB + j) * RPI * BKd]), 16, 0, AUX); \
+    }                                                                                                     \
   } while (0)
 
   f32x16_t acc[TM][TN];
@@ -370,21 +385,22 @@ __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64) void k_gemm_dl(GemmGrou
     for (int j = 0; j < TN; ++j)
 #pragma unroll
       for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
-  const int wm = (wave / NWN) * WM, wn = (wave % NWN) * WN;
+  const int wm = (cw / NWN) * WM, wn = (cw % NWN) * WN;
   const int fr = lane & 31, fh = lane >> 5;
-  // fragment offsets within a stage for its 16-wide k steps
-  int offa[KS][TM], offb[KS][TN];
+  // fragment offsets within a stage for this k group's 16-wide k steps
+  int offa[KPG][TM], offb[KPG][TN];
 #pragma unroll
-  for (int kk = 0; kk < KS; ++kk) {
+  for (int kk = 0; kk < KPG; ++kk) {
+    const int ks = grp * KPG + kk;
 #pragma unroll
     for (int t = 0; t < TM; ++t) {
       const int row = wm + t * 32 + fr;
-      offa[kk][t] = row * BKd + swz(kk * 2 + fh, row) * 8;
+      offa[kk][t] = row * BKd + swz(ks * 2 + fh, row) * 8;
     }
 #pragma unroll
     for (int t = 0; t < TN; ++t) {
       const int row = wn + t * 32 + fr;
-      offb[kk][t] = row * BKd + swz(kk * 2 + fh, row) * 8;
+      offb[kk][t] = row * BKd + swz(ks * 2 + fh, row) * 8;
     }
   }
   const int nk = a.K / BKd;
@@ -400,9 +416,9 @@ __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64) void k_gemm_dl(GemmGrou
   for (int kt = 0; kt < nk; ++kt) {
     const int st = kt % NST;
 #pragma unroll
-    for (int s = 0; s < KS; ++s) {
-      const int cur = s & 1, nxt = cur ^ 1;   // KS is even: stage k step 0 is always buffer 0
-      if (s + 1 < KS) {
+    for (int s = 0; s < KPG; ++s) {
+      const int cur = s & 1, nxt = cur ^ 1;   // KPG is even: stage k step 0 is always buffer 0
+      if (s + 1 < KPG) {
 #pragma unroll
         for (int t = 0; t < TM; ++t) fa[nxt][t] = lds_rd128(&sA[st][offa[s + 1][t]]);
 #pragma unroll
@@ -435,7 +451,27 @@ __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64) void k_gemm_dl(GemmGrou
   }
 #undef FF_ISSUE
   __syncthreads();   // every wave's last fragment reads retired before LDS is reused
-  epilogue_block<TM, TN, EPI, OUT_F32, RES_F32>(a, m0 + wm, n0 + wn, acc, smem + wave * 32 * (WN + 4) * 2);
+  if (KG > 1) {
+    // k group 1 hands its partial sums to k group 0 through LDS (past the epilogue staging)
+    float* red = reinterpret_cast<float*>(smem + kEpi) + cw * TM * TN * 16 * 64 + lane;
+    if (grp == 1) {
+#pragma unroll
+      for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+#pragma unroll
+          for (int v = 0; v < 16; ++v) red[((i * TN + j) * 16 + v) * 64] = acc[i][j][v];
+    }
+    __syncthreads();
+    if (grp == 1) return;   // the epilogue has no workgroup barrier
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+      for (int j = 0; j < TN; ++j)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) acc[i][j][v] += red[((i * TN + j) * 16 + v) * 64];
+  }
+  epilogue_block<TM, TN, EPI, OUT_F32, RES_F32>(a, m0 + wm, n0 + wn, acc, smem + cw * 32 * (WN + 4) * 2);
 }
 
 // ------------------------------------------------------------------ bf16 MFMA GEMM, 64-wide K stages
@@ -614,15 +650,15 @@ void launch_tile(const GemmArgs* a, int n, hipStream_t s) {
   }
 }
 
-template <int BM, int BN, int WM, int WN, int NST, int BKd, int AUX, int EPI, bool OF, bool RF>
+template <int BM, int BN, int WM, int WN, int NST, int BKd, int KG, int AUX, int EPI, bool OF, bool RF>
 void launch_dl(const GemmArgs* a, int n, hipStream_t s) {
   int nwg;
   if (n == 1) {
     const GemmGroup<1> G = make_group<BM, BN, 1>(a, nwg);
-    FF_LAUNCH((k_gemm_dl<BM, BN, WM, WN, NST, BKd, AUX, EPI, OF, RF, 1>), nwg, (BM / WM) * (BN / WN) * 64, 0, s, G);
+    FF_LAUNCH((k_gemm_dl<BM, BN, WM, WN, NST, BKd, KG, AUX, EPI, OF, RF, 1>), nwg, KG * (BM / WM) * (BN / WN) * 64, 0, s, G);
   } else {
     const GemmGroup<2> G = make_group<BM, BN, 2>(a, nwg);
-    FF_LAUNCH((k_gemm_dl<BM, BN, WM, WN, NST, BKd, AUX, EPI, OF, RF, 2>), nwg, (BM / WM) * (BN / WN) * 64, 0, s, G);
+    FF_LAUNCH((k_gemm_dl<BM, BN, WM, WN, NST, BKd, KG, AUX, EPI, OF, RF, 2>), nwg, KG * (BM / WM) * (BN / WN) * 64, 0, s, G);
   }
 }
 
@@ -640,17 +676,19 @@ void launch_dl64(const GemmArgs* a, int n, hipStream_t s) {
 
 // Tile choice for K % 64 == 0: the candidate minimising (rounds of workgroups over the
 // 256 CUs) x (time of one round of that candidate), measured on MI355X with random bf16
-// data and expressed relative to a round of 256x256 tiles.  The round time scales with K
-// alike for all candidates, so the choice depends on the tile counts only.
+// data and expressed relative to a round of 256x256 tiles (the ratio drifts with K, e.g.
+// 0.36 at K = 1152 and 0.29 at K = 4608 for 128x96; the constants sit between).
 //   kTile256     256x256, 8 waves of 128x64, 2 x 64-wide stages, 1 per CU          1.00
 //   kTile256x192 256x192, 8 waves of 64x96,  2 x 64-wide stages, 1 per CU          0.91
 //   kTile128x2   128x128, 8 waves of 64x32, 2 x 64-wide stages, 2 per CU (512/round) 0.80
-//   kTile128     128x128, 8 waves of 64x32, 4 x 64-wide stages, 1 per CU          0.43
-//   kTile128x96  128x96,  4 waves of 32x96, 4 x 64-wide stages, 1 per CU           0.40
-//   kTile128x64  128x64,  4 waves of 64x32, 4 x 32-wide stages, 1 per CU           0.38
+//   kTile128     128x128, 4 blocks of 64x64 x 2 k groups, 4 x 64-wide stages        0.41
+//   kTile128x96  128x96,  4 blocks of 32x96 x 2 k groups, 4 x 64-wide stages        0.34
+//   kTile128x64  128x64,  4 blocks of 32x64 x 2 k groups, 4 x 64-wide stages        0.24
 // Larger tiles need fewer operand bytes per MFMA (LDS traffic per MFMA limits the 128x128
-// tiles), smaller ones fill the CUs on small grids (M = 2048 shapes).  Operands of the
-// 256-row tiles load with sc0|sc1 (they skip the L1; each tile streams its panels once).
+// tiles), smaller ones fill the CUs on small grids (M = 2048 shapes).  The 128-row ring
+// tiles run two k groups of waves per output block (8 waves, two per SIMD): one wave's
+// LDS reads and barrier waits then overlap the other's MFMAs.  Operands of the 256-row
+// tiles load with sc0|sc1 (they skip the L1; each tile streams its panels once).
 // A group is costed by its total tile count.  K % 32 == 0 only: 4 x 32-wide stages,
 // 256x256 from 160 such tiles on, else 128x128; otherwise the register-staged kernel.
 enum { kTile256, kTile256x192, kTile128x2, kTile128, kTile128x96, kTile128x64, kTileCount };
@@ -663,7 +701,7 @@ long tiles_of(const GemmArgs* a, int n, int bm, int bn) {
 }
 
 TilePlan plan_k64(const GemmArgs* a, int n) {
-  static const double kRound[kTileCount] = {1.00, 0.91, 0.80, 0.43, 0.40, 0.38};
+  static const double kRound[kTileCount] = {1.00, 0.91, 0.80, 0.41, 0.34, 0.24};
   const long t[kTileCount] = {tiles_of(a, n, 256, 256), tiles_of(a, n, 256, 192), tiles_of(a, n, 128, 128),
                               tiles_of(a, n, 128, 128), tiles_of(a, n, 128, 96), tiles_of(a, n, 128, 64)};
   const long per_round[kTileCount] = {256, 256, 512, 256, 256, 256};
@@ -686,16 +724,16 @@ void launch_bf16(const GemmArgs* a, int n, hipStream_t s) {
   if (!all_k(a, n, 32)) {
     launch_tile<128, 128, 64, 32, EPI, OF, RF>(a, n, s);
   } else if (!all_k(a, n, 64)) {
-    if (tiles_of(a, n, 256, 256) >= 160) launch_dl<256, 256, 128, 64, 4, 32, 17, EPI, OF, RF>(a, n, s);
-    else launch_dl<128, 128, 64, 32, 4, 32, 0, EPI, OF, RF>(a, n, s);
+    if (tiles_of(a, n, 256, 256) >= 160) launch_dl<256, 256, 128, 64, 4, 32, 1, 17, EPI, OF, RF>(a, n, s);
+    else launch_dl<128, 128, 64, 32, 4, 32, 1, 0, EPI, OF, RF>(a, n, s);
   } else {
     switch (plan_k64(a, n).tile) {
       case kTile256: launch_dl64<256, 256, 128, 64, 17, EPI, OF, RF>(a, n, s); break;
       case kTile256x192: launch_dl64<256, 192, 64, 96, 17, EPI, OF, RF>(a, n, s); break;
       case kTile128x2: launch_dl64<128, 128, 64, 32, 0, EPI, OF, RF>(a, n, s); break;
-      case kTile128: launch_dl<128, 128, 64, 32, 4, 64, 17, EPI, OF, RF>(a, n, s); break;
-      case kTile128x96: launch_dl<128, 96, 32, 96, 4, 64, 17, EPI, OF, RF>(a, n, s); break;
-      default: launch_dl<128, 64, 64, 32, 4, 32, 0, EPI, OF, RF>(a, n, s); break;
+      case kTile128: launch_dl<128, 128, 64, 64, 4, 64, 2, 17, EPI, OF, RF>(a, n, s); break;
+      case kTile128x96: launch_dl<128, 96, 32, 96, 4, 64, 2, 17, EPI, OF, RF>(a, n, s); break;
+      default: launch_dl<128, 64, 32, 64, 4, 64, 2, 0, EPI, OF, RF>(a, n, s); break;
     }
   }
 }

@@ -129,9 +129,9 @@ def test_mmdit_block_full_shape_sampled_rows(name, kind):
 
 
 def test_dit_block_gemm_tile_paths():
-    """A DiT block whose GEMMs take every bf16 tile path: qkv and fc1 256x256 tiles with
-    32-wide K stages (K = 2080 is not a multiple of 64), proj 128x128 with 32-wide stages,
-    fc2 128x128 with 64-wide stages (K = 8320, 272 tiles); attention with head dim 104."""
+    """A DiT block whose GEMMs take the 32-wide K-stage paths: qkv and fc1 256x256 tiles
+    (K = 2080 is not a multiple of 64), proj 128x128; fc2 (K = 8320, 64-wide stages) 128x96
+    tiles with two k groups of waves; attention with head dim 104."""
     need_gpu()
     cfg = ragged_cfg(synth.DIT, synth.BF16, d=104, H=20, B=2, lat=(4, 1, 64, 64), mlp_ratio=4)
     W = boosted(synth.make_layer_weights(cfg, 0, bias_std=0.02, gain_std=0.1), synth.DIT)
@@ -142,7 +142,7 @@ def test_dit_block_gemm_tile_paths():
 def test_dit_block_ragged_wide_tiles():
     """A DiT block with 2000 token rows (ragged against both the 256- and 128-row tiles):
     fc1 (N = 4608) takes 256x192 tiles, proj and fc2 128x96 tiles with four 64-wide K
-    stages, qkv two 128x128 tiles per CU."""
+    stages and two k groups of waves, qkv two 128x128 tiles per CU."""
     need_gpu()
     cfg = ragged_cfg(synth.DIT, synth.BF16, d=72, H=16, B=4, lat=(4, 1, 50, 40), mlp_ratio=4)
     W = boosted(synth.make_layer_weights(cfg, 0, bias_std=0.02, gain_std=0.1), synth.DIT)
@@ -151,12 +151,23 @@ def test_dit_block_ragged_wide_tiles():
 
 
 def test_dit_block_c2048_tiles():
-    """A DiT block with C = 2048 (16 heads of 128) and 2048 rows: qkv and fc1 take 256x256
-    tiles with 64-wide stages, proj and fc2 (N = 2048, 256 tiles) one 128x128 tile per CU
-    with four 64-wide stages; attention with head dim 128."""
+    """A DiT block with C = 2048 (16 heads of 128) and 2048 rows: qkv takes 256x192 and fc1
+    256x256 tiles with 64-wide stages, proj and fc2 (N = 2048, 256 tiles) one 128x128 tile
+    per CU with four 64-wide stages and two k groups; attention with head dim 128."""
     need_gpu()
     cfg = ragged_cfg(synth.DIT, synth.BF16, d=128, H=16, B=2, lat=(4, 1, 64, 64), mlp_ratio=4)
     W = boosted(synth.make_layer_weights(cfg, 0, bias_std=0.02, gain_std=0.1), synth.DIT)
     say("dit block C=2048 d=128 N=1024 B=2 (sampled rows)")
     check_block(cfg, W, rows=np.array([0, 1, 127, 128, 511, 777, 1023]))
 
+
+
+def test_dit_block_narrow_tiles():
+    """A DiT block with 510 token rows (two samples of 255 tokens; the last 128-row tile
+    holds 126): qkv, proj and fc2 take 128x64 tiles and fc1 128x96 tiles, both with two k
+    groups of waves, so the gated epilogue runs on the 128x64 path too."""
+    need_gpu()
+    cfg = ragged_cfg(synth.DIT, synth.BF16, d=72, H=16, B=2, lat=(4, 1, 30, 34), mlp_ratio=4)
+    W = boosted(synth.make_layer_weights(cfg, 0, bias_std=0.02, gain_std=0.1), synth.DIT)
+    say("dit block C=1152 d=72 N=255 B=2")
+    check_block(cfg, W)
