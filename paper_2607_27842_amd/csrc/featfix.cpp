@@ -143,7 +143,7 @@ Ws ws_layout(const Model& m) {
   w.PART = take(verify_partials_floats(m.B) * 4);
   w.mod_slot = (size_t)m.B * mod_width(m);
   w.MODS = take(kModLayers * w.mod_slot * 4);
-  w.XS = take(gemv_split_bytes(std::max(m.C, FF_TEMB_DIM)));
+  w.XS = take(gemv_split_bytes(m.C));
   w.total = off;
   return w;
 }
@@ -217,14 +217,7 @@ struct Exec {
     return timed(FF_PROF_ATTN, 4.0 * a.B * (double)a.N * a.N * a.H * a.d, rows * 4.0 * a.C * es,
                  [&] { return ff::attention(dt, a, st); });
   }
-  hipError_t split(const float* x, int ldx, int K, int B, uint16_t* xs) {
-    return timed(FF_PROF_OTHER, 0, (double)B * K * 8, [&] { return ff::gemv_split(x, ldx, 0, K, B, xs, st); });
-  }
   hipError_t gemv_batch(const GemvBatch& b) {
-    if (dt == DT_BF16 && b.xs && !b.xs_ready) {
-      hipError_t e = timed(FF_PROF_OTHER, 0, (double)b.B * b.K * 8, [&] { return ff::gemv_split(b.x, b.ldx, b.silu_in, b.K, b.B, b.xs, st); });
-      if (e != hipSuccess) return e;
-    }
     double fl = 0, by = 0;
     for (int i = 0; i < b.njobs; ++i) {
       fl += 2.0 * b.B * b.job[i].Nout * b.K;
@@ -233,10 +226,6 @@ struct Exec {
     return timed(FF_PROF_GEMV, fl, by, [&] { return ff::gemv_batch(dt, b, st); });
   }
   hipError_t gemv(const GemvArgs& a) {
-    if (dt == DT_BF16 && a.xs && !a.xs_ready) {
-      hipError_t e = timed(FF_PROF_OTHER, 0, (double)a.B * a.K * 8, [&] { return ff::gemv_split(a.x, a.ldx, a.silu_in, a.K, a.B, a.xs, st); });
-      if (e != hipSuccess) return e;
-    }
     return timed(FF_PROF_GEMV, 2.0 * a.B * a.Nout * a.K, (double)a.Nout * a.K * es, [&] { return ff::gemv(dt, a, st); });
   }
   hipError_t ln(const LnModArgs& a) {
@@ -332,7 +321,7 @@ ff_status exec_block(const Model& m, int kind, const ff_layer_weights& w, const 
     const RowMap all = whole(m);
     const int rows = m.B * m.N;
     if (!mod_pre) {
-      GemvArgs gv{cs, C, 0, s.mod_w, s.mod_b, 3 * C, C, m.B, mod, 3 * C, 0, nullptr, 0, at<uint16_t>(ws, L.XS)};
+      GemvArgs gv{cs, C, 0, s.mod_w, s.mod_b, 3 * C, C, m.B, mod, 3 * C, 0, nullptr, 0};
       HIP_TRY(ex.gemv(gv), "single: modulation");
     }
     LnModArgs ln{u, 0, C, all, rows, C, m.ln_eps, mod, mod + C, 3 * C, lna, C};
@@ -386,7 +375,7 @@ ff_status exec_block(const Model& m, int kind, const ff_layer_weights& w, const 
     const int rows = m.B * nseg[si];
     float* ms = mod + 6 * C * si;
     if (!mod_pre) {
-      GemvArgs gv{cs, C, 0, s.mod_w, s.mod_b, 6 * C, C, m.B, ms, ldm, 0, nullptr, 0, at<uint16_t>(ws, L.XS)};
+      GemvArgs gv{cs, C, 0, s.mod_w, s.mod_b, 6 * C, C, m.B, ms, ldm, 0, nullptr, 0};
       HIP_TRY(ex.gemv(gv), "block: modulation");
     }
     if (rows == 0) continue;
@@ -652,7 +641,7 @@ ff_status ff_block_exact(const ff_model_desc* m, int32_t layer, const ff_layer_w
       return fail(FF_E_SHAPE, "h overlaps u or the workspace");
     Exec ex{reinterpret_cast<hipStream_t>(stream), nullptr, md.dtype, md.es()};
     float* cs = at<float>(ws, L.CS);
-    HIP_TRY(silu_rows(c_t, cs, md.B, md.C, ex.st), "block: silu(c_t)");
+    HIP_TRY(silu_rows(c_t, cs, md.B, md.C, nullptr, ex.st), "block: silu(c_t)");
     e = exec_block(md, md.kinds[layer], *w, cs, u, h, ws, ex);
     if (e) return e;
     return ok();
@@ -810,16 +799,14 @@ ff_status ff_denoise_step(ff_ctx* c, int32_t step, float* x, const float* cond, 
     float* cs = at<float>(ws, W.CS);
     // conditioning: c_t = cond + W_t2 SiLU(W_t1 phi(1000 t) + b_t1) + b_t2
     HIP_TRY(ex.other(FF_TEMB_DIM * 4.0, [&] { return time_embed(1000.0 * t_i, phi, st); }), "time embedding");
-    uint16_t* xsplit = at<uint16_t>(ws, W.XS);
-    GemvArgs g1{phi, 0, 0, c->g.t1_w, c->g.t1_b, C, FF_TEMB_DIM, m.B, tmp, C, 1, nullptr, 0, xsplit};
+    GemvArgs g1{phi, 0, 0, c->g.t1_w, c->g.t1_b, C, FF_TEMB_DIM, m.B, tmp, C, 1, nullptr, 0};
     HIP_TRY(ex.gemv(g1), "time mlp 1");
-    GemvArgs g2{tmp, C, 0, c->g.t2_w, c->g.t2_b, C, C, m.B, ct, C, 0, cond, C, xsplit};
+    GemvArgs g2{tmp, C, 0, c->g.t2_w, c->g.t2_b, C, C, m.B, ct, C, 0, cond, C};
     HIP_TRY(ex.gemv(g2), "time mlp 2");
-    HIP_TRY(ex.other(8.0 * m.B * C, [&] { return silu_rows(ct, cs, m.B, C, st); }), "silu(c_t)");
-    // bf16: the MFMA GEMVs of this step that read SiLU(c_t) (modulation batches, final
-    // modulation) share one hi/lo split of it, made here; xsplit is not reused until then
-    const int cs_split = dt == FF_BF16;
-    if (cs_split) HIP_TRY(ex.split(cs, C, C, m.B, xsplit), "split silu(c_t)");
+    // bf16: SiLU(c_t) also as the hi / lo split that the modulation batches and the final
+    // modulation read (made once here rather than by each of their workgroups)
+    uint16_t* xs = dt == FF_BF16 ? at<uint16_t>(ws, W.XS) : nullptr;
+    HIP_TRY(ex.other(8.0 * m.B * C, [&] { return silu_rows(ct, cs, m.B, C, xs, st); }), "silu(c_t)");
     // Modulation of the layers that run exact this step, computed kModLayers layers at a
     // time in one batched GEMV launch each; mod_of[l] = that layer's vectors.
     auto runs_exact = [&](int l) {
@@ -831,7 +818,7 @@ ff_status ff_denoise_step(ff_ctx* c, int32_t step, float* x, const float* cond, 
     auto ensure_mod = [&](int l) -> ff_status {
       if (mod_of[l]) return FF_OK;
       GemvBatch bt{};
-      bt.x = cs; bt.ldx = C; bt.silu_in = 0; bt.K = C; bt.B = m.B; bt.xs = xsplit; bt.xs_ready = cs_split;
+      bt.x = cs; bt.ldx = C; bt.silu_in = 0; bt.K = C; bt.B = m.B; bt.xs = xs;
       int slot = 0;
       for (int l2 = l; l2 < L && slot < kModLayers; ++l2) {
         if (!runs_exact(l2)) continue;
@@ -919,7 +906,7 @@ ff_status ff_denoise_step(ff_ctx* c, int32_t step, float* x, const float* cond, 
     }
     // final layer on the image rows, unpatchify and Euler
     float* mod = at<float>(ws, W.MOD);
-    GemvArgs gf{cs, C, 0, c->g.fmod_w, c->g.fmod_b, 2 * C, C, m.B, mod, 2 * C, 0, nullptr, 0, xsplit, cs_split};
+    GemvArgs gf{cs, C, 0, c->g.fmod_w, c->g.fmod_b, 2 * C, C, m.B, mod, 2 * C, 0, nullptr, 0, xs};
     HIP_TRY(ex.gemv(gf), "final modulation");
     if (final_layer_ok(dt, m.P, C)) {
       // LN + modulation + final linear + unpatchify + Euler in one launch, one wavefront

@@ -253,35 +253,32 @@ __device__ __forceinline__ void gemv_tile(const GemvArgs a, int blk) {
   }
 }
 
-// bf16 weights, B <= 8: y[b, n0..n0+15] on v_mfma_f32_16x16x32_bf16.  The fp32 activations
-// are split once (k_gemv_split) into bf16 hi + lo parts (x = hi + lo to ~2^-17 relative);
-// MFMA rows 0-7 carry hi of samples 0-7 and rows 8-15 lo, so one instruction covers both
-// halves and output rows b and b+8 are added at the end.  The four wavefronts take
-// interleaved 32-wide K steps and their 16x16 partial tiles are summed through LDS in
-// wavefront order.  16x16x32 layouts: A lane l holds row l%16, k = 8*(l/16)+0..7; B lane
-// l holds column l%16, same k; D lane l holds column l%16, rows 4*(l/16)+0..3.
+// bf16 weights, B <= 8: y[b, n0..n0+15] on v_mfma_f32_16x16x32_bf16.  The fp32
+// activations enter as bf16 hi + lo parts (x = hi + lo to ~2^-17 relative), split by each
+// lane as it loads them, or read from a split made beforehand (xs; the large modulation
+// batches, whose thousands of workgroups would otherwise each split the same x): MFMA
+// rows 0-7 carry hi of samples 0-7 and rows 8-15 lo, so one instruction covers both halves and output rows b and b+8 are added at the
+// end.  The four wavefronts take interleaved 32-wide K steps and their 16x16 partial
+// tiles are summed through LDS in wavefront order.  16x16x32 layouts: A lane l holds row
+// l%16, k = 8*(l/16)+0..7; B lane l holds column l%16, same k; D lane l holds column
+// l%16, rows 4*(l/16)+0..3.
 constexpr int kMvU = 4;   // K steps per wavefront whose loads are issued together
 
-__global__ __launch_bounds__(256) void k_gemv_split(const float* __restrict__ x, int ldx, int silu_in, int K, int B,
-                                                    uint16_t* __restrict__ xs) {
-  const int t = blockIdx.x * 256 + threadIdx.x;   // one 8-wide chunk of one sample
-  const int kc = K / 8;
-  if (t >= B * kc) return;
-  const int b = t / kc, k = (t % kc) * 8;
-  const f32x4_t v0 = *reinterpret_cast<const f32x4_t*>(x + (size_t)b * ldx + k);
-  const f32x4_t v1 = *reinterpret_cast<const f32x4_t*>(x + (size_t)b * ldx + k + 4);
-  u32x4_t hi, lo;
+// The 8 activations x[k..k+7] (SiLU first if silu_in) as bf16 hi parts, or as the bf16
+// rounding of what hi leaves (lo).
+__device__ __forceinline__ u32x4_t split8(const float* x, int silu_in, bool lo_part) {
+  const f32x4_t v0 = *reinterpret_cast<const f32x4_t*>(x);
+  const f32x4_t v1 = *reinterpret_cast<const f32x4_t*>(x + 4);
+  u32x4_t r;
 #pragma unroll
   for (int j = 0; j < 4; ++j) {
     float a0 = j < 2 ? v0[2 * j] : v1[2 * j - 4], a1 = j < 2 ? v0[2 * j + 1] : v1[2 * j - 3];
     if (silu_in) { a0 = silu_f(a0); a1 = silu_f(a1); }
-    const uint16_t h0 = f2bf(a0), h1 = f2bf(a1);
-    const uint16_t l0 = f2bf(a0 - bf2f(h0)), l1 = f2bf(a1 - bf2f(h1));
-    hi[j] = (uint32_t)h0 | ((uint32_t)h1 << 16);
-    lo[j] = (uint32_t)l0 | ((uint32_t)l1 << 16);
+    uint16_t h0 = f2bf(a0), h1 = f2bf(a1);
+    if (lo_part) { h0 = f2bf(a0 - bf2f(h0)); h1 = f2bf(a1 - bf2f(h1)); }
+    r[j] = (uint32_t)h0 | ((uint32_t)h1 << 16);
   }
-  *reinterpret_cast<u32x4_t*>(xs + (size_t)b * K + k) = hi;
-  *reinterpret_cast<u32x4_t*>(xs + (size_t)(8 + b) * K + k) = lo;
+  return r;
 }
 
 __device__ __forceinline__ void gemv_mfma_tile(const GemvArgs a, int blk) {
@@ -291,7 +288,9 @@ __device__ __forceinline__ void gemv_mfma_tile(const GemvArgs a, int blk) {
   const int n = n0 + rc;
   const bool nok = n < a.Nout, bok = (rc & 7) < a.B;
   const uint16_t* wrow = reinterpret_cast<const uint16_t*>(a.W) + (size_t)(nok ? n : 0) * a.K;
-  const uint16_t* xrow = a.xs + (size_t)rc * a.K;
+  const float* xrow = a.x + (size_t)(rc & 7) * a.ldx;   // sample rc % 8 (ldx 0: one shared row)
+  const uint16_t* srow = a.xs + (size_t)rc * a.K;         // or its split, made beforehand
+  const bool lo_part = rc >= 8;
   const int nks = (a.K + 31) / 32;
   const u32x4_t z4 = {0u, 0u, 0u, 0u};
   f32x4_t acc = {0.f, 0.f, 0.f, 0.f};
@@ -302,7 +301,9 @@ __device__ __forceinline__ void gemv_mfma_tile(const GemvArgs a, int blk) {
       const int k = (ks0 + 4 * u) * 32 + kq;
       const bool kin = ks0 + 4 * u < nks && k < a.K;   // K % 8 == 0: a lane's 8 are all in or out
       wv[u] = (kin && nok) ? *reinterpret_cast<const u32x4_t*>(wrow + k) : z4;
-      xv[u] = (kin && bok) ? *reinterpret_cast<const u32x4_t*>(xrow + k) : z4;
+      if (!(kin && bok)) xv[u] = z4;
+      else if (a.xs) xv[u] = *reinterpret_cast<const u32x4_t*>(srow + k);
+      else xv[u] = split8(xrow + k, a.silu_in, lo_part);
     }
 #pragma unroll
     for (int u = 0; u < kMvU; ++u)
@@ -348,7 +349,7 @@ template <int DT>
 __global__ __launch_bounds__(256) void k_gemv_batch(GemvBatch bt) {
   const GemvJob j = bt.job[blockIdx.y];
   if ((int)blockIdx.x * 4 * kGemvRows >= j.Nout) return;   // whole workgroup: no barrier skipped
-  const GemvArgs a{bt.x, bt.ldx, bt.silu_in, j.W, j.bias, j.Nout, bt.K, bt.B, j.y, j.ldy, 0, nullptr, 0, nullptr};
+  const GemvArgs a{bt.x, bt.ldx, bt.silu_in, j.W, j.bias, j.Nout, bt.K, bt.B, j.y, j.ldy, 0, nullptr, 0};
   gemv_tile<DT>(a, blockIdx.x);
 }
 
@@ -359,9 +360,17 @@ __global__ void k_time_embed(double s, float* phi) {
   phi[128 + k] = (float)sin(s * f);
 }
 
-__global__ void k_silu_rows(const float* x, float* y, long n) {
+__global__ void k_silu_rows(const float* x, float* y, int B, int n, uint16_t* xs) {
   const long i = (long)blockIdx.x * 256 + threadIdx.x;
-  if (i < n) y[i] = silu_f(x[i]);
+  if (i >= (long)B * n) return;
+  const float v = silu_f(x[i]);
+  y[i] = v;
+  if (xs) {   // the bf16 hi / lo split the MFMA GEMVs read (as split8 makes it)
+    const int b = (int)(i / n), k = (int)(i % n);
+    const uint16_t h = f2bf(v);
+    xs[(size_t)b * n + k] = h;
+    xs[(size_t)(8 + b) * n + k] = f2bf(v - bf2f(h));
+  }
 }
 
 template <int DT>
@@ -579,19 +588,14 @@ hipError_t rms_qk(int dtype, const RmsQKArgs& a, hipStream_t s) {
 }
 
 hipError_t gemv(int dtype, const GemvArgs& a, hipStream_t s) {
-  if (dtype == DT_BF16 && a.xs) {
+  if (dtype == DT_BF16) {
+    if (a.B > 8 || a.K % 8) return hipErrorInvalidValue;
     FF_LAUNCH(k_gemv_mfma, cdiv(a.Nout, 16), 256, 0, s, a);
     return hipGetLastError();
   }
   const int grid = cdiv(a.Nout, 4 * kGemvRows);
   const size_t lds = (size_t)a.B * kGemvKC * sizeof(float);
-  if (dtype == DT_BF16) FF_LAUNCH(k_gemv<DT_BF16>, grid, 256, lds, s, a);
-  else FF_LAUNCH(k_gemv<DT_F32>, grid, 256, lds, s, a);
-  return hipGetLastError();
-}
-
-hipError_t gemv_split(const float* x, int ldx, int silu_in, int K, int B, uint16_t* xs, hipStream_t s) {
-  FF_LAUNCH(k_gemv_split, cdiv((long)B * (K / 8), 256), 256, 0, s, x, ldx, silu_in, K, B, xs);
+  FF_LAUNCH(k_gemv<DT_F32>, grid, 256, lds, s, a);
   return hipGetLastError();
 }
 
@@ -599,14 +603,14 @@ hipError_t gemv_batch(int dtype, const GemvBatch& bt, hipStream_t s) {
   if (bt.njobs <= 0) return hipSuccess;
   int nmax = 0;
   for (int i = 0; i < bt.njobs; ++i) nmax = max(nmax, bt.job[i].Nout);
-  if (dtype == DT_BF16 && bt.xs) {
+  if (dtype == DT_BF16) {
+    if (bt.B > 8 || bt.K % 8) return hipErrorInvalidValue;
     FF_LAUNCH(k_gemv_mfma_batch, dim3(cdiv(nmax, 16), bt.njobs), 256, 0, s, bt);
     return hipGetLastError();
   }
   const dim3 grid(cdiv(nmax, 4 * kGemvRows), bt.njobs);
   const size_t lds = (size_t)bt.B * kGemvKC * sizeof(float);
-  if (dtype == DT_BF16) FF_LAUNCH(k_gemv_batch<DT_BF16>, grid, 256, lds, s, bt);
-  else FF_LAUNCH(k_gemv_batch<DT_F32>, grid, 256, lds, s, bt);
+  FF_LAUNCH(k_gemv_batch<DT_F32>, grid, 256, lds, s, bt);
   return hipGetLastError();
 }
 
@@ -615,9 +619,10 @@ hipError_t time_embed(double sv, float* phi, hipStream_t st) {
   return hipGetLastError();
 }
 
-hipError_t silu_rows(const float* x, float* y, int B, int n, hipStream_t st) {
+hipError_t silu_rows(const float* x, float* y, int B, int n, uint16_t* xs, hipStream_t st) {
+  if (xs && B > 8) return hipErrorInvalidValue;
   const long tot = (long)B * n;
-  FF_LAUNCH(k_silu_rows, cdiv(tot, 256), 256, 0, st, x, y, tot);
+  FF_LAUNCH(k_silu_rows, cdiv(tot, 256), 256, 0, st, x, y, B, n, xs);
   return hipGetLastError();
 }
 

@@ -55,20 +55,19 @@ hipError_t gemm2(int dtype, const GemmArgs& a0, const GemmArgs& a1, hipStream_t 
 
 // y[b, n] = (add ? add[b*ldadd + n] : 0) + act( sum_k f(x[b*ldx + k]) * W[n, k] + bias[n] )
 // x, y, add fp32; W, bias model dtype; f = SiLU if silu_in; act = SiLU if silu_out.
-// bf16 weights with xs set run on MFMA and read the activations from xs ([16, K] bf16,
-// 16-byte aligned), which gemv_split must have filled from the same x first: f(x) split
-// into bf16 hi (rows 0..B-1) and lo (rows 8..8+B-1) parts, f(x) = hi + lo to ~2^-17.
+// bf16 weights run on MFMA (B <= 8, K % 8 == 0, x 16-byte aligned rows): f(x) enters as
+// bf16 hi + lo parts, f(x) = hi + lo to ~2^-17, split in the kernel, or read from xs when
+// set ([16, K] bf16: rows 0..B-1 hi, 8..8+B-1 lo, as silu_rows writes it; the caller
+// guarantees it holds the split of this f(x)).
 struct GemvArgs {
   const float* x; int ldx; int silu_in;
   const void* W; const void* bias;
   int Nout, K, B;
   float* y; int ldy; int silu_out;
   const float* add; int ldadd;
-  uint16_t* xs;
-  int xs_ready;   // xs already holds gemv_split of this x (the caller skips the split)
+  const uint16_t* xs;
 };
 hipError_t gemv(int dtype, const GemvArgs& a, hipStream_t s);
-hipError_t gemv_split(const float* x, int ldx, int silu_in, int K, int B, uint16_t* xs, hipStream_t s);
 // Up to kGemvJobs GEMVs sharing x (and K, B, SiLU on input) in one launch; no add term,
 // no SiLU on output.  B <= 8.
 constexpr int kGemvJobs = 32;
@@ -79,8 +78,7 @@ struct GemvJob {
 struct GemvBatch {
   const float* x; int ldx; int silu_in;
   int K, B, njobs;
-  uint16_t* xs;   // as GemvArgs::xs (bf16 only)
-  int xs_ready;   // as GemvArgs::xs_ready
+  const uint16_t* xs;   // as GemvArgs::xs
   GemvJob job[kGemvJobs];
 };
 inline size_t gemv_split_bytes(int K) { return (size_t)16 * K * 2; }
@@ -146,8 +144,9 @@ hipError_t verify(int dtype, const Terms& t, const void* u, const void* hf, void
 // ---------------------------------------------------------------- small per-step kernels
 // phi[k] = cos(s f_k), phi[128 + k] = sin(s f_k), f_k = exp(-ln(1e4) k / 128), in fp64.
 hipError_t time_embed(double s, float* phi, hipStream_t st);
-// y[b*ld + k] = silu(x[b*ld + k]) for k < n
-hipError_t silu_rows(const float* x, float* y, int B, int n, hipStream_t st);
+// y[b*n + k] = silu(x[b*n + k]) for k < n; with xs (B <= 8) also its bf16 hi / lo split
+// for the MFMA GEMVs (GemvArgs::xs layout, K = n)
+hipError_t silu_rows(const float* x, float* y, int B, int n, uint16_t* xs, hipStream_t st);
 // patches[(b*n_img + tok), feat] (model dtype) from latent x[B, lat_c, F, H, W] fp32
 struct PatchGeom { int B, lat_c, F, H, W, pt, ph, pw; };
 hipError_t patchify(int dtype, const float* x, void* patches, const PatchGeom& g, hipStream_t st);
