@@ -143,7 +143,7 @@ Ws ws_layout(const Model& m) {
   w.PART = take(verify_partials_floats(m.B) * 4);
   w.mod_slot = (size_t)m.B * mod_width(m);
   w.MODS = take(kModLayers * w.mod_slot * 4);
-  w.XS = take(gemv_split_bytes(m.C));
+  w.XS = take(gemv_xs_bytes(m.C));
   w.total = off;
   return w;
 }

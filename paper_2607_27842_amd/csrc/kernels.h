@@ -81,7 +81,7 @@ struct GemvBatch {
   const uint16_t* xs;   // as GemvArgs::xs
   GemvJob job[kGemvJobs];
 };
-inline size_t gemv_split_bytes(int K) { return (size_t)16 * K * 2; }
+inline size_t gemv_xs_bytes(int K) { return (size_t)16 * K * 2; }
 hipError_t gemv_batch(int dtype, const GemvBatch& bt, hipStream_t s);
 
 // ---------------------------------------------------------------- normalisation
