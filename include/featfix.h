@@ -39,7 +39,7 @@
 extern "C" {
 #endif
 
-#define FF_ABI_VERSION 1
+#define FF_ABI_VERSION 2
 #define FF_MAX_K 3          /* largest supported forecast order K */
 #define FF_MAX_SLOTS 8      /* largest supported ring size S      */
 #define FF_TEMB_DIM 256     /* sinusoidal time-embedding width    */
@@ -126,12 +126,20 @@ typedef struct {
 /* Schedule: T steps, full refresh every R steps (steps i with i % R == 0), forecast
  * order K (0 <= K <= FF_MAX_K), ring of S slots (K+1 <= S <= FF_MAX_SLOTS), rel-L1
  * epsilon eps > 0, mode (FF_VANILLA .. FF_EXACT_ONLY), feature_mode (FF_RESIDUAL caches
- * h - u and drafts u + F; FF_OUTPUT caches h and drafts F). */
+ * h - u and drafts u + F; FF_OUTPUT caches h and drafts F).
+ * tau: 0 keeps that fixed schedule.  tau > 0 (finite; FF_VERIFY and FF_FEATFIX only)
+ * makes the base policy adaptive, discrepancy-triggered in the manner of speculative
+ * caching (the paper's base policies decide when to refresh, Sec. 3.1; its FLUX policy
+ * has a threshold, Sec. 4): step 0 refreshes, and a later step i refreshes when
+ * i - (the last refresh step) >= R, or when step i-1 was a cached step whose largest
+ * paid-site discrepancy max_{l,b} d_b (Eq. 4) is not <= tau (a NaN counts as above).
+ * The finite differences then use the actual refresh steps (Eq. 2). */
 typedef struct {
   int32_t T, R, K, S;
   float eps;
   int32_t mode;
   int32_t feature_mode;
+  float tau;
 } ff_sched_desc;
 
 /* Separate accounting of full-refresh steps, paid exact-block checks and forwarded
@@ -180,8 +188,10 @@ const char* ff_last_error(void);
  * in Vanilla); cached steps read slots (j - m) % S for m = 0..k_eff with coefficients
  * c_m such that F(i) = sum_m c_m * Delta_{j-m} equals the Taylor forecast of Eq. 2.
  * Per (i, l): EXACT on refresh steps, SITE where the mask is set in Verify / FeatFix /
- * Exact-only, DRAFT otherwise.  *out is owned by the caller (ff_plan_destroy).
- * Errors: FF_E_NULL, FF_E_RANGE (T, R, K, S, mode, feature_mode, n_layers, eps). */
+ * Exact-only, DRAFT otherwise.  With tau > 0 this is the schedule of a run in which no
+ * discrepancy exceeds tau; the context realises the actual one step by step
+ * (ff_ctx_step_kinds).  *out is owned by the caller (ff_plan_destroy).
+ * Errors: FF_E_NULL, FF_E_RANGE (T, R, K, S, mode, feature_mode, n_layers, eps, tau). */
 ff_status ff_plan_build(const ff_sched_desc* s, int32_t n_layers, const uint8_t* site_mask,
                         ff_plan** out);
 void ff_plan_destroy(ff_plan* p);
@@ -259,6 +269,12 @@ ff_status ff_ctx_reset(ff_ctx* c);
 /* Counts of the steps executed since creation / the last reset. */
 ff_status ff_get_counts(const ff_ctx* c, ff_counts* out);
 
+/* Realised kind of each step since creation / the last reset: kinds[i] = FF_STEP_REFRESH
+ * or FF_STEP_CACHED for steps already run, -1 for the others (host array [T]).  With
+ * tau == 0 it follows the plan; with tau > 0 it records the adaptive decisions.
+ * Errors: FF_E_NULL. */
+ff_status ff_ctx_step_kinds(const ff_ctx* c, int32_t* kinds);
+
 /* One denoising step i = step (must be the context's next step, 0..T-1 in order):
  *   c_t = cond + TimeMLP(sinusoid(1000 t_i)), t_i = 1 - i/T
  *   X = [txt ; PatchEmbed(patchify(x))]
@@ -272,6 +288,10 @@ ff_status ff_get_counts(const ff_ctx* c, ff_counts* out);
  * cond: device fp32 [B, C].  txt: device dtype [B, n_txt, C] (NULL iff n_txt == 0).
  * audit: device fp32 [T*L*B] or NULL; entry (i*L + l)*B + b receives rel_l1 at paid
  * checks (other entries are not written).
+ * With tau > 0 the step's kind is decided here (ff_sched_desc): a step that follows a
+ * checked cached step first waits on the host for that step's discrepancies (queued
+ * on the same stream as a small device-to-host copy), so the host blocks until the
+ * previous step has finished on the device.
  * Errors: FF_E_NULL, FF_E_STATE (step out of order), FF_E_HIP. */
 ff_status ff_denoise_step(ff_ctx* c, int32_t step, float* x, const float* cond,
                           const void* txt, float* audit, ff_stream_t stream);

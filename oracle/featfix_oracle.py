@@ -345,7 +345,7 @@ def rel_l1(hd, hf, eps):
 
 # ----------------------------------------------------------------------------- the loop
 
-def run(cfg, mode, inputs, weights, mask, feature_mode=RESIDUAL, trace=None):
+def run(cfg, mode, inputs, weights, mask, feature_mode=RESIDUAL, trace=None, tau=0.0):
     """Whole cached denoising loop (Sec. 3.3 framework, Eq. 1-5).
 
     Sampler reading: rectified-flow Euler on t_i = 1 - i/T, x_{i+1} = x_i + (t_{i+1}-t_i) v.
@@ -353,27 +353,52 @@ def run(cfg, mode, inputs, weights, mask, feature_mode=RESIDUAL, trace=None):
     the GPU stores them between layers: the stream after each layer (and after the patch
     embedding), and each cached Delta.
 
-    Returns dict(x=x_T [fp64], audit={(i, l): d[B]}, counts, plan).  If `trace` is a
-    list, the stream after every (step, layer) is appended to it."""
+    tau > 0 (Verify and FeatFix) replaces the fixed refresh rule by an adaptive base
+    policy (Sec. 3.1: the base policy decides when to refresh; Sec. 4: the FLUX policy
+    has a threshold).  Reading: step 0 refreshes; step i refreshes when R steps have
+    passed since the last refresh, or when step i-1 was a cached step with paid sites
+    whose largest discrepancy over those sites and the samples (Eq. 4) is not <= tau
+    (NaN counts as above).  Sites keep the mask; the finite differences use the actual
+    refresh steps (Eq. 2).
+
+    Returns dict(x=x_T [fp64], audit={(i, l): d[B]}, counts, plan, step_kind=[T]).  If
+    `trace` is a list, the stream after every (step, layer) is appended to it."""
     T, R, K, S = cfg["T"], cfg["R"], cfg["K"], cfg["S"]
     kinds = cfg["kinds"]
     L = len(kinds)
     rnd = _rounder(cfg["dtype"])
     layer_w, G = weights
     plan = make_plan(T, L, R, K, S, mask, mode)
+    if tau > 0 and mode not in (VERIFY, FEATFIX):
+        raise ValueError("tau > 0 needs the discrepancy of Verify or FeatFix")
+    site_mask = np.asarray(mask, dtype=np.uint8).reshape(T, L)
     x = _f64(inputs["x"]).copy()
     txt = _f64(inputs["txt"])
     n_txt = cfg["n_txt"]
     caches = [TaylorCache(K) for _ in range(L)]
     audit = {}
+    step_kind = []
+    counts = {"n_full_refresh": 0, "n_paid_checks": 0, "n_forwarded": 0}
+    last, prev_d = -1, None   # last refresh step; largest site discrepancy of the previous step
     for i in range(T):
+        if tau > 0:
+            refresh = i == 0 or i - last >= R or (prev_d is not None and not prev_d <= tau)
+            actions = [EXACT] * L if refresh else [SITE if site_mask[i, l] else DRAFT_ACT for l in range(L)]
+        else:
+            refresh = plan["step_kind"][i] == REFRESH_STEP
+            actions = plan["action"][i]
+        if refresh:
+            last = i
+            counts["n_full_refresh"] += 1
+        step_kind.append(REFRESH_STEP if refresh else CACHED_STEP)
+        step_d = []
         t_i, t_n = 1.0 - i / T, 1.0 - (i + 1) / T
         cs = silu(conditioning(inputs["c"], t_i, G))
         X = rnd(_linear(patchify(x, cfg["patch"]), G["pe_w"], G["pe_b"]))
         if n_txt:
             X = np.concatenate([txt, X], axis=1)
         for l in range(L):
-            act = plan["action"][i, l]
+            act = actions[l]
             u = X
             if act == EXACT:
                 h = rnd(block(kinds[l], u, cs, layer_w[l], cfg))
@@ -386,16 +411,21 @@ def run(cfg, mode, inputs, weights, mask, feature_mode=RESIDUAL, trace=None):
                 if act == DRAFT_ACT:
                     X = hd
                 else:
+                    counts["n_paid_checks"] += 1
                     hf = rnd(block(kinds[l], u, cs, layer_w[l], cfg))
                     if mode != EXACT_ONLY:
                         audit[(i, l)] = rel_l1(hd, hf, cfg["rel_eps"])
+                        step_d.append(audit[(i, l)])
+                    if mode in (FEATFIX, EXACT_ONLY):
+                        counts["n_forwarded"] += 1
                     X = hf if mode in (FEATFIX, EXACT_ONLY) else hd
             if trace is not None:
                 trace.append(X.copy())
+        prev_d = float(np.max(np.concatenate(step_d))) if step_d else None
         y = final_layer(X[:, n_txt:], cs, G, cfg)
         v = unpatchify(y, cfg["patch"], cfg["lat"])
         x = x + (t_n - t_i) * v
-    return {"x": x, "audit": audit, "counts": plan["counts"], "plan": plan}
+    return {"x": x, "audit": audit, "counts": counts, "plan": plan, "step_kind": step_kind}
 
 
 def max_rel_err(a, b):

@@ -10,6 +10,8 @@ from __future__ import annotations
 import ctypes as C
 import os
 
+import numpy as np
+
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libfeatfix.so")
 
 FF_OK, FF_E_NULL, FF_E_SHAPE, FF_E_DTYPE, FF_E_RANGE, FF_E_STATE, FF_E_WORKSPACE, FF_E_HIP, \
@@ -26,7 +28,8 @@ FF_MAX_K, FF_MAX_SLOTS, FF_TEMB_DIM = 3, 8, 256
 EXPORTED = ("ff_abi_version", "ff_last_error", "ff_plan_build", "ff_plan_destroy", "ff_plan_export",
             "ff_cache_bytes", "ff_workspace_bytes", "ff_block_exact", "ff_cache_update",
             "ff_draft_forecast", "ff_verify_replace", "ff_ctx_create", "ff_ctx_destroy",
-            "ff_ctx_reset", "ff_get_counts", "ff_denoise_step", "ff_ctx_profile", "ff_ctx_profile_read")
+            "ff_ctx_reset", "ff_get_counts", "ff_ctx_step_kinds", "ff_denoise_step", "ff_ctx_profile",
+            "ff_ctx_profile_read")
 PROF_CLASSES = ("gemm", "attn", "norm", "gemv", "draft", "verify", "cache", "other")
 
 
@@ -60,7 +63,7 @@ class ff_global_weights(C.Structure):
 
 class ff_sched_desc(C.Structure):
     _fields_ = [("T", C.c_int32), ("R", C.c_int32), ("K", C.c_int32), ("S", C.c_int32),
-                ("eps", C.c_float), ("mode", C.c_int32), ("feature_mode", C.c_int32)]
+                ("eps", C.c_float), ("mode", C.c_int32), ("feature_mode", C.c_int32), ("tau", C.c_float)]
 
 
 class ff_counts(C.Structure):
@@ -112,6 +115,7 @@ def lib():
             "ff_ctx_destroy": (None, [vp]),
             "ff_ctx_reset": (i32, [vp]),
             "ff_get_counts": (i32, [vp, P(ff_counts)]),
+            "ff_ctx_step_kinds": (i32, [vp, P(i32)]),
             "ff_denoise_step": (i32, [vp, i32, vp, vp, vp, vp, vp]),
             "ff_ctx_profile": (i32, [vp, i32]),
             "ff_ctx_profile_read": (i32, [vp, P(ff_prof_stat)]),
@@ -225,6 +229,13 @@ def ff_get_counts(ctx):
     cnt = ff_counts()
     check(lib().ff_get_counts(ctx, C.byref(cnt)))
     return cnt.as_dict()
+
+
+def ff_ctx_step_kinds(ctx, T):
+    """Realised step kinds [T] (FF_STEP_REFRESH / FF_STEP_CACHED, -1 for steps not run)."""
+    out = (C.c_int32 * T)()
+    check(lib().ff_ctx_step_kinds(ctx, out))
+    return np.array(out[:], dtype=np.int32)
 
 
 def ff_denoise_step(ctx, step, x, cond, txt, audit, stream=0):

@@ -107,7 +107,7 @@ ff_status check_model(const ff_model_desc* m, Model* out) {
 
 // ---------------------------------------------------------------- workspace layout
 struct Ws {
-  size_t X0, X1, HF, LNA, QKV, ATT, X1F, HID, MOD, CT, CS, TMP, PHI, PATCH, YF, PART, MODS, XS, total;
+  size_t X0, X1, HF, LNA, QKV, ATT, X1F, HID, MOD, CT, CS, TMP, PHI, PATCH, YF, PART, MODS, XS, REL, total;
   size_t mod_slot;   // floats per layer slot of MODS
 };
 
@@ -144,6 +144,7 @@ Ws ws_layout(const Model& m) {
   w.mod_slot = (size_t)m.B * mod_width(m);
   w.MODS = take(kModLayers * w.mod_slot * 4);
   w.XS = take(gemv_xs_bytes(m.C));
+  w.REL = take((size_t)m.L * m.B * 4);   // one step's site discrepancies (adaptive refresh)
   w.total = off;
   return w;
 }
@@ -431,20 +432,8 @@ struct ff_plan {
   int L;
   std::vector<int32_t> step_kind, refresh_ord, k_eff, read_slots, write_slot, action;
   std::vector<float> coeffs;
+  std::vector<uint8_t> mask;   // [T * L] as given (the adaptive schedule re-reads it)
   ff_counts counts;
-};
-
-struct ff_ctx {
-  Model m;
-  std::vector<ff_layer_weights> lw;
-  ff_global_weights g;
-  ff_plan plan;
-  void* cache;
-  void* ws;
-  int next_step;
-  std::vector<uint8_t> written;  // [L * S]: slot holds a refresh of this run
-  ff_counts counts;
-  Prof prof;
 };
 
 namespace {
@@ -488,6 +477,72 @@ struct CoefState {
   }
 };
 
+// Row i of a plan: a refresh (ordinal j, written to slot j % S) or a cached step that
+// reads the ring with the coefficients of cs at step i, with SITE where the mask is set
+// in the paid modes.  cs must already hold the refreshes up to step i.
+void plan_row(ff_plan* p, int i, bool refresh, int j, const CoefState& cs) {
+  const ff_sched_desc& s = p->s;
+  const int K = s.K, S = s.S, L = p->L;
+  const int ke = j < K ? j : K;
+  p->refresh_ord[i] = j;
+  p->k_eff[i] = ke;
+  for (int q = 0; q <= K; ++q) {
+    p->read_slots[(size_t)i * (K + 1) + q] = -1;
+    p->coeffs[(size_t)i * (K + 1) + q] = 0.f;
+  }
+  if (refresh) {
+    p->step_kind[i] = FF_STEP_REFRESH;
+    p->write_slot[i] = s.mode != FF_VANILLA ? j % S : -1;
+    for (int l = 0; l < L; ++l) p->action[(size_t)i * L + l] = FF_ACT_EXACT;
+    return;
+  }
+  p->step_kind[i] = FF_STEP_CACHED;
+  p->write_slot[i] = -1;
+  for (int q = 0; q <= ke; ++q) p->read_slots[(size_t)i * (K + 1) + q] = ((j - q) % S + S) % S;
+  float c[FF_MAX_K + 2] = {};
+  cs.coeffs((double)i, c);
+  for (int q = 0; q <= ke; ++q) p->coeffs[(size_t)i * (K + 1) + q] = c[q];
+  const bool paid_mode = s.mode == FF_VERIFY || s.mode == FF_FEATFIX || s.mode == FF_EXACT_ONLY;
+  for (int l = 0; l < L; ++l)
+    p->action[(size_t)i * L + l] = paid_mode && p->mask[(size_t)i * L + l] ? FF_ACT_SITE : FF_ACT_DRAFT;
+}
+
+}  // namespace
+
+struct ff_ctx {
+  Model m;
+  std::vector<ff_layer_weights> lw;
+  ff_global_weights g;
+  ff_plan plan;   // with tau > 0, row i is rewritten when step i is decided
+  void* cache;
+  void* ws;
+  int next_step;
+  std::vector<uint8_t> written;  // [L * S]: slot holds a refresh of this run
+  std::vector<int32_t> realised; // [T]: kind of each step run, -1 before
+  ff_counts counts;
+  Prof prof;
+  // adaptive refresh (tau > 0): refresh ordinal and recursion over the actual refresh
+  // steps, the last refresh step, and the previous step's discrepancies on their way to
+  // the host (pinned rel[L * B], event after the copy; checked: that step had sites)
+  int a_j = -1, a_last = -1;
+  CoefState a_cs{0};
+  float* a_rel = nullptr;
+  hipEvent_t a_ev = nullptr;
+  bool a_checked = false;
+  ~ff_ctx() {
+    if (a_ev) (void)hipEventDestroy(a_ev);
+    if (a_rel) (void)hipHostFree(a_rel);
+  }
+  void reset_adaptive() {
+    a_j = -1;
+    a_last = -1;
+    a_cs = CoefState(plan.s.K);
+    a_checked = false;
+  }
+};
+
+namespace {
+
 ff_status check_sched(const ff_sched_desc* s, int L) {
   if (!s) return fail(FF_E_NULL, "schedule descriptor is NULL");
   if (s->T < 1 || s->T > 100000) return fail(FF_E_RANGE, "T=%d out of range", s->T);
@@ -498,12 +553,15 @@ ff_status check_sched(const ff_sched_desc* s, int L) {
   if (s->feature_mode != FF_RESIDUAL && s->feature_mode != FF_OUTPUT)
     return fail(FF_E_RANGE, "feature_mode=%d unknown", s->feature_mode);
   if (!(s->eps > 0.f)) return fail(FF_E_RANGE, "eps must be > 0");
+  if (!(s->tau >= 0.f) || !std::isfinite(s->tau)) return fail(FF_E_RANGE, "tau must be finite and >= 0");
+  if (s->tau > 0.f && s->mode != FF_VERIFY && s->mode != FF_FEATFIX)
+    return fail(FF_E_RANGE, "tau > 0 needs the discrepancy of FF_VERIFY or FF_FEATFIX (mode %d)", s->mode);
   if (L < 1 || L > 4096) return fail(FF_E_RANGE, "n_layers=%d out of range", L);
   return FF_OK;
 }
 
 void build_plan(const ff_sched_desc& s, int L, const uint8_t* mask, ff_plan* p) {
-  const int T = s.T, K = s.K, S = s.S;
+  const int T = s.T, K = s.K;
   p->s = s;
   p->L = L;
   p->step_kind.assign(T, 0);
@@ -513,37 +571,25 @@ void build_plan(const ff_sched_desc& s, int L, const uint8_t* mask, ff_plan* p) 
   p->write_slot.assign(T, -1);
   p->action.assign((size_t)T * L, FF_ACT_EXACT);
   p->coeffs.assign((size_t)T * (K + 1), 0.f);
+  p->mask.assign(mask, mask + (size_t)T * L);
   p->counts = ff_counts{0, 0, 0};
   CoefState cs(K);
   int j = -1;
-  const bool paid_mode = s.mode == FF_VERIFY || s.mode == FF_FEATFIX || s.mode == FF_EXACT_ONLY;
   for (int i = 0; i < T; ++i) {
     const bool refresh = s.mode == FF_VANILLA || i % s.R == 0;
     if (refresh) {
       ++j;
       cs.refresh((double)i);
     }
-    p->refresh_ord[i] = j;
-    const int ke = j < K ? j : K;
-    p->k_eff[i] = ke;
+    plan_row(p, i, refresh, j, cs);
     if (refresh) {
-      p->step_kind[i] = FF_STEP_REFRESH;
-      if (s.mode != FF_VANILLA) p->write_slot[i] = j % S;
       p->counts.n_full_refresh++;
       continue;
     }
-    p->step_kind[i] = FF_STEP_CACHED;
-    for (int q = 0; q <= ke; ++q) p->read_slots[(size_t)i * (K + 1) + q] = ((j - q) % S + S) % S;
-    float c[FF_MAX_K + 2] = {};
-    cs.coeffs((double)i, c);
-    for (int q = 0; q <= ke; ++q) p->coeffs[(size_t)i * (K + 1) + q] = c[q];
     for (int l = 0; l < L; ++l) {
-      const bool site = paid_mode && mask[(size_t)i * L + l];
-      p->action[(size_t)i * L + l] = site ? FF_ACT_SITE : FF_ACT_DRAFT;
-      if (site) {
-        p->counts.n_paid_checks++;
-        if (s.mode == FF_FEATFIX || s.mode == FF_EXACT_ONLY) p->counts.n_forwarded++;
-      }
+      if (p->action[(size_t)i * L + l] != FF_ACT_SITE) continue;
+      p->counts.n_paid_checks++;
+      if (s.mode == FF_FEATFIX || s.mode == FF_EXACT_ONLY) p->counts.n_forwarded++;
     }
   }
 }
@@ -735,7 +781,17 @@ ff_status ff_ctx_create(const ff_model_desc* m, const ff_layer_weights* layer_w,
     c->ws = ws;
     c->next_step = 0;
     c->written.assign((size_t)md.L * p->s.S, 0);
+    c->realised.assign(p->s.T, -1);
     c->counts = ff_counts{0, 0, 0};
+    c->reset_adaptive();
+    if (p->s.tau > 0.f) {
+      hipError_t he = hipHostMalloc((void**)&c->a_rel, (size_t)md.L * md.B * sizeof(float), hipHostMallocDefault);
+      if (he == hipSuccess) he = hipEventCreateWithFlags(&c->a_ev, hipEventDisableTiming);
+      if (he != hipSuccess) {
+        delete c;
+        return fail(FF_E_HIP, "adaptive refresh buffers: %s", hipGetErrorString(he));
+      }
+    }
     *out = c;
     return ok();
   } catch (const std::bad_alloc&) {
@@ -751,7 +807,15 @@ ff_status ff_ctx_reset(ff_ctx* c) {
   if (!c) return fail(FF_E_NULL, "ctx is NULL");
   c->next_step = 0;
   std::fill(c->written.begin(), c->written.end(), 0);
+  std::fill(c->realised.begin(), c->realised.end(), -1);
   c->counts = ff_counts{0, 0, 0};
+  c->reset_adaptive();
+  return ok();
+}
+
+ff_status ff_ctx_step_kinds(const ff_ctx* c, int32_t* kinds) {
+  if (!c || !kinds) return fail(FF_E_NULL, "ctx or kinds is NULL");
+  memcpy(kinds, c->realised.data(), c->realised.size() * sizeof(int32_t));
   return ok();
 }
 
@@ -773,6 +837,31 @@ ff_status ff_denoise_step(ff_ctx* c, int32_t step, float* x, const float* cond, 
       return fail(FF_E_STATE, "step %d out of order (expected %d of %d)", step, c->next_step, s.T);
     if (!aligned16(x) || !aligned16(cond) || (txt && !aligned16(txt))) return fail(FF_E_SHAPE, "pointers must be 16-byte aligned");
     const int L = m.L, K = s.K, S = s.S, i = step;
+    if (s.tau > 0.f) {
+      // adaptive refresh: decide this step from the interval and the previous step's
+      // largest site discrepancy, then write row i of the context's plan
+      bool refresh = i == 0 || i - c->a_last >= s.R;
+      if (!refresh && c->a_checked) {
+        HIP_TRY(hipEventSynchronize(c->a_ev), "adaptive refresh: discrepancy copy");
+        float dmax = 0.f;
+        bool nan = false;
+        for (int l = 0; l < L; ++l) {
+          if (c->plan.action[(size_t)(i - 1) * L + l] != FF_ACT_SITE) continue;
+          for (int b = 0; b < m.B; ++b) {
+            const float d = c->a_rel[(size_t)l * m.B + b];
+            if (d != d) nan = true;
+            else dmax = std::max(dmax, d);
+          }
+        }
+        refresh = nan || !(dmax <= s.tau);
+      }
+      if (refresh) {
+        c->a_j++;
+        c->a_cs.refresh((double)i);
+        c->a_last = i;
+      }
+      plan_row(&c->plan, i, refresh, c->a_j, c->a_cs);
+    }
     // host-side state checks first: nothing is launched if the plan would read an unwritten slot
     if (p.step_kind[i] == FF_STEP_CACHED) {
       for (int l = 0; l < L; ++l) {
@@ -900,7 +989,8 @@ ff_status ff_denoise_step(ff_ctx* c, int32_t step, float* x, const float* cond, 
       if (e) return e;
       e = exec_block(m, m.kinds[l], c->lw[l], cs, cur, hf, ws, ex, mod_of[l]);
       if (e) return e;
-      float* rel = audit ? audit + ((size_t)i * L + l) * m.B : nullptr;
+      float* rel = audit ? audit + ((size_t)i * L + l) * m.B
+                         : s.tau > 0.f ? at<float>(ws, W.REL) + (size_t)l * m.B : nullptr;
       HIP_TRY(ex.verify(tm, resid ? cur : nullptr, hf, cur, mode == FF_FEATFIX ? 1 : 0, m.B, (size_t)m.N * C, s.eps,
                         rel, at<float>(ws, W.PART)), "verify");
     }
@@ -927,6 +1017,18 @@ ff_status ff_denoise_step(ff_ctx* c, int32_t step, float* x, const float* cond, 
               "unpatchify + euler");
     }
     // bookkeeping after a successful enqueue
+    if (s.tau > 0.f) {
+      // this step's site discrepancies go to the host for the next step's decision
+      c->a_checked = false;
+      for (int l = 0; l < L; ++l) c->a_checked |= p.action[(size_t)i * L + l] == FF_ACT_SITE;
+      if (c->a_checked) {
+        const float* src = audit ? audit + (size_t)i * L * m.B : at<float>(ws, W.REL);
+        HIP_TRY(hipMemcpyAsync(c->a_rel, src, (size_t)L * m.B * sizeof(float), hipMemcpyDeviceToHost, st),
+                "adaptive refresh: discrepancy copy");
+        HIP_TRY(hipEventRecord(c->a_ev, st), "adaptive refresh: event");
+      }
+    }
+    c->realised[i] = p.step_kind[i];
     if (p.step_kind[i] == FF_STEP_REFRESH) {
       c->counts.n_full_refresh++;
       if (mode != FF_VANILLA)

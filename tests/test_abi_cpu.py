@@ -22,7 +22,7 @@ def test_every_declared_symbol_is_exported():
     L = abi.lib()
     for name in declared:
         assert hasattr(L, name), name
-    assert abi.ff_abi_version() == 1
+    assert abi.ff_abi_version() == 2
 
 
 def sched(T, R, K, S, mode, fm=abi.FF_RESIDUAL, eps=1e-8):
