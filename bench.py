@@ -11,8 +11,10 @@ loops (10 refresh + 40 cached steps each).  Inputs and weights are resident in H
 the timed region.  Workload (value): DiT-XL/2 shape -- 28 DiT blocks, hidden 1152, 16
 heads of 72, 256 tokens, batch 8, bf16, T=50, refresh every 5 steps, second-order
 forecast, sites at layers 13 and 27 on every cached step.  The FLUX-like shape (19 double
-+ 38 single blocks, 4096 + 512 tokens), the Vanilla loops and a DiT-XL/2 FeatFix loop
-with the adaptive (discrepancy-triggered) refresh policy are reported alongside.
++ 38 single blocks, 4096 + 512 tokens), the Vanilla loops, a DiT-XL/2 FeatFix loop with
+the adaptive (discrepancy-triggered) refresh policy and the DiT-XL/2 matched-compute arms
+(token- / channel-partial forwarding at stride 2, whole-timestep recompute) are reported
+alongside.
 
 Prints ONE JSON line.
 """
@@ -284,6 +286,7 @@ def main():
     ap.add_argument("--no-dit", action="store_true",
                     help="time the FLUX-like loop as the primary workload instead of DiT-XL/2 (profiling)")
     ap.add_argument("--no-vanilla", action="store_true")
+    ap.add_argument("--no-arms", action="store_true", help="skip the matched-compute arm loops reported in extra")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
@@ -302,6 +305,8 @@ def main():
     T = cfg["T"]
     warm_loops = max(1, -(-args.warmup // T))
     modes = ["featfix"] + ([] if args.no_vanilla else ["vanilla"])
+    if name == "dit_xl2" and not args.no_arms:
+        modes += ["tokens_partial", "channels_partial", "recompute"]   # the matched-compute arms
     prim = run_workload(name, modes, warm_loops, args.steps, with_profile=True, adaptive=name == "dit_xl2")
     ff = prim["featfix"]
     ms_step = ff["ms"] / ff["steps"]

@@ -59,10 +59,19 @@ enum {
 
 enum { FF_DIT = 0, FF_MMDIT_DOUBLE = 1, FF_MMDIT_SINGLE = 2 };          /* block kinds  */
 enum { FF_F32 = 0, FF_BF16 = 1 };                                        /* dtypes       */
-enum { FF_VANILLA = 0, FF_DRAFT = 1, FF_VERIFY = 2, FF_FEATFIX = 3, FF_EXACT_ONLY = 4 };
+/* Modes (Sec. 3.3).  The last three are the matched-compute arms the paper weighs
+ * whole-block forwarding against: forwarding the exact output on every part_stride-th
+ * token (FF_TOKENS_PARTIAL) or channel (FF_CHANNELS_PARTIAL) only, and recomputing the
+ * rest of the timestep exactly from the first paid site on (FF_RECOMPUTE). */
+enum { FF_VANILLA = 0, FF_DRAFT = 1, FF_VERIFY = 2, FF_FEATFIX = 3, FF_EXACT_ONLY = 4,
+       FF_TOKENS_PARTIAL = 5, FF_CHANNELS_PARTIAL = 6, FF_RECOMPUTE = 7 };
 enum { FF_RESIDUAL = 0, FF_OUTPUT = 1 };                                 /* feature mode */
 enum { FF_STEP_REFRESH = 0, FF_STEP_CACHED = 1 };                        /* step kinds   */
-enum { FF_ACT_EXACT = 0, FF_ACT_DRAFT = 1, FF_ACT_SITE = 2 };            /* actions      */
+/* actions; FF_ACT_RECOMPUTE: the exact block without a history refresh */
+enum { FF_ACT_EXACT = 0, FF_ACT_DRAFT = 1, FF_ACT_SITE = 2, FF_ACT_RECOMPUTE = 3 };
+/* what ff_verify_replace writes: the draft (Verify), the exact output (FeatFix), or the
+ * exact output on every stride-th token / channel of each sample and the draft elsewhere */
+enum { FF_FWD_DRAFT = 0, FF_FWD_EXACT = 1, FF_FWD_TOKENS = 2, FF_FWD_CHANNELS = 3 };
 
 /* HIP stream handle (the same type as hipStream_t); NULL is the default stream. */
 typedef struct ihipStream_t* ff_stream_t;
@@ -125,7 +134,7 @@ typedef struct {
 
 /* Schedule: T steps, full refresh every R steps (steps i with i % R == 0), forecast
  * order K (0 <= K <= FF_MAX_K), ring of S slots (K+1 <= S <= FF_MAX_SLOTS), rel-L1
- * epsilon eps > 0, mode (FF_VANILLA .. FF_EXACT_ONLY), feature_mode (FF_RESIDUAL caches
+ * epsilon eps > 0, mode (FF_VANILLA .. FF_RECOMPUTE), feature_mode (FF_RESIDUAL caches
  * h - u and drafts u + F; FF_OUTPUT caches h and drafts F).
  * tau: 0 keeps that fixed schedule.  tau > 0 (finite; FF_VERIFY and FF_FEATFIX only)
  * makes the base policy adaptive, discrepancy-triggered in the manner of speculative
@@ -133,19 +142,25 @@ typedef struct {
  * has a threshold, Sec. 4): step 0 refreshes, and a later step i refreshes when
  * i - (the last refresh step) >= R, or when step i-1 was a cached step whose largest
  * paid-site discrepancy max_{l,b} d_b (Eq. 4) is not <= tau (a NaN counts as above).
- * The finite differences then use the actual refresh steps (Eq. 2). */
+ * The finite differences then use the actual refresh steps (Eq. 2).
+ * part_stride (>= 1, FF_TOKENS_PARTIAL and FF_CHANNELS_PARTIAL; ignored otherwise): the
+ * exact output is forwarded on the tokens (rows of the block, text rows included) or
+ * channels whose index within a sample is a multiple of it. */
 typedef struct {
   int32_t T, R, K, S;
   float eps;
   int32_t mode;
   int32_t feature_mode;
   float tau;
+  int32_t part_stride;
 } ff_sched_desc;
 
 /* Separate accounting of full-refresh steps, paid exact-block checks and forwarded
- * corrections (Sec. 3.3, matched-compute controls and accounting). */
+ * corrections (Sec. 3.3, matched-compute controls and accounting); the partial arms
+ * count their partly forwarded sites as forwarded, and n_recomputed counts the exact
+ * blocks the recompute arm adds after its paid sites. */
 typedef struct {
-  int64_t n_full_refresh, n_paid_checks, n_forwarded;
+  int64_t n_full_refresh, n_paid_checks, n_forwarded, n_recomputed;
 } ff_counts;
 
 /* Kernel classes of the optional per-launch profiler (ff_ctx_profile). */
@@ -187,11 +202,14 @@ const char* ff_last_error(void);
  * j = (#refreshes up to i) - 1; k_eff = min(K, j); refresh steps write slot j % S (none
  * in Vanilla); cached steps read slots (j - m) % S for m = 0..k_eff with coefficients
  * c_m such that F(i) = sum_m c_m * Delta_{j-m} equals the Taylor forecast of Eq. 2.
- * Per (i, l): EXACT on refresh steps, SITE where the mask is set in Verify / FeatFix /
- * Exact-only, DRAFT otherwise.  With tau > 0 this is the schedule of a run in which no
- * discrepancy exceeds tau; the context realises the actual one step by step
- * (ff_ctx_step_kinds).  *out is owned by the caller (ff_plan_destroy).
- * Errors: FF_E_NULL, FF_E_RANGE (T, R, K, S, mode, feature_mode, n_layers, eps, tau). */
+ * Per (i, l): EXACT on refresh steps, SITE where the mask is set in the paid modes
+ * (Verify, FeatFix, Exact-only and the three arms), DRAFT otherwise; in FF_RECOMPUTE the
+ * layers after a cached step's first SITE are RECOMPUTE.  With tau > 0 this is the
+ * schedule of a run in which no discrepancy exceeds tau; the context realises the
+ * actual one step by step (ff_ctx_step_kinds).  *out is owned by the caller
+ * (ff_plan_destroy).
+ * Errors: FF_E_NULL, FF_E_RANGE (T, R, K, S, mode, feature_mode, n_layers, eps, tau,
+ * part_stride). */
 ff_status ff_plan_build(const ff_sched_desc* s, int32_t n_layers, const uint8_t* site_mask,
                         ff_plan** out);
 void ff_plan_destroy(ff_plan* p);
@@ -242,14 +260,17 @@ ff_status ff_draft_forecast(const ff_model_desc* m, const void* cache, int32_t n
  * rebuilds h_d = D(u) as ff_draft_forecast does (u == NULL for FF_OUTPUT), computes per
  * sample b the normalised relative-L1 discrepancy
  *     rel_l1[b] = sum|h_d - h_f| / (sum|h_f| + eps)       (Eq. 4; fp32, fixed-order sums)
- * and writes h_out = h_f if forward_exact (FeatFix: bit-identical copy of h_f) or h_d
- * (Verify).  h_out may alias u exactly; it must not overlap h_f.  rel_l1 is a device
- * fp32 [B] array or NULL.  ws holds the partial sums (at least ff_workspace_bytes(m)).
- * Errors: FF_E_NULL, FF_E_RANGE, FF_E_SHAPE, FF_E_WORKSPACE. */
+ * and writes h_out by forward: FF_FWD_EXACT h_f (FeatFix: bit-identical copy of h_f),
+ * FF_FWD_DRAFT h_d (Verify), FF_FWD_TOKENS / FF_FWD_CHANNELS h_f on the tokens (rows n of
+ * each sample's N) / channels c with n or c a multiple of stride (>= 1) and h_d elsewhere
+ * (the partial arms of Sec. 3.3; stride is ignored for the first two).  h_out may alias
+ * u exactly; it must not overlap h_f.  rel_l1 is a device fp32 [B] array or NULL.  ws
+ * holds the partial sums (at least ff_workspace_bytes(m)).
+ * Errors: FF_E_NULL, FF_E_RANGE (forward, stride, ...), FF_E_SHAPE, FF_E_WORKSPACE. */
 ff_status ff_verify_replace(const ff_model_desc* m, const void* cache, int32_t n_slots,
                             int32_t layer, int32_t k_eff, const int32_t* slots,
                             const float* coeffs, const void* u, const void* h_f, void* h_out,
-                            int32_t forward_exact, float eps, float* rel_l1, void* ws,
+                            int32_t forward, int32_t stride, float eps, float* rel_l1, void* ws,
                             size_t ws_bytes, ff_stream_t stream);
 
 /* ---------------------------------------------------------------- step executor
@@ -281,8 +302,10 @@ ff_status ff_ctx_step_kinds(const ff_ctx* c, int32_t* kinds);
  *   for each layer l, by the plan's action:
  *     EXACT: X <- B_l(X); refresh the history of l (not in Vanilla)
  *     DRAFT: X <- D_l(X)
- *     SITE : h_f = B_l(X); audit and forward per mode (FeatFix / Exact-only: h_f,
- *            Verify: the draft); Exact-only skips the draft and the audit
+ *     SITE : h_f = B_l(X); audit and forward per mode (FeatFix / Exact-only / recompute:
+ *            h_f, Verify: the draft, the partial arms: h_f on every part_stride-th
+ *            token or channel); Exact-only skips the draft and the audit
+ *     RECOMPUTE: X <- B_l(X) without a history refresh
  *   v = unpatchify(FinalLayer(X_img)); x <- x + (t_{i+1} - t_i) v
  * x: device fp32 latent [B, lat_c, lat_f, lat_h, lat_w], updated in place.
  * cond: device fp32 [B, C].  txt: device dtype [B, n_txt, C] (NULL iff n_txt == 0).

@@ -26,15 +26,19 @@ import numpy as np
 DIT, MMDIT_DOUBLE, MMDIT_SINGLE = 0, 1, 2
 F32, BF16 = 0, 1
 VANILLA, DRAFT, VERIFY, FEATFIX, EXACT_ONLY = 0, 1, 2, 3, 4
+TOKENS_PARTIAL, CHANNELS_PARTIAL, RECOMPUTE = 5, 6, 7   # the matched-compute arms of Sec. 3.3
+PAID_MODES = (VERIFY, FEATFIX, EXACT_ONLY, TOKENS_PARTIAL, CHANNELS_PARTIAL, RECOMPUTE)
+FORWARDING_MODES = (FEATFIX, EXACT_ONLY, TOKENS_PARTIAL, CHANNELS_PARTIAL, RECOMPUTE)
 RESIDUAL, OUTPUT = 0, 1
 REFRESH_STEP, CACHED_STEP = 0, 1
-EXACT, DRAFT_ACT, SITE = 0, 1, 2
+EXACT, DRAFT_ACT, SITE, RECOMPUTE_ACT = 0, 1, 2, 3
 TEMB_DIM = 256
 
 __all__ = [
     "DIT", "MMDIT_DOUBLE", "MMDIT_SINGLE", "F32", "BF16", "VANILLA", "DRAFT", "VERIFY",
-    "FEATFIX", "EXACT_ONLY", "RESIDUAL", "OUTPUT", "REFRESH_STEP", "CACHED_STEP", "EXACT",
-    "DRAFT_ACT", "SITE", "round_bf16", "silu", "gelu_tanh", "layer_norm", "rms_norm",
+    "FEATFIX", "EXACT_ONLY", "TOKENS_PARTIAL", "CHANNELS_PARTIAL", "RECOMPUTE", "PAID_MODES",
+    "FORWARDING_MODES", "RESIDUAL", "OUTPUT", "REFRESH_STEP", "CACHED_STEP", "EXACT",
+    "DRAFT_ACT", "SITE", "RECOMPUTE_ACT", "forward_partial", "round_bf16", "silu", "gelu_tanh", "layer_norm", "rms_norm",
     "softmax", "attention", "timestep_embedding", "conditioning", "patchify", "unpatchify",
     "dit_block", "double_block", "single_block", "block", "final_layer", "make_plan",
     "TaylorCache", "rel_l1", "run", "max_rel_err", "block_flops",
@@ -275,7 +279,10 @@ def make_plan(T, L, R, K, S, mask, mode):
     step in Vanilla); j(i) = number of refreshes up to i minus one; forecast order
     k_eff = min(K, j); the Delta of refresh j lives in ring slot j mod S; at a cached step
     the forecast reads slots (j - m) mod S, m = 0..k_eff.  Site bits on refresh steps are
-    ignored.  Verify, FeatFix and Exact-only share one plan; Draft has no sites."""
+    ignored.  Verify, FeatFix, Exact-only and the partial arms share one plan; Draft has no
+    sites.  The whole-timestep recompute arm (Sec. 3.3: recomputation repeats the
+    remaining transformer stack) pays the first site of a cached step and recomputes every
+    later layer of that step exactly (RECOMPUTE_ACT, no history refresh)."""
     mask = np.asarray(mask, dtype=np.uint8).reshape(T, L)
     refresh = np.array([mode == VANILLA or i % R == 0 for i in range(T)])
     j = np.cumsum(refresh) - 1
@@ -292,15 +299,33 @@ def make_plan(T, L, R, K, S, mask, mode):
         else:
             for m in range(k_eff[i] + 1):
                 read_slots[i, m] = (j[i] - m) % S
+            paid_seen = False
             for l in range(L):
-                paid = mask[i, l] and mode in (VERIFY, FEATFIX, EXACT_ONLY)
+                if mode == RECOMPUTE and paid_seen:
+                    action[i, l] = RECOMPUTE_ACT
+                    continue
+                paid = mask[i, l] and mode in PAID_MODES
                 action[i, l] = SITE if paid else DRAFT_ACT
+                paid_seen = paid_seen or paid
     n_site = int((action == SITE).sum())
     counts = {"n_full_refresh": int(refresh.sum()), "n_paid_checks": n_site,
-              "n_forwarded": n_site if mode in (FEATFIX, EXACT_ONLY) else 0}
+              "n_forwarded": n_site if mode in FORWARDING_MODES else 0,
+              "n_recomputed": int((action == RECOMPUTE_ACT).sum())}
     return {"step_kind": step_kind, "refresh_ord": j.astype(np.int32),
             "k_eff": k_eff.astype(np.int32), "read_slots": read_slots,
             "write_slot": write_slot, "action": action, "counts": counts}
+
+
+def forward_partial(hd, hf, mode, stride):
+    """The partial arms (Sec. 3.3, token- and channel-level replacement): the exact output
+    at every stride-th token (row of the block, text rows included) or channel, counted
+    from 0 within each sample; the draft elsewhere."""
+    out = hd.copy()
+    if mode == TOKENS_PARTIAL:
+        out[:, ::stride, :] = hf[:, ::stride, :]
+    else:
+        out[:, :, ::stride] = hf[:, :, ::stride]
+    return out
 
 
 class TaylorCache:
@@ -345,7 +370,7 @@ def rel_l1(hd, hf, eps):
 
 # ----------------------------------------------------------------------------- the loop
 
-def run(cfg, mode, inputs, weights, mask, feature_mode=RESIDUAL, trace=None, tau=0.0):
+def run(cfg, mode, inputs, weights, mask, feature_mode=RESIDUAL, trace=None, tau=0.0, stride=2):
     """Whole cached denoising loop (Sec. 3.3 framework, Eq. 1-5).
 
     Sampler reading: rectified-flow Euler on t_i = 1 - i/T, x_{i+1} = x_i + (t_{i+1}-t_i) v.
@@ -360,6 +385,10 @@ def run(cfg, mode, inputs, weights, mask, feature_mode=RESIDUAL, trace=None, tau
     whose largest discrepancy over those sites and the samples (Eq. 4) is not <= tau
     (NaN counts as above).  Sites keep the mask; the finite differences use the actual
     refresh steps (Eq. 2).
+
+    The matched-compute arms (Sec. 3.3) differ from FeatFix only at paid sites: the token
+    and channel arms forward the exact output on every `stride`-th token or channel
+    (forward_partial); the recompute arm forwards it and runs the rest of the step exact.
 
     Returns dict(x=x_T [fp64], audit={(i, l): d[B]}, counts, plan, step_kind=[T]).  If
     `trace` is a list, the stream after every (step, layer) is appended to it."""
@@ -378,7 +407,7 @@ def run(cfg, mode, inputs, weights, mask, feature_mode=RESIDUAL, trace=None, tau
     caches = [TaylorCache(K) for _ in range(L)]
     audit = {}
     step_kind = []
-    counts = {"n_full_refresh": 0, "n_paid_checks": 0, "n_forwarded": 0}
+    counts = {"n_full_refresh": 0, "n_paid_checks": 0, "n_forwarded": 0, "n_recomputed": 0}
     last, prev_d = -1, None   # last refresh step; largest site discrepancy of the previous step
     for i in range(T):
         if tau > 0:
@@ -405,6 +434,9 @@ def run(cfg, mode, inputs, weights, mask, feature_mode=RESIDUAL, trace=None, tau
                 if mode != VANILLA:
                     caches[l].refresh(rnd(h - u) if feature_mode == RESIDUAL else h, i)
                 X = h
+            elif act == RECOMPUTE_ACT:
+                counts["n_recomputed"] += 1
+                X = rnd(block(kinds[l], u, cs, layer_w[l], cfg))
             else:
                 F = caches[l].forecast(i)
                 hd = rnd(u + F) if feature_mode == RESIDUAL else rnd(F)
@@ -416,9 +448,12 @@ def run(cfg, mode, inputs, weights, mask, feature_mode=RESIDUAL, trace=None, tau
                     if mode != EXACT_ONLY:
                         audit[(i, l)] = rel_l1(hd, hf, cfg["rel_eps"])
                         step_d.append(audit[(i, l)])
-                    if mode in (FEATFIX, EXACT_ONLY):
+                    if mode in FORWARDING_MODES:
                         counts["n_forwarded"] += 1
-                    X = hf if mode in (FEATFIX, EXACT_ONLY) else hd
+                    if mode in (TOKENS_PARTIAL, CHANNELS_PARTIAL):
+                        X = forward_partial(hd, hf, mode, stride)
+                    else:
+                        X = hf if mode in (FEATFIX, EXACT_ONLY, RECOMPUTE) else hd
             if trace is not None:
                 trace.append(X.copy())
         prev_d = float(np.max(np.concatenate(step_d))) if step_d else None

@@ -19,9 +19,11 @@ FF_OK, FF_E_NULL, FF_E_SHAPE, FF_E_DTYPE, FF_E_RANGE, FF_E_STATE, FF_E_WORKSPACE
 FF_DIT, FF_MMDIT_DOUBLE, FF_MMDIT_SINGLE = 0, 1, 2
 FF_F32, FF_BF16 = 0, 1
 FF_VANILLA, FF_DRAFT, FF_VERIFY, FF_FEATFIX, FF_EXACT_ONLY = 0, 1, 2, 3, 4
+FF_TOKENS_PARTIAL, FF_CHANNELS_PARTIAL, FF_RECOMPUTE = 5, 6, 7
+FF_FWD_DRAFT, FF_FWD_EXACT, FF_FWD_TOKENS, FF_FWD_CHANNELS = 0, 1, 2, 3
 FF_RESIDUAL, FF_OUTPUT = 0, 1
 FF_STEP_REFRESH, FF_STEP_CACHED = 0, 1
-FF_ACT_EXACT, FF_ACT_DRAFT, FF_ACT_SITE = 0, 1, 2
+FF_ACT_EXACT, FF_ACT_DRAFT, FF_ACT_SITE, FF_ACT_RECOMPUTE = 0, 1, 2, 3
 FF_MAX_K, FF_MAX_SLOTS, FF_TEMB_DIM = 3, 8, 256
 
 # every symbol include/featfix.h declares
@@ -63,15 +65,17 @@ class ff_global_weights(C.Structure):
 
 class ff_sched_desc(C.Structure):
     _fields_ = [("T", C.c_int32), ("R", C.c_int32), ("K", C.c_int32), ("S", C.c_int32),
-                ("eps", C.c_float), ("mode", C.c_int32), ("feature_mode", C.c_int32), ("tau", C.c_float)]
+                ("eps", C.c_float), ("mode", C.c_int32), ("feature_mode", C.c_int32), ("tau", C.c_float),
+                ("part_stride", C.c_int32)]
 
 
 class ff_counts(C.Structure):
-    _fields_ = [("n_full_refresh", C.c_int64), ("n_paid_checks", C.c_int64), ("n_forwarded", C.c_int64)]
+    _fields_ = [("n_full_refresh", C.c_int64), ("n_paid_checks", C.c_int64), ("n_forwarded", C.c_int64),
+                ("n_recomputed", C.c_int64)]
 
     def as_dict(self):
         return {"n_full_refresh": self.n_full_refresh, "n_paid_checks": self.n_paid_checks,
-                "n_forwarded": self.n_forwarded}
+                "n_forwarded": self.n_forwarded, "n_recomputed": self.n_recomputed}
 
 
 class ff_prof_stat(C.Structure):
@@ -109,7 +113,7 @@ def lib():
             "ff_cache_update": (i32, [P(ff_model_desc), vp, i32, i32, i32, vp, vp, i32, vp]),
             "ff_draft_forecast": (i32, [P(ff_model_desc), vp, i32, i32, i32, P(i32), P(C.c_float), vp, vp, vp]),
             "ff_verify_replace": (i32, [P(ff_model_desc), vp, i32, i32, i32, P(i32), P(C.c_float), vp, vp, vp,
-                                        i32, f32, vp, vp, sz, vp]),
+                                        i32, i32, f32, vp, vp, sz, vp]),
             "ff_ctx_create": (i32, [P(ff_model_desc), P(ff_layer_weights), P(ff_global_weights), vp, vp, sz,
                                     vp, sz, P(vp)]),
             "ff_ctx_destroy": (None, [vp]),
@@ -203,11 +207,13 @@ def ff_draft_forecast(model, cache, n_slots, layer, k_eff, slots, coeffs, u, h_d
                                          _f32arr(coeffs), u, h_d, stream))
 
 
-def ff_verify_replace(model, cache, n_slots, layer, k_eff, slots, coeffs, u, h_f, h_out, forward_exact, eps,
-                      rel_l1, ws, ws_bytes, stream=0):
+def ff_verify_replace(model, cache, n_slots, layer, k_eff, slots, coeffs, u, h_f, h_out, forward, eps,
+                      rel_l1, ws, ws_bytes, stream=0, stride=1):
+    """forward: FF_FWD_DRAFT / FF_FWD_EXACT / FF_FWD_TOKENS / FF_FWD_CHANNELS (a bool is
+    read as exact (True) or draft (False)); stride for the partial kinds."""
     return check(lib().ff_verify_replace(C.byref(model), cache, n_slots, layer, k_eff, _i32arr(slots),
-                                         _f32arr(coeffs), u, h_f, h_out, int(forward_exact), eps, rel_l1, ws,
-                                         ws_bytes, stream))
+                                         _f32arr(coeffs), u, h_f, h_out, int(forward), int(stride), eps, rel_l1,
+                                         ws, ws_bytes, stream))
 
 
 def ff_ctx_create(model, layer_weights, global_weights, plan, cache, cache_bytes, ws, ws_bytes):

@@ -246,8 +246,8 @@ struct Exec {
   hipError_t draft(const Terms& t, const void* u, void* hd, size_t E) {
     return timed(FF_PROF_DRAFT, 0, (t.n + (u ? 2.0 : 1.0)) * E * es, [&] { return ff::draft(dt, t, u, hd, E, st); });
   }
-  hipError_t verify(const Terms& t, const void* u, const void* hf, void* hout, int fwd, int B, size_t Eb, float eps,
-                    float* rel, float* part) {
+  hipError_t verify(const Terms& t, const void* u, const void* hf, void* hout, const Forward& fwd, int B, size_t Eb,
+                    float eps, float* rel, float* part) {
     return timed(FF_PROF_VERIFY, 0, (t.n + (u ? 3.0 : 2.0)) * Eb * B * es,
                  [&] { return ff::verify(dt, t, u, hf, hout, fwd, B, Eb, eps, rel, part, st); });
   }
@@ -502,10 +502,18 @@ void plan_row(ff_plan* p, int i, bool refresh, int j, const CoefState& cs) {
   float c[FF_MAX_K + 2] = {};
   cs.coeffs((double)i, c);
   for (int q = 0; q <= ke; ++q) p->coeffs[(size_t)i * (K + 1) + q] = c[q];
-  const bool paid_mode = s.mode == FF_VERIFY || s.mode == FF_FEATFIX || s.mode == FF_EXACT_ONLY;
-  for (int l = 0; l < L; ++l)
-    p->action[(size_t)i * L + l] = paid_mode && p->mask[(size_t)i * L + l] ? FF_ACT_SITE : FF_ACT_DRAFT;
+  const bool paid_mode = s.mode >= FF_VERIFY && s.mode != FF_DRAFT;
+  bool paid_seen = false;
+  for (int l = 0; l < L; ++l) {
+    int a = paid_mode && p->mask[(size_t)i * L + l] ? FF_ACT_SITE : FF_ACT_DRAFT;
+    if (s.mode == FF_RECOMPUTE && paid_seen) a = FF_ACT_RECOMPUTE;   // the rest of the step, exact
+    paid_seen = paid_seen || a == FF_ACT_SITE;
+    p->action[(size_t)i * L + l] = a;
+  }
 }
+
+// the modes that forward (all or part of) the exact output of a paid site
+bool forwards(int mode) { return mode == FF_FEATFIX || mode == FF_EXACT_ONLY || mode >= FF_TOKENS_PARTIAL; }
 
 }  // namespace
 
@@ -549,7 +557,9 @@ ff_status check_sched(const ff_sched_desc* s, int L) {
   if (s->R < 1) return fail(FF_E_RANGE, "R=%d must be >= 1", s->R);
   if (s->K < 0 || s->K > FF_MAX_K) return fail(FF_E_RANGE, "K=%d outside [0, %d]", s->K, FF_MAX_K);
   if (s->S < s->K + 1 || s->S > FF_MAX_SLOTS) return fail(FF_E_RANGE, "S=%d must be in [K+1, %d]", s->S, FF_MAX_SLOTS);
-  if (s->mode < FF_VANILLA || s->mode > FF_EXACT_ONLY) return fail(FF_E_RANGE, "mode=%d unknown", s->mode);
+  if (s->mode < FF_VANILLA || s->mode > FF_RECOMPUTE) return fail(FF_E_RANGE, "mode=%d unknown", s->mode);
+  if ((s->mode == FF_TOKENS_PARTIAL || s->mode == FF_CHANNELS_PARTIAL) && s->part_stride < 1)
+    return fail(FF_E_RANGE, "part_stride=%d must be >= 1", s->part_stride);
   if (s->feature_mode != FF_RESIDUAL && s->feature_mode != FF_OUTPUT)
     return fail(FF_E_RANGE, "feature_mode=%d unknown", s->feature_mode);
   if (!(s->eps > 0.f)) return fail(FF_E_RANGE, "eps must be > 0");
@@ -572,7 +582,7 @@ void build_plan(const ff_sched_desc& s, int L, const uint8_t* mask, ff_plan* p) 
   p->action.assign((size_t)T * L, FF_ACT_EXACT);
   p->coeffs.assign((size_t)T * (K + 1), 0.f);
   p->mask.assign(mask, mask + (size_t)T * L);
-  p->counts = ff_counts{0, 0, 0};
+  p->counts = ff_counts{0, 0, 0, 0};
   CoefState cs(K);
   int j = -1;
   for (int i = 0; i < T; ++i) {
@@ -587,9 +597,11 @@ void build_plan(const ff_sched_desc& s, int L, const uint8_t* mask, ff_plan* p) 
       continue;
     }
     for (int l = 0; l < L; ++l) {
-      if (p->action[(size_t)i * L + l] != FF_ACT_SITE) continue;
+      const int a = p->action[(size_t)i * L + l];
+      if (a == FF_ACT_RECOMPUTE) p->counts.n_recomputed++;
+      if (a != FF_ACT_SITE) continue;
       p->counts.n_paid_checks++;
-      if (s.mode == FF_FEATFIX || s.mode == FF_EXACT_ONLY) p->counts.n_forwarded++;
+      if (forwards(s.mode)) p->counts.n_forwarded++;
     }
   }
 }
@@ -730,7 +742,7 @@ ff_status ff_draft_forecast(const ff_model_desc* m, const void* cache, int32_t n
 
 ff_status ff_verify_replace(const ff_model_desc* m, const void* cache, int32_t n_slots, int32_t layer, int32_t k_eff,
                             const int32_t* slots, const float* coeffs, const void* u, const void* h_f, void* h_out,
-                            int32_t forward_exact, float eps, float* rel_l1, void* ws, size_t ws_bytes,
+                            int32_t forward, int32_t stride, float eps, float* rel_l1, void* ws, size_t ws_bytes,
                             ff_stream_t stream) {
   Model md;
   ff_status e = check_model(m, &md);
@@ -746,7 +758,10 @@ ff_status ff_verify_replace(const ff_model_desc* m, const void* cache, int32_t n
   if ((const char*)h_out < (const char*)h_f + tb && (const char*)h_f < (const char*)h_out + tb)
     return fail(FF_E_SHAPE, "h_out overlaps h_f");
   if (!aligned16(h_f) || !aligned16(h_out) || (u && !aligned16(u))) return fail(FF_E_SHAPE, "pointers must be 16-byte aligned");
-  HIP_TRY(ff::verify(md.dtype, t, u, h_f, h_out, forward_exact ? 1 : 0, md.B, (size_t)md.N * md.C, eps, rel_l1,
+  if (forward < FF_FWD_DRAFT || forward > FF_FWD_CHANNELS) return fail(FF_E_RANGE, "forward=%d unknown", forward);
+  if (forward >= FF_FWD_TOKENS && stride < 1) return fail(FF_E_RANGE, "stride=%d must be >= 1", stride);
+  const Forward fw{forward, stride, md.C};
+  HIP_TRY(ff::verify(md.dtype, t, u, h_f, h_out, fw, md.B, (size_t)md.N * md.C, eps, rel_l1,
                      at<float>(ws, L.PART), reinterpret_cast<hipStream_t>(stream)), "verify");
   return ok();
 }
@@ -782,7 +797,7 @@ ff_status ff_ctx_create(const ff_model_desc* m, const ff_layer_weights* layer_w,
     c->next_step = 0;
     c->written.assign((size_t)md.L * p->s.S, 0);
     c->realised.assign(p->s.T, -1);
-    c->counts = ff_counts{0, 0, 0};
+    c->counts = ff_counts{0, 0, 0, 0};
     c->reset_adaptive();
     if (p->s.tau > 0.f) {
       hipError_t he = hipHostMalloc((void**)&c->a_rel, (size_t)md.L * md.B * sizeof(float), hipHostMallocDefault);
@@ -808,7 +823,7 @@ ff_status ff_ctx_reset(ff_ctx* c) {
   c->next_step = 0;
   std::fill(c->written.begin(), c->written.end(), 0);
   std::fill(c->realised.begin(), c->realised.end(), -1);
-  c->counts = ff_counts{0, 0, 0};
+  c->counts = ff_counts{0, 0, 0, 0};
   c->reset_adaptive();
   return ok();
 }
@@ -865,7 +880,7 @@ ff_status ff_denoise_step(ff_ctx* c, int32_t step, float* x, const float* cond, 
     // host-side state checks first: nothing is launched if the plan would read an unwritten slot
     if (p.step_kind[i] == FF_STEP_CACHED) {
       for (int l = 0; l < L; ++l) {
-        if (p.action[(size_t)i * L + l] == FF_ACT_EXACT) continue;
+        if (p.action[(size_t)i * L + l] == FF_ACT_EXACT || p.action[(size_t)i * L + l] == FF_ACT_RECOMPUTE) continue;
         if (s.mode == FF_EXACT_ONLY && p.action[(size_t)i * L + l] == FF_ACT_SITE) continue;
         for (int q = 0; q <= p.k_eff[i]; ++q) {
           const int sl = p.read_slots[(size_t)i * (K + 1) + q];
@@ -900,7 +915,7 @@ ff_status ff_denoise_step(ff_ctx* c, int32_t step, float* x, const float* cond, 
     // time in one batched GEMV launch each; mod_of[l] = that layer's vectors.
     auto runs_exact = [&](int l) {
       const int a = p.action[(size_t)i * L + l];
-      return a == FF_ACT_EXACT || a == FF_ACT_SITE;
+      return a == FF_ACT_EXACT || a == FF_ACT_SITE || a == FF_ACT_RECOMPUTE;
     };
     float* mods = at<float>(ws, W.MODS);
     std::vector<const float*> mod_of(L, nullptr);
@@ -959,6 +974,14 @@ ff_status ff_denoise_step(ff_ctx* c, int32_t step, float* x, const float* cond, 
         void* t = cur; cur = alt; alt = t;
         continue;
       }
+      if (act == FF_ACT_RECOMPUTE) {   // the recompute arm: the exact block, no history refresh
+        ff_status e = ensure_mod(l);
+        if (e) return e;
+        e = exec_block(m, m.kinds[l], c->lw[l], cs, cur, alt, ws, ex, mod_of[l]);
+        if (e) return e;
+        void* t = cur; cur = alt; alt = t;
+        continue;
+      }
       if (act == FF_ACT_SITE && mode == FF_EXACT_ONLY) {
         ff_status e = ensure_mod(l);
         if (e) return e;
@@ -991,7 +1014,11 @@ ff_status ff_denoise_step(ff_ctx* c, int32_t step, float* x, const float* cond, 
       if (e) return e;
       float* rel = audit ? audit + ((size_t)i * L + l) * m.B
                          : s.tau > 0.f ? at<float>(ws, W.REL) + (size_t)l * m.B : nullptr;
-      HIP_TRY(ex.verify(tm, resid ? cur : nullptr, hf, cur, mode == FF_FEATFIX ? 1 : 0, m.B, (size_t)m.N * C, s.eps,
+      const Forward fw{mode == FF_VERIFY ? FWD_DRAFT
+                       : mode == FF_TOKENS_PARTIAL ? FWD_TOKENS
+                       : mode == FF_CHANNELS_PARTIAL ? FWD_CHANNELS : FWD_EXACT,
+                       s.part_stride, C};
+      HIP_TRY(ex.verify(tm, resid ? cur : nullptr, hf, cur, fw, m.B, (size_t)m.N * C, s.eps,
                         rel, at<float>(ws, W.PART)), "verify");
     }
     // final layer on the image rows, unpatchify and Euler
@@ -1035,9 +1062,11 @@ ff_status ff_denoise_step(ff_ctx* c, int32_t step, float* x, const float* cond, 
         for (int l = 0; l < L; ++l) c->written[(size_t)l * S + p.write_slot[i]] = 1;
     } else {
       for (int l = 0; l < L; ++l) {
-        if (p.action[(size_t)i * L + l] != FF_ACT_SITE) continue;
+        const int a = p.action[(size_t)i * L + l];
+        if (a == FF_ACT_RECOMPUTE) c->counts.n_recomputed++;
+        if (a != FF_ACT_SITE) continue;
         c->counts.n_paid_checks++;
-        if (mode == FF_FEATFIX || mode == FF_EXACT_ONLY) c->counts.n_forwarded++;
+        if (forwards(mode)) c->counts.n_forwarded++;
       }
     }
     c->next_step++;

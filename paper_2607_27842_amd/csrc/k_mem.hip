@@ -122,7 +122,7 @@ constexpr int kMaxVerifyBlocks = 2048;  // partial-sum blocks per sample
 // sum|h_d - h_f| and sum|h_f| for this sample, and forward h_f (FeatFix) or h_d (Verify).
 template <int DT, bool RES>
 __global__ __launch_bounds__(kThreads) void k_verify(Terms t, const void* u, const void* __restrict__ hf,
-                                                     void* hout, int forward_exact, size_t chunks_per_sample,
+                                                     void* hout, Forward fw, size_t chunks_per_sample,
                                                      float* __restrict__ partials) {
   using S = St<DT>;
   const int b = blockIdx.y;
@@ -139,7 +139,20 @@ __global__ __launch_bounds__(kThreads) void k_verify(Terms t, const void* u, con
       num += fabsf(d[j] - f[j]);
       den += fabsf(f[j]);
     }
-    S::store(hout, i, forward_exact ? f : d);
+    if (fw.kind == FWD_DRAFT || fw.kind == FWD_EXACT) {
+      S::store(hout, i, fw.kind == FWD_EXACT ? f : d);
+    } else {
+      // partial forwarding: a chunk lies in one row (C % V == 0); row n = e / C, channel e % C
+      const size_t e = c * S::V;
+      const int n = (int)(e / fw.C), ch = (int)(e % fw.C);
+      float o[S::V];
+#pragma unroll
+      for (int j = 0; j < S::V; ++j) {
+        const bool exact = fw.kind == FWD_TOKENS ? n % fw.stride == 0 : (ch + j) % fw.stride == 0;
+        o[j] = exact ? f[j] : d[j];
+      }
+      S::store(hout, i, o);
+    }
   }
   block_sum2(num, den);
   if (threadIdx.x == 0) {
@@ -221,8 +234,10 @@ hipError_t draft_run(int dtype, const Terms& t, int layers, size_t layer_stride,
 
 size_t verify_partials_floats(int B) { return (size_t)B * kMaxVerifyBlocks * 2; }
 
-hipError_t verify(int dtype, const Terms& t, const void* u, const void* hf, void* hout, int forward_exact,
+hipError_t verify(int dtype, const Terms& t, const void* u, const void* hf, void* hout, const Forward& fw,
                   int B, size_t Eb, float eps, float* rel_l1, float* partials, hipStream_t s) {
+  if (fw.kind < FWD_DRAFT || fw.kind > FWD_CHANNELS) return hipErrorInvalidValue;
+  if (fw.kind >= FWD_TOKENS && (fw.stride < 1 || fw.C < 1 || fw.C % (dtype == DT_BF16 ? 8 : 4))) return hipErrorInvalidValue;
   const int V = dtype == DT_BF16 ? 8 : 4;
   const size_t cps = Eb / V;
   int nblk = cdiv((long)cps, kThreads);
@@ -230,11 +245,11 @@ hipError_t verify(int dtype, const Terms& t, const void* u, const void* hf, void
   if (nblk < 1) nblk = 1;
   dim3 grid(nblk, B);
   if (dtype == DT_BF16) {
-    if (u) FF_LAUNCH((k_verify<DT_BF16, true>), grid, kThreads, 0, s, t, u, hf, hout, forward_exact, cps, partials);
-    else FF_LAUNCH((k_verify<DT_BF16, false>), grid, kThreads, 0, s, t, u, hf, hout, forward_exact, cps, partials);
+    if (u) FF_LAUNCH((k_verify<DT_BF16, true>), grid, kThreads, 0, s, t, u, hf, hout, fw, cps, partials);
+    else FF_LAUNCH((k_verify<DT_BF16, false>), grid, kThreads, 0, s, t, u, hf, hout, fw, cps, partials);
   } else {
-    if (u) FF_LAUNCH((k_verify<DT_F32, true>), grid, kThreads, 0, s, t, u, hf, hout, forward_exact, cps, partials);
-    else FF_LAUNCH((k_verify<DT_F32, false>), grid, kThreads, 0, s, t, u, hf, hout, forward_exact, cps, partials);
+    if (u) FF_LAUNCH((k_verify<DT_F32, true>), grid, kThreads, 0, s, t, u, hf, hout, fw, cps, partials);
+    else FF_LAUNCH((k_verify<DT_F32, false>), grid, kThreads, 0, s, t, u, hf, hout, fw, cps, partials);
   }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;

@@ -137,8 +137,12 @@ hipError_t draft(int dtype, const Terms& t, const void* u, void* hd, size_t E, h
 hipError_t draft_run(int dtype, const Terms& t, int layers, size_t layer_stride, int residual, void* x, size_t E,
                      hipStream_t s);
 // Fused draft rebuild + rel-L1 partial sums + forwarding, then a fixed-order reduction.
+// What the pass writes to hout: the draft, the exact output, or the exact output on every
+// stride-th row (token) / channel of a sample with C channels and the draft elsewhere.
+enum { FWD_DRAFT = 0, FWD_EXACT = 1, FWD_TOKENS = 2, FWD_CHANNELS = 3 };
+struct Forward { int kind, stride, C; };
 size_t verify_partials_floats(int B);
-hipError_t verify(int dtype, const Terms& t, const void* u, const void* hf, void* hout, int forward_exact,
+hipError_t verify(int dtype, const Terms& t, const void* u, const void* hf, void* hout, const Forward& fw,
                   int B, size_t Eb, float eps, float* rel_l1, float* partials, hipStream_t s);
 
 // ---------------------------------------------------------------- small per-step kernels

@@ -119,7 +119,7 @@ class Runner:
     """A plan + cache + workspace + context for one mode of one model."""
 
     def __init__(self, dm: DeviceModel, mode, mask, feature_mode=abi.FF_RESIDUAL, T=None, R=None, K=None,
-                 S=None, eps=None, tau=0.0, device=_DEV):
+                 S=None, eps=None, tau=0.0, part_stride=2, device=_DEV):
         cfg = dm.cfg
         self.dm = dm
         self.T = cfg["T"] if T is None else T
@@ -129,7 +129,7 @@ class Runner:
         self.L = len(cfg["kinds"])
         self.mode = mode
         self.sched = abi.ff_sched_desc(self.T, self.R, self.K, self.S, cfg["rel_eps"] if eps is None else eps,
-                                       mode, feature_mode, tau)
+                                       mode, feature_mode, tau, part_stride)
         self.plan = abi.ff_plan_build(self.sched, self.L, np.asarray(mask, np.uint8).reshape(-1))
         self.cache_bytes = abi.ff_cache_bytes(dm.desc, self.S)
         self.ws_bytes = abi.ff_workspace_bytes(dm.desc)

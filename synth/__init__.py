@@ -22,8 +22,10 @@ import numpy as np
 DIT, MMDIT_DOUBLE, MMDIT_SINGLE = 0, 1, 2
 F32, BF16 = 0, 1
 VANILLA, DRAFT, VERIFY, FEATFIX, EXACT_ONLY = 0, 1, 2, 3, 4
+TOKENS_PARTIAL, CHANNELS_PARTIAL, RECOMPUTE = 5, 6, 7
 MODE_NAMES = {"vanilla": VANILLA, "draft": DRAFT, "verify": VERIFY,
-              "featfix": FEATFIX, "exact_only": EXACT_ONLY}
+              "featfix": FEATFIX, "exact_only": EXACT_ONLY, "tokens_partial": TOKENS_PARTIAL,
+              "channels_partial": CHANNELS_PARTIAL, "recompute": RECOMPUTE}
 RESIDUAL, OUTPUT = 0, 1
 
 WEIGHT_STD = 0.02

@@ -25,8 +25,8 @@ def test_every_declared_symbol_is_exported():
     assert abi.ff_abi_version() == 2
 
 
-def sched(T, R, K, S, mode, fm=abi.FF_RESIDUAL, eps=1e-8):
-    return abi.ff_sched_desc(T, R, K, S, eps, mode, fm)
+def sched(T, R, K, S, mode, fm=abi.FF_RESIDUAL, eps=1e-8, stride=2):
+    return abi.ff_sched_desc(T, R, K, S, eps, mode, fm, 0.0, stride)
 
 
 def compare_plan(T, L, R, K, S, mask, mode):
@@ -41,7 +41,8 @@ def compare_plan(T, L, R, K, S, mask, mode):
 
 
 @pytest.mark.parametrize("name", ["tiny", "dit_xl2", "flux", "qwen", "hunyuan"])
-@pytest.mark.parametrize("mode", [abi.FF_VANILLA, abi.FF_DRAFT, abi.FF_VERIFY, abi.FF_FEATFIX, abi.FF_EXACT_ONLY])
+@pytest.mark.parametrize("mode", [abi.FF_VANILLA, abi.FF_DRAFT, abi.FF_VERIFY, abi.FF_FEATFIX, abi.FF_EXACT_ONLY,
+                                  abi.FF_TOKENS_PARTIAL, abi.FF_CHANNELS_PARTIAL, abi.FF_RECOMPUTE])
 def test_plan_bit_exact_with_oracle_on_workloads(name, mode):
     cfg = synth.get_config(name)
     mask = synth.site_mask(cfg)
@@ -57,7 +58,7 @@ def test_plan_bit_exact_random_schedules():
         K = int(rng.integers(0, 4))
         S = int(rng.integers(K + 1, 9))
         mask = (rng.random((T, L)) < rng.random()).astype(np.uint8)
-        mode = int(rng.integers(0, 5))
+        mode = int(rng.integers(0, 8))
         compare_plan(T, L, R, K, S, mask, mode)
 
 
@@ -101,7 +102,8 @@ def test_plan_coefficients_closed_forms():
 def test_plan_errors():
     mask = np.zeros(10, np.uint8)
     bad = [sched(0, 1, 1, 2, 3), sched(10, 0, 1, 2, 3), sched(10, 1, 4, 5, 3), sched(10, 1, 1, 1, 3),
-           sched(10, 1, 1, 9, 3), sched(10, 1, 1, 2, 7), sched(10, 1, 1, 2, 3, fm=5), sched(10, 1, 1, 2, 3, eps=0.0)]
+           sched(10, 1, 1, 9, 3), sched(10, 1, 1, 2, 8), sched(10, 1, 1, 2, 3, fm=5), sched(10, 1, 1, 2, 3, eps=0.0),
+           sched(10, 1, 1, 2, abi.FF_TOKENS_PARTIAL, stride=0), sched(10, 1, 1, 2, abi.FF_CHANNELS_PARTIAL, stride=0)]
     for s in bad:
         with pytest.raises(abi.FFError) as e:
             abi.ff_plan_build(s, 1, mask)
@@ -178,12 +180,16 @@ def test_block_and_memory_op_errors_are_host_side():
     bad_slots = (C.c_int32 * 4)(0, 2, 0, 0)
     assert L.ff_draft_forecast(C.byref(m), 1 << 24, 2, 0, 1, bad_slots, coef, 16, 32, None) == abi.FF_E_RANGE
     assert L.ff_draft_forecast(C.byref(m), None, 2, 0, 1, slots, coef, 16, 32, None) == abi.FF_E_NULL
-    assert L.ff_verify_replace(C.byref(m), 1 << 24, 2, 0, 1, slots, coef, 16, 1 << 26, 1 << 26, 1, C.c_float(1e-8),
+    assert L.ff_verify_replace(C.byref(m), 1 << 24, 2, 0, 1, slots, coef, 16, 1 << 26, 1 << 26, 1, 1, C.c_float(1e-8),
                                None, 1 << 28, ws, None) == abi.FF_E_SHAPE
-    assert L.ff_verify_replace(C.byref(m), 1 << 24, 2, 0, 1, slots, coef, 16, 1 << 26, 1 << 27, 1, C.c_float(0.0),
+    assert L.ff_verify_replace(C.byref(m), 1 << 24, 2, 0, 1, slots, coef, 16, 1 << 26, 1 << 27, 1, 1, C.c_float(0.0),
                                None, 1 << 28, ws, None) == abi.FF_E_RANGE
-    assert L.ff_verify_replace(C.byref(m), 1 << 24, 2, 0, 1, slots, coef, 16, 1 << 26, 1 << 27, 1, C.c_float(1e-8),
+    assert L.ff_verify_replace(C.byref(m), 1 << 24, 2, 0, 1, slots, coef, 16, 1 << 26, 1 << 27, 1, 1, C.c_float(1e-8),
                                None, 1 << 28, ws - 1, None) == abi.FF_E_WORKSPACE
+    # forward kinds and the partial stride are checked on the host
+    for fwd, stride in ((4, 1), (-1, 1), (abi.FF_FWD_TOKENS, 0), (abi.FF_FWD_CHANNELS, 0)):
+        assert L.ff_verify_replace(C.byref(m), 1 << 24, 2, 0, 1, slots, coef, 16, 1 << 26, 1 << 27, fwd, stride,
+                                   C.c_float(1e-8), None, 1 << 28, ws, None) == abi.FF_E_RANGE
 
 
 def test_context_state_errors_are_host_side():
@@ -204,7 +210,7 @@ def test_context_state_errors_are_host_side():
     # steps must come in order: step 1 before step 0 is refused before any launch
     assert Lb.ff_denoise_step(ctx, 1, 1 << 31, 3 << 30, None, None, None) == abi.FF_E_STATE
     assert Lb.ff_denoise_step(ctx, 0, None, 3 << 30, None, None, None) == abi.FF_E_NULL
-    assert abi.ff_get_counts(ctx) == {"n_full_refresh": 0, "n_paid_checks": 0, "n_forwarded": 0}
+    assert abi.ff_get_counts(ctx) == {"n_full_refresh": 0, "n_paid_checks": 0, "n_forwarded": 0, "n_recomputed": 0}
     abi.ff_ctx_reset(ctx)
     abi.ff_ctx_destroy(ctx)
     abi.ff_plan_destroy(plan)

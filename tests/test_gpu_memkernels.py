@@ -104,6 +104,21 @@ def test_refresh_draft_verify_match_oracle(name, feature_mode):
         got_d = rel.cpu().numpy().astype(np.float64)
         say(f"  verify fwd={fwd}: rel_l1 gpu={got_d} oracle={ref_d}")
         np.testing.assert_allclose(got_d, ref_d, rtol=1e-3)
+    # partial forwarding (the token / channel arms): h_f on every third row / channel of
+    # each sample, the draft elsewhere, bit for bit
+    for fwd in (abi.FF_FWD_TOKENS, abi.FF_FWD_CHANNELS):
+        hout = ud.clone()
+        abi.ff_verify_replace(m, cache.data_ptr(), S, 0, ke, slots, coeffs, hout.data_ptr() if uptr else None,
+                              hf.data_ptr(), hout.data_ptr(), fwd, 1e-8, rel.data_ptr(), ws.data_ptr(), ws_bytes,
+                              stride=3)
+        torch.cuda.synchronize()
+        sel = torch.zeros((B, N, C), dtype=torch.bool, device="cuda")
+        if fwd == abi.FF_FWD_TOKENS:
+            sel[:, ::3, :] = True
+        else:
+            sel[:, :, ::3] = True
+        assert torch.equal(hout, torch.where(sel.reshape(-1), hf, out)), f"partial forward {fwd}"
+        np.testing.assert_allclose(rel.cpu().numpy().astype(np.float64), ref_d, rtol=1e-3)
 
 
 def test_memkernels_deterministic():

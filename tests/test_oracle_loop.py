@@ -12,20 +12,28 @@ import synth
                                                ("hunyuan", 10, 80)])
 def test_counter_closed_forms(name, refresh, paid):
     cfg = synth.get_config(name)
-    T, R = cfg["T"], cfg["R"]
+    T, R, L = cfg["T"], cfg["R"], len(cfg["kinds"])
     mask = synth.site_mask(cfg)
     assert refresh == -(-T // R)
-    for mode in (O.VERIFY, O.FEATFIX, O.EXACT_ONLY, O.DRAFT, O.VANILLA):
-        p = O.make_plan(T, len(cfg["kinds"]), R, cfg["K"], cfg["S"], mask, mode)
+    cached = [i for i in range(T) if i % R]
+    for mode in (O.VERIFY, O.FEATFIX, O.EXACT_ONLY, O.DRAFT, O.VANILLA, O.TOKENS_PARTIAL, O.CHANNELS_PARTIAL,
+                 O.RECOMPUTE):
+        p = O.make_plan(T, L, R, cfg["K"], cfg["S"], mask, mode)
         c = p["counts"]
         if mode == O.VANILLA:
-            assert c == {"n_full_refresh": T, "n_paid_checks": 0, "n_forwarded": 0}
+            assert c == {"n_full_refresh": T, "n_paid_checks": 0, "n_forwarded": 0, "n_recomputed": 0}
             continue
         assert c["n_full_refresh"] == refresh
+        if mode == O.RECOMPUTE:
+            # the first site of each checked step is paid, the layers after it recomputed
+            firsts = [int(np.argmax(mask[i])) for i in cached if mask[i].any()]
+            assert c["n_paid_checks"] == c["n_forwarded"] == len(firsts)
+            assert c["n_recomputed"] == sum(L - 1 - f for f in firsts)
+            continue
         expect_paid = 0 if mode == O.DRAFT else paid
         assert c["n_paid_checks"] == expect_paid
-        assert c["n_forwarded"] == (expect_paid if mode in (O.FEATFIX, O.EXACT_ONLY) else 0)
-        cached = [i for i in range(T) if i % R]
+        assert c["n_forwarded"] == (expect_paid if mode in O.FORWARDING_MODES else 0)
+        assert c["n_recomputed"] == 0
         assert expect_paid == (0 if mode == O.DRAFT else int(sum(mask[i].sum() for i in cached)))
 
 
