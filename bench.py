@@ -14,7 +14,8 @@ forecast, sites at layers 13 and 27 on every cached step.  The FLUX-like shape (
 + 38 single blocks, 4096 + 512 tokens), the Vanilla loops, a DiT-XL/2 FeatFix loop with
 the adaptive (discrepancy-triggered) refresh policy and the DiT-XL/2 matched-compute arms
 (token- / channel-partial forwarding at stride 2, whole-timestep recompute) are reported
-alongside.
+alongside, with a FLUX-like resolution sweep (512^2 to 1024^2: latency and peak memory)
+and a DiT-XL/2 shadow-Vanilla diagnostic (per-layer rel-L1 of FeatFix and Verify).
 
 Prints ONE JSON line.
 """
@@ -236,6 +237,99 @@ def run_workload(name, mode_names, warmup_loops, timed_steps_n, with_profile, ad
     return res
 
 
+def shadow_vanilla(name="dit_xl2"):
+    """Mechanism diagnostic (synthetic weights): FeatFix and Verify each stepped in lockstep
+    with a Vanilla run, every layer's stream compared with Vanilla's (ff_ctx_trace +
+    ff_rel_l1, per sample).  Reports the mean distance over the cached steps' layers and
+    samples, the distance after the last layer of the last step, and Verify minus FeatFix
+    (positive: forwarding lowers the downstream error)."""
+    import numpy as np
+    import torch
+    import synth
+    from paper_2607_27842_amd import abi, pipeline
+    cfg = synth.get_config(name)
+    dm = pipeline.DeviceModel.random(cfg, seed=0)
+    x0, cond, txt = device_inputs(cfg)
+    mask = synth.site_mask(cfg)
+    T, L, B = cfg["T"], len(cfg["kinds"]), cfg["B"]
+    E = B * (cfg["n_img"] + cfg["n_txt"]) * cfg["C"]
+    dt = pipeline.torch_dtype(cfg)
+    out = {}
+    van = pipeline.Runner(dm, abi.FF_VANILLA, mask)
+    vbuf = torch.empty(L * E, dtype=dt, device="cuda")
+    van.trace_into(vbuf)
+    for mode_name, mode in (("featfix", abi.FF_FEATFIX), ("verify", abi.FF_VERIFY)):
+        r = pipeline.Runner(dm, mode, mask)
+        buf = torch.empty(L * E, dtype=dt, device="cuda")
+        r.trace_into(buf)
+        xr, _ = r.start(x0, audit=False)
+        xv, _ = van.start(x0, audit=False)
+        rel = torch.zeros((T, L, B), dtype=torch.float32, device="cuda")
+        kinds = r.export_plan()["step_kind"]
+        for i in range(T):
+            r.step(i, xr, cond, txt)
+            van.step(i, xv, cond, txt)
+            for l in range(L):
+                abi.ff_rel_l1(dm.desc, buf[l * E:].data_ptr(), vbuf[l * E:].data_ptr(), 1e-8, rel[i, l].data_ptr(),
+                              r.ws.data_ptr(), r.ws_bytes)
+        d = rel.cpu().numpy()
+        cached = [i for i in range(T) if kinds[i] == abi.FF_STEP_CACHED]
+        out[mode_name] = {"mean_rel_l1_cached_layers": float(d[cached].mean()),
+                          "last_step_last_layer": float(d[T - 1, L - 1].mean())}
+        r.close()
+    van.close()
+    out["verify_minus_featfix_mean"] = out["verify"]["mean_rel_l1_cached_layers"] - out["featfix"]["mean_rel_l1_cached_layers"]
+    log(f"[bench] shadow vanilla {name}: mean rel-L1 featfix {out['featfix']['mean_rel_l1_cached_layers']:.4g}, "
+        f"verify {out['verify']['mean_rel_l1_cached_layers']:.4g}")
+    del dm
+    torch.cuda.empty_cache()
+    return out
+
+
+def resolution_sweep(sides=(512, 768, 1024)):
+    """FLUX-like loop latency and peak device memory from 512^2 to 1024^2 images (latent
+    side / 8, patch 2: 1024, 2304 and 4096 image tokens + 512 text tokens), FeatFix and
+    Vanilla on the same weights: one untimed loop, then one timed 50-step loop each.
+    Peak memory is torch's peak allocation over the run of one mode (the shared weights
+    included; the previous run's buffers are released first); cache and workspace are
+    the library's exact sizes."""
+    import torch
+    import synth
+    from paper_2607_27842_amd import pipeline
+    out = []
+    for side in sides:
+        g = side // 8
+        cfg = synth.get_config("flux", lat=(16, 1, g, g), n_img=(side // 16) ** 2)
+        dm = pipeline.DeviceModel.random(cfg, seed=0)
+        x0, cond, txt = device_inputs(cfg)
+        mask = synth.site_mask(cfg)
+        row = {"image": f"{side}x{side}", "n_img": cfg["n_img"]}
+        for mode_name in ("featfix", "vanilla"):
+            torch.cuda.synchronize()
+            torch.cuda.empty_cache()
+            torch.cuda.reset_peak_memory_stats()
+            r = pipeline.Runner(dm, synth.MODE_NAMES[mode_name], mask)
+            loop = Loop(r, x0, cond, txt)
+            for _ in range(r.T):
+                loop.step()
+            loop.pos = 0
+            ms = timed_steps(loop, r.T)
+            row[mode_name] = {"s_per_loop": round(ms / 1e3, 4),
+                              "peak_gib": round(torch.cuda.max_memory_allocated() / 2**30, 2),
+                              "cache_gib": round(r.cache_bytes / 2**30, 3),
+                              "workspace_gib": round(r.ws_bytes / 2**30, 3)}
+            r.close()
+            del loop, r
+        row["speedup"] = round(row["vanilla"]["s_per_loop"] / row["featfix"]["s_per_loop"], 3)
+        row["featfix_extra_peak_gib"] = round(row["featfix"]["peak_gib"] - row["vanilla"]["peak_gib"], 2)
+        log(f"[bench] flux {side}^2: featfix {row['featfix']['s_per_loop']} s, vanilla {row['vanilla']['s_per_loop']} s "
+            f"per loop, peak {row['featfix']['peak_gib']} / {row['vanilla']['peak_gib']} GiB")
+        out.append(row)
+        del dm, x0, cond, txt
+        torch.cuda.empty_cache()
+    return out
+
+
 def cpu_baseline(steps=5, layers=10):
     """The oracle on the host, on a bounded sample of the DiT-XL/2 FeatFix loop: the first
     R=5 steps (1 refresh + 4 cached steps) at full width, tokens and batch but `layers`
@@ -287,6 +381,7 @@ def main():
                     help="time the FLUX-like loop as the primary workload instead of DiT-XL/2 (profiling)")
     ap.add_argument("--no-vanilla", action="store_true")
     ap.add_argument("--no-arms", action="store_true", help="skip the matched-compute arm loops reported in extra")
+    ap.add_argument("--no-sweep", action="store_true", help="skip the FLUX-like resolution sweep reported in extra")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
@@ -339,6 +434,10 @@ def main():
         if "vanilla" in flux:
             flux["featfix_over_vanilla"] = round(flux["featfix"]["steps_per_s"] / flux["vanilla"]["steps_per_s"], 3)
         extra["flux"] = flux
+    if name == "dit_xl2" and not args.no_flux and not args.no_sweep:
+        extra["flux_resolution_sweep"] = resolution_sweep()
+    if name == "dit_xl2" and not args.no_arms:
+        extra["dit_xl2_shadow_vanilla"] = shadow_vanilla()
     out = {"metric": METRIC, "value": round(value, 3), "unit": "steps/s", "n_gpus": 1, "steps": ff["steps"],
            "warmup": warm_loops * T, "ms_per_step": round(ms_step, 4), "higher_is_better": True, "scaling": "weak",
            "vs_baseline": None, "dtype": "bf16",

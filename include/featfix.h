@@ -276,8 +276,9 @@ ff_status ff_verify_replace(const ff_model_desc* m, const void* cache, int32_t n
 /* ---------------------------------------------------------------- step executor
  * A context binds a model, its weights (layer_w is a host array [n_layers]; the device
  * pointers inside are kept, the host arrays are copied), a plan (copied), a cache of at
- * least ff_cache_bytes(m, plan S) bytes and a workspace of at least
- * ff_workspace_bytes(m) bytes.  *out is owned by the caller (ff_ctx_destroy).
+ * least ff_cache_bytes(m, plan S) bytes (a Vanilla plan never touches it: cache may then
+ * be NULL with cache_bytes 0) and a workspace of at least ff_workspace_bytes(m) bytes.
+ * *out is owned by the caller (ff_ctx_destroy).
  * Errors: FF_E_NULL, FF_E_SHAPE, FF_E_DTYPE, FF_E_WORKSPACE, FF_E_RANGE. */
 ff_status ff_ctx_create(const ff_model_desc* m, const ff_layer_weights* layer_w,
                         const ff_global_weights* g, const ff_plan* p, void* cache,
@@ -318,6 +319,24 @@ ff_status ff_ctx_step_kinds(const ff_ctx* c, int32_t* kinds);
  * Errors: FF_E_NULL, FF_E_STATE (step out of order), FF_E_HIP. */
 ff_status ff_denoise_step(ff_ctx* c, int32_t step, float* x, const float* cond,
                           const void* txt, float* audit, ff_stream_t stream);
+
+/* ---------------------------------------------------------------- diagnostics
+ * Per-layer feature traces for mechanism studies on synthetic weights (the paper tracks
+ * the downstream relative-L1 error of corrected runs against Vanilla per layer and stage,
+ * Sec. 4).  ff_ctx_trace(c, buf, bytes): while buf is set, every ff_denoise_step copies the
+ * stream after each layer l (the [B, N, C] block output, text rows included) to
+ * buf + l * B*N*C*dtype-size, so after a step buf holds that step's L layer outputs; runs
+ * of drafted layers are then applied layer by layer (same values).  bytes must be at least
+ * L * B*N*C * dtype size; buf NULL stops tracing.  buf is device memory of the caller.
+ * Errors: FF_E_NULL (c), FF_E_WORKSPACE (bytes), FF_E_SHAPE (alignment). */
+ff_status ff_ctx_trace(ff_ctx* c, void* buf, size_t bytes);
+
+/* rel[b] = sum|a - b| / (sum|b| + eps) over sample b's N*C elements of two [B, N, C]
+ * dtype tensors (Eq. 4's form, with b as the reference; fp32, fixed-order sums, as the
+ * audit), rel a device fp32 [B] array.  ws: at least ff_workspace_bytes(m) bytes.
+ * Errors: FF_E_NULL, FF_E_RANGE (eps), FF_E_SHAPE, FF_E_WORKSPACE. */
+ff_status ff_rel_l1(const ff_model_desc* m, const void* a, const void* b, float eps, float* rel, void* ws,
+                    size_t ws_bytes, ff_stream_t stream);
 
 /* ---------------------------------------------------------------- profiling
  * Optional tracing of a context's launches (Sec. 4 reports latency per arm; this

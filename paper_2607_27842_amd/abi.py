@@ -30,8 +30,8 @@ FF_MAX_K, FF_MAX_SLOTS, FF_TEMB_DIM = 3, 8, 256
 EXPORTED = ("ff_abi_version", "ff_last_error", "ff_plan_build", "ff_plan_destroy", "ff_plan_export",
             "ff_cache_bytes", "ff_workspace_bytes", "ff_block_exact", "ff_cache_update",
             "ff_draft_forecast", "ff_verify_replace", "ff_ctx_create", "ff_ctx_destroy",
-            "ff_ctx_reset", "ff_get_counts", "ff_ctx_step_kinds", "ff_denoise_step", "ff_ctx_profile",
-            "ff_ctx_profile_read")
+            "ff_ctx_reset", "ff_get_counts", "ff_ctx_step_kinds", "ff_denoise_step", "ff_ctx_trace", "ff_rel_l1",
+            "ff_ctx_profile", "ff_ctx_profile_read")
 PROF_CLASSES = ("gemm", "attn", "norm", "gemv", "draft", "verify", "cache", "other")
 
 
@@ -120,6 +120,8 @@ def lib():
             "ff_ctx_reset": (i32, [vp]),
             "ff_get_counts": (i32, [vp, P(ff_counts)]),
             "ff_ctx_step_kinds": (i32, [vp, P(i32)]),
+            "ff_ctx_trace": (i32, [vp, vp, sz]),
+            "ff_rel_l1": (i32, [P(ff_model_desc), vp, vp, f32, vp, vp, sz, vp]),
             "ff_denoise_step": (i32, [vp, i32, vp, vp, vp, vp, vp]),
             "ff_ctx_profile": (i32, [vp, i32]),
             "ff_ctx_profile_read": (i32, [vp, P(ff_prof_stat)]),
@@ -242,6 +244,14 @@ def ff_ctx_step_kinds(ctx, T):
     out = (C.c_int32 * T)()
     check(lib().ff_ctx_step_kinds(ctx, out))
     return np.array(out[:], dtype=np.int32)
+
+
+def ff_ctx_trace(ctx, buf, nbytes):
+    return check(lib().ff_ctx_trace(ctx, buf, nbytes))
+
+
+def ff_rel_l1(model, a, b, eps, rel, ws, ws_bytes, stream=0):
+    return check(lib().ff_rel_l1(C.byref(model), a, b, eps, rel, ws, ws_bytes, stream))
 
 
 def ff_denoise_step(ctx, step, x, cond, txt, audit, stream=0):

@@ -537,6 +537,7 @@ struct ff_ctx {
   float* a_rel = nullptr;
   hipEvent_t a_ev = nullptr;
   bool a_checked = false;
+  void* trace = nullptr;   // per-layer stream copies (ff_ctx_trace), [L][B*N*C]
   ~ff_ctx() {
     if (a_ev) (void)hipEventDestroy(a_ev);
     if (a_rel) (void)hipHostFree(a_rel);
@@ -773,7 +774,8 @@ ff_status ff_ctx_create(const ff_model_desc* m, const ff_layer_weights* layer_w,
     Model md;
     ff_status e = check_model(m, &md);
     if (e) return e;
-    if (!layer_w || !g || !p || !cache || !ws) return fail(FF_E_NULL, "weights, plan, cache or ws is NULL");
+    const bool vanilla = p && p->s.mode == FF_VANILLA;   // Vanilla never touches the history
+    if (!layer_w || !g || !p || (!cache && !vanilla) || !ws) return fail(FF_E_NULL, "weights, plan, cache or ws is NULL");
     if (p->L != md.L) return fail(FF_E_SHAPE, "plan has %d layers, model %d", p->L, md.L);
     for (int l = 0; l < md.L; ++l) {
       e = check_layer_weights(&layer_w[l], md.kinds[l], l);
@@ -782,11 +784,11 @@ ff_status ff_ctx_create(const ff_model_desc* m, const ff_layer_weights* layer_w,
     if (!g->t1_w || !g->t1_b || !g->t2_w || !g->t2_b || !g->pe_w || !g->pe_b || !g->fmod_w || !g->fmod_b ||
         !g->f_w || !g->f_b)
       return fail(FF_E_NULL, "a global weight pointer is NULL");
-    const size_t need_cache = (size_t)md.L * p->s.S * md.E() * md.es();
+    const size_t need_cache = vanilla ? 0 : (size_t)md.L * p->s.S * md.E() * md.es();
     if (cache_bytes < need_cache) return fail(FF_E_WORKSPACE, "cache %zu < %zu bytes", cache_bytes, need_cache);
     const Ws L = ws_layout(md);
     if (ws_bytes < L.total) return fail(FF_E_WORKSPACE, "workspace %zu < %zu bytes", ws_bytes, L.total);
-    if (!aligned16(cache) || !aligned16(ws)) return fail(FF_E_SHAPE, "cache and ws must be 16-byte aligned");
+    if ((cache && !aligned16(cache)) || !aligned16(ws)) return fail(FF_E_SHAPE, "cache and ws must be 16-byte aligned");
     ff_ctx* c = new ff_ctx();
     c->m = md;
     c->lw.assign(layer_w, layer_w + md.L);
@@ -960,6 +962,12 @@ ff_status ff_denoise_step(ff_ctx* c, int32_t step, float* x, const float* cond, 
     // layers by the plan
     const int mode = s.mode;
     const bool resid = s.feature_mode == FF_RESIDUAL;
+    // with a trace buffer, the stream after layer l (in cur) is copied to its slot
+    auto trace_to = [&](int l) -> ff_status {
+      if (c->trace)
+        HIP_TRY(hipMemcpyAsync((char*)c->trace + (size_t)l * tb, cur, tb, hipMemcpyDeviceToDevice, st), "trace copy");
+      return FF_OK;
+    };
     for (int l = 0; l < L; ++l) {
       const int act = p.action[(size_t)i * L + l];
       if (act == FF_ACT_EXACT) {
@@ -972,6 +980,7 @@ ff_status ff_denoise_step(ff_ctx* c, int32_t step, float* x, const float* cond, 
         if (e) return e;
         if (dst && !fuse) HIP_TRY(ex.cache(dst, resid ? cur : nullptr, alt, E), "cache update");
         void* t = cur; cur = alt; alt = t;
+        if (ff_status te = trace_to(l)) return te;
         continue;
       }
       if (act == FF_ACT_RECOMPUTE) {   // the recompute arm: the exact block, no history refresh
@@ -980,6 +989,7 @@ ff_status ff_denoise_step(ff_ctx* c, int32_t step, float* x, const float* cond, 
         e = exec_block(m, m.kinds[l], c->lw[l], cs, cur, alt, ws, ex, mod_of[l]);
         if (e) return e;
         void* t = cur; cur = alt; alt = t;
+        if (ff_status te = trace_to(l)) return te;
         continue;
       }
       if (act == FF_ACT_SITE && mode == FF_EXACT_ONLY) {
@@ -988,6 +998,7 @@ ff_status ff_denoise_step(ff_ctx* c, int32_t step, float* x, const float* cond, 
         e = exec_block(m, m.kinds[l], c->lw[l], cs, cur, alt, ws, ex, mod_of[l]);
         if (e) return e;
         void* t = cur; cur = alt; alt = t;
+        if (ff_status te = trace_to(l)) return te;
         continue;
       }
       Terms tm{};
@@ -998,12 +1009,14 @@ ff_status ff_denoise_step(ff_ctx* c, int32_t step, float* x, const float* cond, 
         tm.c[q] = p.coeffs[(size_t)i * (K + 1) + q];
       }
       if (act == FF_ACT_DRAFT) {
-        // the maximal run of drafted layers starting here, applied in one pass (same bits)
+        // the maximal run of drafted layers starting here, applied in one pass (same bits);
+        // layer by layer while tracing
         int l2 = l + 1;
-        while (l2 < L && p.action[(size_t)i * L + l2] == FF_ACT_DRAFT) ++l2;
+        while (!c->trace && l2 < L && p.action[(size_t)i * L + l2] == FF_ACT_DRAFT) ++l2;
         if (l2 - l == 1) HIP_TRY(ex.draft(tm, resid ? cur : nullptr, cur, E), "draft");
         else HIP_TRY(ex.draft_run(tm, l2 - l, (size_t)S * E, resid, cur, E), "draft run");
         l = l2 - 1;
+        if (ff_status te = trace_to(l)) return te;
         continue;
       }
       // paid site: exact output from the same incoming state, then verify + forward
@@ -1020,6 +1033,7 @@ ff_status ff_denoise_step(ff_ctx* c, int32_t step, float* x, const float* cond, 
                        s.part_stride, C};
       HIP_TRY(ex.verify(tm, resid ? cur : nullptr, hf, cur, fw, m.B, (size_t)m.N * C, s.eps,
                         rel, at<float>(ws, W.PART)), "verify");
+      if (ff_status te = trace_to(l)) return te;
     }
     // final layer on the image rows, unpatchify and Euler
     float* mod = at<float>(ws, W.MOD);
@@ -1070,6 +1084,37 @@ ff_status ff_denoise_step(ff_ctx* c, int32_t step, float* x, const float* cond, 
       }
     }
     c->next_step++;
+    return ok();
+  } catch (...) {
+    return fail(FF_E_UNSUPPORTED, "unexpected host exception");
+  }
+}
+
+ff_status ff_ctx_trace(ff_ctx* c, void* buf, size_t bytes) {
+  if (!c) return fail(FF_E_NULL, "ctx is NULL");
+  if (buf) {
+    const size_t need = (size_t)c->m.L * c->m.E() * c->m.es();
+    if (bytes < need) return fail(FF_E_WORKSPACE, "trace buffer %zu < %zu bytes", bytes, need);
+    if (!aligned16(buf)) return fail(FF_E_SHAPE, "trace buffer must be 16-byte aligned");
+  }
+  c->trace = buf;
+  return ok();
+}
+
+ff_status ff_rel_l1(const ff_model_desc* m, const void* a, const void* b, float eps, float* rel, void* ws,
+                    size_t ws_bytes, ff_stream_t stream) {
+  try {
+    Model md;
+    ff_status e = check_model(m, &md);
+    if (e) return e;
+    if (!a || !b || !rel || !ws) return fail(FF_E_NULL, "a, b, rel or ws is NULL");
+    if (!(eps > 0.f)) return fail(FF_E_RANGE, "eps must be > 0");
+    const Ws L = ws_layout(md);
+    if (ws_bytes < L.total) return fail(FF_E_WORKSPACE, "workspace %zu < %zu bytes", ws_bytes, L.total);
+    if (!aligned16(a) || !aligned16(b) || !aligned16(rel) || !aligned16(ws))
+      return fail(FF_E_SHAPE, "pointers must be 16-byte aligned");
+    HIP_TRY(ff::rel_l1(md.dtype, a, b, md.B, (size_t)md.N * md.C, eps, rel, at<float>(ws, L.PART),
+                       reinterpret_cast<hipStream_t>(stream)), "rel_l1");
     return ok();
   } catch (...) {
     return fail(FF_E_UNSUPPORTED, "unexpected host exception");

@@ -162,6 +162,34 @@ __global__ __launch_bounds__(kThreads) void k_verify(Terms t, const void* u, con
   }
 }
 
+// First stage of the rel-L1 distance of two tensors (the audit's reduction without a
+// draft): per block, sum |a - b| and |b| over its share of one sample.
+template <int DT>
+__global__ __launch_bounds__(kThreads) void k_rel_partials(const void* __restrict__ a, const void* __restrict__ b,
+                                                           size_t chunks_per_sample, float* __restrict__ partials) {
+  using S = St<DT>;
+  const int smp = blockIdx.y;
+  const size_t base = (size_t)smp * chunks_per_sample * S::V;
+  float num = 0.f, den = 0.f;
+  for (size_t c = (size_t)blockIdx.x * kThreads + threadIdx.x; c < chunks_per_sample;
+       c += (size_t)gridDim.x * kThreads) {
+    float x[S::V], y[S::V];
+    S::load(a, base + c * S::V, x);
+    S::load(b, base + c * S::V, y);
+#pragma unroll
+    for (int j = 0; j < S::V; ++j) {
+      num += fabsf(x[j] - y[j]);
+      den += fabsf(y[j]);
+    }
+  }
+  block_sum2(num, den);
+  if (threadIdx.x == 0) {
+    float* p = partials + ((size_t)smp * gridDim.x + blockIdx.x) * 2;
+    p[0] = num;
+    p[1] = den;
+  }
+}
+
 // Second stage: per sample, sum the partials in index order and form Eq. 4.
 __global__ __launch_bounds__(kThreads) void k_verify_finish(const float* __restrict__ partials, int nblk,
                                                             float eps, float* __restrict__ rel) {
@@ -254,6 +282,21 @@ hipError_t verify(int dtype, const Terms& t, const void* u, const void* hf, void
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   if (rel_l1) FF_LAUNCH(k_verify_finish, dim3(B), kThreads, 0, s, partials, nblk, eps, rel_l1);
+  return hipGetLastError();
+}
+
+hipError_t rel_l1(int dtype, const void* a, const void* b, int B, size_t Eb, float eps, float* rel, float* partials,
+                  hipStream_t s) {
+  const int V = dtype == DT_BF16 ? 8 : 4;
+  const size_t cps = Eb / V;
+  int nblk = cdiv((long)cps, kThreads);
+  if (nblk > kMaxVerifyBlocks) nblk = kMaxVerifyBlocks;
+  if (nblk < 1) nblk = 1;
+  if (dtype == DT_BF16) FF_LAUNCH(k_rel_partials<DT_BF16>, dim3(nblk, B), kThreads, 0, s, a, b, cps, partials);
+  else FF_LAUNCH(k_rel_partials<DT_F32>, dim3(nblk, B), kThreads, 0, s, a, b, cps, partials);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  FF_LAUNCH(k_verify_finish, dim3(B), kThreads, 0, s, partials, nblk, eps, rel);
   return hipGetLastError();
 }
 

@@ -144,6 +144,10 @@ struct Forward { int kind, stride, C; };
 size_t verify_partials_floats(int B);
 hipError_t verify(int dtype, const Terms& t, const void* u, const void* hf, void* hout, const Forward& fw,
                   int B, size_t Eb, float eps, float* rel_l1, float* partials, hipStream_t s);
+// rel[b] = sum|a - b| / (sum|b| + eps) over sample b's Eb elements (the audit's fixed-order
+// two-stage reduction; partials as for verify)
+hipError_t rel_l1(int dtype, const void* a, const void* b, int B, size_t Eb, float eps, float* rel, float* partials,
+                  hipStream_t s);
 
 // ---------------------------------------------------------------- small per-step kernels
 // phi[k] = cos(s f_k), phi[128 + k] = sin(s f_k), f_k = exp(-ln(1e4) k / 128), in fp64.

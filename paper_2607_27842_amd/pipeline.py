@@ -131,7 +131,8 @@ class Runner:
         self.sched = abi.ff_sched_desc(self.T, self.R, self.K, self.S, cfg["rel_eps"] if eps is None else eps,
                                        mode, feature_mode, tau, part_stride)
         self.plan = abi.ff_plan_build(self.sched, self.L, np.asarray(mask, np.uint8).reshape(-1))
-        self.cache_bytes = abi.ff_cache_bytes(dm.desc, self.S)
+        # Vanilla never reads or writes the history: it gets no cache
+        self.cache_bytes = 0 if mode == abi.FF_VANILLA else abi.ff_cache_bytes(dm.desc, self.S)
         self.ws_bytes = abi.ff_workspace_bytes(dm.desc)
         self.cache = torch.empty(max(self.cache_bytes, 256), dtype=torch.uint8, device=device)
         self.ws = torch.empty(self.ws_bytes, dtype=torch.uint8, device=device)
@@ -154,6 +155,11 @@ class Runner:
         abi.ff_denoise_step(self.ctx, i, x.data_ptr(), cond.data_ptr(),
                             None if txt is None else txt.data_ptr(),
                             None if audit is None else audit.data_ptr(), s)
+
+    def trace_into(self, buf):
+        """Copy the stream after every layer of each step into buf ([L, B*N*C] model dtype
+        tensor, or None to stop)."""
+        abi.ff_ctx_trace(self.ctx, None if buf is None else buf.data_ptr(), 0 if buf is None else buf.numel() * buf.element_size())
 
     def step_kinds(self):
         """Realised kind of each step of the current run (-1 for steps not run yet)."""

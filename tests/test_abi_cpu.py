@@ -211,6 +211,17 @@ def test_context_state_errors_are_host_side():
     assert Lb.ff_denoise_step(ctx, 1, 1 << 31, 3 << 30, None, None, None) == abi.FF_E_STATE
     assert Lb.ff_denoise_step(ctx, 0, None, 3 << 30, None, None, None) == abi.FF_E_NULL
     assert abi.ff_get_counts(ctx) == {"n_full_refresh": 0, "n_paid_checks": 0, "n_forwarded": 0, "n_recomputed": 0}
+    # per-layer traces: the buffer must hold L layer outputs and be aligned
+    need = L * m.B * (m.n_img + m.n_txt) * m.C * 4
+    assert Lb.ff_ctx_trace(None, 1 << 30, need) == abi.FF_E_NULL
+    assert Lb.ff_ctx_trace(ctx, 1 << 30, need - 1) == abi.FF_E_WORKSPACE
+    assert Lb.ff_ctx_trace(ctx, (1 << 30) + 4, need) == abi.FF_E_SHAPE
+    assert Lb.ff_ctx_trace(ctx, 1 << 30, need) == abi.FF_OK
+    assert Lb.ff_ctx_trace(ctx, None, 0) == abi.FF_OK
+    # rel-L1 distance: checked on the host
+    assert Lb.ff_rel_l1(C.byref(m), None, 1 << 30, C.c_float(1e-8), 1 << 29, 2 << 30, wb, None) == abi.FF_E_NULL
+    assert Lb.ff_rel_l1(C.byref(m), 1 << 28, 1 << 30, C.c_float(0.0), 1 << 29, 2 << 30, wb, None) == abi.FF_E_RANGE
+    assert Lb.ff_rel_l1(C.byref(m), 1 << 28, 1 << 30, C.c_float(1e-8), 1 << 29, 2 << 30, wb - 1, None) == abi.FF_E_WORKSPACE
     abi.ff_ctx_reset(ctx)
     abi.ff_ctx_destroy(ctx)
     abi.ff_plan_destroy(plan)
