@@ -15,7 +15,8 @@ forecast, sites at layers 13 and 27 on every cached step.  The FLUX-like shape (
 the adaptive (discrepancy-triggered) refresh policy and the DiT-XL/2 matched-compute arms
 (token- / channel-partial forwarding at stride 2, whole-timestep recompute) are reported
 alongside, with a FLUX-like resolution sweep (512^2 to 1024^2: latency and peak memory)
-and a DiT-XL/2 shadow-Vanilla diagnostic (per-layer rel-L1 of FeatFix and Verify).
+a DiT-XL/2 shadow-Vanilla diagnostic (per-layer rel-L1 of FeatFix and Verify) and the
+FLUX-like FeatFix loop with rotary embedding.
 
 Prints ONE JSON line.
 """
@@ -286,6 +287,30 @@ def shadow_vanilla(name="dit_xl2"):
     return out
 
 
+def rope_loop():
+    """The FLUX-like FeatFix loop with rotary embedding of q and k (axes 16 / 56 / 56 of the
+    128 head dims, theta 1e4; text rows at position 0, image rows at their (frame, row,
+    column)): one untimed loop, then one timed 50-step loop."""
+    import torch
+    import synth
+    from paper_2607_27842_amd import pipeline
+    cfg = synth.get_config("flux", rope_axes=(16, 56, 56), rope_theta=10000.0)
+    dm = pipeline.DeviceModel.random(cfg, seed=0)
+    x0, cond, txt = device_inputs(cfg)
+    r = pipeline.Runner(dm, synth.MODE_NAMES["featfix"], synth.site_mask(cfg))
+    loop = Loop(r, x0, cond, txt)
+    for _ in range(r.T):
+        loop.step()
+    loop.pos = 0
+    ms = timed_steps(loop, r.T)
+    r.close()
+    del loop, r, dm
+    torch.cuda.empty_cache()
+    out = {"rope_axes": [16, 56, 56], "steps": cfg["T"], "ms": round(ms, 3), "steps_per_s": round(cfg["T"] / (ms / 1e3), 2)}
+    log(f"[bench] flux featfix with rope: {out['steps_per_s']} steps/s")
+    return out
+
+
 def resolution_sweep(sides=(512, 768, 1024)):
     """FLUX-like loop latency and peak device memory from 512^2 to 1024^2 images (latent
     side / 8, patch 2: 1024, 2304 and 4096 image tokens + 512 text tokens), FeatFix and
@@ -433,6 +458,7 @@ def main():
         flux["kernels"] = kernel_table(fk)
         if "vanilla" in flux:
             flux["featfix_over_vanilla"] = round(flux["featfix"]["steps_per_s"] / flux["vanilla"]["steps_per_s"], 3)
+        flux["featfix_rope"] = rope_loop()
         extra["flux"] = flux
     if name == "dit_xl2" and not args.no_flux and not args.no_sweep:
         extra["flux_resolution_sweep"] = resolution_sweep()

@@ -81,7 +81,13 @@ typedef struct ihipStream_t* ff_stream_t;
  * set, fused attention+MLP input projection).  FF_DIT requires n_txt == 0.
  * Requirements: C == H*d, d in [8, 128] and d % 8 == 0, C % 8 == 0, mlp_hidden % 8 == 0,
  * 1 <= B, lat_f % pt == lat_h % ph == lat_w % pw == 0,
- * n_img == (lat_f/pt)*(lat_h/ph)*(lat_w/pw), (pt*ph*pw*lat_c) % 8 == 0. */
+ * n_img == (lat_f/pt)*(lat_h/ph)*(lat_w/pw), (pt*ph*pw*lat_c) % 8 == 0.
+ * rope_axes: all 0 for no rotary embedding; otherwise even dims summing to d.  The MMDiT
+ * blocks then rotate q and k after their RMSNorms: the head dims are split into chunks of
+ * rope_axes[0..2] dims and in chunk a the pair (2i, 2i+1) of a row is turned by
+ * pos_a * rope_theta^(-2i / rope_axes[a]), where pos = (0, 0, 0) for text rows and
+ * (frame, row, column) of the patch in the (lat_f/pt, lat_h/ph, lat_w/pw) grid for image
+ * rows (FLUX-style 3-axis ids).  rope_theta > 1 when enabled. */
 typedef struct {
   int32_t n_layers;
   const int32_t* kinds;   /* host array [n_layers]; copied where it is kept */
@@ -91,6 +97,8 @@ typedef struct {
   int32_t pt, ph, pw;
   int32_t dtype;
   float ln_eps;           /* LayerNorm / RMSNorm epsilon */
+  int32_t rope_axes[3];
+  float rope_theta;
 } ff_model_desc;
 
 /* One stream's weights of one block (device pointers, model dtype, [out, in]).

@@ -40,7 +40,7 @@ __all__ = [
     "FORWARDING_MODES", "RESIDUAL", "OUTPUT", "REFRESH_STEP", "CACHED_STEP", "EXACT",
     "DRAFT_ACT", "SITE", "RECOMPUTE_ACT", "forward_partial", "round_bf16", "silu", "gelu_tanh", "layer_norm", "rms_norm",
     "softmax", "attention", "timestep_embedding", "conditioning", "patchify", "unpatchify",
-    "dit_block", "double_block", "single_block", "block", "final_layer", "make_plan",
+    "dit_block", "double_block", "single_block", "block", "rope", "rope_positions", "final_layer", "make_plan",
     "TaylorCache", "rel_l1", "run", "max_rel_err", "block_flops",
 ]
 
@@ -197,6 +197,51 @@ def dit_block(u, cs, W, cfg, rows=None):
     return x1 + g2 * _linear(gelu_tanh(_linear(m, W["fc1_w"], W["fc1_b"])), W["fc2_w"], W["fc2_b"])
 
 
+def rope_positions(cfg):
+    """Position ids [N, 3] of a sample's rows for rotary embedding (FLUX-style 3-axis ids;
+    reading where the configs are silent): (0, 0, 0) for text rows, (frame, row, column)
+    of the image row's patch in the (F/pt, H/ph, W/pw) grid."""
+    _, F, Hh, Wd = cfg["lat"]
+    pt, ph, pw = cfg["patch"]
+    Fp, Hp, Wp = F // pt, Hh // ph, Wd // pw
+    nt = cfg["n_txt"]
+    pos = np.zeros((nt + Fp * Hp * Wp, 3))
+    t = np.arange(Fp * Hp * Wp)
+    pos[nt:, 0] = t // (Hp * Wp)
+    pos[nt:, 1] = (t // Wp) % Hp
+    pos[nt:, 2] = t % Wp
+    return pos
+
+
+def rope(x, pos, axes, theta):
+    """Rotary position embedding of per-head vectors x [B, H, N, d]: the d dims are split
+    into consecutive chunks of axes[0], axes[1], axes[2] dims; in chunk a the pair
+    (2i, 2i+1) is turned by the angle pos[n, a] * theta^(-2i / axes[a])."""
+    out = np.array(x, dtype=np.float64, copy=True)
+    start = 0
+    for a, da in enumerate(axes):
+        if da == 0:
+            continue
+        i = np.arange(da // 2)
+        ang = pos[:, a][:, None] * (float(theta) ** (-2.0 * i / da))[None, :]   # [N, da/2]
+        c, sn = np.cos(ang), np.sin(ang)
+        x0, x1 = x[..., start + 2 * i], x[..., start + 2 * i + 1]
+        out[..., start + 2 * i] = x0 * c - x1 * sn
+        out[..., start + 2 * i + 1] = x0 * sn + x1 * c
+        start += da
+    return out
+
+
+def _qk_rope(q, k, cfg):
+    """q, k after their RMS norms, rotated when the model has rotary axes (rope_axes)."""
+    axes = cfg.get("rope_axes", (0, 0, 0))
+    if not sum(axes):
+        return q, k
+    pos = rope_positions(cfg)
+    th = cfg.get("rope_theta", 10000.0)
+    return rope(q, pos, axes, th), rope(k, pos, axes, th)
+
+
 def double_block(u, cs, W, cfg, rows=None):
     """MMDiT double-stream block (SD3 / FLUX style): text rows [0, n_txt) and image rows
     [n_txt, N) of each sample carry their own DiT weight sets; q and k are RMS-normalised
@@ -218,8 +263,7 @@ def double_block(u, cs, W, cfg, rows=None):
         qs.append(rms_norm(_heads(qkv[..., :C], H), _f64(Ws["q_g"]), eps))
         ks.append(rms_norm(_heads(qkv[..., C:2 * C], H), _f64(Ws["k_g"]), eps))
         vs.append(_heads(qkv[..., 2 * C:], H))
-    q = np.concatenate(qs, axis=2)
-    k = np.concatenate(ks, axis=2)
+    q, k = _qk_rope(np.concatenate(qs, axis=2), np.concatenate(ks, axis=2), cfg)
     v = np.concatenate(vs, axis=2)
     att = _merge(attention(q[:, :, r], k, v))          # [B, len(r), C]
     out = np.empty((u.shape[0], len(r), C), dtype=np.float64)
@@ -247,8 +291,8 @@ def single_block(u, cs, W, cfg, rows=None):
     a_, b_, g_ = [m[:, None, :] for m in np.split(mod, 3, axis=-1)]
     a = layer_norm(u, eps) * (1.0 + b_) + a_
     y = _linear(a, W["lin1_w"], W["lin1_b"])
-    q = rms_norm(_heads(y[..., :C], H), _f64(W["q_g"]), eps)
-    k = rms_norm(_heads(y[..., C:2 * C], H), _f64(W["k_g"]), eps)
+    q, k = _qk_rope(rms_norm(_heads(y[..., :C], H), _f64(W["q_g"]), eps),
+                    rms_norm(_heads(y[..., C:2 * C], H), _f64(W["k_g"]), eps), cfg)
     v = _heads(y[..., 2 * C:3 * C], H)
     att = _merge(attention(q[:, :, r], k, v))
     z = gelu_tanh(y[:, r, 3 * C:])

@@ -41,7 +41,7 @@ class ff_model_desc(C.Structure):
                 ("n_img", C.c_int32), ("n_txt", C.c_int32), ("B", C.c_int32),
                 ("lat_c", C.c_int32), ("lat_f", C.c_int32), ("lat_h", C.c_int32), ("lat_w", C.c_int32),
                 ("pt", C.c_int32), ("ph", C.c_int32), ("pw", C.c_int32),
-                ("dtype", C.c_int32), ("ln_eps", C.c_float)]
+                ("dtype", C.c_int32), ("ln_eps", C.c_float), ("rope_axes", C.c_int32 * 3), ("rope_theta", C.c_float)]
 
 
 _STREAM_FIELDS = ("mod_w", "mod_b", "qkv_w", "qkv_b", "o_w", "o_b", "fc1_w", "fc1_b", "fc2_w", "fc2_b",

@@ -56,12 +56,25 @@ struct Model {
   int lat_c = 0, lat_f = 0, lat_h = 0, lat_w = 0, pt = 0, ph = 0, pw = 0;
   int dtype = 0;
   float ln_eps = 0.f;
+  int rope[3] = {0, 0, 0};
+  float rope_theta = 0.f;
   bool any_single = false;
   size_t es() const { return dsize(dtype); }
   size_t E() const { return (size_t)B * N * C; }
 };
 
 bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
+
+// the rotary embedding of the q / k norm kernel (axes 0: none)
+Rope rope_of(const Model& m) {
+  Rope r{};
+  for (int a = 0; a < 3; ++a) r.axes[a] = m.rope[a];
+  r.log2_theta = m.rope[0] + m.rope[1] + m.rope[2] ? log2f(m.rope_theta) : 0.f;
+  r.n_txt = m.n_txt;
+  r.Hp = m.lat_h / m.ph;
+  r.Wp = m.lat_w / m.pw;
+  return r;
+}
 
 ff_status check_model(const ff_model_desc* m, Model* out) {
   if (!m) return fail(FF_E_NULL, "model descriptor is NULL");
@@ -98,6 +111,15 @@ ff_status check_model(const ff_model_desc* m, Model* out) {
   if (nimg != r.n_img) return fail(FF_E_SHAPE, "n_img=%d but the latent has %ld patches", r.n_img, nimg);
   r.P = r.pt * r.ph * r.pw * r.lat_c;
   if (r.P % 8) return fail(FF_E_SHAPE, "patch features %d must be a multiple of 8", r.P);
+  const int rsum = m->rope_axes[0] + m->rope_axes[1] + m->rope_axes[2];
+  if (rsum != 0) {
+    for (int a = 0; a < 3; ++a)
+      if (m->rope_axes[a] < 0 || m->rope_axes[a] % 2) return fail(FF_E_SHAPE, "rope_axes must be even and >= 0");
+    if (rsum != r.d) return fail(FF_E_SHAPE, "rope_axes sum to %d, head dim is %d", rsum, r.d);
+    if (!(m->rope_theta > 1.f) || !std::isfinite(m->rope_theta)) return fail(FF_E_RANGE, "rope_theta must be > 1");
+    for (int a = 0; a < 3; ++a) r.rope[a] = m->rope_axes[a];
+    r.rope_theta = m->rope_theta;
+  }
   r.N = r.n_img + r.n_txt;
   if ((long)r.B * r.N > (1L << 30) / 8) return fail(FF_E_SHAPE, "too many rows");
   if (!(r.ln_eps > 0.f)) return fail(FF_E_RANGE, "ln_eps must be > 0");
@@ -334,7 +356,7 @@ ff_status exec_block(const Model& m, int kind, const ff_layer_weights& w, const 
                             offset_rows(s.lin1_b, 3 * (size_t)C, 1, es), rows, Mh, C, EPI_BIAS_GELU,
                             at(att, (size_t)C * es), ldy, all);
     HIP_TRY(ex.gemm2(g1, g2), "single: lin1");
-    RmsQKArgs rn{qkv, 3 * C, all, rows, m.H, m.d, s.q_g, s.k_g, m.ln_eps};
+    RmsQKArgs rn{qkv, 3 * C, all, rows, m.H, m.d, s.q_g, s.k_g, m.ln_eps, rope_of(m)};
     HIP_TRY(ex.rms_qk(rn), "single: q/k norm");
     aa.out = att; aa.ldo = ldy;
     HIP_TRY(ex.attention(aa), "single: attention");
@@ -391,7 +413,7 @@ ff_status exec_block(const Model& m, int kind, const ff_layer_weights& w, const 
     for (int si = 0; si < nstreams; ++si) {
       const int rows = m.B * nseg[si];
       if (rows == 0) continue;
-      RmsQKArgs rn{qkv, 3 * C, maps[si], rows, m.H, m.d, w.s[si].q_g, w.s[si].k_g, m.ln_eps};
+      RmsQKArgs rn{qkv, 3 * C, maps[si], rows, m.H, m.d, w.s[si].q_g, w.s[si].k_g, m.ln_eps, rope_of(m)};
       HIP_TRY(ex.rms_qk(rn), "double: q/k norm");
     }
   }

@@ -152,6 +152,26 @@ __global__ __launch_bounds__(256) void k_rms_qk(RmsQKArgs a) {
   const void* g = qk ? a.gk : a.gq;
 #pragma unroll
   for (int j = 0; j < S::V; ++j) v[j] = v[j] * inv * S::ld1(g, e + j);
+  const Rope& ro = a.rope;
+  if (ro.axes[0] + ro.axes[1] + ro.axes[2]) {
+    // the row's token n within its sample; image rows carry (frame, row, column) ids
+    const int n = a.map.off + (int)(r % a.map.n_seg);
+    if (n >= ro.n_txt) {
+      const int t = n - ro.n_txt;
+      const float pos[3] = {(float)(t / (ro.Hp * ro.Wp)), (float)((t / ro.Wp) % ro.Hp), (float)(t % ro.Wp)};
+#pragma unroll
+      for (int j = 0; j < S::V; j += 2) {   // e + j is even: a lane holds whole pairs
+        int p = e + j, ax = 0;
+        if (p >= ro.axes[0]) { p -= ro.axes[0]; ax = 1; if (p >= ro.axes[1]) { p -= ro.axes[1]; ax = 2; } }
+        const float w = exp2f(-(float)p / (float)ro.axes[ax] * ro.log2_theta);   // theta^(-2i/da), p = 2i
+        float sn, cs;
+        sincosf(pos[ax] * w, &sn, &cs);
+        const float x0 = v[j], x1 = v[j + 1];
+        v[j] = x0 * cs - x1 * sn;
+        v[j + 1] = x0 * sn + x1 * cs;
+      }
+    }
+  }
   S::store(a.x, base + col, v);
 }
 

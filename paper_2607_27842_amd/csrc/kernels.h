@@ -101,11 +101,20 @@ struct RmsArgs {
   const void* g; float eps;
 };
 hipError_t rms_heads(int dtype, const RmsArgs& a, hipStream_t s);
+// Rotary embedding applied after the q / k norms: head dims split into chunks of axes[a]
+// (all 0: none); the pair (2i, 2i+1) of chunk a turns by pos_a * theta^(-2i / axes[a]),
+// pos = (0, 0, 0) for rows n < n_txt of a sample, else (frame, row, column) of image row
+// t = n - n_txt in a (., Hp, Wp) patch grid.
+struct Rope {
+  int axes[3]; float log2_theta;
+  int n_txt, Hp, Wp;
+};
 // Both per-head RMSNorms of a qkv row block: q at columns [0, H*d) with gain gq, k at
-// [H*d, 2*H*d) with gain gk (in place).
+// [H*d, 2*H*d) with gain gk (in place), then the rotary embedding of q and k.
 struct RmsQKArgs {
   void* x; int ld; RowMap map; int rows, H, d;
   const void* gq; const void* gk; float eps;
+  Rope rope;
 };
 hipError_t rms_qk(int dtype, const RmsQKArgs& a, hipStream_t s);
 

@@ -28,7 +28,8 @@ def model_desc(cfg):
     c_lat, F, H, W = cfg["lat"]
     pt, ph, pw = cfg["patch"]
     m = abi.ff_model_desc(len(cfg["kinds"]), kinds, cfg["C"], cfg["H"], cfg["d"], cfg["mlp"], cfg["n_img"],
-                          cfg["n_txt"], cfg["B"], c_lat, F, H, W, pt, ph, pw, cfg["dtype"], cfg["ln_eps"])
+                          cfg["n_txt"], cfg["B"], c_lat, F, H, W, pt, ph, pw, cfg["dtype"], cfg["ln_eps"],
+                          (C.c_int32 * 3)(*cfg.get("rope_axes", (0, 0, 0))), cfg.get("rope_theta", 10000.0))
     m._kinds = kinds
     return m
 

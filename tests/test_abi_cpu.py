@@ -237,3 +237,16 @@ def test_text_rows_required_for_mmdit():
     assert abi.lib().ff_denoise_step(ctx, 0, 1 << 31, 3 << 30, None, None, None) == abi.FF_E_NULL
     abi.ff_ctx_destroy(ctx)
     abi.ff_plan_destroy(plan)
+
+
+def test_rope_descriptor_checks():
+    """Rotary axes must be even and sum to the head dim, theta > 1 and finite (checked before
+    anything else of a call)."""
+    import math
+    for axes, theta, code in (((3, 30, 31), 1e4, abi.FF_E_SHAPE), ((16, 24, 16), 1e4, abi.FF_E_SHAPE),
+                              ((16, 24, 24), 1.0, abi.FF_E_RANGE), ((16, 24, 24), math.inf, abi.FF_E_RANGE),
+                              ((16, 24, 24), 1e4, abi.FF_E_NULL), ((0, 0, 0), 0.0, abi.FF_E_NULL)):
+        cfg = synth.get_config("tiny", rope_axes=axes, rope_theta=theta)
+        m = pipeline.model_desc(cfg)
+        got = abi.lib().ff_block_exact(C.byref(m), 0, None, None, None, None, None, 0, None)
+        assert got == code, (axes, theta, got)

@@ -171,3 +171,26 @@ def test_dit_block_narrow_tiles():
     W = boosted(synth.make_layer_weights(cfg, 0, bias_std=0.02, gain_std=0.1), synth.DIT)
     say("dit block C=1152 d=72 N=255 B=2")
     check_block(cfg, W)
+
+
+@pytest.mark.parametrize("dtype", [synth.F32, synth.BF16])
+@pytest.mark.parametrize("kind", [synth.MMDIT_DOUBLE, synth.MMDIT_SINGLE])
+def test_mmdit_blocks_rope(dtype, kind):
+    """Rotary embedding of q and k (3-axis ids: text rows 0, image rows (frame, row,
+    column)) on a two-frame latent with ragged text and image rows."""
+    need_gpu()
+    cfg = ragged_cfg(kind, dtype, d=64, H=3, n_txt=13, lat=(4, 2, 18, 22))
+    cfg["rope_axes"], cfg["rope_theta"] = (16, 24, 24), 10000.0
+    W = boosted(synth.make_layer_weights(cfg, 0, bias_std=0.02, gain_std=0.2), kind)
+    say(f"mmdit rope kind={kind} dtype={dtype}")
+    check_block(cfg, W, seed=kind)
+
+
+@pytest.mark.parametrize("kind", [synth.MMDIT_SINGLE, synth.MMDIT_DOUBLE])
+def test_flux_block_rope_full_shape_sampled_rows(kind):
+    need_gpu()
+    cfg = synth.get_config("flux", kinds=[kind])
+    cfg["rope_axes"], cfg["rope_theta"] = (16, 56, 56), 10000.0
+    W = synth.make_layer_weights(cfg, 0, bias_std=0.02, gain_std=0.1)
+    say(f"flux rope full block kind={kind} (sampled rows)")
+    check_block(cfg, W, rows=np.array(SAMPLE_ROWS["flux"]))

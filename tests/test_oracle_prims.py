@@ -156,3 +156,53 @@ def test_rel_l1_brute_force():
         den = sum(abs(float(hf[b].flat[i])) for i in range(20))
         assert abs(got[b] - num / (den + 1e-8)) <= 1e-14
     assert np.all(O.rel_l1(hf, hf, 1e-8) == 0.0)
+
+
+# ----------------------------------------------------------------------------- rotary embedding
+
+def _rope_x(B=2, H=3, N=7, d=16, seed=3):
+    return np.random.default_rng(seed).standard_normal((B, H, N, d))
+
+
+def test_rope_position_zero_is_identity():
+    x = _rope_x()
+    assert np.array_equal(O.rope(x, np.zeros((7, 3)), (4, 6, 6), 10000.0), x)
+
+
+def test_rope_keeps_pair_norms_and_is_a_rotation_by_pos():
+    # one pair per axis chunk of 2 dims: the angle is pos * theta^0 = pos radians
+    x = np.zeros((1, 1, 1, 6))
+    x[..., 0], x[..., 2], x[..., 4] = 1.0, 2.0, 3.0
+    pos = np.array([[1.0, 2.0, 3.0]])
+    y = O.rope(x, pos, (2, 2, 2), 10000.0)
+    np.testing.assert_allclose(y[0, 0, 0], [np.cos(1), np.sin(1), 2 * np.cos(2), 2 * np.sin(2),
+                                            3 * np.cos(3), 3 * np.sin(3)], rtol=0, atol=1e-15)
+    x = _rope_x(d=16)
+    pos = np.random.default_rng(4).integers(0, 40, (7, 3)).astype(float)
+    y = O.rope(x, pos, (4, 6, 6), 10000.0)
+    np.testing.assert_allclose(np.hypot(y[..., 0::2], y[..., 1::2]), np.hypot(x[..., 0::2], x[..., 1::2]),
+                               rtol=1e-12)
+
+
+def test_rope_scores_depend_only_on_relative_positions():
+    # q . k after rotation at positions p and p' equals the same at p + s and p' + s, for
+    # any shift s per axis: the property rotary embeddings are built for
+    rng = np.random.default_rng(5)
+    q, k = rng.standard_normal((1, 1, 1, 16)), rng.standard_normal((1, 1, 1, 16))
+    p, pp = np.array([[3.0, 5.0, 7.0]]), np.array([[1.0, 9.0, 2.0]])
+    sft = np.array([[4.0, -2.0, 11.0]])
+    dot = lambda a, b: float((a * b).sum())
+    axes, th = (4, 6, 6), 10000.0
+    d0 = dot(O.rope(q, p, axes, th), O.rope(k, pp, axes, th))
+    d1 = dot(O.rope(q, p + sft, axes, th), O.rope(k, pp + sft, axes, th))
+    assert abs(d0 - d1) < 1e-12 and abs(d0 - dot(q, k)) > 1e-3
+
+
+def test_rope_positions_of_text_and_image_rows():
+    cfg = dict(lat=(4, 2, 6, 8), patch=(1, 2, 2), n_txt=3)
+    pos = O.rope_positions(cfg)
+    assert pos.shape == (3 + 2 * 3 * 4, 3)
+    assert np.all(pos[:3] == 0)
+    np.testing.assert_array_equal(pos[3], [0, 0, 0])
+    np.testing.assert_array_equal(pos[3 + 5], [0, 1, 1])          # token 5 of a 3 x 4 grid
+    np.testing.assert_array_equal(pos[3 + 12 + 11], [1, 2, 3])    # last token of frame 1
