@@ -49,7 +49,8 @@ def device_inputs(cfg, seed=1):
     g = torch.Generator(device="cuda")
     g.manual_seed(seed)
     c_lat, F, H, W = cfg["lat"]
-    x0 = torch.randn((cfg["B"], c_lat, F, H, W), generator=g, device="cuda", dtype=torch.float32)
+    Bx = cfg["B"] // 2 if cfg.get("cfg_pairs") else cfg["B"]     # guided pairs share a latent
+    x0 = torch.randn((Bx, c_lat, F, H, W), generator=g, device="cuda", dtype=torch.float32)
     cond = torch.randn((cfg["B"], cfg["C"]), generator=g, device="cuda", dtype=torch.float32)
     txt = None
     dt = torch.bfloat16 if cfg["dtype"] == 1 else torch.float32
@@ -66,7 +67,7 @@ class Loop:
         import torch
         self.r, self.x0, self.cond, self.txt = runner, x0, cond, txt
         self.x = x0.clone()
-        self.audit = torch.full((runner.T * runner.L * x0.shape[0],), float("nan"), device="cuda")
+        self.audit = torch.full((runner.T * runner.L * runner.dm.cfg["B"],), float("nan"), device="cuda")
         self.pos = 0
 
     def step(self):
@@ -311,6 +312,37 @@ def rope_loop():
     return out
 
 
+def guided_loop(scale=4.0):
+    """DiT-XL/2 with classifier-free guidance by batch doubling: 8 guided images, so 16
+    model rows (conditional rows 0-7, their unconditional twins 8-15) and one guided Euler
+    step per row pair; FeatFix and Vanilla, one untimed loop, then one timed 50-step loop
+    each."""
+    import torch
+    import synth
+    from paper_2607_27842_amd import pipeline
+    cfg = synth.get_config("dit_xl2", B=16, cfg_pairs=1, cfg_scale=scale)
+    dm = pipeline.DeviceModel.random(cfg, seed=0)
+    x0, cond, txt = device_inputs(cfg)
+    out = {"model_rows": cfg["B"], "images": cfg["B"] // 2, "cfg_scale": scale}
+    for mode in ("featfix", "vanilla"):
+        r = pipeline.Runner(dm, synth.MODE_NAMES[mode], synth.site_mask(cfg))
+        loop = Loop(r, x0, cond, txt)
+        for _ in range(r.T):
+            loop.step()
+        loop.pos = 0
+        ms = timed_steps(loop, r.T)
+        r.close()
+        del loop, r
+        out[mode] = {"steps": cfg["T"], "ms": round(ms, 3), "steps_per_s": round(cfg["T"] / (ms / 1e3), 2),
+                     "images_per_s": round(cfg["B"] // 2 / (ms / 1e3), 2)}
+    del dm
+    torch.cuda.empty_cache()
+    out["featfix_over_vanilla"] = round(out["featfix"]["steps_per_s"] / out["vanilla"]["steps_per_s"], 3)
+    log(f"[bench] guided dit_xl2 (16 rows): featfix {out['featfix']['steps_per_s']} steps/s, "
+        f"vanilla {out['vanilla']['steps_per_s']} steps/s")
+    return out
+
+
 def resolution_sweep(sides=(512, 768, 1024)):
     """FLUX-like loop latency and peak device memory from 512^2 to 1024^2 images (latent
     side / 8, patch 2: 1024, 2304 and 4096 image tokens + 512 text tokens), FeatFix and
@@ -407,6 +439,7 @@ def main():
     ap.add_argument("--no-vanilla", action="store_true")
     ap.add_argument("--no-arms", action="store_true", help="skip the matched-compute arm loops reported in extra")
     ap.add_argument("--no-sweep", action="store_true", help="skip the FLUX-like resolution sweep reported in extra")
+    ap.add_argument("--no-guided", action="store_true", help="skip the guided (batch-doubled) DiT-XL/2 loops")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
@@ -464,6 +497,8 @@ def main():
         extra["flux_resolution_sweep"] = resolution_sweep()
     if name == "dit_xl2" and not args.no_arms:
         extra["dit_xl2_shadow_vanilla"] = shadow_vanilla()
+    if name == "dit_xl2" and not args.no_guided:
+        extra["dit_xl2_guided"] = guided_loop()
     out = {"metric": METRIC, "value": round(value, 3), "unit": "steps/s", "n_gpus": 1, "steps": ff["steps"],
            "warmup": warm_loops * T, "ms_per_step": round(ms_step, 4), "higher_is_better": True, "scaling": "weak",
            "vs_baseline": None, "dtype": "bf16",

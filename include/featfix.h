@@ -39,7 +39,7 @@
 extern "C" {
 #endif
 
-#define FF_ABI_VERSION 2
+#define FF_ABI_VERSION 3
 #define FF_MAX_K 3          /* largest supported forecast order K */
 #define FF_MAX_SLOTS 8      /* largest supported ring size S      */
 #define FF_TEMB_DIM 256     /* sinusoidal time-embedding width    */
@@ -80,14 +80,19 @@ typedef struct ihipStream_t* ff_stream_t;
  * image weight sets, joint attention, per-head QK RMSNorm), FF_MMDIT_SINGLE (one weight
  * set, fused attention+MLP input projection).  FF_DIT requires n_txt == 0.
  * Requirements: C == H*d, d in [8, 128] and d % 8 == 0, C % 8 == 0, mlp_hidden % 8 == 0,
- * 1 <= B, lat_f % pt == lat_h % ph == lat_w % pw == 0,
+ * 1 <= B <= 32, lat_f % pt == lat_h % ph == lat_w % pw == 0,
  * n_img == (lat_f/pt)*(lat_h/ph)*(lat_w/pw), (pt*ph*pw*lat_c) % 8 == 0.
  * rope_axes: all 0 for no rotary embedding; otherwise even dims summing to d.  The MMDiT
  * blocks then rotate q and k after their RMSNorms: the head dims are split into chunks of
  * rope_axes[0..2] dims and in chunk a the pair (2i, 2i+1) of a row is turned by
  * pos_a * rope_theta^(-2i / rope_axes[a]), where pos = (0, 0, 0) for text rows and
  * (frame, row, column) of the patch in the (lat_f/pt, lat_h/ph, lat_w/pw) grid for image
- * rows (FLUX-style 3-axis ids).  rope_theta > 1 when enabled. */
+ * rows (FLUX-style 3-axis ids).  rope_theta > 1 when enabled.
+ * cfg_pairs: 0, or 1 for classifier-free guidance by batch doubling: B is even and rows
+ * b < B/2 are the conditional samples, rows B/2 + b their unconditional twins (the caller
+ * passes both conditionings in cond / txt); the latent x of ff_denoise_step then holds
+ * B/2 samples, both rows of a pair read latent b, and the Euler step uses
+ * v = v_u + cfg_scale * (v_c - v_u) (cfg_scale finite). */
 typedef struct {
   int32_t n_layers;
   const int32_t* kinds;   /* host array [n_layers]; copied where it is kept */
@@ -99,6 +104,8 @@ typedef struct {
   float ln_eps;           /* LayerNorm / RMSNorm epsilon */
   int32_t rope_axes[3];
   float rope_theta;
+  int32_t cfg_pairs;
+  float cfg_scale;
 } ff_model_desc;
 
 /* One stream's weights of one block (device pointers, model dtype, [out, in]).
@@ -316,7 +323,8 @@ ff_status ff_ctx_step_kinds(const ff_ctx* c, int32_t* kinds);
  *            token or channel); Exact-only skips the draft and the audit
  *     RECOMPUTE: X <- B_l(X) without a history refresh
  *   v = unpatchify(FinalLayer(X_img)); x <- x + (t_{i+1} - t_i) v
- * x: device fp32 latent [B, lat_c, lat_f, lat_h, lat_w], updated in place.
+ * x: device fp32 latent [B, lat_c, lat_f, lat_h, lat_w] ([B/2, ...] with cfg_pairs),
+ * updated in place.
  * cond: device fp32 [B, C].  txt: device dtype [B, n_txt, C] (NULL iff n_txt == 0).
  * audit: device fp32 [T*L*B] or NULL; entry (i*L + l)*B + b receives rel_l1 at paid
  * checks (other entries are not written).

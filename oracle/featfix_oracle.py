@@ -430,6 +430,11 @@ def run(cfg, mode, inputs, weights, mask, feature_mode=RESIDUAL, trace=None, tau
     (NaN counts as above).  Sites keep the mask; the finite differences use the actual
     refresh steps (Eq. 2).
 
+    Classifier-free guidance (cfg["cfg_pairs"] = 1; reading of the usual batch doubling):
+    the B model rows are B/2 conditional samples and their B/2 unconditional twins (rows
+    b and B/2 + b, conditioned by inputs["c"] / inputs["txt"] rows); both read latent b of
+    x ([B/2, ...]), and the Euler step uses v = v_u + s (v_c - v_u), s = cfg["cfg_scale"].
+
     The matched-compute arms (Sec. 3.3) differ from FeatFix only at paid sites: the token
     and channel arms forward the exact output on every `stride`-th token or channel
     (forward_partial); the recompute arm forwards it and runs the rest of the step exact.
@@ -467,7 +472,10 @@ def run(cfg, mode, inputs, weights, mask, feature_mode=RESIDUAL, trace=None, tau
         step_d = []
         t_i, t_n = 1.0 - i / T, 1.0 - (i + 1) / T
         cs = silu(conditioning(inputs["c"], t_i, G))
-        X = rnd(_linear(patchify(x, cfg["patch"]), G["pe_w"], G["pe_b"]))
+        pt = patchify(x, cfg["patch"])
+        if cfg.get("cfg_pairs"):
+            pt = np.concatenate([pt, pt], axis=0)      # rows b and B/2 + b read latent b
+        X = rnd(_linear(pt, G["pe_w"], G["pe_b"]))
         if n_txt:
             X = np.concatenate([txt, X], axis=1)
         for l in range(L):
@@ -503,6 +511,9 @@ def run(cfg, mode, inputs, weights, mask, feature_mode=RESIDUAL, trace=None, tau
         prev_d = float(np.max(np.concatenate(step_d))) if step_d else None
         y = final_layer(X[:, n_txt:], cs, G, cfg)
         v = unpatchify(y, cfg["patch"], cfg["lat"])
+        if cfg.get("cfg_pairs"):
+            half = v.shape[0] // 2
+            v = v[half:] + cfg["cfg_scale"] * (v[:half] - v[half:])
         x = x + (t_n - t_i) * v
     return {"x": x, "audit": audit, "counts": counts, "plan": plan, "step_kind": step_kind}
 

@@ -17,6 +17,7 @@ LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libfeatfix.
 FF_OK, FF_E_NULL, FF_E_SHAPE, FF_E_DTYPE, FF_E_RANGE, FF_E_STATE, FF_E_WORKSPACE, FF_E_HIP, \
     FF_E_UNSUPPORTED = 0, -1, -2, -3, -4, -5, -6, -7, -8
 FF_DIT, FF_MMDIT_DOUBLE, FF_MMDIT_SINGLE = 0, 1, 2
+FF_ABI_VERSION = 3          # the struct layouts below; must equal the library's
 FF_F32, FF_BF16 = 0, 1
 FF_VANILLA, FF_DRAFT, FF_VERIFY, FF_FEATFIX, FF_EXACT_ONLY = 0, 1, 2, 3, 4
 FF_TOKENS_PARTIAL, FF_CHANNELS_PARTIAL, FF_RECOMPUTE = 5, 6, 7
@@ -41,7 +42,8 @@ class ff_model_desc(C.Structure):
                 ("n_img", C.c_int32), ("n_txt", C.c_int32), ("B", C.c_int32),
                 ("lat_c", C.c_int32), ("lat_f", C.c_int32), ("lat_h", C.c_int32), ("lat_w", C.c_int32),
                 ("pt", C.c_int32), ("ph", C.c_int32), ("pw", C.c_int32),
-                ("dtype", C.c_int32), ("ln_eps", C.c_float), ("rope_axes", C.c_int32 * 3), ("rope_theta", C.c_float)]
+                ("dtype", C.c_int32), ("ln_eps", C.c_float), ("rope_axes", C.c_int32 * 3), ("rope_theta", C.c_float),
+                ("cfg_pairs", C.c_int32), ("cfg_scale", C.c_float)]
 
 
 _STREAM_FIELDS = ("mod_w", "mod_b", "qkv_w", "qkv_b", "o_w", "o_b", "fc1_w", "fc1_b", "fc2_w", "fc2_b",
@@ -130,6 +132,9 @@ def lib():
             fn = getattr(L, name)
             fn.restype = res
             fn.argtypes = args
+        if L.ff_abi_version() != FF_ABI_VERSION:
+            raise RuntimeError(f"{LIB_PATH} has ABI version {L.ff_abi_version()}, the binding expects "
+                               f"{FF_ABI_VERSION}: rebuild it")
         _lib = L
     return _lib
 

@@ -44,7 +44,6 @@ ff_status hip_fail(hipError_t e, const char* where) {
     if (_e != hipSuccess) return hip_fail(_e, where); \
   } while (0)
 
-constexpr int kGemvMaxB = 8;
 constexpr size_t kAlign = 256;
 inline size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 
@@ -58,6 +57,8 @@ struct Model {
   float ln_eps = 0.f;
   int rope[3] = {0, 0, 0};
   float rope_theta = 0.f;
+  int cfg = 0;            // classifier-free guidance pairs (rows b, b + B/2)
+  float cfg_scale = 0.f;
   bool any_single = false;
   size_t es() const { return dsize(dtype); }
   size_t E() const { return (size_t)B * N * C; }
@@ -119,6 +120,13 @@ ff_status check_model(const ff_model_desc* m, Model* out) {
     if (!(m->rope_theta > 1.f) || !std::isfinite(m->rope_theta)) return fail(FF_E_RANGE, "rope_theta must be > 1");
     for (int a = 0; a < 3; ++a) r.rope[a] = m->rope_axes[a];
     r.rope_theta = m->rope_theta;
+  }
+  if (m->cfg_pairs != 0 && m->cfg_pairs != 1) return fail(FF_E_RANGE, "cfg_pairs must be 0 or 1");
+  if (m->cfg_pairs) {
+    if (r.B % 2) return fail(FF_E_SHAPE, "guidance pairs need an even batch (B=%d)", r.B);
+    if (!std::isfinite(m->cfg_scale)) return fail(FF_E_RANGE, "cfg_scale must be finite");
+    r.cfg = 1;
+    r.cfg_scale = m->cfg_scale;
   }
   r.N = r.n_img + r.n_txt;
   if ((long)r.B * r.N > (1L << 30) / 8) return fail(FF_E_SHAPE, "too many rows");
@@ -969,6 +977,11 @@ ff_status ff_denoise_step(ff_ctx* c, int32_t step, float* x, const float* cond, 
     };
     // tokens: X = [txt ; patch_embed(patchify(x))]
     PatchGeom pg{m.B, m.lat_c, m.lat_f, m.lat_h, m.lat_w, m.pt, m.ph, m.pw};
+    if (m.cfg) {   // guided pairs: rows b and b + B/2 read latent b; the Euler step combines them
+      pg.lat_B = m.B / 2;
+      pg.cfg_half = m.B / 2;
+      pg.cfg_scale = m.cfg_scale;
+    }
     void* patches = at(ws, W.PATCH);
     const double lat_elems = (double)m.B * m.n_img * m.P;
     void* cur = at(ws, W.X0);
@@ -1061,7 +1074,7 @@ ff_status ff_denoise_step(ff_ctx* c, int32_t step, float* x, const float* cond, 
     float* mod = at<float>(ws, W.MOD);
     GemvArgs gf{cs, C, 0, c->g.fmod_w, c->g.fmod_b, 2 * C, C, m.B, mod, 2 * C, 0, nullptr, 0, xs};
     HIP_TRY(ex.gemv(gf), "final modulation");
-    if (final_layer_ok(dt, m.P, C)) {
+    if (final_layer_ok(dt, m.P, C) && !m.cfg) {
       // LN + modulation + final linear + unpatchify + Euler in one launch, one wavefront
       // per image token (small final weights only)
       const FinalArgs fa{cur, C, img, m.B * m.n_img, C, m.ln_eps, mod, mod + C, 2 * C, c->g.f_w, c->g.f_b,

@@ -175,7 +175,7 @@ __global__ __launch_bounds__(256) void k_rms_qk(RmsQKArgs a) {
   S::store(a.x, base + col, v);
 }
 
-constexpr int kGemvMaxB = 8;
+constexpr int kGemvTileB = 8;   // samples per launch of the generic tile
 constexpr int kGemvRows = 4;     // output features per wavefront
 constexpr int kGemvKC = 1024;    // K chunk of the activations staged in LDS
 
@@ -191,11 +191,11 @@ __device__ __forceinline__ void gemv_tile(const GemvArgs a, int blk) {
   extern __shared__ float xs[];               // [B][kGemvKC]
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int n0 = (blk * 4 + wave) * kGemvRows;
-  float acc[kGemvRows][kGemvMaxB];
+  float acc[kGemvRows][kGemvTileB];
 #pragma unroll
   for (int r = 0; r < kGemvRows; ++r)
 #pragma unroll
-    for (int b = 0; b < kGemvMaxB; ++b) acc[r][b] = 0.f;
+    for (int b = 0; b < kGemvTileB; ++b) acc[r][b] = 0.f;
   for (int k0 = 0; k0 < a.K; k0 += kGemvKC) {
     const int kc = min(kGemvKC, a.K - k0);
     // weight loads first (they do not depend on the activations) ...
@@ -215,14 +215,14 @@ __device__ __forceinline__ void gemv_tile(const GemvArgs a, int blk) {
     }
     // ... then every sample's activation chunk (one float4 per thread and sample, all
     // loads issued before any is stored) into LDS
-    float4 xv4[kGemvMaxB];
+    float4 xv4[kGemvTileB];
     const int k4 = threadIdx.x * 4;   // 256 threads x 4 = kGemvKC
 #pragma unroll
-    for (int b = 0; b < kGemvMaxB; ++b)
+    for (int b = 0; b < kGemvTileB; ++b)
       if (b < a.B && k4 < kc) xv4[b] = *reinterpret_cast<const float4*>(a.x + (size_t)b * a.ldx + k0 + k4);
     __syncthreads();   // the previous chunk's LDS reads are done
 #pragma unroll
-    for (int b = 0; b < kGemvMaxB; ++b) {
+    for (int b = 0; b < kGemvTileB; ++b) {
       if (b < a.B && k4 < kc) {
         float4 v = xv4[b];
         if (a.silu_in) { v.x = silu_f(v.x); v.y = silu_f(v.y); v.z = silu_f(v.z); v.w = silu_f(v.w); }
@@ -235,7 +235,7 @@ __device__ __forceinline__ void gemv_tile(const GemvArgs a, int blk) {
       const int c = lane + 64 * p;
       if (c * S::V >= kc) break;
 #pragma unroll
-      for (int b = 0; b < kGemvMaxB; ++b) {
+      for (int b = 0; b < kGemvTileB; ++b) {
         if (b < a.B) {
           float xv[S::V];
 #pragma unroll
@@ -254,14 +254,14 @@ __device__ __forceinline__ void gemv_tile(const GemvArgs a, int blk) {
   // Cross-lane sums of the kGemvRows * B partials: one transposed pass through LDS (each
   // lane writes its partials, lane v then adds column v over the 64 lanes in order) instead
   // of one 6-step butterfly per value.
-  __shared__ float red[4][kGemvRows * kGemvMaxB][65];
+  __shared__ float red[4][kGemvRows * kGemvTileB][65];
 #pragma unroll
   for (int r = 0; r < kGemvRows; ++r)
 #pragma unroll
-    for (int b = 0; b < kGemvMaxB; ++b) red[wave][r * kGemvMaxB + b][lane] = acc[r][b];
+    for (int b = 0; b < kGemvTileB; ++b) red[wave][r * kGemvTileB + b][lane] = acc[r][b];
   __syncthreads();
-  if (lane < kGemvRows * kGemvMaxB) {
-    const int r = lane / kGemvMaxB, b = lane % kGemvMaxB, n = n0 + r;
+  if (lane < kGemvRows * kGemvTileB) {
+    const int r = lane / kGemvTileB, b = lane % kGemvTileB, n = n0 + r;
     if (b < a.B && n < a.Nout) {
       float sum = 0.f;
       for (int l = 0; l < 64; ++l) sum += red[wave][lane][l];
@@ -273,7 +273,7 @@ __device__ __forceinline__ void gemv_tile(const GemvArgs a, int blk) {
   }
 }
 
-// bf16 weights, B <= 8: y[b, n0..n0+15] on v_mfma_f32_16x16x32_bf16.  The fp32
+// bf16 weights, B <= 32: y[b, n0..n0+15] on v_mfma_f32_16x16x32_bf16.  The fp32
 // activations enter as bf16 hi + lo parts (x = hi + lo to ~2^-17 relative), split by each
 // lane as it loads them, or read from a split made beforehand (xs; the large modulation
 // batches, whose thousands of workgroups would otherwise each split the same x): MFMA
@@ -301,62 +301,79 @@ __device__ __forceinline__ u32x4_t split8(const float* x, int silu_in, bool lo_p
   return r;
 }
 
+// NG groups of 8 samples share each weight load: group g holds samples 8g..8g+7 (its
+// split in xs rows 16g..16g+15) and its own accumulator tile.
+template <int NG>
 __device__ __forceinline__ void gemv_mfma_tile(const GemvArgs a, int blk) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int n0 = blk * 16;
   const int rc = lane & 15, kq = (lane >> 4) * 8;
   const int n = n0 + rc;
-  const bool nok = n < a.Nout, bok = (rc & 7) < a.B;
+  const bool nok = n < a.Nout;
   const uint16_t* wrow = reinterpret_cast<const uint16_t*>(a.W) + (size_t)(nok ? n : 0) * a.K;
-  const float* xrow = a.x + (size_t)(rc & 7) * a.ldx;   // sample rc % 8 (ldx 0: one shared row)
-  const uint16_t* srow = a.xs + (size_t)rc * a.K;         // or its split, made beforehand
   const bool lo_part = rc >= 8;
   const int nks = (a.K + 31) / 32;
   const u32x4_t z4 = {0u, 0u, 0u, 0u};
-  f32x4_t acc = {0.f, 0.f, 0.f, 0.f};
+  f32x4_t acc[NG];
+#pragma unroll
+  for (int g = 0; g < NG; ++g) acc[g] = f32x4_t{0.f, 0.f, 0.f, 0.f};
   for (int ks0 = wave; ks0 < nks; ks0 += 4 * kMvU) {
-    u32x4_t wv[kMvU], xv[kMvU];
+    u32x4_t wv[kMvU], xv[NG][kMvU];
 #pragma unroll
     for (int u = 0; u < kMvU; ++u) {
       const int k = (ks0 + 4 * u) * 32 + kq;
       const bool kin = ks0 + 4 * u < nks && k < a.K;   // K % 8 == 0: a lane's 8 are all in or out
       wv[u] = (kin && nok) ? *reinterpret_cast<const u32x4_t*>(wrow + k) : z4;
-      if (!(kin && bok)) xv[u] = z4;
-      else if (a.xs) xv[u] = *reinterpret_cast<const u32x4_t*>(srow + k);
-      else xv[u] = split8(xrow + k, a.silu_in, lo_part);
+#pragma unroll
+      for (int g = 0; g < NG; ++g) {
+        const int b = 8 * g + (rc & 7);   // sample of this lane's A row (ldx 0: one shared row)
+        if (!(kin && b < a.B)) xv[g][u] = z4;
+        else if (a.xs) xv[g][u] = *reinterpret_cast<const u32x4_t*>(a.xs + (size_t)(16 * g + rc) * a.K + k);
+        else xv[g][u] = split8(a.x + (size_t)b * a.ldx + k, a.silu_in, lo_part);
+      }
     }
 #pragma unroll
     for (int u = 0; u < kMvU; ++u)
-      acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, xv[u]), __builtin_bit_cast(bf16x8_t, wv[u]),
-                                                   acc, 0, 0, 0);
-  }
-  __shared__ float red[4][64][4];
 #pragma unroll
-  for (int j = 0; j < 4; ++j) red[wave][lane][j] = acc[j];
+      for (int g = 0; g < NG; ++g)
+        acc[g] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, xv[g][u]),
+                                                         __builtin_bit_cast(bf16x8_t, wv[u]), acc[g], 0, 0, 0);
+  }
+  __shared__ float red[4][64][4 * NG];
+#pragma unroll
+  for (int g = 0; g < NG; ++g)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) red[wave][lane][4 * g + j] = acc[g][j];
   __syncthreads();
   if (threadIdx.x < 128) {
-    const int ob = threadIdx.x >> 4, on = threadIdx.x & 15;   // output (sample, column)
+    const int ob = threadIdx.x >> 4, on = threadIdx.x & 15;   // output (sample in group, column)
     const int lh = (ob >> 2) * 16 + on, ll = ((ob >> 2) + 2) * 16 + on, j = ob & 3;
-    float hi = 0.f, lw = 0.f;
-#pragma unroll
-    for (int w = 0; w < 4; ++w) { hi += red[w][lh][j]; lw += red[w][ll][j]; }
     const int nn = n0 + on;
-    if (ob < a.B && nn < a.Nout) {
-      float y = (hi + lw) + St<DT_BF16>::ld1(a.bias, nn);
-      if (a.silu_out) y = silu_f(y);
-      if (a.add) y += a.add[(size_t)ob * a.ldadd + nn];
-      a.y[(size_t)ob * a.ldy + nn] = y;
+#pragma unroll
+    for (int g = 0; g < NG; ++g) {
+      float hi = 0.f, lw = 0.f;
+#pragma unroll
+      for (int w = 0; w < 4; ++w) { hi += red[w][lh][4 * g + j]; lw += red[w][ll][4 * g + j]; }
+      const int b = 8 * g + ob;
+      if (b < a.B && nn < a.Nout) {
+        float y = (hi + lw) + St<DT_BF16>::ld1(a.bias, nn);
+        if (a.silu_out) y = silu_f(y);
+        if (a.add) y += a.add[(size_t)b * a.ldadd + nn];
+        a.y[(size_t)b * a.ldy + nn] = y;
+      }
     }
   }
 }
 
-__global__ __launch_bounds__(256) void k_gemv_mfma(GemvArgs a) { gemv_mfma_tile(a, blockIdx.x); }
+template <int NG>
+__global__ __launch_bounds__(256) void k_gemv_mfma(GemvArgs a) { gemv_mfma_tile<NG>(a, blockIdx.x); }
 
+template <int NG>
 __global__ __launch_bounds__(256) void k_gemv_mfma_batch(GemvBatch bt) {
   const GemvJob j = bt.job[blockIdx.y];
   if ((int)blockIdx.x * 16 >= j.Nout) return;   // whole workgroup: no barrier skipped
   const GemvArgs a{bt.x, bt.ldx, bt.silu_in, j.W, j.bias, j.Nout, bt.K, bt.B, j.y, j.ldy, 0, nullptr, 0, bt.xs};
-  gemv_mfma_tile(a, blockIdx.x);
+  gemv_mfma_tile<NG>(a, blockIdx.x);
 }
 
 template <int DT>
@@ -387,9 +404,10 @@ __global__ void k_silu_rows(const float* x, float* y, int B, int n, uint16_t* xs
   y[i] = v;
   if (xs) {   // the bf16 hi / lo split the MFMA GEMVs read (as split8 makes it)
     const int b = (int)(i / n), k = (int)(i % n);
+    const int r = 16 * (b / 8) + b % 8;   // group b/8: hi rows 16g..16g+7, lo 16g+8..
     const uint16_t h = f2bf(v);
-    xs[(size_t)b * n + k] = h;
-    xs[(size_t)(8 + b) * n + k] = f2bf(v - bf2f(h));
+    xs[(size_t)r * n + k] = h;
+    xs[(size_t)(r + 8) * n + k] = f2bf(v - bf2f(h));
   }
 }
 
@@ -405,17 +423,18 @@ __global__ __launch_bounds__(256) void k_patchify(const float* __restrict__ x, v
   const int b = (int)(row / n_img);
   const int tok = (int)(row % n_img);
   const int wx = tok % Wp, hy = (tok / Wp) % Hp, f = tok / (Wp * Hp);
+  const int bl = g.lat_B ? b % g.lat_B : b;   // the latent this row reads (guided pairs share one)
   // feature order (channel, dt, dy, dx)
   const int c = feat % g.pw, bb = (feat / g.pw) % g.ph, a = (feat / (g.pw * g.ph)) % g.pt;
   const int ch = feat / (g.pw * g.ph * g.pt);
-  const size_t src = ((((size_t)b * g.lat_c + ch) * g.F + (f * g.pt + a)) * g.H + (hy * g.ph + bb)) * g.W +
+  const size_t src = ((((size_t)bl * g.lat_c + ch) * g.F + (f * g.pt + a)) * g.H + (hy * g.ph + bb)) * g.W +
                      (wx * g.pw + c);
   St<DT>::st1(out, (size_t)i, x[src]);
 }
 
 __global__ __launch_bounds__(256) void k_unpatchify_euler(const float* __restrict__ yv, float* __restrict__ x,
                                                           float dt, PatchGeom g) {
-  const long n = (long)g.B * g.lat_c * g.F * g.H * g.W;
+  const long n = (long)(g.lat_B ? g.lat_B : g.B) * g.lat_c * g.F * g.H * g.W;
   const long i = (long)blockIdx.x * 256 + threadIdx.x;
   if (i >= n) return;
   const int xx = (int)(i % g.W);
@@ -429,7 +448,12 @@ __global__ __launch_bounds__(256) void k_unpatchify_euler(const float* __restric
   // feature order (dt, dy, dx, channel)
   const int feat = (((ff % g.pt) * g.ph + yy % g.ph) * g.pw + xx % g.pw) * g.lat_c + ch;
   const long n_img = (long)Fp * Hp * Wp;
-  x[i] = x[i] + dt * yv[((long)b * n_img + tok) * P + feat];
+  float v = yv[((long)b * n_img + tok) * P + feat];
+  if (g.cfg_half) {   // guidance: v_u + s (v_c - v_u), v_c from row b, v_u from row b + half
+    const float vu = yv[((long)(b + g.cfg_half) * n_img + tok) * P + feat];
+    v = vu + g.cfg_scale * (v - vu);
+  }
+  x[i] = x[i] + dt * v;
 }
 
 
@@ -608,30 +632,57 @@ hipError_t rms_qk(int dtype, const RmsQKArgs& a, hipStream_t s) {
 }
 
 hipError_t gemv(int dtype, const GemvArgs& a, hipStream_t s) {
+  if (a.B < 1 || a.B > kGemvMaxB) return hipErrorInvalidValue;
   if (dtype == DT_BF16) {
-    if (a.B > 8 || a.K % 8) return hipErrorInvalidValue;
-    FF_LAUNCH(k_gemv_mfma, cdiv(a.Nout, 16), 256, 0, s, a);
+    if (a.K % 8) return hipErrorInvalidValue;
+    const int grid = cdiv(a.Nout, 16), ng = cdiv(a.B, 8);
+    if (ng == 1) FF_LAUNCH(k_gemv_mfma<1>, grid, 256, 0, s, a);
+    else if (ng == 2) FF_LAUNCH(k_gemv_mfma<2>, grid, 256, 0, s, a);
+    else FF_LAUNCH(k_gemv_mfma<4>, grid, 256, 0, s, a);
     return hipGetLastError();
   }
+  // fp32: one launch per group of kGemvTileB samples (each reads the weights)
   const int grid = cdiv(a.Nout, 4 * kGemvRows);
-  const size_t lds = (size_t)a.B * kGemvKC * sizeof(float);
-  FF_LAUNCH(k_gemv<DT_F32>, grid, 256, lds, s, a);
-  return hipGetLastError();
+  for (int b0 = 0; b0 < a.B; b0 += kGemvTileB) {
+    GemvArgs p = a;
+    p.B = min(kGemvTileB, a.B - b0);
+    p.x = a.x + (size_t)b0 * a.ldx;
+    p.y = a.y + (size_t)b0 * a.ldy;
+    if (a.add) p.add = a.add + (size_t)b0 * a.ldadd;
+    const size_t lds = (size_t)p.B * kGemvKC * sizeof(float);
+    FF_LAUNCH(k_gemv<DT_F32>, grid, 256, lds, s, p);
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
 }
 
 hipError_t gemv_batch(int dtype, const GemvBatch& bt, hipStream_t s) {
   if (bt.njobs <= 0) return hipSuccess;
+  if (bt.B < 1 || bt.B > kGemvMaxB) return hipErrorInvalidValue;
   int nmax = 0;
   for (int i = 0; i < bt.njobs; ++i) nmax = max(nmax, bt.job[i].Nout);
   if (dtype == DT_BF16) {
-    if (bt.B > 8 || bt.K % 8) return hipErrorInvalidValue;
-    FF_LAUNCH(k_gemv_mfma_batch, dim3(cdiv(nmax, 16), bt.njobs), 256, 0, s, bt);
+    if (bt.K % 8) return hipErrorInvalidValue;
+    const dim3 grid(cdiv(nmax, 16), bt.njobs);
+    const int ng = cdiv(bt.B, 8);
+    if (ng == 1) FF_LAUNCH(k_gemv_mfma_batch<1>, grid, 256, 0, s, bt);
+    else if (ng == 2) FF_LAUNCH(k_gemv_mfma_batch<2>, grid, 256, 0, s, bt);
+    else FF_LAUNCH(k_gemv_mfma_batch<4>, grid, 256, 0, s, bt);
     return hipGetLastError();
   }
   const dim3 grid(cdiv(nmax, 4 * kGemvRows), bt.njobs);
-  const size_t lds = (size_t)bt.B * kGemvKC * sizeof(float);
-  FF_LAUNCH(k_gemv_batch<DT_F32>, grid, 256, lds, s, bt);
-  return hipGetLastError();
+  for (int b0 = 0; b0 < bt.B; b0 += kGemvTileB) {
+    GemvBatch p = bt;
+    p.B = min(kGemvTileB, bt.B - b0);
+    p.x = bt.x + (size_t)b0 * bt.ldx;
+    for (int i = 0; i < bt.njobs; ++i) p.job[i].y = bt.job[i].y + (size_t)b0 * bt.job[i].ldy;
+    const size_t lds = (size_t)p.B * kGemvKC * sizeof(float);
+    FF_LAUNCH(k_gemv_batch<DT_F32>, grid, 256, lds, s, p);
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
 }
 
 hipError_t time_embed(double sv, float* phi, hipStream_t st) {
@@ -640,7 +691,7 @@ hipError_t time_embed(double sv, float* phi, hipStream_t st) {
 }
 
 hipError_t silu_rows(const float* x, float* y, int B, int n, uint16_t* xs, hipStream_t st) {
-  if (xs && B > 8) return hipErrorInvalidValue;
+  if (xs && B > kGemvMaxB) return hipErrorInvalidValue;
   const long tot = (long)B * n;
   FF_LAUNCH(k_silu_rows, cdiv(tot, 256), 256, 0, st, x, y, B, n, xs);
   return hipGetLastError();
@@ -654,7 +705,7 @@ hipError_t patchify(int dtype, const float* x, void* patches, const PatchGeom& g
 }
 
 hipError_t unpatchify_euler(const float* yv, float* x, float dt, const PatchGeom& g, hipStream_t st) {
-  const long n = (long)g.B * g.lat_c * g.F * g.H * g.W;
+  const long n = (long)(g.lat_B ? g.lat_B : g.B) * g.lat_c * g.F * g.H * g.W;
   FF_LAUNCH(k_unpatchify_euler, cdiv(n, 256), 256, 0, st, yv, x, dt, g);
   return hipGetLastError();
 }

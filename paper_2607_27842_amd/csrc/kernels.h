@@ -55,10 +55,13 @@ hipError_t gemm2(int dtype, const GemmArgs& a0, const GemmArgs& a1, hipStream_t 
 
 // y[b, n] = (add ? add[b*ldadd + n] : 0) + act( sum_k f(x[b*ldx + k]) * W[n, k] + bias[n] )
 // x, y, add fp32; W, bias model dtype; f = SiLU if silu_in; act = SiLU if silu_out.
-// bf16 weights run on MFMA (B <= 8, K % 8 == 0, x 16-byte aligned rows): f(x) enters as
-// bf16 hi + lo parts, f(x) = hi + lo to ~2^-17, split in the kernel, or read from xs when
-// set ([16, K] bf16: rows 0..B-1 hi, 8..8+B-1 lo, as silu_rows writes it; the caller
-// guarantees it holds the split of this f(x)).
+// 1 <= B <= kGemvMaxB.  bf16 weights run on MFMA (K % 8 == 0, x 16-byte aligned rows), each
+// weight load serving up to four groups of 8 samples: f(x) enters as bf16 hi + lo parts,
+// f(x) = hi + lo to ~2^-17, split in the kernel, or read from xs when set ([16 * groups,
+// K] bf16: sample b = 8g + r has hi in row 16g + r and lo in row 16g + 8 + r, as silu_rows
+// writes it; the caller guarantees it holds the split of this f(x)).  fp32 weights run in
+// groups of 8 samples, one launch each.
+constexpr int kGemvMaxB = 32;
 struct GemvArgs {
   const float* x; int ldx; int silu_in;
   const void* W; const void* bias;
@@ -69,7 +72,7 @@ struct GemvArgs {
 };
 hipError_t gemv(int dtype, const GemvArgs& a, hipStream_t s);
 // Up to kGemvJobs GEMVs sharing x (and K, B, SiLU on input) in one launch; no add term,
-// no SiLU on output.  B <= 8.
+// no SiLU on output.  1 <= B <= kGemvMaxB.
 constexpr int kGemvJobs = 32;
 struct GemvJob {
   const void* W; const void* bias; float* y;
@@ -81,7 +84,7 @@ struct GemvBatch {
   const uint16_t* xs;   // as GemvArgs::xs
   GemvJob job[kGemvJobs];
 };
-inline size_t gemv_xs_bytes(int K) { return (size_t)16 * K * 2; }
+inline size_t gemv_xs_bytes(int K) { return (size_t)16 * (kGemvMaxB / 8) * K * 2; }
 hipError_t gemv_batch(int dtype, const GemvBatch& bt, hipStream_t s);
 
 // ---------------------------------------------------------------- normalisation
@@ -161,13 +164,17 @@ hipError_t rel_l1(int dtype, const void* a, const void* b, int B, size_t Eb, flo
 // ---------------------------------------------------------------- small per-step kernels
 // phi[k] = cos(s f_k), phi[128 + k] = sin(s f_k), f_k = exp(-ln(1e4) k / 128), in fp64.
 hipError_t time_embed(double s, float* phi, hipStream_t st);
-// y[b*n + k] = silu(x[b*n + k]) for k < n; with xs (B <= 8) also its bf16 hi / lo split
+// y[b*n + k] = silu(x[b*n + k]) for k < n; with xs (B <= kGemvMaxB) also its bf16 hi / lo split
 // for the MFMA GEMVs (GemvArgs::xs layout, K = n)
 hipError_t silu_rows(const float* x, float* y, int B, int n, uint16_t* xs, hipStream_t st);
 // patches[(b*n_img + tok), feat] (model dtype) from latent x[B, lat_c, F, H, W] fp32
-struct PatchGeom { int B, lat_c, F, H, W, pt, ph, pw; };
+// B: model rows; lat_B: latent samples (0: B), patch sample b reads latent b % lat_B;
+// cfg_half > 0: rows b and b + cfg_half are a conditional / unconditional pair of latent b
+// and the Euler update uses v = v_u + cfg_scale * (v_c - v_u)
+struct PatchGeom { int B, lat_c, F, H, W, pt, ph, pw; int lat_B = 0, cfg_half = 0; float cfg_scale = 0.f; };
 hipError_t patchify(int dtype, const float* x, void* patches, const PatchGeom& g, hipStream_t st);
-// x[b, ch, f, y, x] += dt * yv[(b*n_img + tok), feat], feat order (dt, dy, dx, ch)
+// x[b, ch, f, y, x] += dt * yv[(b*n_img + tok), feat], feat order (dt, dy, dx, ch), for the
+// latent samples b (guided as PatchGeom says)
 hipError_t unpatchify_euler(const float* yv, float* x, float dt, const PatchGeom& g, hipStream_t st);
 // Fused final layer of the image rows + unpatchify + Euler, one wavefront per token:
 // a = round(LN(in[phys(r)]) (1 + scale[b]) + shift[b]) (model dtype, as ln_modulate),

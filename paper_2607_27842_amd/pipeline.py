@@ -29,7 +29,8 @@ def model_desc(cfg):
     pt, ph, pw = cfg["patch"]
     m = abi.ff_model_desc(len(cfg["kinds"]), kinds, cfg["C"], cfg["H"], cfg["d"], cfg["mlp"], cfg["n_img"],
                           cfg["n_txt"], cfg["B"], c_lat, F, H, W, pt, ph, pw, cfg["dtype"], cfg["ln_eps"],
-                          (C.c_int32 * 3)(*cfg.get("rope_axes", (0, 0, 0))), cfg.get("rope_theta", 10000.0))
+                          (C.c_int32 * 3)(*cfg.get("rope_axes", (0, 0, 0))), cfg.get("rope_theta", 10000.0),
+                          cfg.get("cfg_pairs", 0), cfg.get("cfg_scale", 1.0))
     m._kinds = kinds
     return m
 

@@ -211,12 +211,14 @@ def make_weights(cfg: dict, seed: int = 0, bias_std: float = 0.0, gain_std: floa
 
 def make_inputs(cfg: dict, seeds=(1, 2, 3)) -> dict:
     """Initial latent x (fp32, N(0,1)), conditioning vector c [B, C] and text tokens
-    [B, N_txt, C] (both N(0,1), rounded to bf16 values in bf16 workloads)."""
+    [B, N_txt, C] (both N(0,1), rounded to bf16 values in bf16 workloads).  With
+    cfg["cfg_pairs"] the B model rows are B/2 guided pairs, so x holds B/2 latents."""
     B, C = cfg["B"], cfg["C"]
     c_lat, F, Hh, W = cfg["lat"]
     bf16 = cfg["dtype"] == BF16
     fix = to_bf16_values if bf16 else (lambda a: a)
-    x = _rng(seeds[0]).standard_normal((B, c_lat, F, Hh, W), dtype=np.float32)
+    Bx = B // 2 if cfg.get("cfg_pairs") else B
+    x = _rng(seeds[0]).standard_normal((Bx, c_lat, F, Hh, W), dtype=np.float32)
     c = fix(_rng(seeds[1]).standard_normal((B, C), dtype=np.float32))
     txt = fix(_rng(seeds[2]).standard_normal((B, cfg["n_txt"], C), dtype=np.float32))
     return {"x": x, "c": c, "txt": txt}

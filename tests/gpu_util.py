@@ -8,7 +8,7 @@ import oracle as O
 import synth
 from paper_2607_27842_amd import abi, pipeline
 
-# Tolerances (normwise max relative error, max|a-b| / max|b|): the benchmark spec's bounds
+# Tolerances (normwise max relative error, max|a-b| / max|b|): the accuracy bounds set
 # for final latents, reused for block deltas and forecasts.
 TOL = {synth.F32: 1e-5, synth.BF16: 2e-2}
 

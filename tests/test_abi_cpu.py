@@ -22,7 +22,7 @@ def test_every_declared_symbol_is_exported():
     L = abi.lib()
     for name in declared:
         assert hasattr(L, name), name
-    assert abi.ff_abi_version() == 2
+    assert abi.ff_abi_version() == abi.FF_ABI_VERSION == 3
 
 
 def sched(T, R, K, S, mode, fm=abi.FF_RESIDUAL, eps=1e-8, stride=2):
@@ -130,7 +130,8 @@ def test_sizing():
 
 
 @pytest.mark.parametrize("over,code", [
-    (dict(C=260, H=4, d=65), abi.FF_E_SHAPE), (dict(d=60), abi.FF_E_SHAPE), (dict(B=9), abi.FF_E_SHAPE),
+    (dict(C=260, H=4, d=65), abi.FF_E_SHAPE), (dict(d=60), abi.FF_E_SHAPE), (dict(B=33), abi.FF_E_SHAPE),
+    (dict(B=0), abi.FF_E_SHAPE),
     (dict(n_img=63), abi.FF_E_SHAPE), (dict(dtype=7), abi.FF_E_DTYPE), (dict(n_txt=4), abi.FF_E_SHAPE),
     (dict(mlp=1001), abi.FF_E_SHAPE), (dict(ln_eps=0.0), abi.FF_E_RANGE)])
 def test_invalid_model_descriptors(over, code):

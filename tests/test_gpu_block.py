@@ -86,6 +86,18 @@ def test_dit_block_ragged(dtype, d):
 
 
 @pytest.mark.parametrize("dtype", [synth.F32, synth.BF16])
+@pytest.mark.parametrize("B", [9, 16, 27, 32])
+def test_dit_block_batch_groups(dtype, B):
+    # the modulation GEMV takes samples in groups of 8 (one weight read for all groups on
+    # MFMA, one launch per group in fp32): full, ragged and the largest batch
+    need_gpu()
+    cfg = ragged_cfg(synth.DIT, dtype, d=64, H=3, B=B, lat=(4, 1, 8, 10))
+    W = boosted(synth.make_layer_weights(cfg, 0, bias_std=0.02, gain_std=0.1), synth.DIT)
+    say(f"dit batch groups dtype={dtype} B={B}")
+    check_block(cfg, W)
+
+
+@pytest.mark.parametrize("dtype", [synth.F32, synth.BF16])
 @pytest.mark.parametrize("kind", [synth.MMDIT_DOUBLE, synth.MMDIT_SINGLE])
 def test_mmdit_blocks_ragged(dtype, kind):
     need_gpu()

@@ -112,6 +112,16 @@ def test_dit_xl2_reduced_depth_loop():
         check_against_oracle(cfg, W, inp, mode, mask, dm=dm)
 
 
+@pytest.mark.parametrize("dtype", [synth.F32, synth.BF16])
+def test_tiny_loop_batch_of_27(dtype):
+    """27 samples: four groups of 8 in the modulation GEMVs, the last ragged."""
+    need_gpu()
+    cfg = synth.get_config("tiny", B=27, T=6, dtype=dtype)
+    W = synth.make_weights(cfg, bias_std=0.02, gain_std=0.1)
+    say(f"tiny loop B=27 dtype={dtype}")
+    check_against_oracle(cfg, W, synth.make_inputs(cfg), abi.FF_FEATFIX, synth.site_mask(cfg))
+
+
 def mmdit_small(name, kinds, n_txt, lat, C=256, H=2, sites=(1,)):
     cfg = synth.get_config(name, kinds=kinds, C=C, H=H, d=C // H, mlp=4 * C, n_txt=n_txt, lat=lat,
                            n_img=lat[1] * (lat[2] // 2) * (lat[3] // 2), T=8, R=3, sites=list(sites))
