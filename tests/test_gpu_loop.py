@@ -112,6 +112,35 @@ def test_dit_xl2_reduced_depth_loop():
         check_against_oracle(cfg, W, inp, mode, mask, dm=dm)
 
 
+def test_dit_xl2_full_depth_sampled():
+    """The DiT-XL/2 workload as the bench runs it (28 blocks, C=1152, 256 tokens, batch 8,
+    R=5, K=2, sites {13,27}) over a 7-step schedule: two refreshes, five cached steps, the
+    second refresh's history read at step 6.  Samples never interact in a fixed-schedule
+    loop (per-sample LayerNorm rows, attention, modulation and Eq. 4 distance), so the
+    oracle follows samples 0 and 7 of the GPU's batch of 8."""
+    need_gpu()
+    cfg = synth.get_config("dit_xl2", T=7)
+    assert len(cfg["kinds"]) == 28 and cfg["B"] == 8 and cfg["sites"] == [13, 27]
+    W = synth.make_weights(cfg, bias_std=0.02, gain_std=0.1)
+    inp = synth.make_inputs(cfg)
+    mask = synth.site_mask(cfg)
+    say("dit_xl2 full depth, B=8 on the GPU, samples 0 and 7 in the oracle")
+    xt, audit, counts, plan = gpu_run(cfg, W, inp, abi.FF_FEATFIX, mask)
+    idx = [0, 7]
+    cfg2 = synth.get_config("dit_xl2", T=7, B=2)
+    inp2 = {k: v[idx] for k, v in inp.items()}
+    ref = O.run(cfg2, O.FEATFIX, inp2, W, mask)
+    err = O.max_rel_err(host(xt)[idx], ref["x"])
+    say(f"  max rel err {err:.3e} (tol {TOL[synth.BF16]}) counts {counts}")
+    assert err <= TOL[synth.BF16], err
+    assert counts == ref["counts"]
+    for key in ("step_kind", "refresh_ord", "k_eff", "read_slots", "write_slot", "action"):
+        np.testing.assert_array_equal(plan[key], ref["plan"][key])
+    a = audit.cpu().numpy()
+    for (i, l), d in ref["audit"].items():
+        np.testing.assert_allclose(a[i, l][idx], d, rtol=0, atol=TOL[synth.BF16])
+
+
 @pytest.mark.parametrize("dtype", [synth.F32, synth.BF16])
 def test_tiny_loop_batch_of_27(dtype):
     """27 samples: four groups of 8 in the modulation GEMVs, the last ragged."""
