@@ -37,6 +37,9 @@ PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
 CALIB_BYTES = 256 << 20     # plain copy of known size, the scale for FETCH_SIZE / WRITE_SIZE
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_gemm_dit_xl2.json")
 # the GEMM kernels and the device helpers their epilogue uses: traffic counters belong to these exact sources
+# runs of drafted layers applied from per-run history sums formed at the refreshes
+# (ff_ctx_hist_sums); --no-hist-sums drafts layer by layer
+HIST_SUMS = True
 GEMM_SOURCES = [os.path.join(ROOT, "paper_2607_27842_amd", "csrc", f) for f in ("k_gemm.hip", "dev_common.h")]
 
 
@@ -179,7 +182,7 @@ def adaptive_entry(dm, mask, fixed_loop, x0, cond, txt, n):
     a = fixed_loop.audit.view(r0.T, r0.L, -1).cpu().numpy()
     per_step = [float(np.nanmax(a[i])) for i in range(r0.T) if np.isfinite(a[i]).any()]
     tau = float(np.median(per_step))
-    r = pipeline.Runner(dm, abi.FF_FEATFIX, mask, tau=tau)
+    r = pipeline.Runner(dm, abi.FF_FEATFIX, mask, tau=tau, hist_sums=HIST_SUMS)
     loop = Loop(r, x0, cond, txt)
     for _ in range(r.T):
         loop.step()
@@ -213,7 +216,7 @@ def run_workload(name, mode_names, warmup_loops, timed_steps_n, with_profile, ad
     res = {"sites": synth.sites_of(cfg)}
     for mode_name in mode_names:
         mode = synth.MODE_NAMES[mode_name]
-        r = pipeline.Runner(dm, mode, mask)
+        r = pipeline.Runner(dm, mode, mask, hist_sums=HIST_SUMS)
         loop = Loop(r, x0, cond, txt)
         for _ in range(warmup_loops * r.T):
             loop.step()
@@ -226,6 +229,7 @@ def run_workload(name, mode_names, warmup_loops, timed_steps_n, with_profile, ad
         entry["ms_refresh_step"] = round(ref_ms, 4)
         entry["ms_cached_step"] = round(cac_ms, 4)
         entry["counts_per_loop"] = abi.ff_get_counts(r.ctx)
+        entry["hist_sums"] = r.hsum is not None
         if with_profile and mode_name == "featfix":
             entry["kernels"] = profile_loop(loop)
         log(f"[bench] {name} {mode_name}: {entry['steps_per_s']} steps/s "
@@ -257,11 +261,11 @@ def shadow_vanilla(name="dit_xl2"):
     E = B * (cfg["n_img"] + cfg["n_txt"]) * cfg["C"]
     dt = pipeline.torch_dtype(cfg)
     out = {}
-    van = pipeline.Runner(dm, abi.FF_VANILLA, mask)
+    van = pipeline.Runner(dm, abi.FF_VANILLA, mask, hist_sums=HIST_SUMS)
     vbuf = torch.empty(L * E, dtype=dt, device="cuda")
     van.trace_into(vbuf)
     for mode_name, mode in (("featfix", abi.FF_FEATFIX), ("verify", abi.FF_VERIFY)):
-        r = pipeline.Runner(dm, mode, mask)
+        r = pipeline.Runner(dm, mode, mask, hist_sums=HIST_SUMS)
         buf = torch.empty(L * E, dtype=dt, device="cuda")
         r.trace_into(buf)
         xr, _ = r.start(x0, audit=False)
@@ -298,7 +302,7 @@ def rope_loop():
     cfg = synth.get_config("flux", rope_axes=(16, 56, 56), rope_theta=10000.0)
     dm = pipeline.DeviceModel.random(cfg, seed=0)
     x0, cond, txt = device_inputs(cfg)
-    r = pipeline.Runner(dm, synth.MODE_NAMES["featfix"], synth.site_mask(cfg))
+    r = pipeline.Runner(dm, synth.MODE_NAMES["featfix"], synth.site_mask(cfg), hist_sums=HIST_SUMS)
     loop = Loop(r, x0, cond, txt)
     for _ in range(r.T):
         loop.step()
@@ -325,7 +329,7 @@ def guided_loop(scale=4.0):
     x0, cond, txt = device_inputs(cfg)
     out = {"model_rows": cfg["B"], "images": cfg["B"] // 2, "cfg_scale": scale}
     for mode in ("featfix", "vanilla"):
-        r = pipeline.Runner(dm, synth.MODE_NAMES[mode], synth.site_mask(cfg))
+        r = pipeline.Runner(dm, synth.MODE_NAMES[mode], synth.site_mask(cfg), hist_sums=HIST_SUMS)
         loop = Loop(r, x0, cond, txt)
         for _ in range(r.T):
             loop.step()
@@ -365,7 +369,7 @@ def resolution_sweep(sides=(512, 768, 1024)):
             torch.cuda.synchronize()
             torch.cuda.empty_cache()
             torch.cuda.reset_peak_memory_stats()
-            r = pipeline.Runner(dm, synth.MODE_NAMES[mode_name], mask)
+            r = pipeline.Runner(dm, synth.MODE_NAMES[mode_name], mask, hist_sums=HIST_SUMS)
             loop = Loop(r, x0, cond, txt)
             for _ in range(r.T):
                 loop.step()
@@ -374,7 +378,8 @@ def resolution_sweep(sides=(512, 768, 1024)):
             row[mode_name] = {"s_per_loop": round(ms / 1e3, 4),
                               "peak_gib": round(torch.cuda.max_memory_allocated() / 2**30, 2),
                               "cache_gib": round(r.cache_bytes / 2**30, 3),
-                              "workspace_gib": round(r.ws_bytes / 2**30, 3)}
+                              "workspace_gib": round(r.ws_bytes / 2**30, 3),
+                              "hist_sum_gib": round((0 if r.hsum is None else r.hsum.numel()) / 2**30, 3)}
             r.close()
             del loop, r
         row["speedup"] = round(row["vanilla"]["s_per_loop"] / row["featfix"]["s_per_loop"], 3)
@@ -441,7 +446,11 @@ def main():
     ap.add_argument("--no-sweep", action="store_true", help="skip the FLUX-like resolution sweep reported in extra")
     ap.add_argument("--no-guided", action="store_true", help="skip the guided (batch-doubled) DiT-XL/2 loops")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-hist-sums", action="store_true",
+                    help="apply runs of drafted layers layer by layer instead of from history sums")
     args = ap.parse_args()
+    global HIST_SUMS
+    HIST_SUMS = not args.no_hist_sums
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py runs on one GPU only: the FeatFix path here is single-GPU "
               "(no sharding or collectives); use --gpus 1", file=sys.stderr)

@@ -336,6 +336,29 @@ ff_status ff_ctx_step_kinds(const ff_ctx* c, int32_t* kinds);
 ff_status ff_denoise_step(ff_ctx* c, int32_t step, float* x, const float* cond,
                           const void* txt, float* audit, ff_stream_t stream);
 
+/* ---------------------------------------------------------------- history sums
+ * Eq. 2's draft is linear in the feature history.  A run of consecutive drafted layers
+ * l0..l1-1 of a cached step (residual features) therefore moves the stream by
+ * sum_m c_m * P_m, where P_m is the sum over the run's layers of the history slot the
+ * m-th term reads.  That sum changes only when a refresh rewrites the slot.
+ * ff_hist_sum_bytes(m, p): bytes of fp32 sums for plan p: runs * S * B*N*C * 4, where
+ * runs counts the distinct maximal runs of two or more drafted layers over the plan's
+ * cached steps (with tau > 0, over every step that may be cached).  Returns 0 when
+ * there is no such run, with output features, in Vanilla, or on an invalid descriptor.
+ * ff_ctx_hist_sums(c, buf, bytes): with buf set, each refresh step of c forms the sums
+ * of the slot it wrote (one fp32 pass per run, in layer order), and each such run of a
+ * cached step is applied in one pass from them:
+ *   X <- round(X + sum_m c_m P_m), one rounding to the model dtype per run.
+ * Without sums, the stream is rounded after every drafted layer.  The two agree to the
+ * model dtype's rounding; in bf16 this is not bit for bit.  While a trace buffer is set,
+ * runs are applied layer by layer.  buf is the caller's device memory, 16-byte aligned.
+ * It must stay untouched while c uses it.  buf NULL turns the sums off at any time.
+ * Errors: FF_E_NULL (c); FF_E_UNSUPPORTED (output features, Vanilla, or no run of two
+ * drafted layers); FF_E_STATE (enabling after step 0 before ff_ctx_reset: the sums of
+ * earlier refreshes are missing); FF_E_WORKSPACE (bytes); FF_E_SHAPE (alignment). */
+size_t ff_hist_sum_bytes(const ff_model_desc* m, const ff_plan* p);
+ff_status ff_ctx_hist_sums(ff_ctx* c, void* buf, size_t bytes);
+
 /* ---------------------------------------------------------------- diagnostics
  * Per-layer feature traces for mechanism studies on synthetic weights (the paper tracks
  * the downstream relative-L1 error of corrected runs against Vanilla per layer and stage,

@@ -8,7 +8,9 @@
 #include <stdio.h>
 #include <string.h>
 
+#include <algorithm>
 #include <new>
+#include <utility>
 #include <vector>
 
 #include "featfix.h"
@@ -273,6 +275,13 @@ struct Exec {
     return timed(FF_PROF_DRAFT, 0, ((double)t.n * layers + (resid ? 2.0 : 1.0)) * E * es,
                  [&] { return ff::draft_run(dt, t, layers, layer_stride, resid ? 1 : 0, x, E, st); });
   }
+  hipError_t hist_sum(const void* slot0, int layers, size_t layer_stride, float* out, size_t E) {
+    return timed(FF_PROF_CACHE, 0, ((double)layers * es + 4.0) * E,
+                 [&] { return ff::hist_sum(dt, slot0, layers, layer_stride, out, E, st); });
+  }
+  hipError_t draft_sum(const Terms& t, void* x, size_t E) {
+    return timed(FF_PROF_DRAFT, 0, (4.0 * t.n + 2.0 * es) * E, [&] { return ff::draft_sum(dt, t, x, E, st); });
+  }
   hipError_t draft(const Terms& t, const void* u, void* hd, size_t E) {
     return timed(FF_PROF_DRAFT, 0, (t.n + (u ? 2.0 : 1.0)) * E * es, [&] { return ff::draft(dt, t, u, hd, E, st); });
   }
@@ -507,6 +516,21 @@ struct CoefState {
   }
 };
 
+// The layer actions of step i as a cached step: SITE where the mask is set in the paid
+// modes, DRAFT elsewhere; in the recompute arm every layer after the first site is exact.
+void cached_actions(const ff_plan& p, int i, int32_t* row) {
+  const ff_sched_desc& s = p.s;
+  const int L = p.L;
+  const bool paid_mode = s.mode >= FF_VERIFY && s.mode != FF_DRAFT;
+  bool paid_seen = false;
+  for (int l = 0; l < L; ++l) {
+    int a = paid_mode && p.mask[(size_t)i * L + l] ? FF_ACT_SITE : FF_ACT_DRAFT;
+    if (s.mode == FF_RECOMPUTE && paid_seen) a = FF_ACT_RECOMPUTE;   // the rest of the step, exact
+    paid_seen = paid_seen || a == FF_ACT_SITE;
+    row[l] = a;
+  }
+}
+
 // Row i of a plan: a refresh (ordinal j, written to slot j % S) or a cached step that
 // reads the ring with the coefficients of cs at step i, with SITE where the mask is set
 // in the paid modes.  cs must already hold the refreshes up to step i.
@@ -532,14 +556,35 @@ void plan_row(ff_plan* p, int i, bool refresh, int j, const CoefState& cs) {
   float c[FF_MAX_K + 2] = {};
   cs.coeffs((double)i, c);
   for (int q = 0; q <= ke; ++q) p->coeffs[(size_t)i * (K + 1) + q] = c[q];
-  const bool paid_mode = s.mode >= FF_VERIFY && s.mode != FF_DRAFT;
-  bool paid_seen = false;
-  for (int l = 0; l < L; ++l) {
-    int a = paid_mode && p->mask[(size_t)i * L + l] ? FF_ACT_SITE : FF_ACT_DRAFT;
-    if (s.mode == FF_RECOMPUTE && paid_seen) a = FF_ACT_RECOMPUTE;   // the rest of the step, exact
-    paid_seen = paid_seen || a == FF_ACT_SITE;
-    p->action[(size_t)i * L + l] = a;
+  cached_actions(*p, i, &p->action[(size_t)i * L]);
+}
+
+// With history sums, the layers a run may cover: drafted layers off the site set.  A
+// masked layer is a run of its own even in Draft, where it is drafted, so that Draft and
+// Verify round their streams at the same layers and stay bitwise equal.
+inline bool summable(const ff_plan& p, int i, int l, int32_t act) {
+  return act == FF_ACT_DRAFT && !p.mask[(size_t)i * p.L + l];
+}
+
+// Maximal runs [l0, l1) of two or more summable layers on the steps that are, or (with an
+// adaptive schedule) may become, cached steps: the runs a history sum can stand in for.
+std::vector<std::pair<int, int>> plan_runs(const ff_plan& p) {
+  std::vector<std::pair<int, int>> runs;
+  const int L = p.L;
+  std::vector<int32_t> row(L);
+  for (int i = 1; i < p.s.T; ++i) {
+    if (p.s.tau <= 0.f && p.step_kind[i] != FF_STEP_CACHED) continue;
+    cached_actions(p, i, row.data());
+    for (int l = 0; l < L;) {
+      if (!summable(p, i, l, row[l])) { ++l; continue; }
+      int l1 = l + 1;
+      while (l1 < L && summable(p, i, l1, row[l1])) ++l1;
+      if (l1 - l >= 2 && std::find(runs.begin(), runs.end(), std::make_pair(l, l1)) == runs.end())
+        runs.emplace_back(l, l1);
+      l = l1;
+    }
   }
+  return runs;
 }
 
 // the modes that forward (all or part of) the exact output of a paid site
@@ -568,6 +613,9 @@ struct ff_ctx {
   hipEvent_t a_ev = nullptr;
   bool a_checked = false;
   void* trace = nullptr;   // per-layer stream copies (ff_ctx_trace), [L][B*N*C]
+  // history sums (ff_ctx_hist_sums): fp32 [runs][S][B*N*C], formed at every refresh
+  float* hsum = nullptr;
+  std::vector<std::pair<int, int>> runs;
   ~ff_ctx() {
     if (a_ev) (void)hipEventDestroy(a_ev);
     if (a_rel) (void)hipHostFree(a_rel);
@@ -1047,9 +1095,27 @@ ff_status ff_denoise_step(ff_ctx* c, int32_t step, float* x, const float* cond, 
         // the maximal run of drafted layers starting here, applied in one pass (same bits);
         // layer by layer while tracing
         int l2 = l + 1;
-        while (!c->trace && l2 < L && p.action[(size_t)i * L + l2] == FF_ACT_DRAFT) ++l2;
-        if (l2 - l == 1) HIP_TRY(ex.draft(tm, resid ? cur : nullptr, cur, E), "draft");
-        else HIP_TRY(ex.draft_run(tm, l2 - l, (size_t)S * E, resid, cur, E), "draft run");
+        if (c->hsum && !summable(p, i, l, act)) {
+          // a masked layer in Draft: drafted alone, as Verify's site drafts it
+        } else if (c->hsum) {
+          while (!c->trace && l2 < L && summable(p, i, l2, p.action[(size_t)i * L + l2])) ++l2;
+        } else {
+          while (!c->trace && l2 < L && p.action[(size_t)i * L + l2] == FF_ACT_DRAFT) ++l2;
+        }
+        int r = -1;
+        if (c->hsum && resid && l2 - l >= 2)
+          for (int q = 0; q < (int)c->runs.size(); ++q)
+            if (c->runs[q] == std::make_pair(l, l2)) r = q;
+        if (r >= 0) {   // the run from its history sums (formed at the refreshes)
+          Terms ts = tm;
+          for (int q = 0; q < ts.n; ++q)
+            ts.slot[q] = c->hsum + ((size_t)r * S + p.read_slots[(size_t)i * (K + 1) + q]) * E;
+          HIP_TRY(ex.draft_sum(ts, cur, E), "draft from history sums");
+        } else if (l2 - l == 1) {
+          HIP_TRY(ex.draft(tm, resid ? cur : nullptr, cur, E), "draft");
+        } else {
+          HIP_TRY(ex.draft_run(tm, l2 - l, (size_t)S * E, resid, cur, E), "draft run");
+        }
         l = l2 - 1;
         if (ff_status te = trace_to(l)) return te;
         continue;
@@ -1069,6 +1135,15 @@ ff_status ff_denoise_step(ff_ctx* c, int32_t step, float* x, const float* cond, 
       HIP_TRY(ex.verify(tm, resid ? cur : nullptr, hf, cur, fw, m.B, (size_t)m.N * C, s.eps,
                         rel, at<float>(ws, W.PART)), "verify");
       if (ff_status te = trace_to(l)) return te;
+    }
+    // a refresh rewrote slot write_slot of every layer: re-form each run's sum of it
+    if (c->hsum && p.step_kind[i] == FF_STEP_REFRESH && mode != FF_VANILLA) {
+      const int ws_i = p.write_slot[i];
+      for (size_t r = 0; r < c->runs.size(); ++r) {
+        const int l0 = c->runs[r].first, n = c->runs[r].second - l0;
+        HIP_TRY(ex.hist_sum((const char*)c->cache + ((size_t)l0 * S + ws_i) * tb, n, (size_t)S * E,
+                            c->hsum + (r * S + ws_i) * E, E), "history sums");
+      }
     }
     // final layer on the image rows, unpatchify and Euler
     float* mod = at<float>(ws, W.MOD);
@@ -1119,6 +1194,42 @@ ff_status ff_denoise_step(ff_ctx* c, int32_t step, float* x, const float* cond, 
       }
     }
     c->next_step++;
+    return ok();
+  } catch (...) {
+    return fail(FF_E_UNSUPPORTED, "unexpected host exception");
+  }
+}
+
+size_t ff_hist_sum_bytes(const ff_model_desc* m, const ff_plan* p) {
+  Model md;
+  if (!p || check_model(m, &md) != FF_OK || md.L != p->L) return 0;
+  if (p->s.feature_mode != FF_RESIDUAL || p->s.mode == FF_VANILLA) return 0;
+  try {
+    return plan_runs(*p).size() * (size_t)p->s.S * md.E() * sizeof(float);
+  } catch (...) {
+    return 0;
+  }
+}
+
+ff_status ff_ctx_hist_sums(ff_ctx* c, void* buf, size_t bytes) {
+  try {
+    if (!c) return fail(FF_E_NULL, "ctx is NULL");
+    if (!buf) {
+      c->hsum = nullptr;
+      c->runs.clear();
+      return ok();
+    }
+    const ff_plan& p = c->plan;
+    if (p.s.feature_mode != FF_RESIDUAL || p.s.mode == FF_VANILLA)
+      return fail(FF_E_UNSUPPORTED, "history sums need residual features and a cached mode");
+    if (c->next_step != 0) return fail(FF_E_STATE, "history sums are enabled before step 0 (or after ff_ctx_reset)");
+    std::vector<std::pair<int, int>> runs = plan_runs(p);
+    if (runs.empty()) return fail(FF_E_UNSUPPORTED, "the plan has no run of two or more drafted layers");
+    const size_t need = runs.size() * (size_t)p.s.S * c->m.E() * sizeof(float);
+    if (bytes < need) return fail(FF_E_WORKSPACE, "history sum buffer %zu < %zu bytes", bytes, need);
+    if (!aligned16(buf)) return fail(FF_E_SHAPE, "history sum buffer must be 16-byte aligned");
+    c->runs = std::move(runs);
+    c->hsum = static_cast<float*>(buf);
     return ok();
   } catch (...) {
     return fail(FF_E_UNSUPPORTED, "unexpected host exception");

@@ -90,6 +90,59 @@ __global__ __launch_bounds__(kThreads) void k_draft_run(Terms t, int layers, siz
   }
 }
 
+// History sum of a run of drafted layers (residual features): P = sum over the run's
+// layers, in layer order, of one ring slot, in fp32.  Eq. 2's draft is linear in the
+// history, so a run l0..l1-1 of drafted layers moves the stream by sum_m c_m P_m (P_m the
+// sum of slot m over the run): formed once when a refresh rewrites the slot and read by
+// every cached step until the slot is rewritten again.
+template <int DT>
+__global__ __launch_bounds__(kThreads) void k_hist_sum(const void* __restrict__ slot0, int layers, size_t layer_stride,
+                                                       float* __restrict__ out, size_t nchunk) {
+  using S = St<DT>;
+  for (size_t c = (size_t)blockIdx.x * kThreads + threadIdx.x; c < nchunk; c += (size_t)gridDim.x * kThreads) {
+    const size_t i = c * S::V;
+    float acc[S::V], v[S::V];
+    S::load_nt(slot0, i, acc);
+    for (int l = 1; l < layers; ++l) {
+      S::load_nt(slot0, (size_t)l * layer_stride + i, v);
+#pragma unroll
+      for (int j = 0; j < S::V; ++j) acc[j] += v[j];
+    }
+#pragma unroll
+    for (int j = 0; j < S::V; j += 4)
+      *reinterpret_cast<float4*>(out + i + j) = make_float4(acc[j], acc[j + 1], acc[j + 2], acc[j + 3]);
+  }
+}
+
+// A whole run of drafted layers from its history sums: x <- round(x + sum_m c_m P_m), the
+// terms in fp32 (t.slot[m] points at fp32 sums), one rounding to the storage type.
+template <int DT>
+__global__ __launch_bounds__(kThreads) void k_draft_sum(Terms t, void* x, size_t nchunk) {
+  using S = St<DT>;
+  for (size_t c = (size_t)blockIdx.x * kThreads + threadIdx.x; c < nchunk; c += (size_t)gridDim.x * kThreads) {
+    const size_t i = c * S::V;
+    float xv[S::V], f[S::V];
+    S::load(x, i, xv);
+#pragma unroll
+    for (int j = 0; j < S::V; ++j) f[j] = 0.0f;
+#pragma unroll
+    for (int m = 0; m < kMaxTerms; ++m) {
+      if (m < t.n) {
+#pragma unroll
+        for (int j = 0; j < S::V; j += 4) {
+          float p[4];
+          St<DT_F32>::load_nt(t.slot[m], i + j, p);
+#pragma unroll
+          for (int q = 0; q < 4; ++q) f[j + q] = fmaf(t.c[m], p[q], f[j + q]);
+        }
+      }
+    }
+#pragma unroll
+    for (int j = 0; j < S::V; ++j) xv[j] = S::rnd(xv[j] + f[j]);
+    S::store(x, i, xv);
+  }
+}
+
 template <int DT, bool RES>
 __global__ __launch_bounds__(kThreads) void k_draft(Terms t, const void* u, void* hd, size_t nchunk) {
   using S = St<DT>;
@@ -257,6 +310,26 @@ hipError_t draft_run(int dtype, const Terms& t, int layers, size_t layer_stride,
     if (residual) FF_LAUNCH((k_draft_run<DT_F32, true>), grid_for(n), kThreads, 0, s, t, layers, layer_stride, x, n);
     else FF_LAUNCH((k_draft_run<DT_F32, false>), grid_for(n), kThreads, 0, s, t, layers, layer_stride, x, n);
   }
+  return hipGetLastError();
+}
+
+hipError_t hist_sum(int dtype, const void* slot0, int layers, size_t layer_stride, float* out, size_t E,
+                    hipStream_t s) {
+  if (layers < 1) return hipErrorInvalidValue;
+  if (dtype == DT_BF16) {
+    const size_t n = E / 8;
+    FF_LAUNCH((k_hist_sum<DT_BF16>), grid_for(n), kThreads, 0, s, slot0, layers, layer_stride, out, n);
+  } else {
+    const size_t n = E / 4;
+    FF_LAUNCH((k_hist_sum<DT_F32>), grid_for(n), kThreads, 0, s, slot0, layers, layer_stride, out, n);
+  }
+  return hipGetLastError();
+}
+
+hipError_t draft_sum(int dtype, const Terms& t, void* x, size_t E, hipStream_t s) {
+  if (t.n < 1 || t.n > kMaxTerms) return hipErrorInvalidValue;
+  if (dtype == DT_BF16) FF_LAUNCH((k_draft_sum<DT_BF16>), grid_for(E / 8), kThreads, 0, s, t, x, E / 8);
+  else FF_LAUNCH((k_draft_sum<DT_F32>), grid_for(E / 4), kThreads, 0, s, t, x, E / 4);
   return hipGetLastError();
 }
 

@@ -148,6 +148,12 @@ hipError_t draft(int dtype, const Terms& t, const void* u, void* hd, size_t E, h
 // elements further.  Bit-identical to `layers` draft() calls.
 hipError_t draft_run(int dtype, const Terms& t, int layers, size_t layer_stride, int residual, void* x, size_t E,
                      hipStream_t s);
+// History sums for runs of drafted layers (residual features): out = sum_{l < layers} of
+// the slot at slot0 + l * layer_stride, in layer order, fp32 [E].
+hipError_t hist_sum(int dtype, const void* slot0, int layers, size_t layer_stride, float* out, size_t E,
+                    hipStream_t s);
+// A run applied from its history sums: x <- round(x + sum_m c_m P_m), t.slot[m] = fp32 P_m.
+hipError_t draft_sum(int dtype, const Terms& t, void* x, size_t E, hipStream_t s);
 // Fused draft rebuild + rel-L1 partial sums + forwarding, then a fixed-order reduction.
 // What the pass writes to hout: the draft, the exact output, or the exact output on every
 // stride-th row (token) / channel of a sample with C channels and the draft elsewhere.

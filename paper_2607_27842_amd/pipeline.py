@@ -121,7 +121,7 @@ class Runner:
     """A plan + cache + workspace + context for one mode of one model."""
 
     def __init__(self, dm: DeviceModel, mode, mask, feature_mode=abi.FF_RESIDUAL, T=None, R=None, K=None,
-                 S=None, eps=None, tau=0.0, part_stride=2, device=_DEV):
+                 S=None, eps=None, tau=0.0, part_stride=2, hist_sums=False, device=_DEV):
         cfg = dm.cfg
         self.dm = dm
         self.T = cfg["T"] if T is None else T
@@ -140,6 +140,13 @@ class Runner:
         self.ws = torch.empty(self.ws_bytes, dtype=torch.uint8, device=device)
         self.ctx = abi.ff_ctx_create(dm.desc, dm.lw, dm.g, self.plan, self.cache.data_ptr(), self.cache_bytes,
                                      self.ws.data_ptr(), self.ws_bytes)
+        # runs of drafted layers applied from per-run history sums formed at the refreshes
+        self.hsum = None
+        if hist_sums:
+            nb = abi.ff_hist_sum_bytes(dm.desc, self.plan)
+            if nb:
+                self.hsum = torch.empty(nb, dtype=torch.uint8, device=device)
+                abi.ff_ctx_hist_sums(self.ctx, self.hsum.data_ptr(), nb)
 
     def export_plan(self):
         return abi.ff_plan_export(self.plan, self.T, self.L, self.K)

@@ -251,3 +251,86 @@ def test_rope_descriptor_checks():
         m = pipeline.model_desc(cfg)
         got = abi.lib().ff_block_exact(C.byref(m), 0, None, None, None, None, None, 0, None)
         assert got == code, (axes, theta, got)
+
+
+def oracle_runs(T, L, R, K, S, mask, mode):
+    """Maximal runs of two or more drafted layers off the site set over the cached steps of
+    the oracle's schedule: the runs a history sum stands in for (a masked layer is a run of
+    its own in Draft too, so that Draft and Verify round at the same layers)."""
+    ref = O.make_plan(T, L, R, K, S, mask, mode)
+    runs = set()
+    for i in range(T):
+        if ref["step_kind"][i] != O.CACHED_STEP:
+            continue
+        row, l = ref["action"][i], 0
+        summable = [row[q] == O.DRAFT_ACT and not mask[i, q] for q in range(L)]
+        while l < L:
+            if not summable[l]:
+                l += 1
+                continue
+            l1 = l + 1
+            while l1 < L and summable[l1]:
+                l1 += 1
+            if l1 - l >= 2:
+                runs.add((l, l1))
+            l = l1
+    return runs
+
+
+@pytest.mark.parametrize("name", ["tiny", "dit_xl2", "flux", "qwen", "hunyuan"])
+@pytest.mark.parametrize("mode", [abi.FF_VANILLA, abi.FF_DRAFT, abi.FF_VERIFY, abi.FF_FEATFIX, abi.FF_EXACT_ONLY,
+                                  abi.FF_TOKENS_PARTIAL, abi.FF_RECOMPUTE])
+def test_hist_sum_bytes_count_the_drafted_runs(name, mode):
+    cfg = synth.get_config(name)
+    T, L, S = cfg["T"], len(cfg["kinds"]), cfg["S"]
+    m = pipeline.model_desc(cfg)
+    mask = synth.site_mask(cfg)
+    p = abi.ff_plan_build(sched(T, cfg["R"], cfg["K"], S, mode), L, mask.reshape(-1))
+    E = cfg["B"] * (cfg["n_img"] + cfg["n_txt"]) * cfg["C"]
+    runs = oracle_runs(T, L, cfg["R"], cfg["K"], S, mask, mode)
+    want = 0 if mode == abi.FF_VANILLA else len(runs) * S * E * 4
+    assert abi.ff_hist_sum_bytes(m, p) == want
+    if name == "dit_xl2" and mode == abi.FF_FEATFIX:
+        assert runs == {(0, 13), (14, 27)}
+    if name == "flux" and mode == abi.FF_VERIFY:
+        assert runs == {(0, 18), (19, 37), (38, 56)}
+    if mode == abi.FF_DRAFT:
+        assert runs == oracle_runs(T, L, cfg["R"], cfg["K"], S, mask, abi.FF_VERIFY)
+        assert oracle_runs(T, L, cfg["R"], cfg["K"], S, np.zeros_like(mask), mode) == {(0, L)}
+    abi.ff_plan_destroy(p)
+    # output features: the draft does not telescope along a run, no sums
+    po = abi.ff_plan_build(sched(T, cfg["R"], cfg["K"], S, mode, fm=abi.FF_OUTPUT), L, mask.reshape(-1))
+    assert abi.ff_hist_sum_bytes(m, po) == 0
+    abi.ff_plan_destroy(po)
+
+
+def test_hist_sums_errors_are_host_side():
+    cfg, m = tiny_desc()
+    T, L = cfg["T"], 4
+    lw, g = fake_weights(L)
+    cb, wb = abi.ff_cache_bytes(m, 2), abi.ff_workspace_bytes(m)
+    Lb = abi.lib()
+    # tiny: sites {1, 3} leave no run of two drafted layers; Draft without sites has one
+    # run of all four
+    plan = abi.ff_plan_build(sched(T, 3, 1, 2, abi.FF_FEATFIX), L, synth.site_mask(cfg))
+    assert abi.ff_hist_sum_bytes(m, plan) == 0
+    ctx = abi.ff_ctx_create(m, lw, g, plan, 1 << 30, cb, 2 << 30, wb)
+    assert Lb.ff_ctx_hist_sums(ctx, 3 << 30, 1 << 20) == abi.FF_E_UNSUPPORTED
+    abi.ff_ctx_destroy(ctx)
+    abi.ff_plan_destroy(plan)
+    plan = abi.ff_plan_build(sched(T, 3, 1, 2, abi.FF_DRAFT), L, np.zeros(T * L, np.uint8))
+    need = abi.ff_hist_sum_bytes(m, plan)
+    assert need == 2 * m.B * (m.n_img + m.n_txt) * m.C * 4
+    ctx = abi.ff_ctx_create(m, lw, g, plan, 1 << 30, cb, 2 << 30, wb)
+    assert Lb.ff_ctx_hist_sums(None, 3 << 30, need) == abi.FF_E_NULL
+    assert Lb.ff_ctx_hist_sums(ctx, 3 << 30, need - 1) == abi.FF_E_WORKSPACE
+    assert Lb.ff_ctx_hist_sums(ctx, (3 << 30) + 8, need) == abi.FF_E_SHAPE
+    assert Lb.ff_ctx_hist_sums(ctx, 3 << 30, need) == abi.FF_OK
+    assert Lb.ff_ctx_hist_sums(ctx, None, 0) == abi.FF_OK
+    abi.ff_ctx_destroy(ctx)
+    abi.ff_plan_destroy(plan)
+    plan = abi.ff_plan_build(sched(T, 3, 1, 2, abi.FF_VANILLA), L, synth.site_mask(cfg))
+    ctx = abi.ff_ctx_create(m, lw, g, plan, 1 << 30, cb, 2 << 30, wb)
+    assert Lb.ff_ctx_hist_sums(ctx, 3 << 30, need) == abi.FF_E_UNSUPPORTED
+    abi.ff_ctx_destroy(ctx)
+    abi.ff_plan_destroy(plan)
