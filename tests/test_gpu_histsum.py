@@ -171,3 +171,33 @@ def test_flux_like_full_size_with_history_sums():
     say(f"flux full size: sums vs per-layer drafts max rel diff {d:.3e}")
     assert d <= TOL[synth.BF16]
     torch.cuda.empty_cache()
+
+
+@pytest.mark.parametrize("mode", [abi.FF_FEATFIX, abi.FF_VERIFY])
+def test_adaptive_refreshes_with_history_sums_match_oracle(mode):
+    """A threshold that makes some cached steps trigger a refresh (chosen from the oracle's
+    own discrepancies, every deciding value more than 1 % from it): the sums are re-formed
+    at the refreshes the run decides, and the GPU takes the oracle's decisions step for
+    step with runs (0, 3) and (4, 6) applied from them."""
+    from test_gpu_adaptive import pick_tau
+    need_gpu()
+    cfg = dict(tiny6(K=2, S=3), T=10, R=4)
+    W = synth.make_weights(cfg, bias_std=0.02, gain_std=0.1)
+    inp = synth.make_inputs(cfg)
+    mask = synth.site_mask(cfg)
+    tau, ref = pick_tau(cfg, W, inp, O.FEATFIX if mode == abi.FF_FEATFIX else O.VERIFY, mask)
+    dm = pipeline.DeviceModel.from_host(cfg, *W)
+    r = pipeline.Runner(dm, mode, mask, tau=tau, hist_sums=True)
+    assert r.hsum is not None
+    x, audit, counts = r.run(*pipeline.host_inputs_to_device(cfg, inp))
+    torch.cuda.synchronize()
+    kinds = r.step_kinds()
+    r.close()
+    say(f"adaptive tiny6 with sums mode={mode} tau={tau:.4e}: kinds {list(kinds)}")
+    assert list(kinds) == ref["step_kind"]
+    assert counts == ref["counts"]
+    err = O.max_rel_err(host(x), ref["x"])
+    assert err <= TOL[synth.F32], err
+    a = audit.cpu().numpy()
+    for (i, l), d in ref["audit"].items():
+        np.testing.assert_allclose(a[i, l], d, rtol=0, atol=TOL[synth.F32])
