@@ -512,7 +512,9 @@ def main():
            "warmup": warm_loops * T, "ms_per_step": round(ms_step, 4), "higher_is_better": True, "scaling": "weak",
            "vs_baseline": None, "dtype": "bf16",
            "data": "synthetic: seeded N(0,1) latent and class/text vectors, random-init N(0,0.02) weights",
-           "config": {"workload": WORKLOAD_TEXT[name], "global_batch": cfg["B"],
+           "config": {"workload": WORKLOAD_TEXT[name] + ("; drafted runs from history sums" if HIST_SUMS
+                                                         else "; drafted runs layer by layer"),
+                      "global_batch": cfg["B"],
                       "seq_len": cfg["n_img"] + cfg["n_txt"], "parallelism": "none (1 GPU)"},
            "roofline": roof}
     if not args.no_cpu_baseline and name == "dit_xl2":
