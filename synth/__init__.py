@@ -228,3 +228,24 @@ def normal(shape, seed, std=1.0, bf16=False):
     """Generic seeded N(0, std^2) fp32 tensor (optionally bf16-valued) for kernel tests."""
     a = _normal(shape, std, 99, seed)
     return to_bf16_values(a) if bf16 else a
+
+
+def reduced_stack(name: str) -> dict:
+    """Reduced-depth, full-width parity stacks of the MMDiT workloads: every block at the
+    workload's full hidden size, heads, MLP width, token counts and batch, fewer blocks
+    and steps (refresh every 3 steps), sites by the workload's own rule applied to the
+    shorter stack, and enough blocks that a cached step has a run of two or more drafted
+    layers (the runs the history sums stand in for).
+      flux:    3 double + 5 single; sites last double, middle single, last single {2, 4, 7}
+      qwen:    4 double, K = 2, S = 3, 1 site drawn by SplitMix64(0) as the 60-layer rule
+               draws 4; T = 8 puts step 7 at k_eff = 2
+      hunyuan: 5 double over 14 310 + 256 tokens, sites middle (L/2 - 1) and last {1, 4};
+               T = 5 (refreshes 0 and 3)"""
+    if name == "flux":
+        return get_config("flux", kinds=[MMDIT_DOUBLE] * 3 + [MMDIT_SINGLE] * 5, T=8, R=3, sites=[2, 4, 7])
+    if name == "qwen":
+        return get_config("qwen", kinds=[MMDIT_DOUBLE] * 4, T=8, R=3, site_rule="fixed",
+                          sites=splitmix_sites(4, 1, 0))
+    if name == "hunyuan":
+        return get_config("hunyuan", kinds=[MMDIT_DOUBLE] * 5, T=5, R=3, sites=[1, 4])
+    raise KeyError(name)

@@ -8,7 +8,7 @@ import torch
 import oracle as O
 import synth
 from paper_2607_27842_amd import abi, pipeline
-from gpu_util import TOL, host, need_gpu, say
+from gpu_util import TOL, check_audit, host, need_gpu, say
 
 pytestmark = pytest.mark.gpu
 
@@ -43,9 +43,7 @@ def test_arm_loops_match_oracle(arm):
     assert counts == ref["counts"]
     for key in ("step_kind", "refresh_ord", "k_eff", "read_slots", "write_slot", "action"):
         np.testing.assert_array_equal(plan[key], ref["plan"][key])
-    a = audit.cpu().numpy()
-    for (i, l), d in ref["audit"].items():
-        np.testing.assert_allclose(a[i, l], d, rtol=0, atol=TOL[cfg["dtype"]])
+    check_audit(audit.cpu().numpy(), ref["audit"], cfg["dtype"])
 
 
 @pytest.mark.parametrize("dtype", [synth.F32, synth.BF16])

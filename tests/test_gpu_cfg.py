@@ -8,7 +8,7 @@ import torch
 import oracle as O
 import synth
 from paper_2607_27842_amd import abi, pipeline
-from gpu_util import TOL, host, need_gpu, say
+from gpu_util import TOL, check_audit, host, need_gpu, say
 
 pytestmark = pytest.mark.gpu
 
@@ -27,9 +27,7 @@ def check(cfg, W, inp, mode, mask, dm=None):
     say(f"  guided {cfg['name']} B={cfg['B']} s={cfg['cfg_scale']} mode={mode}: max rel err {err:.3e} (tol {tol})")
     assert err <= tol, err
     assert counts == ref["counts"]
-    a = audit.cpu().numpy()
-    for (i, l), d in ref["audit"].items():
-        np.testing.assert_allclose(a[i, l], d, rtol=0, atol=tol)
+    check_audit(audit.cpu().numpy(), ref["audit"], cfg["dtype"])
 
 
 @pytest.mark.parametrize("B", [2, 4])

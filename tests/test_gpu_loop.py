@@ -7,7 +7,7 @@ import torch
 import oracle as O
 import synth
 from paper_2607_27842_amd import abi, pipeline
-from gpu_util import TOL, host, need_gpu, say
+from gpu_util import TOL, check_audit, host, need_gpu, say
 
 pytestmark = pytest.mark.gpu
 
@@ -38,8 +38,7 @@ def check_against_oracle(cfg, W, inp, mode, mask, feature_mode=abi.FF_RESIDUAL, 
         np.testing.assert_array_equal(plan[key], ref["plan"][key])
     a = audit.cpu().numpy()
     L = len(cfg["kinds"])
-    for (i, l), d in ref["audit"].items():
-        np.testing.assert_allclose(a[i, l], d, rtol=0, atol=tol)
+    check_audit(a, ref["audit"], cfg["dtype"])
     paid = np.zeros((cfg["T"], L), bool)
     for (i, l) in ref["audit"]:
         paid[i, l] = True
@@ -136,9 +135,7 @@ def test_dit_xl2_full_depth_sampled():
     assert counts == ref["counts"]
     for key in ("step_kind", "refresh_ord", "k_eff", "read_slots", "write_slot", "action"):
         np.testing.assert_array_equal(plan[key], ref["plan"][key])
-    a = audit.cpu().numpy()
-    for (i, l), d in ref["audit"].items():
-        np.testing.assert_allclose(a[i, l][idx], d, rtol=0, atol=TOL[synth.BF16])
+    check_audit(audit.cpu().numpy(), ref["audit"], synth.BF16, idx)
 
 
 @pytest.mark.parametrize("dtype", [synth.F32, synth.BF16])

@@ -123,3 +123,36 @@ def test_abi_threshold_plan_is_the_fixed_schedule():
             np.testing.assert_array_equal(ea[k], ef[k])
     abi.ff_plan_destroy(pa)
     abi.ff_plan_destroy(pf)
+
+
+def test_decision_takes_the_largest_discrepancy_over_samples():
+    """B = 2 with a threshold that only sample 1's discrepancy exceeds at the first checked
+    step: the step after it must refresh (the rule's maximum runs over sites and samples).
+    tau sits above the mean of the two samples' maxima, so a reading that used sample 0
+    only, or any mean over samples, would keep the step cached; run alone, sample 0 keeps
+    it cached and sample 1 refreshes."""
+    cfg, W, _ = tiny(T=9, R=4)
+    cfg["B"] = 2
+    inp = synth.make_inputs(cfg)
+    mask = synth.site_mask(cfg)
+    fixed = O.run(cfg, O.FEATFIX, inp, W, mask)
+    first = min(i for (i, _l) in fixed["audit"])
+    per_sample = np.max(np.stack([d for (i, _l), d in fixed["audit"].items() if i == first]), axis=0)
+    if per_sample[0] > per_sample[1]:   # put the larger discrepancy on sample 1
+        inp = {k: v[::-1].copy() for k, v in inp.items()}
+        per_sample = per_sample[::-1]
+    lo, hi = float(per_sample[0]), float(per_sample[1])
+    assert hi > lo * 1.01, (lo, hi)
+    tau = 0.5 * (0.5 * (lo + hi)) + 0.5 * hi      # in ((lo + hi) / 2, hi)
+    both = O.run(cfg, O.FEATFIX, inp, W, mask, tau=tau)
+    assert both["step_kind"][first + 1] == O.REFRESH_STEP
+    alone = []
+    for b in (0, 1):
+        one = {k: v[b:b + 1] for k, v in inp.items()}
+        r = O.run(dict(cfg, B=1), O.FEATFIX, one, W, mask, tau=tau)
+        # the pair's audit of the first checked step is each sample's own (samples never mix)
+        for (i, l), d in r["audit"].items():
+            if i == first:
+                np.testing.assert_allclose(d[0], both["audit"][(i, l)][b], rtol=1e-12)
+        alone.append(r["step_kind"][first + 1])
+    assert alone == [O.CACHED_STEP, O.REFRESH_STEP]

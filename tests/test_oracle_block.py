@@ -216,3 +216,76 @@ def test_flux_flop_model_against_table_1():
     for row in fx["rows"]:
         paper = row["tflops"] * 1e12 / row["steps"]
         assert abs(per_step / paper - 1) < fx["tolerance_rel"], (row, per_step)
+
+
+def rope_cfg(kind, n_txt=3, C=64, H=2, axes=(8, 12, 12), theta=10000.0):
+    """A block with rotary q / k over a 2 x 3 x 4 patch grid (frames, rows, columns)."""
+    d = C // H
+    cfg = small_cfg(kind, n_txt=n_txt, C=C, H=H, N=n_txt + 24)
+    cfg.update(lat=(4, 2, 6, 8), patch=(1, 2, 2), rope_axes=axes, rope_theta=theta)
+    assert sum(axes) == d
+    return cfg
+
+
+def torch_rope(x, cfg):
+    """Rotary embedding written as complex multiplication: consecutive dim pairs of each
+    head vector are complex numbers, multiplied by exp(i * pos_a * theta^(-2k / d_a)) per
+    axis chunk; positions from a meshgrid of the patch grid, text rows at the origin."""
+    _, F, Hh, Wd = cfg["lat"]
+    pt, ph, pw = cfg["patch"]
+    grid = torch.meshgrid(torch.arange(F // pt), torch.arange(Hh // ph), torch.arange(Wd // pw), indexing="ij")
+    img = torch.stack([g.reshape(-1) for g in grid], dim=-1).double()
+    pos = torch.cat([torch.zeros(cfg["n_txt"], 3, dtype=torch.float64), img], dim=0)     # [N, 3]
+    rot = []
+    for a, da in enumerate(cfg["rope_axes"]):
+        freq = cfg["rope_theta"] ** (-torch.arange(0, da, 2, dtype=torch.float64) / da)
+        rot.append(torch.polar(torch.ones(pos.shape[0], da // 2, dtype=torch.float64), pos[:, a:a + 1] * freq))
+    rot = torch.cat(rot, dim=-1)                                                        # [N, d/2]
+    xc = torch.view_as_complex(x.reshape(*x.shape[:-1], -1, 2).contiguous())
+    return torch.view_as_real(xc * rot).reshape(x.shape)
+
+
+def test_double_block_with_rope_matches_torch_composition():
+    """q and k are rotated after their per-head RMS norms, over the joint [txt; img] rows."""
+    cfg = rope_cfg(synth.MMDIT_DOUBLE)
+    W = perturbed(cfg)
+    rng = np.random.default_rng(10)
+    N, nt = cfg["n_txt"] + cfg["n_img"], cfg["n_txt"]
+    u = rng.standard_normal((2, N, 64))
+    cs = O.silu(rng.standard_normal((2, 64)))
+    got = O.double_block(u, cs, W, cfg)
+    U = _t(u)
+    parts, mods = {}, {}
+    seg = {"txt": slice(0, nt), "img": slice(nt, N)}
+    for s in ("txt", "img"):
+        mods[s] = Fn.linear(_t(cs), _t(W[s]["mod_w"]), _t(W[s]["mod_b"]))
+        parts[s] = torch_dit_stream(U[:, seg[s]], mods[s], W[s], 2, 1e-6, W[s]["q_g"], W[s]["k_g"])
+    q, k, v = [torch.cat([parts["txt"][i], parts["img"][i]], dim=2) for i in range(3)]
+    att = _merge(Fn.scaled_dot_product_attention(torch_rope(q, cfg), torch_rope(k, cfg), v))
+    ref = torch.cat([torch_dit_post(U[:, seg[s]], att[:, seg[s]], mods[s], W[s], 1e-6)
+                     for s in ("txt", "img")], dim=1).numpy()
+    np.testing.assert_allclose(got, ref, rtol=1e-10, atol=1e-11)
+    # the rotation matters: without it the block differs
+    assert np.abs(got - O.double_block(u, cs, W, dict(cfg, rope_axes=(0, 0, 0)))).max() > 1e-3
+
+
+def test_single_block_with_rope_matches_torch_composition():
+    cfg = rope_cfg(synth.MMDIT_SINGLE, axes=(4, 14, 14))
+    W = perturbed(cfg)
+    rng = np.random.default_rng(11)
+    N = cfg["n_txt"] + cfg["n_img"]
+    u = rng.standard_normal((2, N, 64))
+    cs = O.silu(rng.standard_normal((2, 64)))
+    got = O.single_block(u, cs, W, cfg)
+    U = _t(u)
+    a_, b_, g_ = Fn.linear(_t(cs), _t(W["mod_w"]), _t(W["mod_b"])).chunk(3, dim=-1)
+    a = Fn.layer_norm(U, (64,), eps=1e-6) * (1 + b_[:, None]) + a_[:, None]
+    y = Fn.linear(a, _t(W["lin1_w"]), _t(W["lin1_b"]))
+    q, k, v, z = y.split([64, 64, 64, 96], dim=-1)
+    hv = lambda x: x.view(2, N, 2, 32).transpose(1, 2)
+    q = torch_rope(Fn.rms_norm(hv(q), (32,), weight=_t(W["q_g"]), eps=1e-6), cfg)
+    k = torch_rope(Fn.rms_norm(hv(k), (32,), weight=_t(W["k_g"]), eps=1e-6), cfg)
+    att = _merge(Fn.scaled_dot_product_attention(q, k, hv(v)))
+    ref = U + g_[:, None] * Fn.linear(torch.cat([att, Fn.gelu(z, approximate="tanh")], -1),
+                                      _t(W["lin2_w"]), _t(W["lin2_b"]))
+    np.testing.assert_allclose(got, ref.numpy(), rtol=1e-10, atol=1e-11)
