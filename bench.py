@@ -5,18 +5,22 @@
 
 A bench step is one denoising step of the FeatFix schedule (time embedding, patch
 embedding, every layer's exact block / history refresh / Taylor draft / verify+replace as
-the plan says, final layer and Euler update); steps run in schedule order and wrap
-around to step 0 of a fresh loop after step T-1, so the default K = 2T times two whole
-loops (10 refresh + 40 cached steps each).  Inputs and weights are resident in HBM before
-the timed region.  Workload (value): DiT-XL/2 shape -- 28 DiT blocks, hidden 1152, 16
-heads of 72, 256 tokens, batch 8, bf16, T=50, refresh every 5 steps, second-order
-forecast, sites at layers 13 and 27 on every cached step.  The FLUX-like shape (19 double
-+ 38 single blocks, 4096 + 512 tokens), the Vanilla loops, a DiT-XL/2 FeatFix loop with
-the adaptive (discrepancy-triggered) refresh policy and the DiT-XL/2 matched-compute arms
-(token- / channel-partial forwarding at stride 2, whole-timestep recompute) are reported
-alongside, with a FLUX-like resolution sweep (512^2 to 1024^2: latency and peak memory)
-a DiT-XL/2 shadow-Vanilla diagnostic (per-layer rel-L1 of FeatFix and Verify) and the
-FLUX-like FeatFix loop with rotary embedding.
+the plan says, final layer and Euler update).  Inputs and weights are resident in HBM
+before anything is timed.  Workload (value): DiT-XL/2 shape -- 28 DiT blocks, hidden
+1152, 16 heads of 72, 256 tokens, batch 8, bf16, T=50, refresh every 5 steps,
+second-order forecast, sites at layers 13 and 27 on every cached step.
+
+Timing: W untimed warm-up steps in schedule order; then exactly K steps from step 0 of a
+fresh loop, wrapping to a new loop after step T-1 (the window, HIP events around it);
+then max(5, ceil(K/T)) whole T-step loops, each timed with its own HIP event pair on the
+stream from before step 0 to after step T-1.  value = T / the median loop time (the
+steps of a loop differ in cost: refresh steps run every block exactly, cached steps only
+the sites, so only whole loops give an unbiased rate).  Verify, Exact-only, Vanilla and
+the matched-compute arms are timed the same way, as are the FLUX-like loops; the
+Qwen-like and HunyuanVideo-like loops (FeatFix and Vanilla) and a DiT-XL/2 FeatFix loop
+with the adaptive (discrepancy-triggered) refresh policy are reported alongside, with a
+FLUX-like resolution sweep, a DiT-XL/2 shadow-Vanilla diagnostic, the FLUX-like loop with
+rotary embedding and the guided (batch-doubled) DiT-XL/2 loop.
 
 Prints ONE JSON line.
 """
@@ -84,7 +88,9 @@ class Loop:
 
 
 def timed_steps(loop, n):
+    """Exactly n steps from step 0 of a fresh loop (wrapping after T-1), one event pair."""
     import torch
+    loop.pos = 0
     torch.cuda.synchronize()
     a = torch.cuda.Event(enable_timing=True)
     b = torch.cuda.Event(enable_timing=True)
@@ -94,6 +100,34 @@ def timed_steps(loop, n):
     b.record()
     torch.cuda.synchronize()
     return a.elapsed_time(b)
+
+
+def time_loops(loop, n):
+    """n whole loops, each from step 0 to step T-1 between its own pair of HIP events on
+    the stream; returns the loop times in ms."""
+    import torch
+    T = loop.r.T
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(n)]
+    torch.cuda.synchronize()
+    for a, b in ev:
+        loop.pos = 0
+        a.record()
+        for _ in range(T):
+            loop.step()
+        b.record()
+    torch.cuda.synchronize()
+    return [a.elapsed_time(b) for a, b in ev]
+
+
+def loop_entry(loop, n_loops):
+    """Median whole-loop time and rate of n_loops timed loops, with their spread."""
+    import statistics
+    ms = time_loops(loop, n_loops)
+    med = statistics.median(ms)
+    T = loop.r.T
+    return {"loops": n_loops, "steps_per_loop": T, "loop_ms_median": round(med, 3),
+            "loop_ms_min": round(min(ms), 3), "loop_ms_max": round(max(ms), 3),
+            "steps_per_s": round(T / (med / 1e3), 2)}
 
 
 def per_step_kind_ms(loop):
@@ -170,13 +204,13 @@ def kernel_table(stats):
     return out
 
 
-def adaptive_entry(dm, mask, fixed_loop, x0, cond, txt, n):
+def adaptive_entry(dm, mask, fixed_loop, x0, cond, txt, n_loops):
     """FeatFix with the adaptive (discrepancy-triggered) refresh policy: tau is the median
     of the fixed-schedule loop's per-step largest site discrepancies (from its last loop's
-    audit), so some cached steps trigger a refresh.  Timed like the fixed loop; the time
-    includes the host waits for each checked step's discrepancies."""
+    audit), so some cached steps trigger a refresh.  Timed like the fixed loop (whole
+    loops, median); the time includes the host waits for each checked step's
+    discrepancies."""
     import numpy as np
-    import torch
     from paper_2607_27842_amd import abi, pipeline
     r0 = fixed_loop.r
     a = fixed_loop.audit.view(r0.T, r0.L, -1).cpu().numpy()
@@ -186,23 +220,23 @@ def adaptive_entry(dm, mask, fixed_loop, x0, cond, txt, n):
     loop = Loop(r, x0, cond, txt)
     for _ in range(r.T):
         loop.step()
-    loop.pos = 0
-    ms = timed_steps(loop, n)
-    loop.pos = 0
-    for _ in range(r.T):
-        loop.step()
-    torch.cuda.synchronize()
+    entry = {"tau": tau}
+    entry.update(loop_entry(loop, n_loops))
     kinds = r.step_kinds()
-    entry = {"tau": tau, "steps": n, "ms": round(ms, 3), "steps_per_s": round(n / (ms / 1e3), 2),
-             "counts_per_loop": abi.ff_get_counts(r.ctx),
-             "refresh_steps": [i for i, k in enumerate(kinds) if k == abi.FF_STEP_REFRESH]}
+    entry["counts_per_loop"] = abi.ff_get_counts(r.ctx)
+    entry["refresh_steps"] = [i for i, k in enumerate(kinds) if k == abi.FF_STEP_REFRESH]
     log(f"[bench] adaptive featfix (tau {tau:.4g}): {entry['steps_per_s']} steps/s, "
         f"{entry['counts_per_loop']['n_full_refresh']} refreshes per loop")
     r.close()
     return entry
 
 
-def run_workload(name, mode_names, warmup_loops, timed_steps_n, with_profile, adaptive=False):
+def run_workload(name, mode_names, warmup_steps, n_loops, with_profile, adaptive=False, window_steps=0,
+                 loops_for=None, clock=None, per_kind=True):
+    """Per mode: warmup_steps untimed steps, the exact window of window_steps steps
+    (featfix only, when > 0), n_loops whole timed loops (loops_for[mode] overrides), the
+    mean refresh / cached step time of one more loop (per_kind), and (featfix,
+    with_profile) one loop with per-launch events."""
     import torch
     import synth
     from paper_2607_27842_amd import abi, pipeline
@@ -218,29 +252,119 @@ def run_workload(name, mode_names, warmup_loops, timed_steps_n, with_profile, ad
         mode = synth.MODE_NAMES[mode_name]
         r = pipeline.Runner(dm, mode, mask, hist_sums=HIST_SUMS)
         loop = Loop(r, x0, cond, txt)
-        for _ in range(warmup_loops * r.T):
+        for _ in range(warmup_steps):
             loop.step()
-        n = timed_steps_n if timed_steps_n else r.T
-        loop.pos = 0
-        ms = timed_steps(loop, n)
-        entry = {"steps": n, "ms": round(ms, 3), "steps_per_s": round(n / (ms / 1e3), 2),
-                 "counts_per_loop": None}
-        ref_ms, cac_ms = per_step_kind_ms(loop)
-        entry["ms_refresh_step"] = round(ref_ms, 4)
-        entry["ms_cached_step"] = round(cac_ms, 4)
+        entry = {"warmup_steps": warmup_steps}
+        if window_steps and mode_name == "featfix":
+            ms = timed_steps(loop, window_steps)
+            entry["window"] = {"steps": window_steps, "ms": round(ms, 3),
+                               "steps_per_s": round(window_steps / (ms / 1e3), 2)}
+        if clock and mode_name == "featfix":
+            clock.start()
+        entry.update(loop_entry(loop, (loops_for or {}).get(mode_name, n_loops)))
+        if clock and mode_name == "featfix":
+            entry["gpu_clock"] = clock.stop()
+        ref_ms, cac_ms = per_step_kind_ms(loop) if per_kind else (float("nan"), float("nan"))
+        if per_kind:
+            entry["ms_refresh_step"] = round(ref_ms, 4)
+            entry["ms_cached_step"] = round(cac_ms, 4)
         entry["counts_per_loop"] = abi.ff_get_counts(r.ctx)
         entry["hist_sums"] = r.hsum is not None
         if with_profile and mode_name == "featfix":
             entry["kernels"] = profile_loop(loop)
-        log(f"[bench] {name} {mode_name}: {entry['steps_per_s']} steps/s "
+            entry["plan"] = r.export_plan()
+        log(f"[bench] {name} {mode_name}: {entry['steps_per_s']} steps/s over {entry['loops']} loops "
             f"(refresh {ref_ms:.3f} ms, cached {cac_ms:.3f} ms)")
         res[mode_name] = entry
         if adaptive and mode_name == "featfix":
-            res["featfix_adaptive"] = adaptive_entry(dm, mask, loop, x0, cond, txt, n)
+            res["featfix_adaptive"] = adaptive_entry(dm, mask, loop, x0, cond, txt, n_loops)
         r.close()
+        del loop, r
+    if "featfix" in res and "vanilla" in res:
+        res["featfix_over_vanilla"] = round(res["featfix"]["steps_per_s"] / res["vanilla"]["steps_per_s"], 3)
+    if "featfix" in res and "verify" in res:
+        res["verify_over_featfix_loop_time"] = round(res["verify"]["loop_ms_median"] / res["featfix"]["loop_ms_median"], 4)
     del dm
     torch.cuda.empty_cache()
     return res
+
+
+def per_layer_draft_profile(name="dit_xl2"):
+    """One FeatFix loop drafting layer by layer (no history sums), with per-launch events:
+    the HBM rate of the per-layer draft passes under their own byte count."""
+    import torch
+    import synth
+    from paper_2607_27842_amd import pipeline
+    cfg = synth.get_config(name)
+    dm = pipeline.DeviceModel.random(cfg, seed=0)
+    x0, cond, txt = device_inputs(cfg)
+    r = pipeline.Runner(dm, synth.MODE_NAMES["featfix"], synth.site_mask(cfg), hist_sums=False)
+    loop = Loop(r, x0, cond, txt)
+    for _ in range(r.T):
+        loop.step()
+    k = profile_loop(loop)
+    r.close()
+    del loop, r, dm
+    torch.cuda.empty_cache()
+    return k
+
+
+class ClockSampler:
+    """The GFX clock of the benchmark's GPU sampled every ~10 ms from a side thread
+    (amdsmi) while a timed region runs."""
+
+    def __init__(self):
+        self.handle, self.err = None, None
+        try:
+            import amdsmi
+            import torch
+            amdsmi.amdsmi_init()
+            handles = amdsmi.amdsmi_get_processor_handles()
+            bus = getattr(torch.cuda.get_device_properties(0), "pci_bus_id", None)
+            pick = handles[0] if len(handles) == 1 else None
+            for h in handles:
+                bdf = amdsmi.amdsmi_get_gpu_device_bdf(h)
+                if bus is not None and int(bdf.split(":")[1], 16) == int(bus):
+                    pick = h
+            if pick is None:
+                raise RuntimeError(f"{len(handles)} GPUs visible to amdsmi and none matched the device's PCI bus")
+            self.amdsmi, self.handle = amdsmi, pick
+            self.read()
+        except Exception as e:   # reported, not fatal: the clock is context for the rates
+            self.err = f"{type(e).__name__}: {e}"
+
+    def read(self):
+        info = self.amdsmi.amdsmi_get_clock_info(self.handle, self.amdsmi.AmdSmiClkType.GFX)
+        return float(info["clk"])
+
+    def start(self):
+        import threading
+        self.samples, self.run = [], True
+        if self.handle is None:
+            return
+
+        def body():
+            while self.run:
+                try:
+                    self.samples.append(self.read())
+                except Exception as e:
+                    self.err = f"{type(e).__name__}: {e}"
+                    return
+                time.sleep(0.01)
+        self.th = threading.Thread(target=body, daemon=True)
+        self.th.start()
+
+    def stop(self):
+        import statistics
+        self.run = False
+        if self.handle is None:
+            return {"error": self.err}
+        self.th.join()
+        if not self.samples:
+            return {"error": self.err or "no samples"}
+        return {"source": "amdsmi GFX clock, sampled every ~10 ms during the timed loops",
+                "samples": len(self.samples), "mhz_median": statistics.median(self.samples),
+                "mhz_min": min(self.samples), "mhz_max": max(self.samples)}
 
 
 def shadow_vanilla(name="dit_xl2"):
@@ -392,16 +516,17 @@ def resolution_sweep(sides=(512, 768, 1024)):
     return out
 
 
-def cpu_baseline(steps=5, layers=10):
-    """The oracle on the host, on a bounded sample of the DiT-XL/2 FeatFix loop: the first
-    R=5 steps (1 refresh + 4 cached steps) at full width, tokens and batch but `layers`
-    blocks with sites at the middle (L/2 - 1) and last block, the rule that gives {13, 27}
-    at 28 blocks.  Exact blocks dominate the oracle's time (drafts are elementwise), so the
-    full-depth rate is extrapolated by exact-block count: 28 + 4*2 = 36 blocks per 5 steps
-    at full depth against layers + 4*2 in the sample."""
+def cpu_baseline(steps=12):
+    """The oracle on the host's cores, on a bounded sample of the DiT-XL/2 FeatFix loop:
+    the first `steps` steps (refreshes at 0, 5, 10, so cached steps at k_eff = 0, 1 and 2)
+    at full depth (28 blocks), width and tokens, for one sample of the batch of 8.
+    Samples never interact and exact blocks dominate the oracle's time (drafts are
+    elementwise), so the 50-step, batch-8 rate is extrapolated by exact-block count (this
+    sample's 3 x 28 + 9 x 2 = 102 against 10 x 28 + 40 x 2 = 360 per loop) and batch, and
+    labelled so.  The tiny fp32 workload's whole 10-step loop is timed in every mode."""
     import oracle as O
     import synth
-    cfg = synth.get_config("dit_xl2", T=steps, kinds=[synth.DIT] * layers, sites=[layers // 2 - 1, layers - 1])
+    cfg = synth.get_config("dit_xl2", T=steps, B=1)
     W = synth.make_weights(cfg)
     inp = synth.make_inputs(cfg)
     mask = synth.site_mask(cfg)
@@ -411,18 +536,31 @@ def cpu_baseline(steps=5, layers=10):
     except Exception:
         blas_threads = 0
     t0 = time.perf_counter()
-    O.run(cfg, O.FEATFIX, inp, W, mask)
+    ref = O.run(cfg, O.FEATFIX, inp, W, mask)
     dt = time.perf_counter() - t0
-    sample_blocks = layers + (steps - 1) * 2
-    full_blocks = 28 + (steps - 1) * 2
-    est = dt * full_blocks / sample_blocks
+    full = synth.get_config("dit_xl2")
+    sample_blocks = sum(28 if k == O.REFRESH_STEP else 2 for k in ref["step_kind"])
+    R = full["R"]
+    loop_blocks = sum(28 if i % R == 0 else 2 for i in range(full["T"]))
+    loop_s = dt * (loop_blocks / sample_blocks) * full["B"]
     cores = len(os.sched_getaffinity(0))
-    return {"value": round(steps / est, 5), "unit": "steps/s", "cores": min(cores, blas_threads or cores),
-            "kind": "oracle",
-            "sample": f"fp64 NumPy oracle: first {steps} steps (1 refresh + {steps - 1} cached, 2 paid sites each) "
-                      f"of the DiT-XL/2-shaped FeatFix loop with {layers} of 28 blocks (B=8, N=256, C=1152) took "
-                      f"{dt:.1f} s; scaled to 28 blocks by exact-block count ({sample_blocks} -> {full_blocks}); "
-                      f"host affinity {cores} cores, BLAS threads {blas_threads}"}
+    tiny = synth.get_config("tiny")
+    Wt = synth.make_weights(tiny)
+    it = synth.make_inputs(tiny)
+    mt = synth.site_mask(tiny)
+    tiny_rates = {}
+    for name in ("vanilla", "draft", "verify", "featfix", "exact_only"):
+        t1 = time.perf_counter()
+        O.run(tiny, synth.MODE_NAMES[name], it, Wt, mt)
+        tiny_rates[name] = round(tiny["T"] / (time.perf_counter() - t1), 2)
+    return {"value": round(full["T"] / loop_s, 5), "unit": "steps/s", "cores": min(cores, blas_threads or cores),
+            "kind": "oracle", "extrapolated": True,
+            "sample": f"fp64 NumPy oracle, DiT-XL/2-shaped FeatFix loop: the first {steps} steps (refreshes 0, 5, 10; "
+                      f"k_eff up to 2) at full depth, width and tokens for 1 of the 8 samples took {dt:.1f} s "
+                      f"({sample_blocks} exact blocks); extrapolated to the 50-step loop by exact-block count "
+                      f"({sample_blocks} -> {loop_blocks}) and to batch 8 (samples are independent): "
+                      f"{loop_s:.0f} s per loop; host affinity {cores} cores, BLAS threads {blas_threads}",
+            "tiny_fp32_steps_per_s": tiny_rates}
 
 
 WORKLOAD_TEXT = {
@@ -433,14 +571,48 @@ WORKLOAD_TEXT = {
 }
 
 
+def hbm_rates(kern, keys=("draft", "verify", "cache")):
+    out = {}
+    for k in keys:
+        s = kern[k]
+        if s["launches"]:
+            gbs = s["bytes"] / (s["ms"] / 1e3) / 1e9
+            out[k] = {"achieved_gbs": round(gbs, 1), "frac": round(gbs / PEAK_HBM_GBS, 4),
+                      "avg_launch_us": round(s["ms"] * 1e3 / s["launches"], 3),
+                      "bytes_per_launch": s["bytes"] / s["launches"], "launches": s["launches"]}
+    return out
+
+
+def draft_per_layer_accounting(kern, plan, cfg):
+    """The loop's drafted layers priced at the per-layer unit of Eq. 2's draft, (k_eff + 3)
+    bytes-per-element x E per drafted layer (read u and k_eff + 1 history slots, write the
+    draft), over the time of every launch that drafts (the run passes from history sums)
+    or feeds them (the history sums formed at refresh steps)."""
+    es = 2 if cfg["dtype"] == 1 else 4
+    E = cfg["B"] * (cfg["n_img"] + cfg["n_txt"]) * cfg["C"]
+    k_eff, action, kinds = plan["k_eff"], plan["action"], plan["step_kind"]
+    layers = 0
+    nbytes = 0.0
+    for i in range(cfg["T"]):
+        if kinds[i] != 1:
+            continue
+        n = int((action[i] == 1).sum())
+        layers += n
+        nbytes += n * (int(k_eff[i]) + 3) * E * es
+    ms = kern["draft"]["ms"] + kern["cache"]["ms"]
+    gbs = nbytes / (ms / 1e3) / 1e9
+    return {"drafted_layers_per_loop": layers, "per_layer_bytes_per_loop": nbytes,
+            "draft_plus_hist_sum_ms_per_loop": round(ms, 4), "effective_gbs": round(gbs, 1),
+            "effective_frac": round(gbs / PEAK_HBM_GBS, 4)}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=100)
-    ap.add_argument("--warmup", type=int, default=50)
+    ap.add_argument("--steps", type=int, default=250, help="steps of the exact timed window (K)")
+    ap.add_argument("--warmup", type=int, default=50, help="untimed warm-up steps (W)")
     ap.add_argument("--no-flux", action="store_true", help="skip the FLUX-like loops reported in extra")
-    ap.add_argument("--no-dit", action="store_true",
-                    help="time the FLUX-like loop as the primary workload instead of DiT-XL/2 (profiling)")
+    ap.add_argument("--no-large", action="store_true", help="skip the Qwen-like and HunyuanVideo-like loops")
     ap.add_argument("--no-vanilla", action="store_true")
     ap.add_argument("--no-arms", action="store_true", help="skip the matched-compute arm loops reported in extra")
     ap.add_argument("--no-sweep", action="store_true", help="skip the FLUX-like resolution sweep reported in extra")
@@ -462,62 +634,66 @@ def main():
     abi.lib()
 
     calibration_copy()
-    name = "flux" if args.no_dit else "dit_xl2"
+    clock = ClockSampler()
+    name = "dit_xl2"
     cfg = synth.get_config(name)
     T = cfg["T"]
-    warm_loops = max(1, -(-args.warmup // T))
-    modes = ["featfix"] + ([] if args.no_vanilla else ["vanilla"])
-    if name == "dit_xl2" and not args.no_arms:
+    K, W = args.steps, args.warmup
+    n_loops = max(5, -(-K // T))
+    modes = ["featfix", "verify", "exact_only"] + ([] if args.no_vanilla else ["vanilla"])
+    if not args.no_arms:
         modes += ["tokens_partial", "channels_partial", "recompute"]   # the matched-compute arms
-    prim = run_workload(name, modes, warm_loops, args.steps, with_profile=True, adaptive=name == "dit_xl2")
+    prim = run_workload(name, modes, W, n_loops, with_profile=True, adaptive=True, window_steps=K, clock=clock)
     ff = prim["featfix"]
-    ms_step = ff["ms"] / ff["steps"]
-    value = ff["steps"] / (ff["ms"] / 1e3)
+    value = ff["steps_per_s"]
+    ms_step = 1e3 / value
     kern = ff.pop("kernels")
+    plan = ff.pop("plan")
     g = kern["gemm"]
     achieved = g["flops"] / (g["ms"] / 1e3) / 1e12
     roof = {"bound": "mfma", "achieved": round(achieved, 1), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
-            "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": gemm_traffic() if name == "dit_xl2" else None,
+            "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": gemm_traffic(),
             "kernel": "k_gemm_dl64 / k_gemm_dl / k_gemm_bf16 (all exact-block GEMM launches of one FeatFix loop)",
             "avg_launch_us": round(g["ms"] * 1e3 / g["launches"], 3),
             "flop_per_launch": g["flops"] / g["launches"]}
-    hbm = {}
-    for k in ("draft", "verify", "cache"):
-        s = kern[k]
-        if s["launches"]:
-            gbs = s["bytes"] / (s["ms"] / 1e3) / 1e9
-            hbm[k] = {"achieved_gbs": round(gbs, 1), "frac": round(gbs / PEAK_HBM_GBS, 4),
-                      "avg_launch_us": round(s["ms"] * 1e3 / s["launches"], 3),
-                      "bytes_per_launch": s["bytes"] / s["launches"]}
-    key = "dit" if name == "dit_xl2" else "flux"
-    extra = {name: prim, f"{key}_kernels": kernel_table(kern), "hbm_roofline": hbm}
-    if "vanilla" in prim:
-        extra[f"{key}_featfix_over_vanilla"] = round(value / prim["vanilla"]["steps_per_s"], 3)
-    if name == "dit_xl2" and not args.no_flux:
-        flux = run_workload("flux", ["featfix"] + ([] if args.no_vanilla else ["vanilla"]), 1, 0,
-                            with_profile=True)
+    hbm = hbm_rates(kern)
+    if HIST_SUMS:
+        hbm["draft_per_layer_unit"] = draft_per_layer_accounting(kern, plan, cfg)
+        hbm["per_layer_path"] = hbm_rates(per_layer_draft_profile(name), ("draft", "verify"))
+    extra = {name: prim, "dit_kernels": kernel_table(kern), "hbm_roofline": hbm}
+    if not args.no_flux:
+        flux = run_workload("flux", ["featfix", "verify", "exact_only"] + ([] if args.no_vanilla else ["vanilla"]),
+                            T, 3, with_profile=True, loops_for={"featfix": 5})
         fk = flux["featfix"].pop("kernels")
+        flux["featfix"].pop("plan")
         flux["kernels"] = kernel_table(fk)
-        if "vanilla" in flux:
-            flux["featfix_over_vanilla"] = round(flux["featfix"]["steps_per_s"] / flux["vanilla"]["steps_per_s"], 3)
+        flux["hbm_roofline"] = hbm_rates(fk)
         flux["featfix_rope"] = rope_loop()
         extra["flux"] = flux
-    if name == "dit_xl2" and not args.no_flux and not args.no_sweep:
-        extra["flux_resolution_sweep"] = resolution_sweep()
-    if name == "dit_xl2" and not args.no_arms:
+        if not args.no_sweep:
+            extra["flux_resolution_sweep"] = resolution_sweep()
+    if not args.no_large:
+        for big in ("qwen", "hunyuan"):
+            extra[big] = run_workload(big, ["featfix"] + ([] if args.no_vanilla else ["vanilla"]), synth.get_config(big)["T"],
+                                      2, with_profile=False, loops_for={"vanilla": 1}, per_kind=False)
+    if not args.no_arms:
         extra["dit_xl2_shadow_vanilla"] = shadow_vanilla()
-    if name == "dit_xl2" and not args.no_guided:
+    if not args.no_guided:
         extra["dit_xl2_guided"] = guided_loop()
-    out = {"metric": METRIC, "value": round(value, 3), "unit": "steps/s", "n_gpus": 1, "steps": ff["steps"],
-           "warmup": warm_loops * T, "ms_per_step": round(ms_step, 4), "higher_is_better": True, "scaling": "weak",
+    out = {"metric": METRIC, "value": round(value, 3), "unit": "steps/s", "n_gpus": 1, "steps": K,
+           "warmup": W, "ms_per_step": round(ms_step, 4), "higher_is_better": True, "scaling": "weak",
            "vs_baseline": None, "dtype": "bf16",
            "data": "synthetic: seeded N(0,1) latent and class/text vectors, random-init N(0,0.02) weights",
            "config": {"workload": WORKLOAD_TEXT[name] + ("; drafted runs from history sums" if HIST_SUMS
                                                          else "; drafted runs layer by layer"),
                       "global_batch": cfg["B"],
                       "seq_len": cfg["n_img"] + cfg["n_txt"], "parallelism": "none (1 GPU)"},
+           "timing": {"value_from": f"median of {n_loops} whole {T}-step loops (HIP events per loop) after {W} "
+                                    f"warm-up steps and the {K}-step window",
+                      "loops": n_loops, "loop_ms_median": ff["loop_ms_median"], "window": ff.get("window"),
+                      "gpu_clock": ff.get("gpu_clock")},
            "roofline": roof}
-    if not args.no_cpu_baseline and name == "dit_xl2":
+    if not args.no_cpu_baseline:
         log("[bench] timing the CPU oracle sample ...")
         out["cpu_baseline"] = cpu_baseline()
     out["extra"] = extra
