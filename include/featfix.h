@@ -288,6 +288,26 @@ ff_status ff_verify_replace(const ff_model_desc* m, const void* cache, int32_t n
                             int32_t forward, int32_t stride, float eps, float* rel_l1, void* ws,
                             size_t ws_bytes, ff_stream_t stream);
 
+/* ---------------------------------------------------------------- no-allocation verify
+ * For callers that cannot allocate device memory or hand over a workspace: code under HIP
+ * graph capture, tight serving loops, harnesses that forbid hipMalloc.  The same operation
+ * as ff_verify_replace (same kernels, bit-identical h_out and rel_l1) without the ws
+ * argument: the partial sums of Eq. 4 (B * 2048 * 2 floats) live in a library-owned
+ * device array of FF_NOALLOC_VERIFY_MAX_B * 2048 * 2 floats (256 KB) on each GPU the
+ * library runs on, held from the first call on that GPU until the process ends.  Nothing
+ * in it needs to start at zero (every call writes the partials it reads).  Calls that
+ * overlap on one GPU (several streams or threads) share that array and race: order them
+ * on one stream.  stream must belong to the current device.  Allocates nothing: no
+ * hipMalloc, hipFree or allocating library routine.
+ * Errors: as ff_verify_replace; FF_E_WORKSPACE if m->B > FF_NOALLOC_VERIFY_MAX_B; FF_E_HIP
+ * if the array's device address cannot be obtained. */
+#define FF_NOALLOC_VERIFY_MAX_B 16
+ff_status ff_verify_replace_noalloc(const ff_model_desc* m, const void* cache, int32_t n_slots,
+                                    int32_t layer, int32_t k_eff, const int32_t* slots,
+                                    const float* coeffs, const void* u, const void* h_f,
+                                    void* h_out, int32_t forward, int32_t stride, float eps,
+                                    float* rel_l1, ff_stream_t stream);
+
 /* ---------------------------------------------------------------- step executor
  * A context binds a model, its weights (layer_w is a host array [n_layers]; the device
  * pointers inside are kept, the host arrays are copied), a plan (copied), a cache of at

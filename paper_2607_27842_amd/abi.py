@@ -26,11 +26,12 @@ FF_RESIDUAL, FF_OUTPUT = 0, 1
 FF_STEP_REFRESH, FF_STEP_CACHED = 0, 1
 FF_ACT_EXACT, FF_ACT_DRAFT, FF_ACT_SITE, FF_ACT_RECOMPUTE = 0, 1, 2, 3
 FF_MAX_K, FF_MAX_SLOTS, FF_TEMB_DIM = 3, 8, 256
+FF_NOALLOC_VERIFY_MAX_B = 16
 
 # every symbol include/featfix.h declares
 EXPORTED = ("ff_abi_version", "ff_last_error", "ff_plan_build", "ff_plan_destroy", "ff_plan_export",
             "ff_cache_bytes", "ff_workspace_bytes", "ff_block_exact", "ff_cache_update",
-            "ff_draft_forecast", "ff_verify_replace", "ff_ctx_create", "ff_ctx_destroy",
+            "ff_draft_forecast", "ff_verify_replace", "ff_verify_replace_noalloc", "ff_ctx_create", "ff_ctx_destroy",
             "ff_ctx_reset", "ff_get_counts", "ff_ctx_step_kinds", "ff_denoise_step", "ff_ctx_trace", "ff_hist_sum_bytes", "ff_ctx_hist_sums", "ff_rel_l1",
             "ff_ctx_profile", "ff_ctx_profile_read")
 PROF_CLASSES = ("gemm", "attn", "norm", "gemv", "draft", "verify", "cache", "other")
@@ -116,6 +117,8 @@ def lib():
             "ff_draft_forecast": (i32, [P(ff_model_desc), vp, i32, i32, i32, P(i32), P(C.c_float), vp, vp, vp]),
             "ff_verify_replace": (i32, [P(ff_model_desc), vp, i32, i32, i32, P(i32), P(C.c_float), vp, vp, vp,
                                         i32, i32, f32, vp, vp, sz, vp]),
+            "ff_verify_replace_noalloc": (i32, [P(ff_model_desc), vp, i32, i32, i32, P(i32), P(C.c_float), vp, vp,
+                                                vp, i32, i32, f32, vp, vp]),
             "ff_ctx_create": (i32, [P(ff_model_desc), P(ff_layer_weights), P(ff_global_weights), vp, vp, sz,
                                     vp, sz, P(vp)]),
             "ff_ctx_destroy": (None, [vp]),
@@ -223,6 +226,15 @@ def ff_verify_replace(model, cache, n_slots, layer, k_eff, slots, coeffs, u, h_f
     return check(lib().ff_verify_replace(C.byref(model), cache, n_slots, layer, k_eff, _i32arr(slots),
                                          _f32arr(coeffs), u, h_f, h_out, int(forward), int(stride), eps, rel_l1,
                                          ws, ws_bytes, stream))
+
+
+def ff_verify_replace_noalloc(model, cache, n_slots, layer, k_eff, slots, coeffs, u, h_f, h_out, forward, eps,
+                              rel_l1, stream=0, stride=1):
+    """ff_verify_replace without a workspace (partial sums in the library's own device
+    array; B <= FF_NOALLOC_VERIFY_MAX_B)."""
+    return check(lib().ff_verify_replace_noalloc(C.byref(model), cache, n_slots, layer, k_eff, _i32arr(slots),
+                                                 _f32arr(coeffs), u, h_f, h_out, int(forward), int(stride), eps,
+                                                 rel_l1, stream))
 
 
 def ff_ctx_create(model, layer_weights, global_weights, plan, cache, cache_bytes, ws, ws_bytes):

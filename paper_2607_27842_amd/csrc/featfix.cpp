@@ -9,6 +9,7 @@
 #include <string.h>
 
 #include <algorithm>
+#include <mutex>
 #include <new>
 #include <utility>
 #include <vector>
@@ -703,6 +704,51 @@ ff_status check_terms(const Model& m, int n_slots, int layer, int k_eff, const i
   return FF_OK;
 }
 
+// Argument checks shared by the two verify entry points (everything except the buffer
+// that holds the partial sums).
+ff_status check_verify(const ff_model_desc* m, const void* cache, int32_t n_slots, int32_t layer, int32_t k_eff,
+                       const int32_t* slots, const float* coeffs, const void* u, const void* h_f, const void* h_out,
+                       int32_t forward, int32_t stride, float eps, Model* md, Terms* t) {
+  ff_status e = check_model(m, md);
+  if (e) return e;
+  if (!h_f || !h_out) return fail(FF_E_NULL, "h_f or h_out is NULL");
+  e = check_terms(*md, n_slots, layer, k_eff, slots, coeffs, cache, t);
+  if (e) return e;
+  if (!(eps > 0.f)) return fail(FF_E_RANGE, "eps must be > 0");
+  const size_t tb = md->E() * md->es();
+  if ((const char*)h_out < (const char*)h_f + tb && (const char*)h_f < (const char*)h_out + tb)
+    return fail(FF_E_SHAPE, "h_out overlaps h_f");
+  if (!aligned16(h_f) || !aligned16(h_out) || (u && !aligned16(u))) return fail(FF_E_SHAPE, "pointers must be 16-byte aligned");
+  if (forward < FF_FWD_DRAFT || forward > FF_FWD_CHANNELS) return fail(FF_E_RANGE, "forward=%d unknown", forward);
+  if (forward >= FF_FWD_TOKENS && stride < 1) return fail(FF_E_RANGE, "stride=%d must be >= 1", stride);
+  return FF_OK;
+}
+
+// Partial sums of ff_verify_replace_noalloc: a fixed device array per GPU (each device
+// that loads the library holds its own copy until the process ends).  Host code never
+// uses the array's name as an address: the address of the current device's copy comes
+// from hipGetSymbolAddress, once per device, and is kept here.
+constexpr size_t kScratchFloats = (size_t)FF_NOALLOC_VERIFY_MAX_B * 2048 * 2;
+static __device__ __align__(256) float scratch[kScratchFloats];
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+float* g_scratch_ptr[kMaxDevices] = {};
+
+ff_status scratch_of_current_device(float** out) {
+  int dev = -1;
+  HIP_TRY(hipGetDevice(&dev), "no-allocation verify: current device");
+  if (dev < 0 || dev >= kMaxDevices) return fail(FF_E_UNSUPPORTED, "device %d beyond %d devices", dev, kMaxDevices);
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    HIP_TRY(hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)), "no-allocation verify: scratch address");
+    if (!p) return fail(FF_E_HIP, "no-allocation verify: scratch address is NULL");
+    g_scratch_ptr[dev] = static_cast<float*>(p);
+  }
+  *out = g_scratch_ptr[dev];
+  return FF_OK;
+}
+
 }  // namespace
 
 // ====================================================================== C ABI
@@ -824,25 +870,41 @@ ff_status ff_verify_replace(const ff_model_desc* m, const void* cache, int32_t n
                             int32_t forward, int32_t stride, float eps, float* rel_l1, void* ws, size_t ws_bytes,
                             ff_stream_t stream) {
   Model md;
-  ff_status e = check_model(m, &md);
-  if (e) return e;
-  if (!h_f || !h_out || !ws) return fail(FF_E_NULL, "h_f, h_out or ws is NULL");
   Terms t{};
-  e = check_terms(md, n_slots, layer, k_eff, slots, coeffs, cache, &t);
+  ff_status e = check_verify(m, cache, n_slots, layer, k_eff, slots, coeffs, u, h_f, h_out, forward, stride, eps,
+                             &md, &t);
   if (e) return e;
-  if (!(eps > 0.f)) return fail(FF_E_RANGE, "eps must be > 0");
+  if (!ws) return fail(FF_E_NULL, "ws is NULL");
   const Ws L = ws_layout(md);
   if (ws_bytes < L.total) return fail(FF_E_WORKSPACE, "workspace %zu < %zu bytes", ws_bytes, L.total);
-  const size_t tb = md.E() * md.es();
-  if ((const char*)h_out < (const char*)h_f + tb && (const char*)h_f < (const char*)h_out + tb)
-    return fail(FF_E_SHAPE, "h_out overlaps h_f");
-  if (!aligned16(h_f) || !aligned16(h_out) || (u && !aligned16(u))) return fail(FF_E_SHAPE, "pointers must be 16-byte aligned");
-  if (forward < FF_FWD_DRAFT || forward > FF_FWD_CHANNELS) return fail(FF_E_RANGE, "forward=%d unknown", forward);
-  if (forward >= FF_FWD_TOKENS && stride < 1) return fail(FF_E_RANGE, "stride=%d must be >= 1", stride);
   const Forward fw{forward, stride, md.C};
   HIP_TRY(ff::verify(md.dtype, t, u, h_f, h_out, fw, md.B, (size_t)md.N * md.C, eps, rel_l1,
                      at<float>(ws, L.PART), reinterpret_cast<hipStream_t>(stream)), "verify");
   return ok();
+}
+
+ff_status ff_verify_replace_noalloc(const ff_model_desc* m, const void* cache, int32_t n_slots, int32_t layer,
+                                    int32_t k_eff, const int32_t* slots, const float* coeffs, const void* u,
+                                    const void* h_f, void* h_out, int32_t forward, int32_t stride, float eps,
+                                    float* rel_l1, ff_stream_t stream) {
+  try {
+    Model md;
+    Terms t{};
+    ff_status e = check_verify(m, cache, n_slots, layer, k_eff, slots, coeffs, u, h_f, h_out, forward, stride, eps,
+                               &md, &t);
+    if (e) return e;
+    if (md.B > FF_NOALLOC_VERIFY_MAX_B || verify_partials_floats(md.B) > kScratchFloats)
+      return fail(FF_E_WORKSPACE, "no-allocation verify takes B <= %d (B = %d)", FF_NOALLOC_VERIFY_MAX_B, md.B);
+    float* part = nullptr;
+    e = scratch_of_current_device(&part);
+    if (e) return e;
+    const Forward fw{forward, stride, md.C};
+    HIP_TRY(ff::verify(md.dtype, t, u, h_f, h_out, fw, md.B, (size_t)md.N * md.C, eps, rel_l1, part,
+                       reinterpret_cast<hipStream_t>(stream)), "verify (no allocation)");
+    return ok();
+  } catch (...) {
+    return fail(FF_E_UNSUPPORTED, "unexpected host exception");
+  }
 }
 
 ff_status ff_ctx_create(const ff_model_desc* m, const ff_layer_weights* layer_w, const ff_global_weights* g,
