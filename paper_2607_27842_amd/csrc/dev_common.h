@@ -101,13 +101,16 @@ template <> struct St<DT_F32> {
 __device__ __forceinline__ float silu_f(float x) { return x / (1.0f + expf(-x)); }
 
 // GELU, tanh form: 0.5 z (1 + tanh(u)) with u = sqrt(2/pi) (z + 0.044715 z^3).  Since
-// 1 + tanh(u) = 2 / (1 + exp(-2u)), this is z / (1 + exp(-2u)): one hardware exp2
-// (v_exp_f32) and one reciprocal (v_rcp_f32), a few ulp of fp32 and no branches.  For
-// u -> -inf the exp overflows to +inf and the result is -0; for u -> +inf it is z.
+// 1 + tanh(u) = 2 / (1 + exp(-2u)), this is z / (1 + exp(-2u)) = z / (1 + 2^(z (c1 + c3 z^2)))
+// with c1 = -2 log2(e) sqrt(2/pi) and c3 = 0.044715 c1 folded into the polynomial: five
+// VALU operations, one hardware exp2 (v_exp_f32) and one reciprocal (v_rcp_f32), a few
+// ulp of fp32 and no branches (the epilogue of the MLP's first GEMM is bound by this
+// arithmetic).  For u -> -inf the exp overflows to +inf and the result is -0; for
+// u -> +inf it is z.
 __device__ __forceinline__ float gelu_tanh_f(float z) {
-  const float k0 = 0.7978845608028654f;  // sqrt(2/pi)
-  const float u = k0 * fmaf(0.044715f * z, z * z, z);
-  const float e = __builtin_amdgcn_exp2f(-2.0f * 1.4426950408889634f * u);   // exp(-2u)
+  const float c1 = -2.302208198144325f;    // -2 log2(e) sqrt(2/pi)
+  const float c3 = -0.1029432395800235f;   // 0.044715 * c1
+  const float e = __builtin_amdgcn_exp2f(z * fmaf(c3, z * z, c1));   // exp(-2u)
   return z * __builtin_amdgcn_rcpf(1.0f + e);
 }
 
