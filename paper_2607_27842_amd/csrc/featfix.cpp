@@ -263,7 +263,10 @@ struct Exec {
     return timed(FF_PROF_GEMV, 2.0 * a.B * a.Nout * a.K, (double)a.Nout * a.K * es, [&] { return ff::gemv(dt, a, st); });
   }
   hipError_t ln(const LnModArgs& a) {
-    return timed(FF_PROF_NORM, 0, (double)a.rows * a.C * ((a.in_f32 ? 4 : es) + es),
+    // with a run draft in front (pre.n > 0) the launch also moves the draft's bytes: the
+    // history sums read and the updated stream written back; it is counted as a draft
+    const double pre = a.pre.n ? 4.0 * a.pre.n + es : 0.0;
+    return timed(a.pre.n ? FF_PROF_DRAFT : FF_PROF_NORM, 0, (double)a.rows * a.C * ((a.in_f32 ? 4 : es) + es + pre),
                  [&] { return ff::ln_modulate(dt, a, st); });
   }
   hipError_t rms_qk(const RmsQKArgs& a) {
@@ -339,9 +342,12 @@ const void* offset_rows(const void* p, size_t rows, size_t cols, size_t es) {
 // cache_slot (bf16 only): the history refresh of this layer (slot = h - u, or h when
 // !cache_resid) is written by the epilogue of the block's last GEMM, from the same rounded
 // h that the separate cache kernel would read back.
+// pre (bf16 or fp32 stream): a run of drafted layers in front of the block, applied by the
+// block's first LayerNorm(s) from its history sums (u is updated in place, every row
+// exactly once: all rows, or the text and the image rows of a double block).
 ff_status exec_block(const Model& m, int kind, const ff_layer_weights& w, const float* cs, const void* u,
                      void* h, void* ws, Exec& ex, const float* mod_pre = nullptr, void* cache_slot = nullptr,
-                     bool cache_resid = true) {
+                     bool cache_resid = true, const Terms* pre = nullptr) {
   const Ws L = ws_layout(m);
   const int C = m.C, Mh = m.M, dt = m.dtype;
   const size_t es = m.es();
@@ -366,6 +372,7 @@ ff_status exec_block(const Model& m, int kind, const ff_layer_weights& w, const 
       HIP_TRY(ex.gemv(gv), "single: modulation");
     }
     LnModArgs ln{u, 0, C, all, rows, C, m.ln_eps, mod, mod + C, 3 * C, lna, C};
+    if (pre) ln.pre = *pre;
     HIP_TRY(ex.ln(ln), "single: ln");
     // lin1 = [qkv | MLP] over the same input: the two parts (bias, bias + GELU) in one launch
     GemmArgs g1 = gemm_args(lna, C, all, s.lin1_w, s.lin1_b, rows, 3 * C, C, EPI_BIAS, qkv, 3 * C, all);
@@ -421,6 +428,7 @@ ff_status exec_block(const Model& m, int kind, const ff_layer_weights& w, const 
     }
     if (rows == 0) continue;
     LnModArgs ln{u, 0, C, maps[si], rows, C, m.ln_eps, ms, ms + C, ldm, lna, C};
+    if (pre) ln.pre = *pre;
     HIP_TRY(ex.ln(ln), "block: ln1");
   }
   for (int si = 0; si < nstreams; ++si)
@@ -1113,6 +1121,10 @@ ff_status ff_denoise_step(ff_ctx* c, int32_t step, float* x, const float* cond, 
         HIP_TRY(hipMemcpyAsync((char*)c->trace + (size_t)l * tb, cur, tb, hipMemcpyDeviceToDevice, st), "trace copy");
       return FF_OK;
     };
+    // a run of drafted layers applied from history sums and followed by a paid site is
+    // left to that site block's first LayerNorm (one pass fewer over the stream)
+    Terms pending{};
+    const Terms* defer = nullptr;
     for (int l = 0; l < L; ++l) {
       const int act = p.action[(size_t)i * L + l];
       if (act == FF_ACT_EXACT) {
@@ -1140,7 +1152,8 @@ ff_status ff_denoise_step(ff_ctx* c, int32_t step, float* x, const float* cond, 
       if (act == FF_ACT_SITE && mode == FF_EXACT_ONLY) {
         ff_status e = ensure_mod(l);
         if (e) return e;
-        e = exec_block(m, m.kinds[l], c->lw[l], cs, cur, alt, ws, ex, mod_of[l]);
+        e = exec_block(m, m.kinds[l], c->lw[l], cs, cur, alt, ws, ex, mod_of[l], nullptr, true, defer);
+        defer = nullptr;
         if (e) return e;
         void* t = cur; cur = alt; alt = t;
         if (ff_status te = trace_to(l)) return te;
@@ -1172,7 +1185,12 @@ ff_status ff_denoise_step(ff_ctx* c, int32_t step, float* x, const float* cond, 
           Terms ts = tm;
           for (int q = 0; q < ts.n; ++q)
             ts.slot[q] = c->hsum + ((size_t)r * S + p.read_slots[(size_t)i * (K + 1) + q]) * E;
-          HIP_TRY(ex.draft_sum(ts, cur, E), "draft from history sums");
+          if (l2 < L && p.action[(size_t)i * L + l2] == FF_ACT_SITE) {
+            pending = ts;
+            defer = &pending;
+          } else {
+            HIP_TRY(ex.draft_sum(ts, cur, E), "draft from history sums");
+          }
         } else if (l2 - l == 1) {
           HIP_TRY(ex.draft(tm, resid ? cur : nullptr, cur, E), "draft");
         } else {
@@ -1186,7 +1204,8 @@ ff_status ff_denoise_step(ff_ctx* c, int32_t step, float* x, const float* cond, 
       void* hf = at(ws, W.HF);
       ff_status e = ensure_mod(l);
       if (e) return e;
-      e = exec_block(m, m.kinds[l], c->lw[l], cs, cur, hf, ws, ex, mod_of[l]);
+      e = exec_block(m, m.kinds[l], c->lw[l], cs, cur, hf, ws, ex, mod_of[l], nullptr, true, defer);
+      defer = nullptr;
       if (e) return e;
       float* rel = audit ? audit + ((size_t)i * L + l) * m.B
                          : s.tau > 0.f ? at<float>(ws, W.REL) + (size_t)l * m.B : nullptr;

@@ -44,7 +44,7 @@ template <int DT> __device__ __forceinline__ void st8(void* p, size_t i, const f
   if (St<DT>::V == 4) St<DT>::store(p, i + 4, v + 4);
 }
 
-template <int DT_IN, int DT_OUT, int U>   // U: 8-element units per lane, C <= 512 U
+template <int DT_IN, int DT_OUT, int U, bool PRE>   // U: 8-element units per lane, C <= 512 U
 __global__ __launch_bounds__(256) void k_ln_modulate(LnModArgs a) {
   const int lane = threadIdx.x % 64;
   const int r = blockIdx.x * 4 + threadIdx.x / 64;
@@ -63,6 +63,35 @@ __global__ __launch_bounds__(256) void k_ln_modulate(LnModArgs a) {
       ld8<DT_IN>(a.in, pr * a.ldi + u * 8, v[k]);
       ld8<DT_F32>(sh, u * 8, s8[k]);
       ld8<DT_F32>(sc, u * 8, c8[k]);
+    }
+  }
+  if (PRE) {
+    // the run of drafted layers that precedes this block, from its history sums: the same
+    // fmas in the same order as k_draft_sum, one rounding, written back to the stream
+#pragma unroll
+    for (int k = 0; k < U; ++k) {
+      const int u = k * 64 + lane;
+      if (u < units) {
+        const size_t i = pr * a.ldi + u * 8;
+        float f[8];
+#pragma unroll
+        for (int j = 0; j < 8; ++j) f[j] = 0.0f;
+#pragma unroll
+        for (int m = 0; m < kMaxTerms; ++m) {
+          if (m < a.pre.n) {
+#pragma unroll
+            for (int j = 0; j < 8; j += 4) {
+              float p[4];
+              St<DT_F32>::load_nt(a.pre.slot[m], i + j, p);
+#pragma unroll
+              for (int q = 0; q < 4; ++q) f[j + q] = fmaf(a.pre.c[m], p[q], f[j + q]);
+            }
+          }
+        }
+#pragma unroll
+        for (int j = 0; j < 8; ++j) v[k][j] = St<DT_IN>::rnd(v[k][j] + f[j]);
+        st8<DT_IN>(const_cast<void*>(a.in), i, v[k]);
+      }
     }
   }
 #pragma unroll
@@ -579,14 +608,18 @@ hipError_t ln_modulate(int dtype, const LnModArgs& a, hipStream_t s) {
   if (a.rows == 0) return hipSuccess;
   const int grid = cdiv(a.rows, 4);
   const int units = cdiv(a.C / 8, 64);   // 8-element units per lane (C % 8 == 0, C <= 4096 checked on the host)
-#define FF_LN(U)                                                                          \
-  do {                                                                                    \
-    if (dtype == DT_BF16) {                                                               \
-      if (a.in_f32) FF_LAUNCH((k_ln_modulate<DT_F32, DT_BF16, U>), grid, 256, 0, s, a);   \
-      else FF_LAUNCH((k_ln_modulate<DT_BF16, DT_BF16, U>), grid, 256, 0, s, a);           \
-    } else {                                                                              \
-      FF_LAUNCH((k_ln_modulate<DT_F32, DT_F32, U>), grid, 256, 0, s, a);                  \
-    }                                                                                     \
+  if (a.pre.n < 0 || a.pre.n > kMaxTerms || (a.pre.n > 0 && a.in_f32)) return hipErrorInvalidValue;
+#define FF_LN(U)                                                                                 \
+  do {                                                                                           \
+    if (dtype == DT_BF16) {                                                                      \
+      if (a.in_f32) FF_LAUNCH((k_ln_modulate<DT_F32, DT_BF16, U, false>), grid, 256, 0, s, a);   \
+      else if (a.pre.n) FF_LAUNCH((k_ln_modulate<DT_BF16, DT_BF16, U, true>), grid, 256, 0, s, a); \
+      else FF_LAUNCH((k_ln_modulate<DT_BF16, DT_BF16, U, false>), grid, 256, 0, s, a);           \
+    } else if (a.pre.n) {                                                                        \
+      FF_LAUNCH((k_ln_modulate<DT_F32, DT_F32, U, true>), grid, 256, 0, s, a);                   \
+    } else {                                                                                     \
+      FF_LAUNCH((k_ln_modulate<DT_F32, DT_F32, U, false>), grid, 256, 0, s, a);                  \
+    }                                                                                            \
   } while (0)
   if (units <= 1) FF_LN(1);
   else if (units <= 3) FF_LN(3);

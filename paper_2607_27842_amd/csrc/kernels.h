@@ -87,13 +87,27 @@ struct GemvBatch {
 inline size_t gemv_xs_bytes(int K) { return (size_t)16 * (kGemvMaxB / 8) * K * 2; }
 hipError_t gemv_batch(int dtype, const GemvBatch& bt, hipStream_t s);
 
+// ---------------------------------------------------------------- history / draft terms
+// Terms of a draft: sum_m c[m] * slot[m], m < n, in a fixed order (fp32 fmas from zero).
+struct Terms {
+  int n;                         // k_eff + 1
+  const void* slot[kMaxTerms];   // cache slots (model dtype, E elements each) or fp32 history sums
+  float c[kMaxTerms];            // forecast coefficients
+};
+
 // ---------------------------------------------------------------- normalisation
 // out[phys(r), :C] = LN(in[phys(r), :C]) * (1 + scale[b*ldm + :]) + shift[b*ldm + :]
+// With pre.n > 0 (input in the model dtype, not in_f32): a run of drafted layers is
+// applied to the row first from its fp32 history sums laid out like in,
+//   in[phys(r), :] <- round(in + sum_m pre.c[m] * pre.slot[m][phys(r), :])
+// exactly as draft_sum computes it, the row is written back to in, and the LayerNorm
+// normalises the updated row.
 struct LnModArgs {
   const void* in; int in_f32; int ldi;
   RowMap map; int rows, C; float eps;
   const float* shift; const float* scale; int ldm;
   void* out; int ldo;   // model dtype
+  Terms pre;
 };
 hipError_t ln_modulate(int dtype, const LnModArgs& a, hipStream_t s);
 
@@ -133,11 +147,6 @@ struct AttnArgs {
 hipError_t attention(int dtype, const AttnArgs& a, hipStream_t s);
 
 // ---------------------------------------------------------------- history / draft / verify
-struct Terms {
-  int n;                         // k_eff + 1
-  const void* slot[kMaxTerms];   // cache slots (model dtype, E elements each)
-  float c[kMaxTerms];            // forecast coefficients
-};
 // slot = round(h - u) (residual) or h (u == nullptr)
 hipError_t cache_update(int dtype, void* slot, const void* u, const void* h, size_t E, hipStream_t s);
 // hd = round((u ? u : 0) + sum_m c_m slot_m)
