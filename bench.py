@@ -259,11 +259,9 @@ def run_workload(name, mode_names, warmup_steps, n_loops, with_profile, adaptive
             ms = timed_steps(loop, window_steps)
             entry["window"] = {"steps": window_steps, "ms": round(ms, 3),
                                "steps_per_s": round(window_steps / (ms / 1e3), 2)}
-        if clock and mode_name == "featfix":
-            clock.start()
         entry.update(loop_entry(loop, (loops_for or {}).get(mode_name, n_loops)))
         if clock and mode_name == "featfix":
-            entry["gpu_clock"] = clock.stop()
+            entry["gpu_clock"] = clock.measure(loop)
         ref_ms, cac_ms = per_step_kind_ms(loop) if per_kind else (float("nan"), float("nan"))
         if per_kind:
             entry["ms_refresh_step"] = round(ref_ms, 4)
@@ -337,34 +335,43 @@ class ClockSampler:
         info = self.amdsmi.amdsmi_get_clock_info(self.handle, self.amdsmi.AmdSmiClkType.GFX)
         return float(info["clk"])
 
-    def start(self):
+    def measure(self, loop, seconds=3.0):
+        """The clock while the loop runs back to back for `seconds` (untimed): the SMU's
+        readings refresh every ~0.1 s and lag the load, so the first second's samples are
+        dropped and the median of the rest is reported."""
+        import statistics
         import threading
-        self.samples, self.run = [], True
+        import torch
         if self.handle is None:
-            return
+            return {"error": self.err}
+        samples, run = [], [True]
 
         def body():
-            while self.run:
+            t0 = time.time()
+            while run[0]:
                 try:
-                    self.samples.append(self.read())
+                    v = self.read()
                 except Exception as e:
                     self.err = f"{type(e).__name__}: {e}"
                     return
+                if time.time() - t0 > 1.0:
+                    samples.append(v)
                 time.sleep(0.01)
-        self.th = threading.Thread(target=body, daemon=True)
-        self.th.start()
-
-    def stop(self):
-        import statistics
-        self.run = False
-        if self.handle is None:
-            return {"error": self.err}
-        self.th.join()
-        if not self.samples:
+        th = threading.Thread(target=body, daemon=True)
+        th.start()
+        t0 = time.time()
+        while time.time() - t0 < seconds:
+            for _ in range(loop.r.T):
+                loop.step()
+            torch.cuda.synchronize()
+        run[0] = False
+        th.join()
+        if not samples:
             return {"error": self.err or "no samples"}
-        return {"source": "amdsmi GFX clock, sampled every ~10 ms during the timed loops",
-                "samples": len(self.samples), "mhz_median": statistics.median(self.samples),
-                "mhz_min": min(self.samples), "mhz_max": max(self.samples)}
+        return {"source": f"amdsmi GFX clock sampled every ~10 ms while the FeatFix loop ran back to back for "
+                          f"{seconds:.0f} s (first second dropped)",
+                "samples": len(samples), "mhz_median": statistics.median(samples),
+                "mhz_min": min(samples), "mhz_max": max(samples)}
 
 
 def shadow_vanilla(name="dit_xl2"):
@@ -618,6 +625,7 @@ def main():
     ap.add_argument("--no-sweep", action="store_true", help="skip the FLUX-like resolution sweep reported in extra")
     ap.add_argument("--no-guided", action="store_true", help="skip the guided (batch-doubled) DiT-XL/2 loops")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-clock", action="store_true", help="skip the 3 s clock-sampling run (profiling runs)")
     ap.add_argument("--no-hist-sums", action="store_true",
                     help="apply runs of drafted layers layer by layer instead of from history sums")
     args = ap.parse_args()
@@ -634,7 +642,7 @@ def main():
     abi.lib()
 
     calibration_copy()
-    clock = ClockSampler()
+    clock = None if args.no_clock else ClockSampler()
     name = "dit_xl2"
     cfg = synth.get_config(name)
     T = cfg["T"]
