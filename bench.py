@@ -613,6 +613,32 @@ def draft_per_layer_accounting(kern, plan, cfg):
             "effective_frac": round(gbs / PEAK_HBM_GBS, 4)}
 
 
+def exact_blocks_only(reps, name="dit_xl2"):
+    """Every layer of the workload through ff_block_exact `reps` times and nothing else:
+    the loop's exact-block kernels at its shapes, for counter profiles that need few
+    dispatches (each layer's fc2 here writes no history slot)."""
+    import torch
+    import synth
+    from paper_2607_27842_amd import abi, pipeline
+    cfg = synth.get_config(name)
+    dm = pipeline.DeviceModel.random(cfg)
+    n = cfg["n_img"] + cfg["n_txt"]
+    g = torch.Generator(device="cuda")
+    g.manual_seed(3)
+    u = torch.randn(cfg["B"], n, cfg["C"], device="cuda", generator=g).to(torch.bfloat16)
+    h = torch.empty_like(u)
+    c = torch.randn(cfg["B"], cfg["C"], device="cuda", generator=g)
+    ws_bytes = abi.ff_workspace_bytes(dm.desc)
+    ws = torch.empty(ws_bytes, dtype=torch.uint8, device="cuda")
+    s = torch.cuda.current_stream().cuda_stream
+    for r in range(reps):
+        for l in range(len(cfg["kinds"])):
+            abi.ff_block_exact(dm.desc, l, dm.lw[l], c.data_ptr(), u.data_ptr(), h.data_ptr(), ws.data_ptr(),
+                               ws_bytes, s)
+        torch.cuda.synchronize()
+        log(f"[bench] exact blocks only: pass {r + 1} of {reps} done")
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -626,6 +652,8 @@ def main():
     ap.add_argument("--no-guided", action="store_true", help="skip the guided (batch-doubled) DiT-XL/2 loops")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-clock", action="store_true", help="skip the 3 s clock-sampling run (profiling runs)")
+    ap.add_argument("--exact-blocks-only", type=int, default=0, metavar="REPS",
+                    help="run only the copy calibration and REPS passes of exact blocks (counter profiles)")
     ap.add_argument("--no-hist-sums", action="store_true",
                     help="apply runs of drafted layers layer by layer instead of from history sums")
     args = ap.parse_args()
@@ -642,6 +670,9 @@ def main():
     abi.lib()
 
     calibration_copy()
+    if args.exact_blocks_only:
+        exact_blocks_only(args.exact_blocks_only)
+        return
     clock = None if args.no_clock else ClockSampler()
     name = "dit_xl2"
     cfg = synth.get_config(name)
