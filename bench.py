@@ -530,7 +530,8 @@ def cpu_baseline(steps=12):
     Samples never interact and exact blocks dominate the oracle's time (drafts are
     elementwise), so the 50-step, batch-8 rate is extrapolated by exact-block count (this
     sample's 3 x 28 + 9 x 2 = 102 against 10 x 28 + 40 x 2 = 360 per loop) and batch, and
-    labelled so.  The tiny fp32 workload's whole 10-step loop is timed in every mode."""
+    labelled so.  The tiny fp32 workload's whole 10-step loop is timed in every mode, and
+    the MMDiT loops are priced per operation (mmdit_cpu_extrapolation)."""
     import oracle as O
     import synth
     cfg = synth.get_config("dit_xl2", T=steps, B=1)
@@ -567,7 +568,91 @@ def cpu_baseline(steps=12):
                       f"({sample_blocks} exact blocks); extrapolated to the 50-step loop by exact-block count "
                       f"({sample_blocks} -> {loop_blocks}) and to batch 8 (samples are independent): "
                       f"{loop_s:.0f} s per loop; host affinity {cores} cores, BLAS threads {blas_threads}",
-            "tiny_fp32_steps_per_s": tiny_rates}
+            "tiny_fp32_steps_per_s": tiny_rates,
+            "mmdit_per_block": mmdit_cpu_extrapolation()}
+
+
+def mmdit_cpu_extrapolation(tokens=256, row_frac=8):
+    """The oracle on the host for the MMDiT workloads, per operation, scaled to full size
+    and labelled extrapolated: one exact block of each kind at the workload's full width
+    over `tokens` rows (a quarter text), scaled to the full token count by the block's
+    FLOP count (projections and MLP linear in the tokens, attention quadratic); one draft
+    pass (forecast from a two-refresh history, Eq. 2, rounded to bf16) and one verify
+    pass (Eq. 4's distance) over 1/row_frac of the rows at full width, scaled linearly
+    (both are elementwise), each timed after one untimed pass.  The 50-step FeatFix loop
+    is priced from the plan's counts of exact blocks, drafted layers and paid checks.
+    Weight values do not change the oracle's time, so the matrices are a small random
+    block repeated to shape (fp64, as the oracle computes)."""
+    import numpy as np
+    import oracle as O
+    import synth
+    rng = np.random.default_rng(5)
+    base = rng.standard_normal(1 << 20) * 0.02
+
+    def fake_set(cfg, kind):
+        out = {}
+        for name, shp in synth.layer_shapes(cfg, kind).items():
+            out[name + "_w"] = np.resize(base, shp)
+            out[name + "_b"] = np.zeros((shp[0],))
+        if kind != synth.DIT:
+            out["q_g"] = np.ones((cfg["d"],))
+            out["k_g"] = np.ones((cfg["d"],))
+        return out
+
+    def timed(fn):
+        fn()
+        t0 = time.perf_counter()
+        fn()
+        return time.perf_counter() - t0
+
+    res = {}
+    for name in ("flux", "qwen", "hunyuan"):
+        full = synth.get_config(name)
+        L, T = len(full["kinds"]), full["T"]
+        entry = {"block_s": {}}
+        n_txt = min(full["n_txt"], tokens // 4)
+        cfg = dict(full, n_txt=n_txt, n_img=tokens - n_txt)
+        for kind in sorted(set(full["kinds"])):
+            W = {"txt": fake_set(cfg, kind), "img": fake_set(cfg, kind)} if kind == synth.MMDIT_DOUBLE \
+                else fake_set(cfg, kind)
+            u = rng.standard_normal((1, tokens, cfg["C"]))
+            cs = O.silu(rng.standard_normal((1, cfg["C"])))
+            t0 = time.perf_counter()
+            O.block(kind, u, cs, W, cfg)
+            dt = time.perf_counter() - t0
+            scale = O.block_flops(full, kind) / O.block_flops(cfg, kind)
+            entry["block_s"]["double" if kind == synth.MMDIT_DOUBLE else "single"] = {
+                "sample_tokens": tokens, "sample_s": round(dt, 3), "flop_scale": round(scale, 2),
+                "full_s": round(dt * scale, 2)}
+            del W
+        rows = (full["n_img"] + full["n_txt"]) // row_frac
+        shp = (1, rows, full["C"])
+        cache = O.TaylorCache(full["K"])
+        cache.refresh(rng.standard_normal(shp), 0)
+        cache.refresh(rng.standard_normal(shp), full["R"])
+        u, hf = rng.standard_normal(shp), rng.standard_normal(shp)
+        rnd = O.round_bf16 if full["dtype"] == synth.BF16 else (lambda a: a)
+        t_draft = timed(lambda: rnd(u + cache.forecast(full["R"] + 1))) * row_frac
+        hd = rnd(u + cache.forecast(full["R"] + 1))
+        t_verify = timed(lambda: O.rel_l1(hd, hf, full["rel_eps"])) * row_frac
+        del cache, u, hd, hf
+        plan = O.make_plan(T, L, full["R"], full["K"], full["S"], synth.site_mask(full), O.FEATFIX)
+        act = np.asarray(plan["action"])
+        kinds = np.asarray(full["kinds"])
+        exact = (act == O.EXACT) | (act == O.SITE)
+        loop_s = 0.0
+        for kind, key in ((synth.MMDIT_DOUBLE, "double"), (synth.MMDIT_SINGLE, "single")):
+            if key in entry["block_s"]:
+                loop_s += int(exact[:, kinds == kind].sum()) * entry["block_s"][key]["full_s"]
+        n_draft, n_check = int((act == O.DRAFT_ACT).sum()), int((act == O.SITE).sum())
+        loop_s += (n_draft + n_check) * t_draft + n_check * t_verify
+        entry.update({"draft_pass_s": round(t_draft, 3), "verify_pass_s": round(t_verify, 3),
+                      "exact_blocks_per_loop": int(exact.sum()), "drafted_layers_per_loop": n_draft,
+                      "paid_checks_per_loop": n_check, "loop_s": round(loop_s, 1),
+                      "steps_per_s": round(T / loop_s, 6), "extrapolated": True})
+        res[name] = entry
+        log(f"[bench] CPU oracle {name}: {entry['steps_per_s']} steps/s extrapolated ({loop_s:.0f} s per loop)")
+    return res
 
 
 WORKLOAD_TEXT = {
