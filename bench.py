@@ -44,6 +44,7 @@ TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_gemm_dit_xl2.json")
 # runs of drafted layers applied from per-run history sums formed at the refreshes
 # (ff_ctx_hist_sums); --no-hist-sums drafts layer by layer
 HIST_SUMS = True
+COND_CACHE = True   # conditioning of the whole schedule formed at step 0 (ff_ctx_cond_cache)
 GEMM_SOURCES = [os.path.join(ROOT, "paper_2607_27842_amd", "csrc", f) for f in ("k_gemm.hip", "dev_common.h")]
 
 
@@ -216,7 +217,7 @@ def adaptive_entry(dm, mask, fixed_loop, x0, cond, txt, n_loops):
     a = fixed_loop.audit.view(r0.T, r0.L, -1).cpu().numpy()
     per_step = [float(np.nanmax(a[i])) for i in range(r0.T) if np.isfinite(a[i]).any()]
     tau = float(np.median(per_step))
-    r = pipeline.Runner(dm, abi.FF_FEATFIX, mask, tau=tau, hist_sums=HIST_SUMS)
+    r = pipeline.Runner(dm, abi.FF_FEATFIX, mask, tau=tau, hist_sums=HIST_SUMS, cond_cache=COND_CACHE)
     loop = Loop(r, x0, cond, txt)
     for _ in range(r.T):
         loop.step()
@@ -250,7 +251,7 @@ def run_workload(name, mode_names, warmup_steps, n_loops, with_profile, adaptive
     res = {"sites": synth.sites_of(cfg)}
     for mode_name in mode_names:
         mode = synth.MODE_NAMES[mode_name]
-        r = pipeline.Runner(dm, mode, mask, hist_sums=HIST_SUMS)
+        r = pipeline.Runner(dm, mode, mask, hist_sums=HIST_SUMS, cond_cache=COND_CACHE)
         loop = Loop(r, x0, cond, txt)
         for _ in range(warmup_steps):
             loop.step()
@@ -296,7 +297,7 @@ def per_layer_draft_profile(name="dit_xl2"):
     cfg = synth.get_config(name)
     dm = pipeline.DeviceModel.random(cfg, seed=0)
     x0, cond, txt = device_inputs(cfg)
-    r = pipeline.Runner(dm, synth.MODE_NAMES["featfix"], synth.site_mask(cfg), hist_sums=False)
+    r = pipeline.Runner(dm, synth.MODE_NAMES["featfix"], synth.site_mask(cfg), hist_sums=False, cond_cache=COND_CACHE)
     loop = Loop(r, x0, cond, txt)
     for _ in range(r.T):
         loop.step()
@@ -392,11 +393,11 @@ def shadow_vanilla(name="dit_xl2"):
     E = B * (cfg["n_img"] + cfg["n_txt"]) * cfg["C"]
     dt = pipeline.torch_dtype(cfg)
     out = {}
-    van = pipeline.Runner(dm, abi.FF_VANILLA, mask, hist_sums=HIST_SUMS)
+    van = pipeline.Runner(dm, abi.FF_VANILLA, mask, hist_sums=HIST_SUMS, cond_cache=COND_CACHE)
     vbuf = torch.empty(L * E, dtype=dt, device="cuda")
     van.trace_into(vbuf)
     for mode_name, mode in (("featfix", abi.FF_FEATFIX), ("verify", abi.FF_VERIFY)):
-        r = pipeline.Runner(dm, mode, mask, hist_sums=HIST_SUMS)
+        r = pipeline.Runner(dm, mode, mask, hist_sums=HIST_SUMS, cond_cache=COND_CACHE)
         buf = torch.empty(L * E, dtype=dt, device="cuda")
         r.trace_into(buf)
         xr, _ = r.start(x0, audit=False)
@@ -433,7 +434,7 @@ def rope_loop():
     cfg = synth.get_config("flux", rope_axes=(16, 56, 56), rope_theta=10000.0)
     dm = pipeline.DeviceModel.random(cfg, seed=0)
     x0, cond, txt = device_inputs(cfg)
-    r = pipeline.Runner(dm, synth.MODE_NAMES["featfix"], synth.site_mask(cfg), hist_sums=HIST_SUMS)
+    r = pipeline.Runner(dm, synth.MODE_NAMES["featfix"], synth.site_mask(cfg), hist_sums=HIST_SUMS, cond_cache=COND_CACHE)
     loop = Loop(r, x0, cond, txt)
     for _ in range(r.T):
         loop.step()
@@ -460,7 +461,7 @@ def guided_loop(scale=4.0):
     x0, cond, txt = device_inputs(cfg)
     out = {"model_rows": cfg["B"], "images": cfg["B"] // 2, "cfg_scale": scale}
     for mode in ("featfix", "vanilla"):
-        r = pipeline.Runner(dm, synth.MODE_NAMES[mode], synth.site_mask(cfg), hist_sums=HIST_SUMS)
+        r = pipeline.Runner(dm, synth.MODE_NAMES[mode], synth.site_mask(cfg), hist_sums=HIST_SUMS, cond_cache=COND_CACHE)
         loop = Loop(r, x0, cond, txt)
         for _ in range(r.T):
             loop.step()
@@ -500,7 +501,7 @@ def resolution_sweep(sides=(512, 768, 1024)):
             torch.cuda.synchronize()
             torch.cuda.empty_cache()
             torch.cuda.reset_peak_memory_stats()
-            r = pipeline.Runner(dm, synth.MODE_NAMES[mode_name], mask, hist_sums=HIST_SUMS)
+            r = pipeline.Runner(dm, synth.MODE_NAMES[mode_name], mask, hist_sums=HIST_SUMS, cond_cache=COND_CACHE)
             loop = Loop(r, x0, cond, txt)
             for _ in range(r.T):
                 loop.step()
@@ -510,7 +511,8 @@ def resolution_sweep(sides=(512, 768, 1024)):
                               "peak_gib": round(torch.cuda.max_memory_allocated() / 2**30, 2),
                               "cache_gib": round(r.cache_bytes / 2**30, 3),
                               "workspace_gib": round(r.ws_bytes / 2**30, 3),
-                              "hist_sum_gib": round((0 if r.hsum is None else r.hsum.numel()) / 2**30, 3)}
+                              "hist_sum_gib": round((0 if r.hsum is None else r.hsum.numel()) / 2**30, 3),
+                              "cond_cache_gib": round((0 if r.ccache is None else r.ccache.numel()) / 2**30, 3)}
             r.close()
             del loop, r
         row["speedup"] = round(row["vanilla"]["s_per_loop"] / row["featfix"]["s_per_loop"], 3)
@@ -739,11 +741,14 @@ def main():
     ap.add_argument("--no-clock", action="store_true", help="skip the 3 s clock-sampling run (profiling runs)")
     ap.add_argument("--exact-blocks-only", type=int, default=0, metavar="REPS",
                     help="run only the copy calibration and REPS passes of exact blocks (counter profiles)")
+    ap.add_argument("--no-cond-cache", action="store_true",
+                    help="form the conditioning (time MLP, modulation) at every step instead of once per loop")
     ap.add_argument("--no-hist-sums", action="store_true",
                     help="apply runs of drafted layers layer by layer instead of from history sums")
     args = ap.parse_args()
-    global HIST_SUMS
+    global HIST_SUMS, COND_CACHE
     HIST_SUMS = not args.no_hist_sums
+    COND_CACHE = not args.no_cond_cache
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py runs on one GPU only: the FeatFix path here is single-GPU "
               "(no sharding or collectives); use --gpus 1", file=sys.stderr)
@@ -809,7 +814,9 @@ def main():
            "vs_baseline": None, "dtype": "bf16",
            "data": "synthetic: seeded N(0,1) latent and class/text vectors, random-init N(0,0.02) weights",
            "config": {"workload": WORKLOAD_TEXT[name] + ("; drafted runs from history sums" if HIST_SUMS
-                                                         else "; drafted runs layer by layer"),
+                                                         else "; drafted runs layer by layer")
+                                  + ("; conditioning of all steps formed at step 0" if COND_CACHE
+                                     else "; conditioning formed at every step"),
                       "global_batch": cfg["B"],
                       "seq_len": cfg["n_img"] + cfg["n_txt"], "parallelism": "none (1 GPU)"},
            "timing": {"value_from": f"median of {n_loops} whole {T}-step loops (HIP events per loop) after {W} "

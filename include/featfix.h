@@ -379,6 +379,27 @@ ff_status ff_denoise_step(ff_ctx* c, int32_t step, float* x, const float* cond,
 size_t ff_hist_sum_bytes(const ff_model_desc* m, const ff_plan* p);
 ff_status ff_ctx_hist_sums(ff_ctx* c, void* buf, size_t bytes);
 
+/* ---------------------------------------------------------------- conditioning cache
+ * The conditioning c_t = c + TimeMLP(phi(1000 t_i)) and the adaLN modulation of every
+ * exact block (Eq. 1) depend on the class / text vector and the step only, never on the
+ * latent.  ff_cond_cache_bytes(m, p): bytes of the cache for plan p (0 on an invalid
+ * descriptor).  ff_ctx_cond_cache(c, buf, bytes): with buf set, step 0 of c forms the
+ * conditioning of the whole schedule into buf from the cond it is given: the time
+ * embedding and MLP of all T steps, SiLU(c_t), the modulation vectors of every layer at
+ * the steps where the plan may run it exact (every step for layers that are sites of a
+ * cached step, that run exact at a cached step, or when tau > 0; the refresh steps
+ * otherwise), and the final layer's modulation of every step, as one GEMM per weight set
+ * (bf16: SiLU(c_t) as the same bf16 hi + lo parts the per-step GEMVs use).  Later steps
+ * read them and launch no conditioning work.  Every step must then pass the same cond
+ * pointer as step 0, holding the same values (a different pointer is FF_E_STATE).  The
+ * vectors agree with the per-step ones to fp32 rounding (other summation order), not bit
+ * for bit.  buf is the caller's device memory, 256-byte aligned, untouched by the caller
+ * while c uses it; buf NULL turns the cache off at any time.
+ * Errors: FF_E_NULL (c); FF_E_STATE (enabling after step 0 before ff_ctx_reset);
+ * FF_E_WORKSPACE (bytes); FF_E_SHAPE (alignment). */
+size_t ff_cond_cache_bytes(const ff_model_desc* m, const ff_plan* p);
+ff_status ff_ctx_cond_cache(ff_ctx* c, void* buf, size_t bytes);
+
 /* ---------------------------------------------------------------- diagnostics
  * Per-layer feature traces for mechanism studies on synthetic weights (the paper tracks
  * the downstream relative-L1 error of corrected runs against Vanilla per layer and stage,

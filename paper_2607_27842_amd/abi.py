@@ -32,7 +32,7 @@ FF_NOALLOC_VERIFY_MAX_B = 16
 EXPORTED = ("ff_abi_version", "ff_last_error", "ff_plan_build", "ff_plan_destroy", "ff_plan_export",
             "ff_cache_bytes", "ff_workspace_bytes", "ff_block_exact", "ff_cache_update",
             "ff_draft_forecast", "ff_verify_replace", "ff_verify_replace_noalloc", "ff_ctx_create", "ff_ctx_destroy",
-            "ff_ctx_reset", "ff_get_counts", "ff_ctx_step_kinds", "ff_denoise_step", "ff_ctx_trace", "ff_hist_sum_bytes", "ff_ctx_hist_sums", "ff_rel_l1",
+            "ff_ctx_reset", "ff_get_counts", "ff_ctx_step_kinds", "ff_denoise_step", "ff_ctx_trace", "ff_hist_sum_bytes", "ff_ctx_hist_sums", "ff_cond_cache_bytes", "ff_ctx_cond_cache", "ff_rel_l1",
             "ff_ctx_profile", "ff_ctx_profile_read")
 PROF_CLASSES = ("gemm", "attn", "norm", "gemv", "draft", "verify", "cache", "other")
 
@@ -128,6 +128,8 @@ def lib():
             "ff_ctx_trace": (i32, [vp, vp, sz]),
             "ff_hist_sum_bytes": (sz, [P(ff_model_desc), vp]),
             "ff_ctx_hist_sums": (i32, [vp, vp, sz]),
+            "ff_cond_cache_bytes": (sz, [P(ff_model_desc), vp]),
+            "ff_ctx_cond_cache": (i32, [vp, vp, sz]),
             "ff_rel_l1": (i32, [P(ff_model_desc), vp, vp, f32, vp, vp, sz, vp]),
             "ff_denoise_step": (i32, [vp, i32, vp, vp, vp, vp, vp]),
             "ff_ctx_profile": (i32, [vp, i32]),
@@ -275,6 +277,14 @@ def ff_hist_sum_bytes(model, plan):
 
 def ff_ctx_hist_sums(ctx, buf, nbytes):
     return check(lib().ff_ctx_hist_sums(ctx, buf, nbytes))
+
+
+def ff_cond_cache_bytes(model, plan):
+    return lib().ff_cond_cache_bytes(C.byref(model), plan)
+
+
+def ff_ctx_cond_cache(ctx, buf, nbytes):
+    return check(lib().ff_ctx_cond_cache(ctx, buf, nbytes))
 
 
 def ff_rel_l1(model, a, b, eps, rel, ws, ws_bytes, stream=0):

@@ -259,6 +259,11 @@ struct Exec {
     }
     return timed(FF_PROF_GEMV, fl, by, [&] { return ff::gemv_batch(dt, b, st); });
   }
+  // a modulation GEMM of the conditioning cache (counted with the GEMVs it replaces)
+  hipError_t mod_gemm(const GemmArgs& a) {
+    const double bytes = ((double)a.M * a.K + (double)a.N * a.K) * es + (double)a.M * a.N * (a.out_f32 ? 4 : es);
+    return timed(FF_PROF_GEMV, 2.0 * a.M * a.N * a.K, bytes, [&] { return ff::gemm(dt, a, st); });
+  }
   hipError_t gemv(const GemvArgs& a) {
     return timed(FF_PROF_GEMV, 2.0 * a.B * a.Nout * a.K, (double)a.Nout * a.K * es, [&] { return ff::gemv(dt, a, st); });
   }
@@ -601,6 +606,74 @@ bool forwards(int mode) { return mode == FF_FEATFIX || mode == FF_EXACT_ONLY || 
 
 }  // namespace
 
+namespace {
+
+// Conditioning cache (ff_ctx_cond_cache).  The conditioning c_t = cond + TimeMLP(phi(1000 t_i))
+// and every adaLN modulation vector depend on the class / text vector and the step only,
+// never on the latent, so with the cache the context forms them for the whole schedule at
+// step 0: the time embeddings and MLP of all T steps, SiLU(c_t) (bf16: as hi / lo rows),
+// then one GEMM per weight set over the steps at which that layer runs exact, and the
+// final layer's modulation for every step.  Layout of the caller's buffer (each part
+// 256-byte aligned): PHI [T, 256], TMP and U [T, C] fp32; bf16: XS [T, 16 * groups, C]
+// bf16, ZB (zeros, 6C bf16), OUT [T * 16 * groups, 6C] fp32 (the GEMM's hi / lo rows);
+// fp32: CSA [T, B, C]; then per layer its modulation vectors [nb, B, ldy] fp32 and FMOD
+// [T, B, 2C] fp32.
+struct CondLayer { bool all; int nb; size_t off; int ldy; };
+struct CondLayout {
+  size_t PHI = 0, TMP = 0, U = 0, XS = 0, CSA = 0, ZB = 0, OUT = 0, FMOD = 0, total = 0;
+  int R16 = 0;   // bf16: GEMM rows per step (16 per group of 8 model rows)
+  std::vector<CondLayer> layer;
+};
+
+// Which steps' modulation a layer's GEMM covers: every step, or only the refresh steps
+// (i % R == 0), the latter when the plan runs the layer exact at refresh steps only and
+// the mask puts no site on it at a cached step.  The choice follows the mask, not the
+// mode, so modes whose exact blocks coincide (FeatFix and Exact-only, Verify and Draft)
+// read identical vectors; with tau > 0 every step may refresh.
+bool cond_all_steps(const ff_plan& p, int l) {
+  const int T = p.s.T, L = p.L, R = p.s.R;
+  if (p.s.tau > 0.f) return true;
+  for (int i = 0; i < T; ++i) {
+    const int a = p.action[(size_t)i * L + l];
+    const bool exact = a == FF_ACT_EXACT || a == FF_ACT_SITE || a == FF_ACT_RECOMPUTE;
+    if (exact && i % R != 0) return true;
+    if (p.step_kind[i] == FF_STEP_CACHED && p.mask[(size_t)i * L + l]) return true;
+  }
+  return false;
+}
+
+CondLayout cond_layout(const Model& m, const ff_plan& p) {
+  CondLayout cl;
+  size_t off = 0;
+  auto take = [&](size_t bytes) { size_t o = off; off += align_up(bytes); return o; };
+  const size_t T = p.s.T, C = m.C, B = m.B;
+  const bool bf = m.dtype == FF_BF16;
+  cl.R16 = 16 * ((m.B + 7) / 8);
+  cl.PHI = take(T * FF_TEMB_DIM * 4);
+  cl.TMP = take(T * C * 4);
+  cl.U = take(T * C * 4);
+  if (bf) {
+    cl.XS = take(T * cl.R16 * C * 2);
+    cl.ZB = take(6 * C * 2);
+    cl.OUT = take(T * cl.R16 * 6 * C * 4);
+  } else {
+    cl.CSA = take(T * B * C * 4);
+  }
+  for (int l = 0; l < m.L; ++l) {
+    CondLayer cy;
+    cy.all = cond_all_steps(p, l);
+    cy.nb = cy.all ? p.s.T : (p.s.T + p.s.R - 1) / p.s.R;
+    cy.ldy = mod_floats(m.kinds[l], m.C);
+    cy.off = take((size_t)cy.nb * B * cy.ldy * 4);
+    cl.layer.push_back(cy);
+  }
+  cl.FMOD = take(T * B * 2 * C * 4);
+  cl.total = off;
+  return cl;
+}
+
+}  // namespace
+
 struct ff_ctx {
   Model m;
   std::vector<ff_layer_weights> lw;
@@ -625,6 +698,11 @@ struct ff_ctx {
   // history sums (ff_ctx_hist_sums): fp32 [runs][S][B*N*C], formed at every refresh
   float* hsum = nullptr;
   std::vector<std::pair<int, int>> runs;
+  // conditioning cache (ff_ctx_cond_cache): formed at step 0 from cond, which every later
+  // step must pass again
+  char* cc = nullptr;
+  CondLayout cc_lay;
+  const float* cc_cond = nullptr;
   ~ff_ctx() {
     if (a_ev) (void)hipEventDestroy(a_ev);
     if (a_rel) (void)hipHostFree(a_rel);
@@ -990,6 +1068,73 @@ ff_status ff_get_counts(const ff_ctx* c, ff_counts* out) {
   return ok();
 }
 
+namespace {
+
+// The conditioning of every step of c's schedule into its cache (CondLayout): the same
+// time embedding, time MLP and SiLU as each step forms, for all T steps at once, then each
+// layer's modulation as one GEMM over the steps it needs and the final layer's for all.
+// bf16: SiLU(c_t) enters the GEMM as bf16 hi / lo rows (the split the GEMVs use), whose two
+// products are summed with the bias afterwards; fp32: the fp32 rows directly.
+ff_status cond_precompute(ff_ctx* c, const float* cond, Exec& ex) {
+  const Model& m = c->m;
+  const CondLayout& cl = c->cc_lay;
+  const int T = c->plan.s.T, R = c->plan.s.R, C = m.C, B = m.B;
+  const bool bf = m.dtype == FF_BF16;
+  char* base = c->cc;
+  hipStream_t st = ex.st;
+  float* phi = reinterpret_cast<float*>(base + cl.PHI);
+  float* tmp = reinterpret_cast<float*>(base + cl.TMP);
+  float* u = reinterpret_cast<float*>(base + cl.U);
+  HIP_TRY(ex.other((double)T * FF_TEMB_DIM * 4, [&] { return time_embed_steps((double)T, T, phi, st); }),
+          "conditioning cache: time embedding");
+  for (int r0 = 0; r0 < T; r0 += kGemvMaxB) {
+    const int nr = std::min(kGemvMaxB, T - r0);
+    GemvArgs g1{phi + (size_t)r0 * FF_TEMB_DIM, FF_TEMB_DIM, 0, c->g.t1_w, c->g.t1_b, C, FF_TEMB_DIM, nr,
+                tmp + (size_t)r0 * C, C, 1, nullptr, 0};
+    HIP_TRY(ex.gemv(g1), "conditioning cache: time mlp 1");
+    GemvArgs g2{tmp + (size_t)r0 * C, C, 0, c->g.t2_w, c->g.t2_b, C, C, nr, u + (size_t)r0 * C, C, 0, nullptr, 0};
+    HIP_TRY(ex.gemv(g2), "conditioning cache: time mlp 2");
+  }
+  uint16_t* xs = bf ? reinterpret_cast<uint16_t*>(base + cl.XS) : nullptr;
+  float* csa = bf ? nullptr : reinterpret_cast<float*>(base + cl.CSA);
+  uint16_t* zb = bf ? reinterpret_cast<uint16_t*>(base + cl.ZB) : nullptr;
+  HIP_TRY(ex.other((double)T * B * C * 8, [&] { return cond_split(u, cond, T, B, C, xs, csa, zb, bf ? 6 * C : 0, st); }),
+          "conditioning cache: silu(c_t)");
+  float* out = bf ? reinterpret_cast<float*>(base + cl.OUT) : nullptr;
+  // one weight set over nb step blocks (every step, or every R-th) -> dst [nb, B, ldy]
+  auto modulate = [&](const void* W, const void* bias, int N, bool all, int nb, float* dst, int ldy) -> ff_status {
+    if (bf) {
+      const int M = nb * cl.R16;
+      const RowMap am = all ? RowMap{M, M, 0} : RowMap{cl.R16, cl.R16 * R, 0};
+      GemmArgs g = gemm_args(xs, C, am, W, zb, M, N, C, EPI_BIAS, out, N, RowMap{M, M, 0});
+      g.out_f32 = 1;
+      HIP_TRY(ex.mod_gemm(g), "conditioning cache: modulation");
+      HIP_TRY(ex.other(((double)M + nb * B) * N * 4.0,
+                       [&] { return mod_combine(m.dtype, out, N, bias, dst, ldy, nb, B, st); }),
+              "conditioning cache: modulation sum");
+    } else {
+      const int M = nb * B;
+      const RowMap am = all ? RowMap{M, M, 0} : RowMap{B, B * R, 0};
+      GemmArgs g = gemm_args(csa, C, am, W, bias, M, N, C, EPI_BIAS, dst, ldy, RowMap{M, M, 0});
+      HIP_TRY(ex.mod_gemm(g), "conditioning cache: modulation");
+    }
+    return FF_OK;
+  };
+  for (int l = 0; l < m.L; ++l) {
+    const CondLayer& cy = cl.layer[l];
+    float* dst = reinterpret_cast<float*>(base + cy.off);
+    const ff_stream_weights* sw = c->lw[l].s;
+    const int kind = m.kinds[l];
+    const int N = kind == FF_MMDIT_SINGLE ? 3 * C : 6 * C;
+    ff_status e = modulate(sw[0].mod_w, sw[0].mod_b, N, cy.all, cy.nb, dst, cy.ldy);
+    if (!e && kind == FF_MMDIT_DOUBLE) e = modulate(sw[1].mod_w, sw[1].mod_b, N, cy.all, cy.nb, dst + 6 * C, cy.ldy);
+    if (e) return e;
+  }
+  return modulate(c->g.fmod_w, c->g.fmod_b, 2 * C, true, T, reinterpret_cast<float*>(base + cl.FMOD), 2 * C);
+}
+
+}  // namespace
+
 ff_status ff_denoise_step(ff_ctx* c, int32_t step, float* x, const float* cond, const void* txt, float* audit,
                           ff_stream_t stream) {
   try {
@@ -1001,6 +1146,8 @@ ff_status ff_denoise_step(ff_ctx* c, int32_t step, float* x, const float* cond, 
     if (step != c->next_step || step >= s.T)
       return fail(FF_E_STATE, "step %d out of order (expected %d of %d)", step, c->next_step, s.T);
     if (!aligned16(x) || !aligned16(cond) || (txt && !aligned16(txt))) return fail(FF_E_SHAPE, "pointers must be 16-byte aligned");
+    if (c->cc && step > 0 && cond != c->cc_cond)
+      return fail(FF_E_STATE, "step %d: cond is not the buffer the conditioning cache was formed from at step 0", step);
     const int L = m.L, K = s.K, S = s.S, i = step;
     if (s.tau > 0.f) {
       // adaptive refresh: decide this step from the interval and the previous step's
@@ -1051,16 +1198,23 @@ ff_status ff_denoise_step(ff_ctx* c, int32_t step, float* x, const float* cond, 
     float* tmp = at<float>(ws, W.TMP);
     float* ct = at<float>(ws, W.CT);
     float* cs = at<float>(ws, W.CS);
-    // conditioning: c_t = cond + W_t2 SiLU(W_t1 phi(1000 t) + b_t1) + b_t2
-    HIP_TRY(ex.other(FF_TEMB_DIM * 4.0, [&] { return time_embed(1000.0 * t_i, phi, st); }), "time embedding");
-    GemvArgs g1{phi, 0, 0, c->g.t1_w, c->g.t1_b, C, FF_TEMB_DIM, m.B, tmp, C, 1, nullptr, 0};
-    HIP_TRY(ex.gemv(g1), "time mlp 1");
-    GemvArgs g2{tmp, C, 0, c->g.t2_w, c->g.t2_b, C, C, m.B, ct, C, 0, cond, C};
-    HIP_TRY(ex.gemv(g2), "time mlp 2");
-    // bf16: SiLU(c_t) also as the hi / lo split that the modulation batches and the final
-    // modulation read (made once here rather than by each of their workgroups)
     uint16_t* xs = dt == FF_BF16 ? at<uint16_t>(ws, W.XS) : nullptr;
-    HIP_TRY(ex.other(8.0 * m.B * C, [&] { return silu_rows(ct, cs, m.B, C, xs, st); }), "silu(c_t)");
+    const CondLayout& cl = c->cc_lay;
+    if (c->cc && i == 0) {   // the conditioning of the whole schedule (cond is checked at later steps)
+      if (ff_status e = cond_precompute(c, cond, ex)) return e;
+      c->cc_cond = cond;
+    }
+    if (!c->cc) {
+      // conditioning: c_t = cond + W_t2 SiLU(W_t1 phi(1000 t) + b_t1) + b_t2
+      HIP_TRY(ex.other(FF_TEMB_DIM * 4.0, [&] { return time_embed(1000.0 * t_i, phi, st); }), "time embedding");
+      GemvArgs g1{phi, 0, 0, c->g.t1_w, c->g.t1_b, C, FF_TEMB_DIM, m.B, tmp, C, 1, nullptr, 0};
+      HIP_TRY(ex.gemv(g1), "time mlp 1");
+      GemvArgs g2{tmp, C, 0, c->g.t2_w, c->g.t2_b, C, C, m.B, ct, C, 0, cond, C};
+      HIP_TRY(ex.gemv(g2), "time mlp 2");
+      // bf16: SiLU(c_t) also as the hi / lo split that the modulation batches and the final
+      // modulation read (made once here rather than by each of their workgroups)
+      HIP_TRY(ex.other(8.0 * m.B * C, [&] { return silu_rows(ct, cs, m.B, C, xs, st); }), "silu(c_t)");
+    }
     // Modulation of the layers that run exact this step, computed kModLayers layers at a
     // time in one batched GEMV launch each; mod_of[l] = that layer's vectors.
     auto runs_exact = [&](int l) {
@@ -1071,6 +1225,12 @@ ff_status ff_denoise_step(ff_ctx* c, int32_t step, float* x, const float* cond, 
     std::vector<const float*> mod_of(L, nullptr);
     auto ensure_mod = [&](int l) -> ff_status {
       if (mod_of[l]) return FF_OK;
+      if (c->cc) {   // formed at step 0
+        const CondLayer& cy = cl.layer[l];
+        if (!cy.all && i % s.R) return fail(FF_E_STATE, "step %d layer %d: no cached modulation", i, l);
+        mod_of[l] = reinterpret_cast<const float*>(c->cc + cy.off) + (size_t)(cy.all ? i : i / s.R) * m.B * cy.ldy;
+        return FF_OK;
+      }
       GemvBatch bt{};
       bt.x = cs; bt.ldx = C; bt.silu_in = 0; bt.K = C; bt.B = m.B; bt.xs = xs;
       int slot = 0;
@@ -1228,8 +1388,12 @@ ff_status ff_denoise_step(ff_ctx* c, int32_t step, float* x, const float* cond, 
     }
     // final layer on the image rows, unpatchify and Euler
     float* mod = at<float>(ws, W.MOD);
-    GemvArgs gf{cs, C, 0, c->g.fmod_w, c->g.fmod_b, 2 * C, C, m.B, mod, 2 * C, 0, nullptr, 0, xs};
-    HIP_TRY(ex.gemv(gf), "final modulation");
+    if (c->cc) {
+      mod = reinterpret_cast<float*>(c->cc + cl.FMOD) + (size_t)i * m.B * 2 * C;
+    } else {
+      GemvArgs gf{cs, C, 0, c->g.fmod_w, c->g.fmod_b, 2 * C, C, m.B, mod, 2 * C, 0, nullptr, 0, xs};
+      HIP_TRY(ex.gemv(gf), "final modulation");
+    }
     if (final_layer_ok(dt, m.P, C) && !m.cfg) {
       // LN + modulation + final linear + unpatchify + Euler in one launch, one wavefront
       // per image token (small final weights only)
@@ -1311,6 +1475,38 @@ ff_status ff_ctx_hist_sums(ff_ctx* c, void* buf, size_t bytes) {
     if (!aligned16(buf)) return fail(FF_E_SHAPE, "history sum buffer must be 16-byte aligned");
     c->runs = std::move(runs);
     c->hsum = static_cast<float*>(buf);
+    return ok();
+  } catch (...) {
+    return fail(FF_E_UNSUPPORTED, "unexpected host exception");
+  }
+}
+
+size_t ff_cond_cache_bytes(const ff_model_desc* m, const ff_plan* p) {
+  Model md;
+  if (!p || check_model(m, &md) != FF_OK || md.L != p->L) return 0;
+  try {
+    return cond_layout(md, *p).total;
+  } catch (...) {
+    return 0;
+  }
+}
+
+ff_status ff_ctx_cond_cache(ff_ctx* c, void* buf, size_t bytes) {
+  try {
+    if (!c) return fail(FF_E_NULL, "ctx is NULL");
+    if (!buf) {
+      c->cc = nullptr;
+      c->cc_cond = nullptr;
+      return ok();
+    }
+    if (c->next_step != 0)
+      return fail(FF_E_STATE, "the conditioning cache is enabled before step 0 (or after ff_ctx_reset)");
+    CondLayout cl = cond_layout(c->m, c->plan);
+    if (bytes < cl.total) return fail(FF_E_WORKSPACE, "conditioning cache %zu < %zu bytes", bytes, cl.total);
+    if ((uintptr_t)buf % kAlign) return fail(FF_E_SHAPE, "conditioning cache must be %zu-byte aligned", (size_t)kAlign);
+    c->cc_lay = std::move(cl);
+    c->cc = static_cast<char*>(buf);
+    c->cc_cond = nullptr;
     return ok();
   } catch (...) {
     return fail(FF_E_UNSUPPORTED, "unexpected host exception");

@@ -426,6 +426,58 @@ __global__ void k_time_embed(double s, float* phi) {
   phi[128 + k] = (float)sin(s * f);
 }
 
+__global__ void k_time_embed_steps(double T, int n, float* phi) {
+  const int k = threadIdx.x, i = blockIdx.x;   // 0..127, step
+  if (i >= n) return;
+  const double s = 1000.0 * (1.0 - (double)i / T);
+  const double f = exp(-log(10000.0) * (double)k / 128.0);
+  phi[(size_t)i * 256 + k] = (float)cos(s * f);
+  phi[(size_t)i * 256 + 128 + k] = (float)sin(s * f);
+}
+
+__global__ void k_cond_split(const float* u, const float* cond, int nsteps, int B, int C, uint16_t* xs, float* cs,
+                             uint16_t* zb, int nzb) {
+  const long idx = (long)blockIdx.x * 256 + threadIdx.x;
+  if (zb && idx < nzb) zb[idx] = 0;
+  const int G8 = xs ? (B + 7) / 8 * 8 : B;   // rows per step, absent samples included
+  if (idx >= (long)nsteps * G8 * C) return;
+  const int k = (int)(idx % C);
+  const long ib = idx / C;
+  const int b = (int)(ib % G8), i = (int)(ib / G8);
+  // c_t = cond + u and its SiLU as the per-step path forms them (fp32)
+  const float v = b < B ? silu_f(cond[(size_t)b * C + k] + u[(size_t)i * C + k]) : 0.f;
+  if (xs) {
+    uint16_t* x = xs + (size_t)i * 2 * G8 * C;   // 16 rows per group of 8
+    const int r = 16 * (b / 8) + b % 8;
+    const uint16_t h = f2bf(v);
+    x[(size_t)r * C + k] = h;
+    x[(size_t)(r + 8) * C + k] = f2bf(v - bf2f(h));
+  } else {
+    cs[((size_t)i * B + b) * C + k] = v;
+  }
+}
+
+template <int DT>
+__global__ void k_mod_combine(const float* __restrict__ out, int N, const void* __restrict__ bias,
+                              float* __restrict__ dst, int ldy, int nb, int B) {
+  const int n4 = N / 4;
+  const long idx = (long)blockIdx.x * 256 + threadIdx.x;
+  if (idx >= (long)nb * B * n4) return;
+  const int n = (int)(idx % n4) * 4;
+  const long jb = idx / n4;
+  const int b = (int)(jb % B), j = (int)(jb / B);
+  const int R16 = 16 * ((B + 7) / 8), r = j * R16 + 16 * (b / 8) + b % 8;
+  const f32x4_t hi = *reinterpret_cast<const f32x4_t*>(out + (size_t)r * N + n);
+  const f32x4_t lo = *reinterpret_cast<const f32x4_t*>(out + (size_t)(r + 8) * N + n);
+  float bv[4];
+#pragma unroll
+  for (int e = 0; e < 4; ++e) bv[e] = St<DT>::ld1(bias, n + e);
+  f32x4_t y;
+#pragma unroll
+  for (int e = 0; e < 4; ++e) y[e] = (hi[e] + lo[e]) + bv[e];
+  *reinterpret_cast<f32x4_t*>(dst + (size_t)jb * ldy + n) = y;
+}
+
 __global__ void k_silu_rows(const float* x, float* y, int B, int n, uint16_t* xs) {
   const long i = (long)blockIdx.x * 256 + threadIdx.x;
   if (i >= (long)B * n) return;
@@ -720,6 +772,31 @@ hipError_t gemv_batch(int dtype, const GemvBatch& bt, hipStream_t s) {
 
 hipError_t time_embed(double sv, float* phi, hipStream_t st) {
   FF_LAUNCH(k_time_embed, 1, 128, 0, st, sv, phi);
+  return hipGetLastError();
+}
+
+hipError_t time_embed_steps(double T, int n, float* phi, hipStream_t st) {
+  if (n <= 0) return hipSuccess;
+  FF_LAUNCH(k_time_embed_steps, n, 128, 0, st, T, n, phi);
+  return hipGetLastError();
+}
+
+hipError_t cond_split(const float* u, const float* cond, int nsteps, int B, int C, uint16_t* xs, float* cs,
+                      uint16_t* zb, int nzb, hipStream_t st) {
+  const long rows = xs ? (long)(B + 7) / 8 * 8 : B;
+  const long tot = std::max((long)nsteps * rows * C, (long)nzb);
+  if (tot <= 0) return hipSuccess;
+  FF_LAUNCH(k_cond_split, cdiv(tot, 256), 256, 0, st, u, cond, nsteps, B, C, xs, cs, zb, nzb);
+  return hipGetLastError();
+}
+
+hipError_t mod_combine(int dtype, const float* out, int N, const void* bias, float* dst, int ldy, int nb, int B,
+                       hipStream_t st) {
+  if (N % 4) return hipErrorInvalidValue;
+  const long tot = (long)nb * B * (N / 4);
+  if (tot <= 0) return hipSuccess;
+  if (dtype == DT_BF16) FF_LAUNCH(k_mod_combine<DT_BF16>, cdiv(tot, 256), 256, 0, st, out, N, bias, dst, ldy, nb, B);
+  else FF_LAUNCH(k_mod_combine<DT_F32>, cdiv(tot, 256), 256, 0, st, out, N, bias, dst, ldy, nb, B);
   return hipGetLastError();
 }
 

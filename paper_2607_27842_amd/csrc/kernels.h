@@ -179,6 +179,21 @@ hipError_t rel_l1(int dtype, const void* a, const void* b, int B, size_t Eb, flo
 // ---------------------------------------------------------------- small per-step kernels
 // phi[k] = cos(s f_k), phi[128 + k] = sin(s f_k), f_k = exp(-ln(1e4) k / 128), in fp64.
 hipError_t time_embed(double s, float* phi, hipStream_t st);
+// The same embedding for every step of a schedule: phi[i * 256 + :] for s_i = 1000 (1 - i / T),
+// i < n (the conditioning does not depend on the latent, so all steps can be formed at once).
+hipError_t time_embed_steps(double T, int n, float* phi, hipStream_t st);
+// SiLU(c_t) of steps i < nsteps and model rows b < B, c_t = cond[b, :] + u[i, :] (fp32).
+// xs set (bf16 models): its bf16 hi / lo split in the GemvArgs::xs layout of step i at
+// xs + i * 16 * groups * C (groups = ceil(B / 8)); rows of absent samples are zero.
+// Otherwise (fp32 models): cs[(i * B + b) * C + :].  zb[0, nzb) is zeroed (a bias of zeros).
+hipError_t cond_split(const float* u, const float* cond, int nsteps, int B, int C, uint16_t* xs, float* cs,
+                      uint16_t* zb, int nzb, hipStream_t st);
+// Modulation vectors from a GEMM over hi / lo split rows: for step blocks j < nb and model
+// rows b < B (R16 = 16 * ceil(B / 8) GEMM rows per block, hi row 16 (b/8) + b%8, lo row 8
+// further):  dst[(j * B + b) * ldy + n] = (out[hi, n] + out[lo, n]) + bias[n],  n < N.
+// out fp32 [nb * R16, N]; bias model dtype; N % 4 == 0.
+hipError_t mod_combine(int dtype, const float* out, int N, const void* bias, float* dst, int ldy, int nb, int B,
+                       hipStream_t st);
 // y[b*n + k] = silu(x[b*n + k]) for k < n; with xs (B <= kGemvMaxB) also its bf16 hi / lo split
 // for the MFMA GEMVs (GemvArgs::xs layout, K = n)
 hipError_t silu_rows(const float* x, float* y, int B, int n, uint16_t* xs, hipStream_t st);

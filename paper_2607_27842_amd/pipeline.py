@@ -121,7 +121,7 @@ class Runner:
     """A plan + cache + workspace + context for one mode of one model."""
 
     def __init__(self, dm: DeviceModel, mode, mask, feature_mode=abi.FF_RESIDUAL, T=None, R=None, K=None,
-                 S=None, eps=None, tau=0.0, part_stride=2, hist_sums=False, device=_DEV):
+                 S=None, eps=None, tau=0.0, part_stride=2, hist_sums=False, cond_cache=False, device=_DEV):
         cfg = dm.cfg
         self.dm = dm
         self.T = cfg["T"] if T is None else T
@@ -147,6 +147,13 @@ class Runner:
             if nb:
                 self.hsum = torch.empty(nb, dtype=torch.uint8, device=device)
                 abi.ff_ctx_hist_sums(self.ctx, self.hsum.data_ptr(), nb)
+        # the conditioning of the whole schedule formed at step 0 (every step then passes
+        # the same cond tensor)
+        self.ccache = None
+        if cond_cache:
+            nb = abi.ff_cond_cache_bytes(dm.desc, self.plan)
+            self.ccache = torch.empty(nb, dtype=torch.uint8, device=device)
+            abi.ff_ctx_cond_cache(self.ctx, self.ccache.data_ptr(), nb)
 
     def export_plan(self):
         return abi.ff_plan_export(self.plan, self.T, self.L, self.K)

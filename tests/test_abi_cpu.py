@@ -334,3 +334,75 @@ def test_hist_sums_errors_are_host_side():
     assert Lb.ff_ctx_hist_sums(ctx, 3 << 30, need) == abi.FF_E_UNSUPPORTED
     abi.ff_ctx_destroy(ctx)
     abi.ff_plan_destroy(plan)
+
+
+def cond_cache_layout(cfg, T, R, mask, mode, tau=0.0):
+    """Bytes of the conditioning cache as its header states the parts: time embedding and
+    MLP rows of all T steps, SiLU(c_t) (bf16: hi / lo rows, a zero bias and the GEMM's
+    rows), per layer the modulation of every step or of the refresh steps, and the final
+    modulation of every step; each part rounded up to 256 bytes."""
+    up = lambda b: (b + 255) // 256 * 256
+    C, B, L = cfg["C"], cfg["B"], len(cfg["kinds"])
+    plan = O.make_plan(T, L, R, cfg["K"], cfg["S"], mask, mode)
+    act, kind = np.asarray(plan["action"]), plan["step_kind"]
+    total = up(T * 256 * 4) + 2 * up(T * C * 4)
+    R16 = 16 * ((B + 7) // 8)
+    if cfg["dtype"] == synth.BF16:
+        total += up(T * R16 * C * 2) + up(6 * C * 2) + up(T * R16 * 6 * C * 4)
+    else:
+        total += up(T * B * C * 4)
+    m = np.asarray(mask, np.uint8).reshape(T, L)
+    for l, k in enumerate(cfg["kinds"]):
+        exact = np.isin(act[:, l], (O.EXACT, O.SITE, O.RECOMPUTE_ACT))
+        every = tau > 0 or any(exact[i] and i % R for i in range(T)) or \
+            any(kind[i] == O.CACHED_STEP and m[i, l] for i in range(T))
+        nb = T if every else (T + R - 1) // R
+        ldy = 12 * C if k == synth.MMDIT_DOUBLE else 3 * C if k == synth.MMDIT_SINGLE else 6 * C
+        total += up(nb * B * ldy * 4)
+    return total + up(T * B * 2 * C * 4)
+
+
+@pytest.mark.parametrize("name", ["tiny", "dit_xl2", "flux", "qwen", "hunyuan"])
+def test_cond_cache_bytes_cover_the_steps_each_layer_runs_exact(name):
+    cfg = synth.get_config(name)
+    T, L, R = cfg["T"], len(cfg["kinds"]), cfg["R"]
+    m = pipeline.model_desc(cfg)
+    mask = synth.site_mask(cfg)
+    got = {}
+    for mode in (abi.FF_FEATFIX, abi.FF_EXACT_ONLY, abi.FF_VERIFY, abi.FF_DRAFT, abi.FF_VANILLA, abi.FF_RECOMPUTE):
+        p = abi.ff_plan_build(sched(T, R, cfg["K"], cfg["S"], mode), L, mask.reshape(-1))
+        got[mode] = abi.ff_cond_cache_bytes(m, p)
+        assert got[mode] == cond_cache_layout(cfg, T, R, mask, mode), mode
+        abi.ff_plan_destroy(p)
+    # the per-layer step sets follow the mask, not the mode: modes with the same exact
+    # blocks (and Draft, whose sites are drafted) size the cache alike
+    assert got[abi.FF_FEATFIX] == got[abi.FF_EXACT_ONLY] == got[abi.FF_VERIFY] == got[abi.FF_DRAFT]
+    assert got[abi.FF_VANILLA] > got[abi.FF_FEATFIX]
+    pa = abi.ff_plan_build(abi.ff_sched_desc(T, R, cfg["K"], cfg["S"], 1e-8, abi.FF_FEATFIX, abi.FF_RESIDUAL,
+                                             0.05, 2), L, mask.reshape(-1))
+    assert abi.ff_cond_cache_bytes(m, pa) == cond_cache_layout(cfg, T, R, mask, abi.FF_FEATFIX, tau=0.05)
+    assert abi.ff_cond_cache_bytes(m, pa) == got[abi.FF_VANILLA]
+    abi.ff_plan_destroy(pa)
+    if name == "dit_xl2":   # 26 layers at the 10 refresh steps, the two sites at all 50
+        assert got[abi.FF_FEATFIX] < got[abi.FF_VANILLA] / 3
+
+
+def test_cond_cache_errors_are_host_side():
+    cfg, m = tiny_desc(dtype=synth.BF16)
+    T, L = cfg["T"], 4
+    lw, g = fake_weights(L)
+    cb, wb = abi.ff_cache_bytes(m, 2), abi.ff_workspace_bytes(m)
+    Lb = abi.lib()
+    plan = abi.ff_plan_build(sched(T, 3, 1, 2, abi.FF_FEATFIX), L, synth.site_mask(cfg))
+    need = abi.ff_cond_cache_bytes(m, plan)
+    assert need > 0
+    bad = pipeline.model_desc(dict(cfg, C=250))
+    assert abi.ff_cond_cache_bytes(bad, plan) == 0
+    ctx = abi.ff_ctx_create(m, lw, g, plan, 1 << 30, cb, 2 << 30, wb)
+    assert Lb.ff_ctx_cond_cache(None, 3 << 30, need) == abi.FF_E_NULL
+    assert Lb.ff_ctx_cond_cache(ctx, 3 << 30, need - 1) == abi.FF_E_WORKSPACE
+    assert Lb.ff_ctx_cond_cache(ctx, (3 << 30) + 16, need) == abi.FF_E_SHAPE
+    assert Lb.ff_ctx_cond_cache(ctx, 3 << 30, need) == abi.FF_OK
+    assert Lb.ff_ctx_cond_cache(ctx, None, 0) == abi.FF_OK
+    abi.ff_ctx_destroy(ctx)
+    abi.ff_plan_destroy(plan)
