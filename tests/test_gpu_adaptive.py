@@ -109,7 +109,8 @@ def test_adaptive_dit_width_bf16_batch_matches_oracle():
     """The adaptive policy where the bench runs it: DiT-XL/2 width (C = 1152, 16 heads of
     72, 256 tokens), bf16, batch 4, K = 2, sites on two layers; the threshold gives a mixed
     schedule with every deciding value (largest discrepancy over sites and samples) more
-    than 1 % away from it.  The GPU must take the oracle's decisions step for step."""
+    than 1 % away from it.  The GPU must take the oracle's decisions step for step, on the
+    benchmarked path (history sums, conditioning cache) and layer by layer."""
     need_gpu()
     cfg = synth.get_config("dit_xl2", kinds=[synth.DIT] * 4, sites=[1, 3], B=4, T=12, R=4)
     W = synth.make_weights(cfg, bias_std=0.02, gain_std=0.1)
@@ -125,7 +126,7 @@ def test_adaptive_dit_width_bf16_batch_matches_oracle():
     assert mixed_schedule(ref, cfg) and margin > 1e-2
     for hist_sums in (False, True):
         dm = pipeline.DeviceModel.from_host(cfg, *W)
-        run = pipeline.Runner(dm, abi.FF_FEATFIX, mask, tau=tau, hist_sums=hist_sums)
+        run = pipeline.Runner(dm, abi.FF_FEATFIX, mask, tau=tau, hist_sums=hist_sums, cond_cache=hist_sums)
         x, c, txt = pipeline.host_inputs_to_device(cfg, inp)
         xt, audit, counts = run.run(x, c, txt)
         torch.cuda.synchronize()

@@ -17,8 +17,8 @@ MODES = {"vanilla": abi.FF_VANILLA, "draft": abi.FF_DRAFT, "verify": abi.FF_VERI
          "exact_only": abi.FF_EXACT_ONLY}
 
 
-def run(dm, mode, mask, inputs, hist_sums=True, tau=0.0):
-    r = pipeline.Runner(dm, mode, mask, hist_sums=hist_sums, tau=tau)
+def run(dm, mode, mask, inputs, hist_sums=True, tau=0.0, cond_cache=False):
+    r = pipeline.Runner(dm, mode, mask, hist_sums=hist_sums, tau=tau, cond_cache=cond_cache)
     used = r.hsum is not None
     x, audit, counts = r.run(*inputs)
     torch.cuda.synchronize()
@@ -122,8 +122,9 @@ def test_dit_xl2_full_depth_with_history_sums_sampled():
     """The DiT-XL/2 workload at full depth and batch 8 (runs 0-12 and 14-26) over 12 steps:
     refreshes at 0, 5 and 10, so steps 11 drafts at second order (k_eff = 2, three history
     terms, the ring of 3 slots full) -- the draft of 32 of the 40 cached steps of the
-    50-step loop.  With history sums (the benchmarked path) and layer by layer, both
-    against the oracle, which follows samples 0 and 7 (samples never interact)."""
+    50-step loop.  With history sums and the conditioning cache (the benchmarked path) and
+    layer by layer, both against the oracle, which follows samples 0 and 7 (samples never
+    interact)."""
     need_gpu()
     cfg = synth.get_config("dit_xl2", T=12)
     W = synth.make_weights(cfg, bias_std=0.02, gain_std=0.1)
@@ -131,7 +132,7 @@ def test_dit_xl2_full_depth_with_history_sums_sampled():
     mask = synth.site_mask(cfg)
     dm = pipeline.DeviceModel.from_host(cfg, *W)
     dev_inp = pipeline.host_inputs_to_device(cfg, inp)
-    sums = run(dm, abi.FF_FEATFIX, mask, dev_inp)
+    sums = run(dm, abi.FF_FEATFIX, mask, dev_inp, cond_cache=True)   # the benchmarked path
     assert sums[4]
     per_layer = run(dm, abi.FF_FEATFIX, mask, dev_inp, hist_sums=False)
     del dm

@@ -1,7 +1,8 @@
 """Whole-loop parity of the MMDiT workloads at full width and token count (Eq. 1-5 on the
 FLUX-like shape of Table 1 and the Qwen-Image-like and HunyuanVideo-like shapes of
 Tables 3-4): reduced-depth stacks (synth.reduced_stack) run through ff_denoise_step in
-FeatFix mode, with history sums (the benchmarked path) and layer by layer, against the
+FeatFix mode, with history sums and the conditioning cache (the benchmarked path) and
+layer by layer with per-step conditioning, against the
 oracle's results stored by tests/golden/make_mmdit_golden.py (the fp64 oracle needs
 20-60 minutes per stack on the host)."""
 import json
@@ -51,8 +52,10 @@ def test_full_width_mmdit_loop_matches_oracle(name):
     audit_ref = {(i, l): g["audit"][i, l] for i in range(T) for l in range(L) if np.isfinite(g["audit"][i, l]).all()}
     counts_ref = dict(zip(COUNT_KEYS, (int(v) for v in g["counts"])))
     ref_x = g["x"].astype(np.float64)
+    # the benchmarked path (history sums and the conditioning cache), and layer by layer
+    # with the conditioning formed at every step
     for hist_sums in (True, False):
-        r = pipeline.Runner(dm, abi.FF_FEATFIX, mask, hist_sums=hist_sums)
+        r = pipeline.Runner(dm, abi.FF_FEATFIX, mask, hist_sums=hist_sums, cond_cache=hist_sums)
         assert (r.hsum is not None) == hist_sums
         x, audit, counts = r.run(*dev_inp)
         torch.cuda.synchronize()
