@@ -53,7 +53,9 @@ __global__ __launch_bounds__(NW * SPLIT * 64) void k_attn32(AttnArgs a) {
   auto Vt = [&](int g, int b) { return smem + SPLIT * 2 * KSZ + (g * 2 + b) * VSZ; };
 
   // SPLIT groups of NW wavefronts take the same queries over disjoint key ranges
-  const int grp = threadIdx.x / NT, gtid = threadIdx.x % NT;
+  // a group is whole wavefronts (NT % 64 == 0): grp in a scalar register keeps the key tile
+  // origin, and with it the tile base address and the in-range test, scalar
+  const int grp = __builtin_amdgcn_readfirstlane(threadIdx.x / NT), gtid = threadIdx.x % NT;
   const int lane = threadIdx.x & 63, wave = (threadIdx.x >> 6) % NW;
   const int c32 = lane & 31, h = lane >> 5;
   const int b = blockIdx.z, hd = blockIdx.y;
@@ -87,23 +89,50 @@ __global__ __launch_bounds__(NW * SPLIT * 64) void k_attn32(AttnArgs a) {
   // V: group g -> keys 4 (g % (KTL/4)) + 0..3, dims (g / (KTL/4))*8: each transposed row piece
   // (4 keys of one dim) is one 8-byte LDS store, and the 16 consecutive lanes of a store
   // fill one 128-byte V^T row segment (no bank conflicts).
+  // Each load is a uniform 64-bit tile base (the tile's first key row) plus this lane's
+  // 32-bit byte offset, fixed before the loop, so the per-tile address work is scalar and the
+  // loads take the scalar-base form.  Tiles whose chunks are all in range (every key below
+  // N, d equal to the padded head dims, every chunk owned) load without lane masks.
   u32x4_t pk[PK], pv[PV][4];
+  uint32_t kbo[PK], vbo[PV];
+  int kkr[PK], vk4[PV];
+  bool kok[PK], vok[PV];
+  const size_t rowb = (size_t)a.ldq * 2;   // bytes per token row of qkv
+#pragma unroll
+  for (int i = 0; i < PK; ++i) {
+    const int c = gtid + i * NT;
+    const int kr = c / (DQ / 8), e = (c % (DQ / 8)) * 8;
+    kkr[i] = kr;
+    kok[i] = c < KCH && e < d;
+    kbo[i] = kok[i] ? (uint32_t)(kr * rowb + (koff + e) * 2) : 0u;
+  }
+#pragma unroll
+  for (int i = 0; i < PV; ++i) {
+    const int g = gtid + i * NT;
+    const int k4 = (g % (KTL / 4)) * 4, e = (g / (KTL / 4)) * 8;
+    vk4[i] = k4;
+    vok[i] = g < VG && e < d;
+    vbo[i] = vok[i] ? (uint32_t)(k4 * rowb + (voff + e) * 2) : 0u;
+  }
+  const bool dense_dims = d == DQ && d == DV && KCH % NT == 0 && VG % NT == 0;
   auto fetch = [&](int kv0) {
+    const char* tb = reinterpret_cast<const char*>(qkv + (rb + kv0) * a.ldq);
+    auto ld = [&](uint32_t off) { return *reinterpret_cast<const u32x4_t*>(tb + off); };
+    if (dense_dims && kv0 + KTL <= N) {
 #pragma unroll
-    for (int i = 0; i < PK; ++i) {
-      const int c = gtid + i * NT;
-      const int kr = c / (DQ / 8), e = (c % (DQ / 8)) * 8, key = kv0 + kr;
-      pk[i] = (c < KCH && key < N && e < d) ? *reinterpret_cast<const u32x4_t*>(qkv + (rb + key) * a.ldq + koff + e) : z4;
-    }
+      for (int i = 0; i < PK; ++i) pk[i] = ld(kbo[i]);
 #pragma unroll
-    for (int i = 0; i < PV; ++i) {
-      const int g = gtid + i * NT;
-      const int k4 = (g % (KTL / 4)) * 4, e = (g / (KTL / 4)) * 8;
+      for (int i = 0; i < PV; ++i)
 #pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int key = kv0 + k4 + r;
-        pv[i][r] = (g < VG && key < N && e < d) ? *reinterpret_cast<const u32x4_t*>(qkv + (rb + key) * a.ldq + voff + e) : z4;
-      }
+        for (int r = 0; r < 4; ++r) pv[i][r] = ld(vbo[i] + (uint32_t)(r * rowb));
+    } else {
+      const int lim = N - kv0;   // keys at or past it are masked
+#pragma unroll
+      for (int i = 0; i < PK; ++i) pk[i] = (kok[i] && kkr[i] < lim) ? ld(kbo[i]) : z4;
+#pragma unroll
+      for (int i = 0; i < PV; ++i)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) pv[i][r] = (vok[i] && vk4[i] + r < lim) ? ld(vbo[i] + (uint32_t)(r * rowb)) : z4;
     }
   };
   auto stage = [&](int buf) {
@@ -354,6 +383,8 @@ __global__ __launch_bounds__(64) void k_attn_f32(AttnArgs a) {
 hipError_t attention(int dtype, const AttnArgs& a, hipStream_t s) {
   if (a.N <= 0) return hipSuccess;
   if (dtype == DT_BF16) {
+    // a lane's byte offset within a key tile (at most 132 rows of qkv) must fit 32 bits
+    if ((uint64_t)a.ldq * 2 * 132 > 0xffffffffull) return hipErrorInvalidValue;
     // 8 wavefronts (256 queries) per workgroup when that still gives >= 256 workgroups;
     // else 4 wavefronts (128 queries), and when even those are fewer than 2 per CU on
     // average, two groups of 4 over the two halves of the keys
