@@ -653,6 +653,172 @@ __global__ __launch_bounds__(256) void k_final_layer(FinalArgs a) {
   }
 }
 
+// The same final layer in bf16 on v_mfma_f32_32x32x16_bf16, for at most 32 outputs per
+// token and C <= kFinMfmaMaxC (C % 16 == 0).  A workgroup of 8 wavefronts takes ROWS token
+// rows: each wavefront loads its ROWS / 8 rows at once, normalises them (LN + modulation,
+// rounded to bf16 as ln_modulate stores it) into an LDS tile [ROWS][C + 8]; wavefront w
+// then accumulates the 16-wide k steps w, w + 8, ... of v^T = W a^T, with its W fragments
+// loaded at the start (rows of W past P read as zero; the MFMA's 32 token columns repeat
+// the ROWS rows); the eight partial sums meet in LDS in wavefront order, and wavefront 0
+// adds the bias and applies the Euler update to the latent values it read at the start.
+// W is read once per ROWS tokens instead of once per token.
+constexpr int kFinMfmaMaxC = 1536;
+
+// latent index of output o (feature order (dt, dy, dx, ch)) of image token tok of sample b
+__device__ __forceinline__ size_t fin_pixel(const PatchGeom& g, int b, int tok, int o) {
+  const int Hp = g.H / g.ph, Wp = g.W / g.pw;
+  const int wx = tok % Wp, hy = (tok / Wp) % Hp, f = tok / (Wp * Hp);
+  const int ch = o % g.lat_c, dx = (o / g.lat_c) % g.pw, dy = (o / (g.lat_c * g.pw)) % g.ph;
+  const int da = o / (g.lat_c * g.pw * g.ph);
+  return ((((size_t)b * g.lat_c + ch) * g.F + (f * g.pt + da)) * g.H + (hy * g.ph + dy)) * g.W + (wx * g.pw + dx);
+}
+
+template <int ROWS>   // token rows per workgroup: 8 or 16
+__global__ __launch_bounds__(512) void k_final_mfma(FinalArgs a) {
+  constexpr int kFinMfmaRows = ROWS;
+  static_assert(ROWS == 8 || ROWS == 16, "rows per workgroup");
+  constexpr int LDA = kFinMfmaMaxC + 8;         // LDS row pitch (elements): 16-byte aligned rows
+  constexpr int U8 = kFinMfmaMaxC / 8 / 64;     // 8-element units per lane and row
+  constexpr int KW = kFinMfmaMaxC / 16 / 8;     // k steps per wavefront
+  constexpr int RPW = kFinMfmaRows / 8;         // rows per wavefront
+  constexpr int kXch = 7 * 16 * 64 * 2;         // the exchange of wavefronts 1-7 (uint16 units)
+  __shared__ __attribute__((aligned(16))) uint16_t sA[kFinMfmaRows * LDA > kXch ? kFinMfmaRows * LDA : kXch];
+  const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int r0 = blockIdx.x * kFinMfmaRows;
+  const int C = a.C, units = C / 8, nks = C / 16;
+  const int P = a.g.pt * a.g.ph * a.g.pw * a.g.lat_c;
+  const uint16_t* Wt = reinterpret_cast<const uint16_t*>(a.W);
+  const uint16_t* in = reinterpret_cast<const uint16_t*>(a.in);
+  const u32x4_t z4 = {0u, 0u, 0u, 0u};
+  // wavefront 0 reads the latent values it will update first: lane l, output 8 (v/4) +
+  // 4 (l/32) + v%4 of token row l%32
+  const int n_img = (a.g.F / a.g.pt) * (a.g.H / a.g.ph) * (a.g.W / a.g.pw);
+  const int me = lane & 31, re = r0 + me;
+  const bool eout = wave == 0 && me < kFinMfmaRows && re < a.rows;
+  float xv[16];
+  size_t xi[16];
+  if (eout) {
+    const int b = a.map.sample(re), tok = re - b * n_img;
+#pragma unroll
+    for (int v = 0; v < 16; ++v) {
+      const int o = 8 * (v >> 2) + 4 * (lane >> 5) + (v & 3);
+      xi[v] = o < P ? fin_pixel(a.g, b, tok, o) : 0;
+      xv[v] = o < P ? a.x[xi[v]] : 0.f;
+    }
+  }
+  // this wavefront's rows, all loads in flight together
+  u32x4_t raw[RPW][U8];
+#pragma unroll
+  for (int j = 0; j < RPW; ++j) {
+    const int r = r0 + wave * RPW + j;
+    const size_t pr = r < a.rows ? (size_t)a.map.phys(r) : 0;
+#pragma unroll
+    for (int k = 0; k < U8; ++k) {
+      const int u = k * 64 + lane;
+      raw[j][k] = (r < a.rows && u < units) ? *reinterpret_cast<const u32x4_t*>(in + pr * a.ldi + u * 8) : z4;
+    }
+  }
+  // W fragments of this wavefront's k steps: lane l holds output l%32, k 16 s + 8 (l/32) + 0..7
+  bf16x8_t wf[KW];
+#pragma unroll
+  for (int j = 0; j < KW; ++j) {
+    const int s = wave + 8 * j, n = lane & 31;
+    const u32x4_t v = (s < nks && n < P) ? *reinterpret_cast<const u32x4_t*>(Wt + (size_t)n * C + 16 * s + 8 * (lane >> 5)) : z4;
+    wf[j] = __builtin_bit_cast(bf16x8_t, v);
+  }
+  // LN + modulation (rows past the end are left unwritten: their outputs are never stored)
+  int bcur = -1;
+  float s8[U8][8], c8[U8][8];
+#pragma unroll
+  for (int j = 0; j < RPW; ++j) {
+    const int rr = wave * RPW + j, r = r0 + rr;
+    if (r >= a.rows) break;
+    const int b = a.map.sample(r);
+    if (b != bcur) {   // the shift / scale of this row's sample (uniform per wavefront)
+      bcur = b;
+      const float* sh = a.shift + (size_t)b * a.ldm;
+      const float* sc = a.scale + (size_t)b * a.ldm;
+#pragma unroll
+      for (int k = 0; k < U8; ++k) {
+        const int u = k * 64 + lane;
+        if (u < units) {
+          St<DT_F32>::load(sh, u * 8, s8[k]);
+          St<DT_F32>::load(sh, u * 8 + 4, s8[k] + 4);
+          St<DT_F32>::load(sc, u * 8, c8[k]);
+          St<DT_F32>::load(sc, u * 8 + 4, c8[k] + 4);
+        }
+      }
+    }
+    float v[U8][8];
+    float s = 0.f;
+#pragma unroll
+    for (int k = 0; k < U8; ++k) {
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        v[k][2 * q] = __uint_as_float(raw[j][k][q] << 16);
+        v[k][2 * q + 1] = __uint_as_float(raw[j][k][q] & 0xffff0000u);
+      }
+      if (k * 64 + lane < units) {
+#pragma unroll
+        for (int q = 0; q < 8; q += 2) s += v[k][q] + v[k][q + 1];
+      }
+    }
+    const float mean = wave_sum(s) / (float)C;
+    float qv = 0.f;
+#pragma unroll
+    for (int k = 0; k < U8; ++k)
+      if (k * 64 + lane < units) {
+#pragma unroll
+        for (int q = 0; q < 8; ++q) {
+          const float dlt = v[k][q] - mean;
+          qv += dlt * dlt;
+        }
+      }
+    const float rstd = 1.0f / sqrtf(wave_sum(qv) / (float)C + a.eps);
+#pragma unroll
+    for (int k = 0; k < U8; ++k) {
+      const int u = k * 64 + lane;
+      if (u < units) {
+        float o[8];
+#pragma unroll
+        for (int q = 0; q < 8; ++q) o[q] = (v[k][q] - mean) * rstd * (1.0f + c8[k][q]) + s8[k][q];
+        St<DT_BF16>::store(sA + rr * LDA, u * 8, o);
+      }
+    }
+  }
+  __syncthreads();
+  // lane l: token row (l%32) % 16; D[v] holds output 8 (v/4) + 4 (l/32) + v%4
+  f32x16_t acc;
+#pragma unroll
+  for (int v = 0; v < 16; ++v) acc[v] = 0.f;
+#pragma unroll
+  for (int j = 0; j < KW; ++j) {
+    const int s = wave + 8 * j;
+    if (s < nks) {
+      const bf16x8_t af = *reinterpret_cast<const bf16x8_t*>(sA + (lane & (kFinMfmaRows - 1)) * LDA + 16 * s + 8 * (lane >> 5));
+      acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(wf[j], af, acc, 0, 0, 0);
+    }
+  }
+  __syncthreads();   // every wavefront's tile reads are done: the tile becomes the exchange
+  float* red = reinterpret_cast<float*>(sA);
+  static_assert(7 * 16 * 64 * 4 <= sizeof(sA), "exchange space");
+  if (wave > 0) {
+#pragma unroll
+    for (int v = 0; v < 16; ++v) red[((wave - 1) * 16 + v) * 64 + lane] = acc[v];
+  }
+  __syncthreads();
+  if (wave > 0) return;
+#pragma unroll
+  for (int w = 1; w < 8; ++w)
+#pragma unroll
+    for (int v = 0; v < 16; ++v) acc[v] += red[((w - 1) * 16 + v) * 64 + lane];
+  if (!eout) return;
+#pragma unroll
+  for (int v = 0; v < 16; ++v) {
+    const int o = 8 * (v >> 2) + 4 * (lane >> 5) + (v & 3);
+    if (o < P) a.x[xi[v]] = xv[v] + a.dt * (acc[v] + St<DT_BF16>::ld1(a.bias, o));
+  }
+}
 
 }  // namespace
 
@@ -821,14 +987,27 @@ hipError_t unpatchify_euler(const float* yv, float* x, float dt, const PatchGeom
 }
 
 
+#ifndef FF_FIN_ROWS
+#define FF_FIN_ROWS 8
+#endif
+// bf16 with at most 32 outputs per token and C <= kFinMfmaMaxC: the MFMA kernel
+bool final_mfma(int dtype, int P, int C) {
+  return dtype == DT_BF16 && P >= 1 && P <= 32 && C % 16 == 0 && C >= 16 && C <= kFinMfmaMaxC;
+}
+
 bool final_layer_ok(int dtype, int P, int C) {
-  return (P == 16 || P == 32 || P == 64) && C % 4 == 0 && C <= 4096 && (size_t)P * C * dsize(dtype) <= kFinalMaxWeightBytes;
+  return final_mfma(dtype, P, C) ||
+         ((P == 16 || P == 32 || P == 64) && C % 4 == 0 && C <= 4096 && (size_t)P * C * dsize(dtype) <= kFinalMaxWeightBytes);
 }
 
 hipError_t final_layer(int dtype, const FinalArgs& a, hipStream_t s) {
   if (a.rows == 0) return hipSuccess;
   const int P = a.g.pt * a.g.ph * a.g.pw * a.g.lat_c;
   if (!final_layer_ok(dtype, P, a.C)) return hipErrorInvalidValue;
+  if (final_mfma(dtype, P, a.C)) {
+    FF_LAUNCH(k_final_mfma<FF_FIN_ROWS>, cdiv(a.rows, FF_FIN_ROWS), 512, 0, s, a);
+    return hipGetLastError();
+  }
   const int grid = cdiv(a.rows, 4);
   const int units = cdiv(a.C / 4, 64);
 #define FF_FIN(U, NP)                                                                   \
