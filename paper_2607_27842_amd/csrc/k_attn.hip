@@ -58,8 +58,20 @@ __global__ __launch_bounds__(NW * SPLIT * 64) void k_attn32(AttnArgs a) {
   const int grp = __builtin_amdgcn_readfirstlane(threadIdx.x / NT), gtid = threadIdx.x % NT;
   const int lane = threadIdx.x & 63, wave = (threadIdx.x >> 6) % NW;
   const int c32 = lane & 31, h = lane >> 5;
-  const int b = blockIdx.z, hd = blockIdx.y;
-  const int q0 = blockIdx.x * (NW * 32) + wave * 32;
+  // Workgroups go to the 8 XCDs (each with its own L2) round-robin in launch order; the
+  // first floor(n/8)*8 are renumbered so that each XCD takes a contiguous range of
+  // (sample, head, query block) triples, query blocks fastest: the query blocks of one
+  // head then read its K/V tiles through one L2 instead of all eight.
+  int qb, hd, b;
+  {
+    const int nqb = (a.N + NW * 32 - 1) / (NW * 32), n = gridDim.x, id = blockIdx.x;
+    const int full = n / 8 * 8;
+    const int t = id < full ? (id % 8) * (full / 8) + id / 8 : id;
+    qb = __builtin_amdgcn_readfirstlane(t % nqb);
+    hd = __builtin_amdgcn_readfirstlane((t / nqb) % a.H);
+    b = __builtin_amdgcn_readfirstlane(t / (nqb * a.H));
+  }
+  const int q0 = qb * (NW * 32) + wave * 32;
   const int N = a.N, d = a.d;
   const uint16_t* qkv = reinterpret_cast<const uint16_t*>(a.qkv);
   const size_t rb = (size_t)b * N;
@@ -390,7 +402,9 @@ hipError_t attention(int dtype, const AttnArgs& a, hipStream_t s) {
     // average, two groups of 4 over the two halves of the keys
     const bool wide = (long)((a.N + 255) / 256) * a.H * a.B >= 256;
     const bool split = !wide && (long)((a.N + 127) / 128) * a.H * a.B < 512 && a.N > KT;
-    const dim3 grid((a.N + (wide ? 255 : 127)) / (wide ? 256 : 128), a.H, a.B);
+    const long nwg = (long)((a.N + (wide ? 255 : 127)) / (wide ? 256 : 128)) * a.H * a.B;
+    if (nwg > 0x7fffffffL) return hipErrorInvalidValue;
+    const dim3 grid((unsigned)nwg);   // one dimension: the kernel maps it to (sample, head, query block)
 #define FF_ATTN(DQ, DV)                                                              \
     do {                                                                             \
       if (wide) FF_LAUNCH((k_attn32<DQ, DV, 8, 1, 128>), grid, 512, 0, s, a);        \
