@@ -174,6 +174,17 @@ def test_dit_block_c2048_tiles():
 
 
 
+def test_dit_block_attention_wide_ragged():
+    """Head dim 128 on the 8-wavefront attention grid (4 query blocks x 16 heads x 4
+    samples = 256 workgroups, 128-key tiles): 1000 tokens per sample, so the last query
+    block holds 232 queries and the last key tile 104 keys."""
+    need_gpu()
+    cfg = ragged_cfg(synth.DIT, synth.BF16, d=128, H=16, B=4, lat=(4, 1, 50, 80), mlp_ratio=4)
+    W = boosted(synth.make_layer_weights(cfg, 0, bias_std=0.02, gain_std=0.1), synth.DIT)
+    say("dit block C=2048 d=128 N=1000 B=4 (sampled rows)")
+    check_block(cfg, W, rows=np.array([0, 1, 255, 256, 511, 767, 768, 959, 960, 998, 999]))
+
+
 def test_dit_block_narrow_tiles():
     """A DiT block with 510 token rows (two samples of 255 tokens; the last 128-row tile
     holds 126): qkv, proj and fc2 take 128x64 tiles and fc1 128x96 tiles, both with two k
