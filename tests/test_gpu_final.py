@@ -1,8 +1,8 @@
 """The bf16 final layer (LN + modulation + final linear + unpatchify + Euler, Eq. 1's output
 head) on MFMA: whole loops against the oracle at shapes that take that kernel (at most 32
 outputs per token, C a multiple of 16 up to 1536) with token rows ragged against its
-32-row workgroups, k steps that do not split evenly over its eight wavefronts, 32 outputs
-per token, and the widest C it takes."""
+8-row workgroups, k steps that do not split evenly over its eight wavefronts, 8, 24 and
+32 outputs per token, and the widest C it takes."""
 import numpy as np
 import pytest
 
@@ -16,12 +16,15 @@ pytestmark = pytest.mark.gpu
 PLAN_KEYS = ("step_kind", "refresh_ord", "k_eff", "read_slots", "write_slot", "action")
 
 CASES = {
-    # 3 x 90 = 270 rows (8 workgroups, the last with 14 rows); C = 240: 15 k steps
+    # 3 x 90 = 270 rows (34 workgroups of 8 rows, the last with 6); C = 240: 15 k steps
     "ragged_c240": dict(C=240, H=5, d=48, mlp=960, lat=(4, 1, 20, 18), n_img=90, B=3),
     # lat_c = 8: 32 outputs per token
     "p32": dict(C=256, H=4, d=64, mlp=1024, lat=(8, 1, 16, 16), n_img=64, B=2),
     # the widest C (96 k steps, 12 per wavefront), 48 rows
     "c1536": dict(C=1536, H=12, d=128, mlp=3072, lat=(4, 1, 8, 8), n_img=16, B=3),
+    # 8 and 24 outputs per token: weight rows masked inside the MFMA's 32 output columns
+    "p8": dict(C=256, H=4, d=64, mlp=1024, lat=(2, 1, 16, 16), n_img=64, B=2),
+    "p24": dict(C=256, H=4, d=64, mlp=1024, lat=(6, 1, 12, 12), n_img=36, B=3),
 }
 
 
