@@ -741,6 +741,8 @@ def main():
     ap.add_argument("--no-clock", action="store_true", help="skip the 3 s clock-sampling run (profiling runs)")
     ap.add_argument("--exact-blocks-only", type=int, default=0, metavar="REPS",
                     help="run only the copy calibration and REPS passes of exact blocks (counter profiles)")
+    ap.add_argument("--exact-blocks-workload", default="dit_xl2", choices=["dit_xl2", "flux", "qwen", "hunyuan"],
+                    help="the workload whose exact blocks --exact-blocks-only runs")
     ap.add_argument("--no-cond-cache", action="store_true",
                     help="form the conditioning (time MLP, modulation) at every step instead of once per loop")
     ap.add_argument("--no-hist-sums", action="store_true",
@@ -761,7 +763,7 @@ def main():
 
     calibration_copy()
     if args.exact_blocks_only:
-        exact_blocks_only(args.exact_blocks_only)
+        exact_blocks_only(args.exact_blocks_only, args.exact_blocks_workload)
         return
     clock = None if args.no_clock else ClockSampler()
     name = "dit_xl2"
