@@ -33,6 +33,15 @@ constexpr float kLazy = 8.0f;  // log2 headroom before the running max is raised
 // Head dims are zero-padded: QK^T to a multiple of 16 (DQ), PV to a multiple of 32 (DV).
 __device__ __forceinline__ int vpos(int k) { return (k & ~12) | ((k & 4) << 1) | ((k & 8) >> 1); }
 
+// The two halves of a wavefront exchanged in registers (v_permlane32_swap, no LDS round
+// trip): every lane gets lo = x of lane l % 32 and hi = x of lane l % 32 + 32, so a
+// combination of lo and hi is the same value in lanes l and l ^ 32.
+__device__ __forceinline__ void wave_halves(float x, float& lo, float& hi) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  lo = __uint_as_float(r[0]);
+  hi = __uint_as_float(r[1]);
+}
+
 template <int DQ, int DV, int NW, int SPLIT, int KTL>   // KTL: keys per LDS tile (64 or 128)
 __global__ __launch_bounds__(NW * SPLIT * 64) void k_attn32(AttnArgs a) {
   constexpr int NS = KTL / 32;        // 32-key score tiles per LDS tile
@@ -221,7 +230,11 @@ __global__ __launch_bounds__(NW * SPLIT * 64) void k_attn32(AttnArgs a) {
     for (int t = 0; t < NS; ++t)
 #pragma unroll
       for (int v = 0; v < 16; ++v) mx = fmaxf(mx, sc[t][v]);
-    mx = fmaxf(mx, __shfl_xor(mx, 32, 64)) * sl2;   // scale > 0: max commutes with it
+    {
+      float lo, hi;
+      wave_halves(mx, lo, hi);
+      mx = fmaxf(lo, hi) * sl2;   // scale > 0: max commutes with it
+    }
     if (mx > mrow + kLazy) {
       const float alpha = __builtin_amdgcn_exp2f(mrow - mx);   // v_exp_f32: exp2(-inf) = 0
       lrow *= alpha;
@@ -241,8 +254,11 @@ __global__ __launch_bounds__(NW * SPLIT * 64) void k_attn32(AttnArgs a) {
         sc[t][v] = pr;
         ls += pr;
       }
-    ls += __shfl_xor(ls, 32, 64);
-    lrow += ls;
+    {
+      float lo, hi;
+      wave_halves(ls, lo, hi);
+      lrow += lo + hi;
+    }
     // O^T += V^T P^T over the 16-key groups (keys 16g + ...)
 #pragma unroll
     for (int g = 0; g < 2 * NS; ++g) {
