@@ -34,8 +34,11 @@ template <> __device__ __forceinline__ void st4<DT_BF16>(void* p, size_t i, cons
 // Sum over the 64 lanes of a wavefront for the row statistics, every lane receiving it, in
 // a fixed order: within each row of 16 lanes by DPP moves (xor 1, xor 2, then the 8- and
 // 16-lane mirrors, which pair each partial sum with one covering the other lanes), then the
-// four rows by two swizzles.  The DPP steps replace four of the six LDS-crossbar shuffles
-// of the butterfly (about 0.2 us per LayerNorm launch at DiT-XL/2 size).
+// four rows by the gfx950 row-pair and half-wavefront swaps (v_permlane16_swap,
+// v_permlane32_swap), each adding the even-row (lower-half) value to the odd-row
+// (upper-half) one in every lane.  No step goes through the LDS crossbar (the DPP steps
+// alone took about 0.2 us off a LayerNorm launch at DiT-XL/2 size against the butterfly of
+// six crossbar shuffles).
 template <int CTL>
 __device__ __forceinline__ float dpp_mov(float x) {
   return __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, x), CTL, 0xf, 0xf, false));
@@ -45,9 +48,10 @@ __device__ __forceinline__ float row_sum(float v) {
   v += dpp_mov<0x4E>(v);    // quad_perm [2, 3, 0, 1]
   v += dpp_mov<0x141>(v);   // row_half_mirror
   v += dpp_mov<0x140>(v);   // row_mirror
-  v += __shfl_xor(v, 16, 64);
-  v += __shfl_xor(v, 32, 64);
-  return v;
+  const auto r16 = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  v = __uint_as_float(r16[0]) + __uint_as_float(r16[1]);
+  const auto r32 = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return __uint_as_float(r32[0]) + __uint_as_float(r32[1]);
 }
 
 // One wavefront per row: LN over C (biased variance, no affine), then adaLN modulation.
