@@ -77,46 +77,61 @@ __global__ __launch_bounds__(256) void k_ln_modulate(LnModArgs a) {
   const int units = a.C / 8;
   const float* sh = a.shift + (size_t)b * a.ldm;
   const float* sc = a.scale + (size_t)b * a.ldm;
+  // Every load of the row is issued before any value is used: a lane's units past the row
+  // end load unit 0 (in range) and take no part in the arithmetic.  Under the per-unit lane
+  // test the loads were serialised: the compiler waited for each unit's values inside the
+  // test that the sums below share with it, one memory round trip per unit.
   float v[U][8], s8[U][8], c8[U][8];
-  float s = 0.f;
 #pragma unroll
   for (int k = 0; k < U; ++k) {
-    const int u = k * 64 + lane;
-    if (u < units) {
-      ld8<DT_IN>(a.in, pr * a.ldi + u * 8, v[k]);
-      ld8<DT_F32>(sh, u * 8, s8[k]);
-      ld8<DT_F32>(sc, u * 8, c8[k]);
-    }
+    const int u = k * 64 + lane, uc = u < units ? u : 0;
+    ld8<DT_IN>(a.in, pr * a.ldi + uc * 8, v[k]);
+    ld8<DT_F32>(sh, uc * 8, s8[k]);
+    ld8<DT_F32>(sc, uc * 8, c8[k]);
   }
   if (PRE) {
     // the run of drafted layers that precedes this block, from its history sums: the same
-    // fmas in the same order as k_draft_sum, one rounding, written back to the stream
+    // fmas in the same order as k_draft_sum, one rounding, written back to the stream.
+    // The history terms of UB units are all loaded before their fmas (UB = U while the
+    // registers allow), so they too are one round trip rather than one per unit and term.
+    constexpr int UB = U <= 4 ? U : 1;
 #pragma unroll
-    for (int k = 0; k < U; ++k) {
-      const int u = k * 64 + lane;
-      if (u < units) {
-        const size_t i = pr * a.ldi + u * 8;
-        float f[8];
+    for (int k0 = 0; k0 < U; k0 += UB) {
+      float p[UB][kMaxTerms][8];
 #pragma unroll
-        for (int j = 0; j < 8; ++j) f[j] = 0.0f;
+      for (int m = 0; m < kMaxTerms; ++m) {
+        if (m < a.pre.n) {
 #pragma unroll
-        for (int m = 0; m < kMaxTerms; ++m) {
-          if (m < a.pre.n) {
-#pragma unroll
-            for (int j = 0; j < 8; j += 4) {
-              float p[4];
-              St<DT_F32>::load_nt(a.pre.slot[m], i + j, p);
-#pragma unroll
-              for (int q = 0; q < 4; ++q) f[j + q] = fmaf(a.pre.c[m], p[q], f[j + q]);
-            }
+          for (int kk = 0; kk < UB; ++kk) {
+            const int u = (k0 + kk) * 64 + lane, uc = u < units ? u : 0;
+            const size_t i = pr * a.ldi + uc * 8;
+            St<DT_F32>::load_nt(a.pre.slot[m], i, p[kk][m]);
+            St<DT_F32>::load_nt(a.pre.slot[m], i + 4, p[kk][m] + 4);
           }
         }
+      }
 #pragma unroll
-        for (int j = 0; j < 8; ++j) v[k][j] = St<DT_IN>::rnd(v[k][j] + f[j]);
-        st8<DT_IN>(const_cast<void*>(a.in), i, v[k]);
+      for (int kk = 0; kk < UB; ++kk) {
+        const int k = k0 + kk, u = k * 64 + lane;
+        if (u < units) {
+          float f[8];
+#pragma unroll
+          for (int j = 0; j < 8; ++j) f[j] = 0.0f;
+#pragma unroll
+          for (int m = 0; m < kMaxTerms; ++m) {
+            if (m < a.pre.n) {
+#pragma unroll
+              for (int j = 0; j < 8; ++j) f[j] = fmaf(a.pre.c[m], p[kk][m][j], f[j]);
+            }
+          }
+#pragma unroll
+          for (int j = 0; j < 8; ++j) v[k][j] = St<DT_IN>::rnd(v[k][j] + f[j]);
+          st8<DT_IN>(const_cast<void*>(a.in), pr * a.ldi + u * 8, v[k]);
+        }
       }
     }
   }
+  float s = 0.f;
 #pragma unroll
   for (int k = 0; k < U; ++k)
     if (k * 64 + lane < units) {
