@@ -85,54 +85,106 @@ __device__ __forceinline__ void epilogue_block(const GemmArgs a, int rbase, int 
           *reinterpret_cast<u32x2_t*>(lds + off) = u32x2_t{pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3])};
         }
       }
+    if (!kF32) {
 #pragma unroll
-    for (int p = 0; p < NPASS; ++p) {
-      const int rr = p * RPP + lane / CPR, cc = (lane % CPR) * 8;
-      const int src = rr < 32 ? rr : 0;
-      const size_t pr = (size_t)__shfl(prow, src, 64);
-      const int sr = EPI == EPI_GATED ? __shfl(srow, src, 64) : 0;
-      const int r = rbase + i * 32 + rr, c = cbase + cc;
-      if (lane >= RPP * CPR || rr >= 32 || r >= a.M || c >= a.N) continue;
-      if (!kF32) {
+      for (int p = 0; p < NPASS; ++p) {
+        const int rr = p * RPP + lane / CPR, cc = (lane % CPR) * 8;
+        const int src = rr < 32 ? rr : 0;
+        const size_t pr = (size_t)__shfl(prow, src, 64);
+        const int r = rbase + i * 32 + rr, c = cbase + cc;
+        if (lane >= RPP * CPR || rr >= 32 || r >= a.M || c >= a.N) continue;
         *reinterpret_cast<u32x4_t*>(reinterpret_cast<uint16_t*>(a.out) + pr * a.ldo + c) =
             *reinterpret_cast<const u32x4_t*>(lds + rr * LDW + cc);
-        continue;
       }
-      const f32x4_t x0 = *reinterpret_cast<const f32x4_t*>(lf + rr * LDW + cc);
-      const f32x4_t x1 = *reinterpret_cast<const f32x4_t*>(lf + rr * LDW + cc + 4);
-      float v[8] = {x0[0], x0[1], x0[2], x0[3], x1[0], x1[1], x1[2], x1[3]};
-      if (EPI == EPI_GATED) {
-        float rs[8], g[8];
-        if (RES_F32) {
-          St<DT_F32>::load(a.resid, pr * a.ldr + c, rs);
-          St<DT_F32>::load(a.resid, pr * a.ldr + c + 4, rs + 4);
-        } else {
-          St<DT_BF16>::load(a.resid, pr * a.ldr + c, rs);
+      continue;
+    }
+    // fp32-staged rows, in groups of PG passes: every global load of a group (residual,
+    // gate, and the layer input of the history refresh) is requested before the group's
+    // first use.  Lanes that store nothing load row pr, column 0 (in range) and skip the
+    // rest.  With the loads under the per-pass lane test, each pass waited for its own
+    // loads (twice with the history refresh): up to 14 memory round trips per row block.
+    constexpr int PG = NPASS < 4 ? NPASS : 4;
+    const bool want_u = kCache && a.cache_out && a.cache_u;
+#pragma unroll
+    for (int p0 = 0; p0 < NPASS; p0 += PG) {
+      size_t gpr[PG];
+      int gc[PG], grr[PG], gcc[PG];
+      bool ok[PG];
+      f32x4_t rsf[PG][2], gg[PG][2];
+      u32x4_t rsb[PG], uu[PG];
+#pragma unroll
+      for (int q = 0; q < PG; ++q) {
+        const int p = p0 + q;
+        if (p >= NPASS) break;
+        const int rr = p * RPP + lane / CPR, cc = (lane % CPR) * 8;
+        const int src = rr < 32 ? rr : 0;
+        const size_t pr = (size_t)__shfl(prow, src, 64);
+        const int sr = EPI == EPI_GATED ? __shfl(srow, src, 64) : 0;
+        const int r = rbase + i * 32 + rr, c = cbase + cc;
+        ok[q] = !(lane >= RPP * CPR || rr >= 32 || r >= a.M || c >= a.N);
+        const int cl = ok[q] ? c : 0;
+        gpr[q] = pr; gc[q] = c; grr[q] = rr; gcc[q] = cc;
+        if (EPI == EPI_GATED) {
+          if (RES_F32) {
+            const float* rp = reinterpret_cast<const float*>(a.resid) + pr * a.ldr + cl;
+            rsf[q][0] = *reinterpret_cast<const f32x4_t*>(rp);
+            rsf[q][1] = *reinterpret_cast<const f32x4_t*>(rp + 4);
+          } else {
+            rsb[q] = *reinterpret_cast<const u32x4_t*>(reinterpret_cast<const uint16_t*>(a.resid) + pr * a.ldr + cl);
+          }
+          const float* gp = a.gate + (size_t)sr * a.ldg + cl;
+          gg[q][0] = *reinterpret_cast<const f32x4_t*>(gp);
+          gg[q][1] = *reinterpret_cast<const f32x4_t*>(gp + 4);
         }
-        const float* gp = a.gate + (size_t)sr * a.ldg + c;
-        St<DT_F32>::load(gp, 0, g);
-        St<DT_F32>::load(gp, 4, g + 4);
-#pragma unroll
-        for (int e = 0; e < 8; ++e) v[e] = rs[e] + g[e] * v[e];
+        if (want_u) uu[q] = *reinterpret_cast<const u32x4_t*>(reinterpret_cast<const uint16_t*>(a.cache_u) + pr * a.ldo + cl);
       }
-      if (OUT_F32) {
-        St<DT_F32>::store(a.out, pr * a.ldo + c, v);
-        St<DT_F32>::store(a.out, pr * a.ldo + c + 4, v + 4);
-        continue;
-      }
-      St<DT_BF16>::store(a.out, pr * a.ldo + c, v);
-      if (kCache && a.cache_out) {
-        // history refresh from the stored (rounded) output, as the separate kernel does
-        float h[8];
 #pragma unroll
-        for (int e = 0; e < 8; ++e) h[e] = St<DT_BF16>::rnd(v[e]);
-        if (a.cache_u) {
-          float u[8];
-          St<DT_BF16>::load(a.cache_u, pr * a.ldo + c, u);
+      for (int q = 0; q < PG; ++q) {
+        if (p0 + q >= NPASS) break;
+        if (!ok[q]) continue;
+        const size_t pr = gpr[q];
+        const int c = gc[q], rr = grr[q], cc = gcc[q];
+        const f32x4_t x0 = *reinterpret_cast<const f32x4_t*>(lf + rr * LDW + cc);
+        const f32x4_t x1 = *reinterpret_cast<const f32x4_t*>(lf + rr * LDW + cc + 4);
+        float v[8] = {x0[0], x0[1], x0[2], x0[3], x1[0], x1[1], x1[2], x1[3]};
+        if (EPI == EPI_GATED) {
+          float rs[8];
+          if (RES_F32) {
 #pragma unroll
-          for (int e = 0; e < 8; ++e) h[e] -= u[e];
+            for (int e = 0; e < 4; ++e) { rs[e] = rsf[q][0][e]; rs[e + 4] = rsf[q][1][e]; }
+          } else {
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+              rs[2 * e] = __uint_as_float(rsb[q][e] << 16);
+              rs[2 * e + 1] = __uint_as_float(rsb[q][e] & 0xffff0000u);
+            }
+          }
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            v[e] = rs[e] + gg[q][0][e] * v[e];
+            v[e + 4] = rs[e + 4] + gg[q][1][e] * v[e + 4];
+          }
         }
-        St<DT_BF16>::store(a.cache_out, pr * a.ldo + c, h);
+        if (OUT_F32) {
+          St<DT_F32>::store(a.out, pr * a.ldo + c, v);
+          St<DT_F32>::store(a.out, pr * a.ldo + c + 4, v + 4);
+          continue;
+        }
+        St<DT_BF16>::store(a.out, pr * a.ldo + c, v);
+        if (kCache && a.cache_out) {
+          // history refresh from the stored (rounded) output, as the separate kernel does
+          float h[8];
+#pragma unroll
+          for (int e = 0; e < 8; ++e) h[e] = St<DT_BF16>::rnd(v[e]);
+          if (a.cache_u) {
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+              h[2 * e] -= __uint_as_float(uu[q][e] << 16);
+              h[2 * e + 1] -= __uint_as_float(uu[q][e] & 0xffff0000u);
+            }
+          }
+          St<DT_BF16>::store(a.cache_out, pr * a.ldo + c, h);
+        }
       }
     }
   }
