@@ -728,12 +728,14 @@ __global__ __launch_bounds__(512) void k_final_mfma(FinalArgs a) {
   const uint16_t* Wt = reinterpret_cast<const uint16_t*>(a.W);
   const uint16_t* in = reinterpret_cast<const uint16_t*>(a.in);
   const u32x4_t z4 = {0u, 0u, 0u, 0u};
-  // wavefront 0 reads the latent values it will update first: lane l, output 8 (v/4) +
-  // 4 (l/32) + v%4 of token row l%32
+  // wavefront 0 reads the latent values it will update, and their output biases, first:
+  // lane l, output 8 (v/4) + 4 (l/32) + v%4 of token row l%32 (a bias read at the end
+  // made each of the 16 updates wait for its own load)
   const int n_img = (a.g.F / a.g.pt) * (a.g.H / a.g.ph) * (a.g.W / a.g.pw);
   const int me = lane & 31, re = r0 + me;
   const bool eout = wave == 0 && me < kFinMfmaRows && re < a.rows;
   float xv[16];
+  uint16_t bv[16];   // raw bf16: converted where it is used, so no load waits here
   size_t xi[16];
   if (eout) {
     const int b = a.map.sample(re), tok = re - b * n_img;
@@ -742,6 +744,7 @@ __global__ __launch_bounds__(512) void k_final_mfma(FinalArgs a) {
       const int o = 8 * (v >> 2) + 4 * (lane >> 5) + (v & 3);
       xi[v] = o < P ? fin_pixel(a.g, b, tok, o) : 0;
       xv[v] = o < P ? a.x[xi[v]] : 0.f;
+      bv[v] = o < P ? reinterpret_cast<const uint16_t*>(a.bias)[o] : (uint16_t)0;
     }
   }
   // this wavefront's rows, all loads in flight together
@@ -854,7 +857,7 @@ __global__ __launch_bounds__(512) void k_final_mfma(FinalArgs a) {
 #pragma unroll
   for (int v = 0; v < 16; ++v) {
     const int o = 8 * (v >> 2) + 4 * (lane >> 5) + (v & 3);
-    if (o < P) a.x[xi[v]] = xv[v] + a.dt * (acc[v] + St<DT_BF16>::ld1(a.bias, o));
+    if (o < P) a.x[xi[v]] = xv[v] + a.dt * (acc[v] + bf2f(bv[v]));
   }
 }
 
