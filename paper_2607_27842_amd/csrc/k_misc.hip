@@ -203,10 +203,16 @@ __global__ __launch_bounds__(256) void k_rms_qk(RmsQKArgs a) {
   const int col = (int)(wv % nseg) * 64 * S::V + lane * S::V;
   const bool on = col < span;
   const size_t base = (size_t)a.map.phys((int)r) * a.ld;
-  float v[S::V];
+  const int qk = col >= a.H * a.d;
+  const int e = (col - qk * a.H * a.d) % a.d;   // a multiple of V: the gain chunk is one access
+  const void* g = qk ? a.gk : a.gq;
+  float v[S::V], gv[S::V];
   float ss = 0.f;
   if (on) {
+    // the gain chunk is requested with the row chunk (read after the reduction, one
+    // element at a time, each of its loads waited on its own)
     S::load(a.x, base + col, v);
+    S::load(g, e, gv);
 #pragma unroll
     for (int j = 0; j < S::V; ++j) ss = fmaf(v[j], v[j], ss);
   }
@@ -214,11 +220,8 @@ __global__ __launch_bounds__(256) void k_rms_qk(RmsQKArgs a) {
   for (int o = LPH / 2; o >= 1; o /= 2) ss += __shfl_xor(ss, o, 64);
   if (!on) return;
   const float inv = 1.0f / sqrtf(ss / (float)a.d + a.eps);
-  const int qk = col >= a.H * a.d;
-  const int e = (col - qk * a.H * a.d) % a.d;
-  const void* g = qk ? a.gk : a.gq;
 #pragma unroll
-  for (int j = 0; j < S::V; ++j) v[j] = v[j] * inv * S::ld1(g, e + j);
+  for (int j = 0; j < S::V; ++j) v[j] = v[j] * inv * gv[j];
   const Rope& ro = a.rope;
   if (ro.axes[0] + ro.axes[1] + ro.axes[2]) {
     // the row's token n within its sample; image rows carry (frame, row, column) ids
@@ -230,9 +233,13 @@ __global__ __launch_bounds__(256) void k_rms_qk(RmsQKArgs a) {
       for (int j = 0; j < S::V; j += 2) {   // e + j is even: a lane holds whole pairs
         int p = e + j, ax = 0;
         if (p >= ro.axes[0]) { p -= ro.axes[0]; ax = 1; if (p >= ro.axes[1]) { p -= ro.axes[1]; ax = 2; } }
-        const float w = exp2f(-(float)p / (float)ro.axes[ax] * ro.log2_theta);   // theta^(-2i/da), p = 2i
+        // selects, not ro.axes[ax] / pos[ax]: a lane-varying index into the argument block
+        // became a memory load (and a wait) per pair
+        const int da = ax == 0 ? ro.axes[0] : (ax == 1 ? ro.axes[1] : ro.axes[2]);
+        const float ps = ax == 0 ? pos[0] : (ax == 1 ? pos[1] : pos[2]);
+        const float w = exp2f(-(float)p / (float)da * ro.log2_theta);   // theta^(-2i/da), p = 2i
         float sn, cs;
-        sincosf(pos[ax] * w, &sn, &cs);
+        sincosf(ps * w, &sn, &cs);
         const float x0 = v[j], x1 = v[j + 1];
         v[j] = x0 * cs - x1 * sn;
         v[j + 1] = x0 * sn + x1 * cs;
