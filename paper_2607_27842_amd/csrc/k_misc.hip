@@ -92,9 +92,10 @@ __global__ __launch_bounds__(256) void k_ln_modulate(LnModArgs a) {
   if (PRE) {
     // the run of drafted layers that precedes this block, from its history sums: the same
     // fmas in the same order as k_draft_sum, one rounding, written back to the stream.
-    // The history terms of UB units are all loaded before their fmas (UB = U while the
-    // registers allow), so they too are one round trip rather than one per unit and term.
-    constexpr int UB = U <= 4 ? U : 1;
+    // The history terms of UB units are all loaded before their fmas (all units up to
+    // C = 2048, two at a time above), so they take one round trip per batch rather than
+    // one per unit and term.
+    constexpr int UB = U <= 4 ? U : 2;
 #pragma unroll
     for (int k0 = 0; k0 < U; k0 += UB) {
       float p[UB][kMaxTerms][8];
