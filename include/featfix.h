@@ -54,7 +54,7 @@ enum {
   FF_E_STATE = -5,       /* slot never written, draft before first refresh, step order */
   FF_E_WORKSPACE = -6,   /* workspace or cache buffer too small                      */
   FF_E_HIP = -7,         /* a HIP runtime call failed                                 */
-  FF_E_UNSUPPORTED = -8  /* valid request this build does not implement              */
+  FF_E_UNSUPPORTED = -8  /* valid request the library does not implement           */
 };
 
 enum { FF_DIT = 0, FF_MMDIT_DOUBLE = 1, FF_MMDIT_SINGLE = 2 };          /* block kinds  */

@@ -1,7 +1,7 @@
 """CPU oracle of the FeatFix cached denoising loop -- TEST INFRASTRUCTURE ONLY.
 
 Plain, slow NumPy code in fp64 that states what the GPU path must compute.  Only the
-tests, the graft smoke check and the benchmark's CPU-baseline leg may import it; the
+tests, the `__graft_entry__.smoke()` check and the benchmark's CPU-baseline leg may import it; the
 product path (the C-ABI library and its Python binding) never does, and this package
 imports nothing from the product.
 
