@@ -1,10 +1,10 @@
 """The bf16 loop refreshes the feature history (Eq. 2: slot <- h - u, rounded to bf16) from
-the epilogue of each exact block's last GEMM rather than in a separate pass.  At a refresh
-step every layer is exact, so the per-layer traces give each layer's input u (the
-previous layer's output) and output h: the slot the loop wrote must equal
-ff_cache_update(u, h) bit for bit.  Shapes are ragged against the GEMM tiles (rows and
-columns cut at the ends), for DiT blocks and for MMDiT double (text, then image stream)
-and single blocks."""
+the epilogue of each exact block's last GEMM rather than in a separate pass (or slot <- h
+when the history holds block outputs).  At a refresh step every layer is exact, so the
+per-layer traces give each layer's input u (the previous layer's output) and output h:
+the slot the loop wrote must equal ff_cache_update(u, h) bit for bit.  Shapes are ragged
+against the GEMM tiles (rows and columns cut at the ends), for DiT blocks and for MMDiT
+double (text, then image stream) and single blocks."""
 import numpy as np
 import pytest
 import torch
@@ -26,8 +26,9 @@ CASES = {
 }
 
 
+@pytest.mark.parametrize("feature_mode", [abi.FF_RESIDUAL, abi.FF_OUTPUT])
 @pytest.mark.parametrize("case", list(CASES))
-def test_fused_refresh_equals_cache_update(case):
+def test_fused_refresh_equals_cache_update(case, feature_mode):
     need_gpu()
     cfg = CASES[case]()
     assert cfg["dtype"] == synth.BF16
@@ -36,7 +37,7 @@ def test_fused_refresh_equals_cache_update(case):
     W = synth.make_weights(cfg, bias_std=0.02, gain_std=0.1)
     inp = synth.make_inputs(cfg)
     dm = pipeline.DeviceModel.from_host(cfg, *W)
-    r = pipeline.Runner(dm, abi.FF_FEATFIX, synth.site_mask(cfg))
+    r = pipeline.Runner(dm, abi.FF_FEATFIX, synth.site_mask(cfg), feature_mode=feature_mode)
     trace = torch.empty(L * E, dtype=torch.bfloat16, device="cuda")
     r.trace_into(trace)
     x0, c, txt = pipeline.host_inputs_to_device(cfg, inp)
@@ -46,8 +47,8 @@ def test_fused_refresh_equals_cache_update(case):
     ref = torch.zeros_like(r.cache)
     s = torch.cuda.current_stream().cuda_stream
     for l in range(1, L):
-        abi.ff_cache_update(dm.desc, ref.data_ptr(), r.S, l, slot, trace[(l - 1) * E:].data_ptr(),
-                            trace[l * E:].data_ptr(), abi.FF_RESIDUAL, s)
+        u = trace[(l - 1) * E:].data_ptr() if feature_mode == abi.FF_RESIDUAL else None
+        abi.ff_cache_update(dm.desc, ref.data_ptr(), r.S, l, slot, u, trace[l * E:].data_ptr(), feature_mode, s)
     torch.cuda.synchronize()
     got = r.cache.view(torch.int16)[: L * r.S * E].view(L, r.S, E)
     exp = ref.view(torch.int16)[: L * r.S * E].view(L, r.S, E)
@@ -55,6 +56,6 @@ def test_fused_refresh_equals_cache_update(case):
     for l in range(1, L):
         g, e = got[l, slot].cpu().numpy(), exp[l, slot].cpu().numpy()
         nbad = int(np.count_nonzero(g != e))
-        say(f"fused refresh {case} layer {l} ({cfg['kinds'][l]}): {E} values, {nbad} differ")
+        say(f"fused refresh {case} mode {feature_mode} layer {l} ({cfg['kinds'][l]}): {E} values, {nbad} differ")
         assert nbad == 0, f"{case}: layer {l}: {nbad} of {E} history values differ from ff_cache_update"
-        assert np.count_nonzero(e) > E // 2   # the slot holds the residual, not a cleared buffer
+        assert np.count_nonzero(e) > E // 2   # the slot holds data, not a cleared buffer
