@@ -63,8 +63,6 @@ CONFIGS = {
 def get_config(name: str, **overrides) -> dict:
     cfg = copy.deepcopy(CONFIGS[name])
     cfg.update(overrides)
-    if "kinds" in overrides or "n_layers" in overrides:
-        pass
     return cfg
 
 

@@ -79,14 +79,12 @@ def test_refresh_draft_verify_match_oracle(name, feature_mode):
     say(f"  draft: k_eff={ke} slots={slots} max|d|={np.abs(got - ref).max():.3e} ulp-misses={nbad}")
     assert nbad <= max(2, E // 100000), nbad
     # in-place draft gives the same bits
+    # (in FF_OUTPUT mode the draft ignores u: the output overwrites the buffer it was given)
     inplace = ud.clone()
     abi.ff_draft_forecast(m, cache.data_ptr(), S, 0, ke, slots, coeffs, inplace.data_ptr() if uptr else None,
                           inplace.data_ptr())
-    if uptr is None:
-        pass
     torch.cuda.synchronize()
-    if uptr is not None:
-        assert torch.equal(inplace, out)
+    assert torch.equal(inplace, out)
     # verify + replace
     hf_np = synth.normal((E,), 555, bf16=bf)
     hf = dev(hf_np, dt)
@@ -140,3 +138,59 @@ def test_memkernels_deterministic():
         outs.append(o)
         rels.append(r)
     assert torch.equal(outs[0], outs[1]) and torch.equal(rels[0], rels[1])
+
+
+@pytest.mark.parametrize("dtype", [synth.F32, synth.BF16])
+@pytest.mark.parametrize("feature_mode", [abi.FF_RESIDUAL, abi.FF_OUTPUT])
+def test_verify_degenerate_samples(dtype, feature_mode):
+    """Eq. 4 at its edges, one case per sample of a single call, at k_eff = 0 (Eq. 2 reduces
+    to the last refresh alone) on a shape that fills no tile evenly (35 tokens x 40
+    channels): h_f equal to the draft (d = 0 exactly), h_f all zero (d = sum|h_d| / eps),
+    draft and h_f both zero (0 / eps = 0 exactly), and an ordinary sample.  Both
+    verification entry points must agree bit for bit."""
+    need_gpu()
+    bf = dtype == synth.BF16
+    cfg = synth.get_config("tiny", dtype=dtype, C=40, H=5, d=8, mlp=160, lat=(4, 1, 14, 10), n_img=35, B=4)
+    B, N, C = cfg["B"], cfg["n_img"], cfg["C"]
+    E, S, eps = B * N * C, 2, 1e-3
+    say(f"verify degenerate samples dtype={dtype} feature_mode={feature_mode} E={E}")
+    m = pipeline.model_desc(cfg)
+    dt = pipeline.torch_dtype(cfg)
+    store = O.round_bf16 if bf else (lambda a: np.asarray(a, np.float64).astype(np.float32).astype(np.float64))
+    slot_np = synth.normal((S, B, N * C), 31, bf16=bf)
+    u_np = synth.normal((B, N * C), 32, bf16=bf)
+    slot_np[1, 2] = 0.0   # sample 2: the read slot and u are zero, so the draft is zero
+    u_np[2] = 0.0
+    res = feature_mode == abi.FF_RESIDUAL
+    hd_ref = store(slot_np[1].astype(np.float64) + (u_np if res else 0.0))
+    hf_np = synth.normal((B, N * C), 33, bf16=bf).astype(np.float64)
+    hf_np[0] = hd_ref[0]   # h_f equal to the draft
+    hf_np[1] = 0.0         # h_f zero
+    hf_np[2] = 0.0         # h_f zero, draft zero
+    cache = dev(slot_np.reshape(-1), dt)
+    ud = dev(u_np.reshape(-1), dt) if res else None
+    hf = dev(hf_np.reshape(-1), dt)
+    ws_bytes = abi.ff_workspace_bytes(m)
+    ws = torch.empty(ws_bytes, dtype=torch.uint8, device="cuda")
+    hd = torch.empty(E, dtype=dt, device="cuda")
+    uptr = ud.data_ptr() if res else None
+    abi.ff_draft_forecast(m, cache.data_ptr(), S, 0, 0, [1], [1.0], uptr, hd.data_ptr())
+    outs, rels = [], []
+    for call in (abi.ff_verify_replace, abi.ff_verify_replace_noalloc):
+        hout = torch.full((E,), 7.0, dtype=dt, device="cuda")
+        rel = torch.full((B,), -1.0, dtype=torch.float32, device="cuda")
+        extra = (ws.data_ptr(), ws_bytes) if call is abi.ff_verify_replace else ()
+        call(m, cache.data_ptr(), S, 0, 0, [1], [1.0], uptr, hf.data_ptr(), hout.data_ptr(), abi.FF_FWD_DRAFT, eps,
+             rel.data_ptr(), *extra)
+        outs.append(hout)
+        rels.append(rel)
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(host(hd).reshape(B, -1), hd_ref)   # one rounding of one exact sum
+    assert torch.equal(outs[0], hd) and torch.equal(outs[1], hd), "Verify forwards the draft"
+    assert torch.equal(rels[0], rels[1]), "both entry points take the same fixed-order sums"
+    got = rels[0].cpu().numpy().astype(np.float64)
+    ref = O.rel_l1(hd_ref, hf_np, eps)
+    say(f"  rel_l1 gpu={got} oracle={ref}")
+    assert got[0] == 0.0 and got[2] == 0.0, got
+    assert ref[1] > 1e3   # sum|h_d| over eps
+    np.testing.assert_allclose(got[[1, 3]], ref[[1, 3]], rtol=1e-4)
