@@ -138,3 +138,32 @@ def test_adaptive_dit_width_bf16_batch_matches_oracle():
         assert counts == ref["counts"]
         assert err <= TOL[synth.BF16], err
         check_audit(audit.cpu().numpy(), ref["audit"], synth.BF16)
+
+
+def test_adaptive_largest_batch_matches_oracle():
+    """The adaptive decision at the largest batch the boundary accepts (32 samples): the
+    value that decides a step is the largest discrepancy over sites and all samples.  With
+    this threshold (pick_tau's choice for these inputs) the early refresh at step 3 is
+    triggered by samples 16-31 alone, so a maximum over part of the batch would take a
+    different decision there."""
+    need_gpu()
+    cfg = dict(synth.get_config("tiny", B=32), T=10, R=4)
+    W = synth.make_weights(cfg, bias_std=0.02, gain_std=0.1)
+    inp = synth.make_inputs(cfg)
+    mask = synth.site_mask(cfg)
+    tau = 0.02166
+    ref = O.run(cfg, O.FEATFIX, inp, W, mask, tau=tau)
+    dec = list(step_maxima(ref["audit"], cfg["T"]).values())
+    margin = min(abs(d - tau) / tau for d in dec)
+    low = max(float(np.max(ref["audit"][(2, l)][:16])) for l in cfg["sites"])
+    say(f"adaptive tiny fp32 B=32 tau={tau} oracle kinds {ref['step_kind']}, margin {margin:.3f}, "
+        f"step 2 max over samples 0-15 {low:.4e}")
+    assert mixed_schedule(ref, cfg) and margin > 1e-2
+    assert ref["step_kind"][3] == O.REFRESH_STEP and low < tau
+    x, audit, counts, kinds = gpu_run(cfg, W, inp, abi.FF_FEATFIX, mask, tau)
+    assert list(kinds) == ref["step_kind"]
+    assert counts == ref["counts"]
+    err = O.max_rel_err(x, ref["x"])
+    say(f"  max rel err {err:.3e}")
+    assert err <= TOL[cfg["dtype"]], err
+    check_audit(audit.cpu().numpy(), ref["audit"], cfg["dtype"])

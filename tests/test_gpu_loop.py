@@ -138,13 +138,16 @@ def test_dit_xl2_full_depth_sampled():
     check_audit(audit.cpu().numpy(), ref["audit"], synth.BF16, idx)
 
 
+@pytest.mark.parametrize("B", [27, 32])
 @pytest.mark.parametrize("dtype", [synth.F32, synth.BF16])
-def test_tiny_loop_batch_of_27(dtype):
-    """27 samples: four groups of 8 in the modulation GEMVs, the last ragged."""
+def test_tiny_loop_large_batches(dtype, B):
+    """27 samples: four groups of 8 in the modulation GEMVs, the last ragged; 32, the
+    largest batch the boundary accepts: four full groups, and the per-sample verify sums
+    and audit columns at their widest."""
     need_gpu()
-    cfg = synth.get_config("tiny", B=27, T=6, dtype=dtype)
+    cfg = synth.get_config("tiny", B=B, T=6, dtype=dtype)
     W = synth.make_weights(cfg, bias_std=0.02, gain_std=0.1)
-    say(f"tiny loop B=27 dtype={dtype}")
+    say(f"tiny loop B={B} dtype={dtype}")
     check_against_oracle(cfg, W, synth.make_inputs(cfg), abi.FF_FEATFIX, synth.site_mask(cfg))
 
 
