@@ -151,6 +151,21 @@ def test_tiny_loop_large_batches(dtype, B):
     check_against_oracle(cfg, W, synth.make_inputs(cfg), abi.FF_FEATFIX, synth.site_mask(cfg))
 
 
+@pytest.mark.parametrize("feature_mode", [abi.FF_RESIDUAL, abi.FF_OUTPUT])
+@pytest.mark.parametrize("dtype", [synth.F32, synth.BF16])
+def test_first_layer_site_zeroth_order(dtype, feature_mode):
+    """A site at layer 0, whose input is the patch embedding of the step, and a zeroth-order
+    forecast (K = 0, a one-slot history: Eq. 2 keeps only the last refresh's difference, or
+    reuses the last output in output mode), in FeatFix and Verify."""
+    need_gpu()
+    cfg = synth.get_config("tiny", K=0, S=1, sites=[0, 2], dtype=dtype)
+    W = synth.make_weights(cfg, bias_std=0.02, gain_std=0.1)
+    inp = synth.make_inputs(cfg)
+    for mode in (abi.FF_FEATFIX, abi.FF_VERIFY):
+        say(f"tiny K=0 sites [0, 2] dtype={dtype} feature_mode={feature_mode} mode={mode}")
+        check_against_oracle(cfg, W, inp, mode, synth.site_mask(cfg), feature_mode)
+
+
 def mmdit_small(name, kinds, n_txt, lat, C=256, H=2, sites=(1,)):
     cfg = synth.get_config(name, kinds=kinds, C=C, H=H, d=C // H, mlp=4 * C, n_txt=n_txt, lat=lat,
                            n_img=lat[1] * (lat[2] // 2) * (lat[3] // 2), T=8, R=3, sites=list(sites))
