@@ -61,3 +61,52 @@ def test_profile_records_match_the_plan(dtype, hist_sums):
     for k, v in st.items():
         assert (v["ms"] > 0) == (v["launches"] > 0), (k, v)
     assert all(v["launches"] == 0 and v["ms"] == 0 for v in again.values()), "reading clears the record"
+
+
+@pytest.mark.parametrize("C", [256, 768])
+def test_profile_flops_mmdit_blocks(C):
+    """MMDiT double blocks (text and image streams, possibly one grouped launch per
+    projection) and single blocks: the recorded GEMM and attention FLOPs equal the block
+    shapes' count, with joint attention over text + image rows, plus per step the patch
+    embedding and, where the final layer's weight (64 patch features x C, bf16) exceeds
+    the 64 KB that the fused final-layer kernel holds (C = 768), the final linear."""
+    need_gpu()
+    D, S1 = synth.MMDIT_DOUBLE, synth.MMDIT_SINGLE
+    cfg = synth.get_config("flux", kinds=[D] * 2 + [S1] * 2, C=C, H=C // 128, d=128, mlp=4 * C, n_txt=24,
+                           lat=(16, 1, 20, 18), n_img=90, B=2, T=4, R=2, sites=[1], dtype=synth.BF16)
+    W = synth.make_weights(cfg, bias_std=0.02, gain_std=0.1)
+    inp = synth.make_inputs(cfg)
+    mask = synth.site_mask(cfg)
+    T, B, M = cfg["T"], cfg["B"], cfg["mlp"]
+    n_img, n_txt, P = cfg["n_img"], cfg["n_txt"], synth.derived(cfg)["P"]
+    final_gemm = P * C * 2 > 64 * 1024
+    N = n_img + n_txt
+    dm = pipeline.DeviceModel.from_host(cfg, *W)
+    r = pipeline.Runner(dm, abi.FF_FEATFIX, mask)
+    abi.ff_ctx_profile(r.ctx, 1)
+    r.run(*pipeline.host_inputs_to_device(cfg, inp))
+    st = abi.ff_ctx_profile_read(r.ctx)
+    kinds = r.step_kinds()
+    r.close()
+    torch.cuda.synchronize()
+    ref = O.run(cfg, O.FEATFIX, inp, W, mask)
+    assert list(kinds) == ref["step_kind"]
+    # exact blocks by kind: every layer at refresh steps, the site layers on cached steps
+    n_ref = ref["counts"]["n_full_refresh"]
+    exact = {D: 0, S1: 0}
+    for l, k in enumerate(cfg["kinds"]):
+        exact[k] += n_ref
+    for (i, l) in ref["audit"]:
+        exact[cfg["kinds"][l]] += 1
+    per_double = sum(2.0 * B * n * (3 * C * C + C * C + M * C + C * M) for n in (n_txt, n_img))
+    per_single = 2.0 * B * N * ((3 * C + M) * C + C * (C + M))
+    per_step = 2.0 * B * n_img * C * P * (2 if final_gemm else 1)
+    gemm = exact[D] * per_double + exact[S1] * per_single + T * per_step
+    attn = (exact[D] + exact[S1]) * 4.0 * B * N * N * cfg["H"] * cfg["d"]
+    say(f"mmdit profile C={C}: exact double {exact[D]}, single {exact[S1]}, final GEMM {final_gemm}; "
+        f"gemm launches {st['gemm']['launches']}, flops {st['gemm']['flops']:.6e} (count {gemm:.6e}); "
+        f"attn {st['attn']['launches']}")
+    np.testing.assert_allclose(st["gemm"]["flops"], gemm, rtol=1e-12)
+    assert st["attn"]["launches"] == exact[D] + exact[S1]
+    np.testing.assert_allclose(st["attn"]["flops"], attn, rtol=1e-12)
+    assert st["verify"]["launches"] == ref["counts"]["n_paid_checks"]
