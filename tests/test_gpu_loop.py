@@ -197,6 +197,36 @@ def test_video_like_reduced_loop():
     check_against_oracle(cfg, W, inp, abi.FF_FEATFIX, synth.site_mask(cfg))
 
 
+def test_rope_video_loop_benchmarked_path():
+    """Rotary embedding in whole loops: a 3-D latent (3 frames of 4 x 5 patches) whose
+    image rows take (frame, row, column) positions on 16 + 56 + 56 of the 128 head
+    dimensions, text rows position 0, through double and single blocks; FeatFix on the
+    path the benchmark runs (history sums, conditioning cache) and layer by layer, against
+    the oracle's latent, plan, counters and audit."""
+    need_gpu()
+    cfg = mmdit_small("hunyuan", [synth.MMDIT_DOUBLE] * 2 + [synth.MMDIT_SINGLE] * 3, 16, (16, 3, 8, 10),
+                      sites=(1, 2, 4))
+    cfg["rope_axes"], cfg["rope_theta"] = (16, 56, 56), 10000.0
+    W = synth.make_weights(cfg, bias_std=0.02, gain_std=0.1)
+    inp = synth.make_inputs(cfg)
+    mask = synth.site_mask(cfg)
+    ref = O.run(cfg, O.FEATFIX, inp, W, mask)
+    dm = pipeline.DeviceModel.from_host(cfg, *W)
+    for fused in (True, False):
+        r = pipeline.Runner(dm, abi.FF_FEATFIX, mask, hist_sums=fused, cond_cache=fused)
+        xt, audit, counts = r.run(*pipeline.host_inputs_to_device(cfg, inp))
+        torch.cuda.synchronize()
+        plan = r.export_plan()
+        r.close()
+        err = O.max_rel_err(host(xt), ref["x"])
+        say(f"rope video loop fused={fused}: max rel err {err:.3e} counts {counts}")
+        assert err <= TOL[cfg["dtype"]], err
+        assert counts == ref["counts"]
+        for key in ("step_kind", "refresh_ord", "k_eff", "read_slots", "write_slot", "action"):
+            np.testing.assert_array_equal(plan[key], ref["plan"][key])
+        check_audit(audit.cpu().numpy(), ref["audit"], cfg["dtype"])
+
+
 def test_out_of_order_step_refused_on_gpu():
     need_gpu()
     cfg = synth.get_config("tiny")
