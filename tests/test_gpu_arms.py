@@ -74,3 +74,33 @@ def test_arm_reductions_bitwise(dtype):
     rc = gpu_run(cfg, W, inp, abi.FF_RECOMPUTE, last, dm=dm)
     ffl = gpu_run(cfg, W, inp, abi.FF_FEATFIX, last, dm=dm)
     assert torch.equal(rc[0], ffl[0]), "recompute with last-layer sites differs from FeatFix"
+
+
+@pytest.mark.parametrize("arm", list(ARMS))
+def test_arm_loops_dit_width_benchmarked_path(arm):
+    """The arms as the benchmark times them: bf16 at DiT-XL/2 width (C = 1152, 16 heads of
+    72, 256 tokens), batch 2, K = 2 (step 7 drafts from three refreshes), sites at layers
+    2 and 5 of 6, so that runs of two drafted layers come from history sums, with the
+    conditioning cache; against the oracle's latent, plan, counters and audit."""
+    need_gpu()
+    cfg = synth.get_config("dit_xl2", kinds=[synth.DIT] * 6, sites=[2, 5], B=2, T=8, R=3)
+    W = synth.make_weights(cfg, bias_std=0.02, gain_std=0.1)
+    inp = synth.make_inputs(cfg)
+    mask = synth.site_mask(cfg)
+    gmode, omode = ARMS[arm]
+    ref = O.run(cfg, omode, inp, W, mask, stride=3)
+    dm = pipeline.DeviceModel.from_host(cfg, *W)
+    run = pipeline.Runner(dm, gmode, mask, part_stride=3, hist_sums=True, cond_cache=True)
+    assert run.hsum is not None
+    xt, audit, counts = run.run(*pipeline.host_inputs_to_device(cfg, inp))
+    torch.cuda.synchronize()
+    plan = run.export_plan()
+    run.close()
+    err = O.max_rel_err(host(xt), ref["x"])
+    say(f"  DiT-width bf16 arm={arm} (history sums, conditioning cache): max rel err {err:.3e} counts {counts}")
+    assert int(np.max(plan["k_eff"])) == 2
+    assert err <= TOL[cfg["dtype"]], err
+    assert counts == ref["counts"]
+    for key in ("step_kind", "refresh_ord", "k_eff", "read_slots", "write_slot", "action"):
+        np.testing.assert_array_equal(plan[key], ref["plan"][key])
+    check_audit(audit.cpu().numpy(), ref["audit"], cfg["dtype"])
