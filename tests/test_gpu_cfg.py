@@ -13,9 +13,10 @@ from gpu_util import TOL, check_audit, host, need_gpu, say
 pytestmark = pytest.mark.gpu
 
 
-def check(cfg, W, inp, mode, mask, dm=None):
+def check(cfg, W, inp, mode, mask, dm=None, fused=False):
     dm = dm or pipeline.DeviceModel.from_host(cfg, *W)
-    run = pipeline.Runner(dm, mode, mask)
+    run = pipeline.Runner(dm, mode, mask, hist_sums=fused, cond_cache=fused)
+    assert (run.hsum is not None) == fused and (run.ccache is not None) == fused
     x, c, txt = pipeline.host_inputs_to_device(cfg, inp)
     assert x.shape[0] == cfg["B"] // 2
     xt, audit, counts = run.run(x, c, txt)
@@ -70,3 +71,16 @@ def test_mmdit_guided_loop_with_text():
     W = synth.make_weights(cfg, bias_std=0.02, gain_std=0.1)
     say("guided mmdit with text")
     check(cfg, W, synth.make_inputs(cfg), abi.FF_FEATFIX, synth.site_mask(cfg))
+
+
+def test_dit_width_guided_loop_benchmarked_path():
+    """Guidance on the path the benchmark's guided loop runs: DiT-XL/2 width and tokens,
+    2 guided pairs, bf16, K = 2 (step 7 drafts from three refreshes), sites at layers 2
+    and 5 of 6 so that runs of two drafted layers come from history sums, and the
+    conditioning cache holding both twins' c_t."""
+    need_gpu()
+    cfg = synth.get_config("dit_xl2", kinds=[synth.DIT] * 6, B=4, T=8, R=3, sites=[2, 5], cfg_pairs=1,
+                           cfg_scale=4.0)
+    W = synth.make_weights(cfg, bias_std=0.02, gain_std=0.1)
+    say("guided dit_xl2 width, history sums and conditioning cache")
+    check(cfg, W, synth.make_inputs(cfg), abi.FF_FEATFIX, synth.site_mask(cfg), fused=True)
