@@ -227,6 +227,36 @@ def test_rope_video_loop_benchmarked_path():
         check_audit(audit.cpu().numpy(), ref["audit"], cfg["dtype"])
 
 
+@pytest.mark.parametrize("dtype,hist_sums,S", [(synth.F32, False, 4), (synth.BF16, False, 8), (synth.BF16, True, 4)],
+                         ids=["fp32_S4", "bf16_S8", "bf16_hist_sums_S4"])
+def test_highest_forecast_order(dtype, hist_sums, S):
+    """The highest forecast order the boundary accepts (K = 3: Eq. 2 with four history
+    terms, k_eff = 3 from step 10 on with refreshes every 3 steps), with the smallest ring
+    that holds it (S = 4) and the largest (S = 8), and in bf16 with runs of two drafted
+    layers applied from four history sums."""
+    need_gpu()
+    cfg = synth.get_config("tiny", kinds=[synth.DIT] * 6, sites=[2, 5], K=3, S=S, T=14, R=3, dtype=dtype)
+    W = synth.make_weights(cfg, bias_std=0.02, gain_std=0.1)
+    inp = synth.make_inputs(cfg)
+    mask = synth.site_mask(cfg)
+    ref = O.run(cfg, O.FEATFIX, inp, W, mask)
+    dm = pipeline.DeviceModel.from_host(cfg, *W)
+    r = pipeline.Runner(dm, abi.FF_FEATFIX, mask, hist_sums=hist_sums)
+    assert (r.hsum is not None) == hist_sums
+    xt, audit, counts = r.run(*pipeline.host_inputs_to_device(cfg, inp))
+    torch.cuda.synchronize()
+    plan = r.export_plan()
+    r.close()
+    err = O.max_rel_err(host(xt), ref["x"])
+    say(f"K=3 S={S} dtype={dtype} hist_sums={hist_sums}: k_eff {plan['k_eff'].tolist()}, max rel err {err:.3e}")
+    assert int(np.max(plan["k_eff"])) == 3
+    assert err <= TOL[dtype], err
+    assert counts == ref["counts"]
+    for key in ("step_kind", "refresh_ord", "k_eff", "read_slots", "write_slot", "action"):
+        np.testing.assert_array_equal(plan[key], ref["plan"][key])
+    check_audit(audit.cpu().numpy(), ref["audit"], dtype)
+
+
 def test_out_of_order_step_refused_on_gpu():
     need_gpu()
     cfg = synth.get_config("tiny")
