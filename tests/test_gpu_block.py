@@ -76,10 +76,15 @@ def check_block(cfg, W, seed=0, rows=None, tol=None):
 
 
 @pytest.mark.parametrize("dtype", [synth.F32, synth.BF16])
-@pytest.mark.parametrize("d", [64, 72])
-def test_dit_block_ragged(dtype, d):
+@pytest.mark.parametrize("d,H", [(8, 40), (40, 8), (64, 5), (72, 5), (96, 5)])
+def test_dit_block_ragged(dtype, d, H):
+    # head dims from the smallest the boundary accepts (8, zero-padded to the 64-wide
+    # attention tile) through the 80- and 96-wide tiles.  The small dims take many heads:
+    # at C = 40 the block's update h - u is so small against h (0.12 against 3.9) that one
+    # bf16 step of the stored output is 13 % of it, which the update-relative error
+    # cannot tell from a wrong result.
     need_gpu()
-    cfg = ragged_cfg(synth.DIT, dtype, d=d)
+    cfg = ragged_cfg(synth.DIT, dtype, d=d, H=H)
     W = boosted(synth.make_layer_weights(cfg, 0, bias_std=0.02, gain_std=0.1), synth.DIT)
     say(f"dit ragged dtype={dtype} d={d}")
     check_block(cfg, W)
