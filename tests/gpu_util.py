@@ -56,13 +56,13 @@ AUDIT_RTOL = {synth.F32: 0.0, synth.BF16: 2e-2}
 AUDIT_ATOL = {synth.F32: 1e-5, synth.BF16: 1e-4}
 
 
-def check_audit(a, ref_audit, dtype, idx=None, label=""):
+def check_audit(a, ref_audit, dtype, idx=None, label="", atol=None):
     """GPU audit a [T, L, B] (numpy) against the oracle's {(i, l): d[B]}; idx selects the
     GPU's samples that the oracle followed.  Returns the largest relative deviation."""
     worst = 0.0
     for (i, l), d in ref_audit.items():
         g = a[i, l] if idx is None else a[i, l][idx]
-        np.testing.assert_allclose(g, d, rtol=AUDIT_RTOL[dtype], atol=AUDIT_ATOL[dtype],
+        np.testing.assert_allclose(g, d, rtol=AUDIT_RTOL[dtype], atol=AUDIT_ATOL[dtype] if atol is None else atol,
                                    err_msg=f"audit step {i} layer {l}")
         worst = max(worst, float(np.max(np.abs(g - d) / np.maximum(np.abs(d), 1e-30))))
     say(f"  {label}audit: {len(ref_audit)} paid checks, largest relative deviation {worst:.3e}")

@@ -26,7 +26,7 @@ def gpu_run(cfg, W, inp, mode, mask, feature_mode=abi.FF_RESIDUAL, dm=None):
     return xt, audit, counts, plan
 
 
-def check_against_oracle(cfg, W, inp, mode, mask, feature_mode=abi.FF_RESIDUAL, dm=None):
+def check_against_oracle(cfg, W, inp, mode, mask, feature_mode=abi.FF_RESIDUAL, dm=None, audit_atol=None):
     xt, audit, counts, plan = gpu_run(cfg, W, inp, mode, mask, feature_mode, dm)
     ref = O.run(cfg, mode, inp, W, mask, feature_mode=feature_mode)
     err = O.max_rel_err(host(xt), ref["x"])
@@ -38,7 +38,7 @@ def check_against_oracle(cfg, W, inp, mode, mask, feature_mode=abi.FF_RESIDUAL, 
         np.testing.assert_array_equal(plan[key], ref["plan"][key])
     a = audit.cpu().numpy()
     L = len(cfg["kinds"])
-    check_audit(a, ref["audit"], cfg["dtype"])
+    check_audit(a, ref["audit"], cfg["dtype"], atol=audit_atol)
     paid = np.zeros((cfg["T"], L), bool)
     for (i, l) in ref["audit"]:
         paid[i, l] = True
@@ -255,6 +255,23 @@ def test_highest_forecast_order(dtype, hist_sums, S):
     for key in ("step_kind", "refresh_ord", "k_eff", "read_slots", "write_slot", "action"):
         np.testing.assert_array_equal(plan[key], ref["plan"][key])
     check_audit(audit.cpu().numpy(), ref["audit"], dtype)
+
+
+@pytest.mark.parametrize("B", [1, 3])
+@pytest.mark.parametrize("dtype", [synth.F32, synth.BF16])
+def test_one_token_per_sample_loop(dtype, B):
+    """The smallest token count: a 2 x 2 latent patchified to one token per sample, so
+    attention has a single key (and, where the keys are split between two groups of
+    waves, one group has none) and every GEMM tile holds B rows of 128."""
+    need_gpu()
+    cfg = synth.get_config("tiny", dtype=dtype, lat=(4, 1, 2, 2), n_img=1, B=B)
+    W = synth.make_weights(cfg, bias_std=0.02, gain_std=0.1)
+    say(f"one-token loop dtype={dtype} B={B}")
+    # Eq. 4 sums one token's C = 256 values per sample here: where the fp32 and fp64 sides
+    # round h_f or h_d to neighbouring bf16 values (a step of 2^-8 of |h|), the audit moves
+    # by about 2^-8 / sqrt(C) of a unit per such element, not in proportion to d (~0.02)
+    atol = 4 * 2.0 ** -8 / np.sqrt(cfg["C"]) if dtype == synth.BF16 else None
+    check_against_oracle(cfg, W, synth.make_inputs(cfg), abi.FF_FEATFIX, synth.site_mask(cfg), audit_atol=atol)
 
 
 def test_out_of_order_step_refused_on_gpu():
